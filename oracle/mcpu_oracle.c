@@ -1,0 +1,432 @@
+/*
+ * mcpu_oracle.c -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow CPU reference of one decode step of a gpt-oss-20b-shaped
+ * decoder layer, the generation work that the paper's Run stage is bound by
+ * (Sec. 3.2: the run stage is GPU bound and dominated by generation; the
+ * policy is gpt-oss-20b, Sec. 4 and its training details appendix). Each
+ * turn's tool observation joins the context (Sec. 1, Sec. 3.2), which is why
+ * the step also takes multi-token chunks ("chunked prefill").
+ *
+ * The paper fixes none of the layer's arithmetic; the definitions below are
+ * the public gpt-oss conventions, each stated where it is used. Everything is
+ * computed in float64 with plain loops, in the order the definition gives, with
+ * no blocking, splitting or reordering. Values are rounded only where the
+ * layer stores them: new keys and values are rounded to the cache dtype
+ * (bfloat16 for bf16 layers) when written to the paged cache.
+ *
+ * Only the tests, the smoke check and the benchmark's CPU-baseline leg use
+ * this file. It shares no code, header or table with the GPU library.
+ *
+ * Paged cache format (the library's documented page format, restated here):
+ * a pool holds n_pages pages; page p, KV head g holds 16 tokens x d dims at
+ * base ((p * Hkv + g) * 16 * d). Within it, K element (slot s, dim i) sits at
+ *   ((i / 8) * 16 + s) * 8 + i % 8
+ * and V element (slot s, dim i) at
+ *   (((i / 16) * 4 + s / 4) * 16 + i % 16) * 4 + s % 4.
+ *
+ * Parity pins: every function is checked by tests/test_oracle_pins.py against
+ * brute force, closed forms, library routines and invariants.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_PAGE 16
+
+typedef struct {
+  int32_t hidden, n_q_heads, n_kv_heads, head_dim, n_experts, top_k, ffn_dim;
+  int32_t page_size; /* must be 16 */
+  int32_t window;    /* 0: full attention; else keys p-window+1 .. p */
+  int32_t kv_bf16;   /* 1: the cache stores bfloat16 */
+  double rms_eps, swiglu_alpha, swiglu_limit, swiglu_beta;
+} orc_cfg;
+
+/* Layer parameters, all as fp32 arrays (bfloat16 values are exact in fp32). */
+typedef struct {
+  const float *g1, *w_qkv, *b_qkv, *w_o, *b_o, *g2, *w_r, *b_r;
+  const float *w_gu, *b_gu, *w_d, *b_d, *sinks, *rope_cos, *rope_sin;
+  int32_t rope_max_pos;
+} orc_weights;
+
+enum { ORC_OK = 0, ORC_EINVAL = -1 };
+
+/* ------------------------------------------------------------------------ */
+/* bfloat16: the upper 16 bits of binary32, rounded to nearest, ties to even */
+/* ------------------------------------------------------------------------ */
+
+double orc_round_bf16(double v) {
+  if (v == 0.0 || !isfinite(v)) return v;
+  int e;
+  frexp(v, &e);              /* |v| = m * 2^e, 0.5 <= m < 1 */
+  int q = e - 8;             /* 8 significant bits: ulp = 2^(e-8) */
+  if (q < -133) q = -133;    /* binary32 exponent range: subnormal spacing 2^-133 */
+  double r = ldexp(nearbyint(ldexp(v, -q)), q); /* default mode: nearest, ties even */
+  if (fabs(r) > 3.3895313892515355e38) r = copysign(INFINITY, v);
+  return r;
+}
+
+void orc_round_bf16_array(int64_t n, const double* in, double* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_round_bf16(in[i]);
+}
+
+/* ------------------------------------------------------------------------ */
+/* page format                                                              */
+/* ------------------------------------------------------------------------ */
+
+static int64_t k_index(const orc_cfg* c, int64_t page, int g, int s, int i) {
+  int64_t base = (page * c->n_kv_heads + g) * (int64_t)ORC_PAGE * c->head_dim;
+  return base + ((i / 8) * ORC_PAGE + s) * 8 + i % 8;
+}
+
+static int64_t v_index(const orc_cfg* c, int64_t page, int g, int s, int i) {
+  int64_t base = (page * c->n_kv_heads + g) * (int64_t)ORC_PAGE * c->head_dim;
+  return base + (((i / 16) * (ORC_PAGE / 4) + s / 4) * 16 + i % 16) * 4 + s % 4;
+}
+
+/* physical page that holds position pos of sequence b, or -1 if not present */
+static int64_t page_of(const int32_t* page_table, int max_pages, int n_pages, int b, int pos) {
+  int lp = pos / ORC_PAGE;
+  if (lp < 0 || lp >= max_pages) return -1;
+  int32_t p = page_table[(int64_t)b * max_pages + lp];
+  if (p < 0 || p >= n_pages) return -1;
+  return p;
+}
+
+/* logical <-> page-format conversion of whole pools, for tests */
+void orc_pool_to_logical(const orc_cfg* c, int n_pages, const float* k_pool, const float* v_pool,
+                         float* k_out, float* v_out) {
+  int d = c->head_dim;
+  for (int64_t p = 0; p < n_pages; ++p)
+    for (int g = 0; g < c->n_kv_heads; ++g)
+      for (int s = 0; s < ORC_PAGE; ++s)
+        for (int i = 0; i < d; ++i) {
+          int64_t lin = ((p * c->n_kv_heads + g) * ORC_PAGE + s) * d + i;
+          k_out[lin] = k_pool[k_index(c, p, g, s, i)];
+          v_out[lin] = v_pool[v_index(c, p, g, s, i)];
+        }
+}
+
+void orc_pool_from_logical(const orc_cfg* c, int n_pages, const float* k_in, const float* v_in,
+                           float* k_pool, float* v_pool) {
+  int d = c->head_dim;
+  for (int64_t p = 0; p < n_pages; ++p)
+    for (int g = 0; g < c->n_kv_heads; ++g)
+      for (int s = 0; s < ORC_PAGE; ++s)
+        for (int i = 0; i < d; ++i) {
+          int64_t lin = ((p * c->n_kv_heads + g) * ORC_PAGE + s) * d + i;
+          k_pool[k_index(c, p, g, s, i)] = k_in[lin];
+          v_pool[v_index(c, p, g, s, i)] = v_in[lin];
+        }
+}
+
+/* ------------------------------------------------------------------------ */
+/* RMSNorm: y_i = x_i / sqrt(mean_j x_j^2 + eps) * g_i                       */
+/* ------------------------------------------------------------------------ */
+
+void orc_rmsnorm(int64_t rows, int dim, const double* x, const float* g, double eps, double* y) {
+  for (int64_t r = 0; r < rows; ++r) {
+    const double* xr = x + r * dim;
+    double ss = 0.0;
+    for (int i = 0; i < dim; ++i) ss += xr[i] * xr[i];
+    double inv = 1.0 / sqrt(ss / dim + eps);
+    for (int i = 0; i < dim; ++i) y[r * dim + i] = xr[i] * inv * (double)g[i];
+  }
+}
+
+/* y[r][n] = sum_k x[r][k] * w[n][k] + (b ? b[n] : 0); w is [N][K] row-major */
+static void linear(int64_t rows, int K, int N, const double* x, const float* w, const float* b,
+                   double* y) {
+  for (int64_t r = 0; r < rows; ++r)
+    for (int n = 0; n < N; ++n) {
+      double acc = 0.0;
+      const float* wn = w + (int64_t)n * K;
+      for (int k = 0; k < K; ++k) acc += x[r * K + k] * (double)wn[k];
+      y[r * N + n] = acc + (b ? (double)b[n] : 0.0);
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Rotary position embedding on one head vector of length d at position pos: */
+/* the pair (v_j, v_{j+d/2}) is rotated by the angle whose cosine and sine   */
+/* are cos_tab[pos][j], sin_tab[pos][j].                                     */
+/* ------------------------------------------------------------------------ */
+
+void orc_rope(int d, int pos, const float* cos_tab, const float* sin_tab, double* v) {
+  int h = d / 2;
+  for (int j = 0; j < h; ++j) {
+    double c = cos_tab[(int64_t)pos * h + j], s = sin_tab[(int64_t)pos * h + j];
+    double a = v[j], b = v[j + h];
+    v[j] = a * c - b * s;
+    v[j + h] = a * s + b * c;
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* KV append: token t of sequence tok_seq[t] at position tok_pos[t] stores   */
+/* its key and value ([Hkv][d] each) into the pools, rounded to the cache    */
+/* dtype.                                                                    */
+/* ------------------------------------------------------------------------ */
+
+int orc_kv_append(const orc_cfg* c, int T, const int32_t* tok_seq, const int32_t* tok_pos,
+                  const double* k_new, const double* v_new, float* k_pool, float* v_pool,
+                  const int32_t* page_table, int max_pages, int n_pages) {
+  int d = c->head_dim, G = c->n_kv_heads;
+  for (int t = 0; t < T; ++t) {
+    int64_t page = page_of(page_table, max_pages, n_pages, tok_seq[t], tok_pos[t]);
+    if (page < 0) return ORC_EINVAL;
+    int s = tok_pos[t] % ORC_PAGE;
+    for (int g = 0; g < G; ++g)
+      for (int i = 0; i < d; ++i) {
+        double kv = k_new[((int64_t)t * G + g) * d + i];
+        double vv = v_new[((int64_t)t * G + g) * d + i];
+        if (c->kv_bf16) { kv = orc_round_bf16(kv); vv = orc_round_bf16(vv); }
+        k_pool[k_index(c, page, g, s, i)] = (float)kv;
+        v_pool[v_index(c, page, g, s, i)] = (float)vv;
+      }
+  }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Attention with a sink, one query token.                                   */
+/*   Query head h reads KV head g = h / (Hq / Hkv).                           */
+/*   Visible keys: j in [lo, p], lo = 0 (full) or max(0, p - window + 1).    */
+/*   z_j = q_h . k_j / sqrt(d);  M = max(s_h, max_j z_j)                      */
+/*   o_h = sum_j e^{z_j - M} v_j / (e^{s_h - M} + sum_j e^{z_j - M})          */
+/* The sink logit s_h enters the normaliser only; it carries no value.       */
+/* ------------------------------------------------------------------------ */
+
+int orc_attention(const orc_cfg* c, int T, const int32_t* tok_seq, const int32_t* tok_pos,
+                  const double* q, const float* k_pool, const float* v_pool,
+                  const int32_t* page_table, int max_pages, int n_pages, const float* sinks,
+                  double* o) {
+  int d = c->head_dim, Hq = c->n_q_heads, Hkv = c->n_kv_heads, grp = Hq / Hkv;
+  int bad = 0;
+#pragma omp parallel for schedule(dynamic) reduction(| : bad)
+  for (int t = 0; t < T; ++t) {
+    int b = tok_seq[t], p = tok_pos[t];
+    int lo = c->window > 0 ? (p - c->window + 1 > 0 ? p - c->window + 1 : 0) : 0;
+    int n = p - lo + 1;
+    double* z = (double*)malloc(sizeof(double) * (size_t)n);
+    for (int h = 0; h < Hq; ++h) {
+      int g = h / grp;
+      const double* qh = q + ((int64_t)t * Hq + h) * d;
+      double M = sinks ? (double)sinks[h] : -INFINITY;
+      for (int j = lo; j <= p; ++j) {
+        int64_t page = page_of(page_table, max_pages, n_pages, b, j);
+        if (page < 0) { bad = 1; z[j - lo] = -INFINITY; continue; }
+        double dot = 0.0;
+        for (int i = 0; i < d; ++i) dot += qh[i] * (double)k_pool[k_index(c, page, g, j % ORC_PAGE, i)];
+        z[j - lo] = dot / sqrt((double)d);
+        if (z[j - lo] > M) M = z[j - lo];
+      }
+      double L = sinks ? exp((double)sinks[h] - M) : 0.0;
+      double* oh = o + ((int64_t)t * Hq + h) * d;
+      for (int i = 0; i < d; ++i) oh[i] = 0.0;
+      for (int j = lo; j <= p; ++j) {
+        int64_t page = page_of(page_table, max_pages, n_pages, b, j);
+        if (page < 0) continue;
+        double e = exp(z[j - lo] - M);
+        L += e;
+        for (int i = 0; i < d; ++i) oh[i] += e * (double)v_pool[v_index(c, page, g, j % ORC_PAGE, i)];
+      }
+      for (int i = 0; i < d; ++i) oh[i] /= L;
+    }
+    free(z);
+  }
+  return bad ? ORC_EINVAL : ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Router and experts.                                                       */
+/* ------------------------------------------------------------------------ */
+
+/* SwiGLU in the clamped gpt-oss form: gate is capped above at L, up is      */
+/* clamped to [-L, L]; a = gate * sigmoid(alpha * gate) * (up + beta).        */
+/* alpha = 1, L = inf, beta = 0 is the plain SiLU(gate) * up.                 */
+double orc_swiglu(double gate, double up, double alpha, double limit, double beta) {
+  if (gate > limit) gate = limit;
+  if (up > limit) up = limit;
+  if (up < -limit) up = -limit;
+  return gate / (1.0 + exp(-alpha * gate)) * (up + beta);
+}
+
+void orc_swiglu_array(int64_t n, const double* gate, const double* up, double alpha,
+                      double limit, double beta, double* out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_swiglu(gate[i], up[i], alpha, limit, beta);
+}
+
+/* Top-k selection over E logits: the k largest by value, ties to the lower   */
+/* index; written in descending order. The comparison is made on the logits   */
+/* rounded to fp32, the precision the GPU router decides in.                  */
+void orc_topk(int E, int k, const double* logits, int32_t* idx) {
+  int used[256] = {0};
+  for (int s = 0; s < k; ++s) {
+    int best = -1;
+    float bv = 0.0f;
+    for (int e = 0; e < E; ++e) {
+      if (used[e]) continue;
+      float v = (float)logits[e];
+      if (best < 0 || v > bv) { best = e; bv = v; }
+    }
+    used[best] = 1;
+    idx[s] = best;
+  }
+}
+
+/* One token through one expert: gu = hn . W_gu[e]^T + b_gu[e], rows 2j/2j+1  */
+/* are gate_j/up_j; a_j = swiglu(gate_j, up_j); y = a . W_d[e]^T + b_d[e].    */
+static void expert_ffn(const orc_cfg* c, const orc_weights* w, int e, const double* hn, double* y,
+                       double* gu, double* act) {
+  int H = c->hidden, I = c->ffn_dim;
+  linear(1, H, 2 * I, hn, w->w_gu + (int64_t)e * 2 * I * H, w->b_gu + (int64_t)e * 2 * I, gu);
+  for (int j = 0; j < I; ++j)
+    act[j] = orc_swiglu(gu[2 * j], gu[2 * j + 1], c->swiglu_alpha, c->swiglu_limit, c->swiglu_beta);
+  linear(1, I, H, act, w->w_d + (int64_t)e * H * I, w->b_d + (int64_t)e * H, y);
+}
+
+/* MoE sub-block on the residual stream h [T][H]:                             */
+/*   hn = RMSNorm(h; g2); logits = hn . W_r^T + b_r;                          */
+/*   S = top-k set; w_e = softmax over {logits_e : e in S};                   */
+/*   out = h + sum_{e in S} w_e * FFN_e(hn).                                  */
+/* force_idx (optional [T][k]) replaces the selected set (used where the      */
+/* k-th and (k+1)-th logits are within rounding of each other).              */
+int orc_moe(const orc_cfg* c, const orc_weights* w, int T, const double* h, double* out,
+            int32_t* idx_out, double* w_out, double* logits_out, double* moe_out,
+            const int32_t* force_idx) {
+  int H = c->hidden, E = c->n_experts, k = c->top_k, I = c->ffn_dim;
+  if (k > E || E > 256) return ORC_EINVAL;
+#pragma omp parallel for schedule(dynamic)
+  for (int t = 0; t < T; ++t) {
+    double* hn = (double*)malloc(sizeof(double) * (size_t)H);
+    double* lg = (double*)malloc(sizeof(double) * (size_t)E);
+    double* y = (double*)malloc(sizeof(double) * (size_t)H);
+    double* acc = (double*)calloc((size_t)H, sizeof(double));
+    double* gu = (double*)malloc(sizeof(double) * (size_t)2 * I);
+    double* act = (double*)malloc(sizeof(double) * (size_t)I);
+    int32_t sel[256];
+    double wt[256];
+    orc_rmsnorm(1, H, h + (int64_t)t * H, w->g2, c->rms_eps, hn);
+    linear(1, H, E, hn, w->w_r, w->b_r, lg);
+    if (force_idx) memcpy(sel, force_idx + (int64_t)t * k, sizeof(int32_t) * (size_t)k);
+    else orc_topk(E, k, lg, sel);
+    double mx = -INFINITY, den = 0.0;
+    for (int s = 0; s < k; ++s) if (lg[sel[s]] > mx) mx = lg[sel[s]];
+    for (int s = 0; s < k; ++s) { wt[s] = exp(lg[sel[s]] - mx); den += wt[s]; }
+    for (int s = 0; s < k; ++s) wt[s] /= den;
+    for (int s = 0; s < k; ++s) {
+      expert_ffn(c, w, sel[s], hn, y, gu, act);
+      for (int n = 0; n < H; ++n) acc[n] += wt[s] * y[n];
+    }
+    for (int n = 0; n < H; ++n) out[(int64_t)t * H + n] = h[(int64_t)t * H + n] + acc[n];
+    if (moe_out) memcpy(moe_out + (int64_t)t * H, acc, sizeof(double) * (size_t)H);
+    if (idx_out) memcpy(idx_out + (int64_t)t * k, sel, sizeof(int32_t) * (size_t)k);
+    if (w_out) memcpy(w_out + (int64_t)t * k, wt, sizeof(double) * (size_t)k);
+    if (logits_out) memcpy(logits_out + (int64_t)t * E, lg, sizeof(double) * (size_t)E);
+    free(hn); free(lg); free(y); free(acc); free(gu); free(act);
+  }
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* One decoder-layer step over a batch of sequences.                        */
+/*   seq_lens[b]: tokens already cached; cu_q (optional, [B+1]): token b's    */
+/*   new tokens are rows cu_q[b] .. cu_q[b+1]-1 of x_in, at positions         */
+/*   seq_lens[b] + i. cu_q = NULL means one new token per sequence.           */
+/* Per token at position p:                                                  */
+/*   xn = RMSNorm(x; g1); [q | k | v] = xn . W_qkv^T + b_qkv;                 */
+/*   q, k rotated at p; k, v stored in the cache;                            */
+/*   o = attention with sink (after every new k, v is stored);               */
+/*   h1 = x + o . W_o^T + b_o;  out = MoE(h1).                                */
+/* ------------------------------------------------------------------------ */
+
+int orc_decode_layer(const orc_cfg* c, const orc_weights* w, int B, const int32_t* page_table,
+                     int max_pages, int n_pages, const int32_t* seq_lens, const int32_t* cu_q,
+                     float* k_pool, float* v_pool, const double* x_in, double* x_out,
+                     double* q_out, double* o_out, double* h1_out, int32_t* idx_out,
+                     double* w_out, double* logits_out, double* moe_out,
+                     const int32_t* force_idx) {
+  int H = c->hidden, d = c->head_dim, Hq = c->n_q_heads, Hkv = c->n_kv_heads;
+  int QKV = (Hq + 2 * Hkv) * d, A = Hq * d;
+  if (c->page_size != ORC_PAGE || Hq % Hkv) return ORC_EINVAL;
+  int T = cu_q ? cu_q[B] : B;
+  int32_t* tok_seq = (int32_t*)malloc(sizeof(int32_t) * (size_t)T);
+  int32_t* tok_pos = (int32_t*)malloc(sizeof(int32_t) * (size_t)T);
+  for (int b = 0; b < B; ++b) {
+    int r0 = cu_q ? cu_q[b] : b, r1 = cu_q ? cu_q[b + 1] : b + 1;
+    for (int r = r0; r < r1; ++r) { tok_seq[r] = b; tok_pos[r] = seq_lens[b] + (r - r0); }
+  }
+  double* xn = (double*)malloc(sizeof(double) * (size_t)T * H);
+  double* qkv = (double*)malloc(sizeof(double) * (size_t)T * QKV);
+  double* q = (double*)malloc(sizeof(double) * (size_t)T * A);
+  double* kn = (double*)malloc(sizeof(double) * (size_t)T * Hkv * d);
+  double* vn = (double*)malloc(sizeof(double) * (size_t)T * Hkv * d);
+  double* o = (double*)malloc(sizeof(double) * (size_t)T * A);
+  double* h1 = (double*)malloc(sizeof(double) * (size_t)T * H);
+  int rc = ORC_OK;
+
+  orc_rmsnorm(T, H, x_in, w->g1, c->rms_eps, xn);
+#pragma omp parallel for schedule(static)
+  for (int t = 0; t < T; ++t) linear(1, H, QKV, xn + (int64_t)t * H, w->w_qkv, w->b_qkv, qkv + (int64_t)t * QKV);
+  for (int t = 0; t < T; ++t) {
+    if (tok_pos[t] >= w->rope_max_pos) { rc = ORC_EINVAL; goto done; }
+    for (int h = 0; h < Hq; ++h) {
+      double* qh = q + ((int64_t)t * Hq + h) * d;
+      memcpy(qh, qkv + (int64_t)t * QKV + h * d, sizeof(double) * (size_t)d);
+      orc_rope(d, tok_pos[t], w->rope_cos, w->rope_sin, qh);
+    }
+    for (int g = 0; g < Hkv; ++g) {
+      double* kh = kn + ((int64_t)t * Hkv + g) * d;
+      memcpy(kh, qkv + (int64_t)t * QKV + A + g * d, sizeof(double) * (size_t)d);
+      orc_rope(d, tok_pos[t], w->rope_cos, w->rope_sin, kh);
+      memcpy(vn + ((int64_t)t * Hkv + g) * d, qkv + (int64_t)t * QKV + A + Hkv * d + g * d,
+             sizeof(double) * (size_t)d);
+    }
+  }
+  rc = orc_kv_append(c, T, tok_seq, tok_pos, kn, vn, k_pool, v_pool, page_table, max_pages, n_pages);
+  if (rc) goto done;
+  rc = orc_attention(c, T, tok_seq, tok_pos, q, k_pool, v_pool, page_table, max_pages, n_pages,
+                     w->sinks, o);
+  if (rc) goto done;
+#pragma omp parallel for schedule(static)
+  for (int t = 0; t < T; ++t) {
+    linear(1, A, H, o + (int64_t)t * A, w->w_o, w->b_o, h1 + (int64_t)t * H);
+    for (int n = 0; n < H; ++n) h1[(int64_t)t * H + n] += x_in[(int64_t)t * H + n];
+  }
+  rc = orc_moe(c, w, T, h1, x_out, idx_out, w_out, logits_out, moe_out, force_idx);
+  if (q_out) memcpy(q_out, q, sizeof(double) * (size_t)T * A);
+  if (o_out) memcpy(o_out, o, sizeof(double) * (size_t)T * A);
+  if (h1_out) memcpy(h1_out, h1, sizeof(double) * (size_t)T * H);
+done:
+  free(tok_seq); free(tok_pos); free(xn); free(qkv); free(q); free(kn); free(vn); free(o); free(h1);
+  return rc;
+}
+
+/* ------------------------------------------------------------------------ */
+/* MXFP4 (OCP Microscaling Formats v1.0): blocks of 32 along a row share one  */
+/* E8M0 scale 2^(s - 127); each element is FP4 E2M1 (sign, 2-bit exponent,   */
+/* 1-bit mantissa, bias 1): magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6.            */
+/* codes: [rows][cols/2], low nibble = even column. scales: [rows][cols/32].  */
+/* ------------------------------------------------------------------------ */
+
+double orc_e2m1(int code) {
+  int sign = (code >> 3) & 1, ex = (code >> 1) & 3, man = code & 1;
+  double mag = ex == 0 ? 0.5 * man : ldexp(1.0 + 0.5 * man, ex - 1);
+  return sign ? -mag : mag;
+}
+
+int orc_mxfp4_dequant(int64_t rows, int cols, const uint8_t* codes, const uint8_t* scales,
+                      float* out) {
+  if (cols % 32) return ORC_EINVAL;
+  for (int64_t r = 0; r < rows; ++r)
+    for (int j = 0; j < cols; ++j) {
+      uint8_t byte = codes[r * (cols / 2) + j / 2];
+      int code = (j % 2 == 0) ? (byte & 0xF) : (byte >> 4);
+      uint8_t s = scales[r * (cols / 32) + j / 32];
+      if (s == 0xFF) return ORC_EINVAL; /* NaN scale is not a weight */
+      out[r * cols + j] = (float)ldexp(orc_e2m1(code), (int)s - 127);
+    }
+  return ORC_OK;
+}
