@@ -1,0 +1,226 @@
+/*
+ * mcpu.h -- C ABI of the MI355X (gfx950) decode-layer library.
+ *
+ * What it computes. The paper's rollout pipeline keeps the GPU busy with
+ * generation while trajectories wait on tools: the Run stage is GPU bound and
+ * dominated by generation (Sec. 3.2), the policy is gpt-oss-20b (Sec. 4), and
+ * each turn's tool observation is appended to the context (Sec. 1, Sec. 3.2).
+ * This library runs that generation's per-layer work for a batch of
+ * concurrent trajectories: one decoder-layer step of a gpt-oss-20b-shaped MoE
+ * transformer over a paged KV cache, where every sequence brings one new token
+ * (decode) or a chunk of new tokens (an appended tool observation).
+ *
+ * Conventions shared by every entry point:
+ *  - All device buffers belong to the caller. The library never allocates
+ *    device memory; scratch comes from a caller-provided workspace.
+ *  - Launches are asynchronous on the caller's stream; no entry point except
+ *    mcpu_check_device_errors synchronises or copies device data to the host.
+ *  - Return value: MCPU_OK or a negative mcpu_status; on error nothing was
+ *    launched (host-detected) and mcpu_last_error() describes the cause. No
+ *    C++ exception crosses the ABI.
+ *  - Results are deterministic: no floating-point atomics, fixed reduction
+ *    orders, independent of the physical page placement.
+ *  - Workspace: device memory of at least the *_workspace_size() bytes,
+ *    256-byte aligned. Its first 256 bytes hold the device error word and must
+ *    be zero before the first call (e.g. allocate it zero-filled); errors then
+ *    accumulate until mcpu_check_device_errors() reads and clears them.
+ *
+ * Paged KV cache (the page format). A pool holds n_pages pages. Page p, KV
+ * head g holds 16 consecutive token positions x head_dim dims, at element
+ * base (p * n_kv_heads + g) * 16 * head_dim of the K pool and of the V pool.
+ * Within that block:
+ *   K(slot s, dim i) at ((i / 8) * 16 + s) * 8 + i % 8
+ *   V(slot s, dim i) at (((i / 16) * 4 + s / 4) * 16 + i % 16) * 4 + s % 4
+ * so one 64-lane wavefront reads a page as whole contiguous segments already
+ * in matrix-core operand order. Token position pos of sequence b lives in page
+ * page_table[b * max_pages + pos / 16], slot pos % 16. Unused page-table
+ * entries are -1. The element type is the layer dtype (fp32 or bf16).
+ *
+ * Positions. seq_lens[b] counts the tokens of sequence b already in the cache
+ * before the step. A step writes its new tokens at positions seq_lens[b] ..
+ * seq_lens[b] + q_len_b - 1 and then attends; the caller advances seq_lens
+ * afterwards. Pages covering the new positions must be allocated beforehand.
+ * Sliding-window layers read only pages that intersect [pos - window + 1, pos],
+ * so pages left of the window may be freed (page-table entry -1).
+ */
+#ifndef MCPU_H
+#define MCPU_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MCPU_OK = 0,
+  MCPU_EINVAL = -1,       /* bad shape, pointer, size or configuration */
+  MCPU_ENOMEM = -2,       /* page pool exhausted (kv_pages_alloc) or workspace too small */
+  MCPU_EHIP = -3,         /* a HIP runtime call or kernel launch failed */
+  MCPU_EUNSUPPORTED = -4, /* valid but not implemented (e.g. head_dim other than 32/64) */
+  MCPU_EDEVICE = -5       /* a kernel found invalid data (see mcpu_check_device_errors) */
+} mcpu_status;
+
+enum { MCPU_F32 = 0, MCPU_BF16 = 1 };               /* layer dtype */
+enum { MCPU_EXPERT_DENSE = 0, MCPU_EXPERT_MXFP4 = 1 }; /* expert weight format */
+
+/* Device error bits (mcpu_check_device_errors). */
+enum {
+  MCPU_DEVERR_PAGE = 1,  /* a needed page-table entry was -1 or >= n_pages; its keys were skipped */
+  MCPU_DEVERR_ROPE = 2,  /* a position was >= rope_max_pos; that token's q/k were not written */
+  MCPU_DEVERR_EXPERT = 4, /* a top-k expert id outside [0, n_experts) was passed in */
+  MCPU_DEVERR_PLAN = 8    /* device seq_lens / cu_q disagree with the host copies */
+};
+
+/* Layer configuration (host struct, by value semantics).
+ *  hidden H, n_q_heads Hq, n_kv_heads Hkv (Hq % Hkv == 0, Hq / Hkv <= 16),
+ *  head_dim d in {32, 64}, n_experts E <= 64, top_k k <= min(E, 8),
+ *  ffn_dim I (expert SwiGLU width); H, I and Hq * d multiples of 32.
+ *  page_size must be 16. window 0 = full attention, else keys
+ *  [pos - window + 1, pos]. dtype: MCPU_F32 or MCPU_BF16 for the matrices,
+ *  the KV cache and matrix-core operands. expert_fmt: MCPU_EXPERT_DENSE
+ *  (experts in dtype) or MCPU_EXPERT_MXFP4.
+ *  SwiGLU: a = min(gate, L) * sigmoid(alpha * min(gate, L)) * (clamp(up, -L, L) + beta)
+ *  with alpha = swiglu_alpha, L = swiglu_limit (may be +inf), beta = swiglu_beta. */
+typedef struct mcpu_layer_cfg {
+  int32_t hidden, n_q_heads, n_kv_heads, head_dim, n_experts, top_k, ffn_dim;
+  int32_t page_size, window, dtype, expert_fmt;
+  float rms_eps, swiglu_alpha, swiglu_limit, swiglu_beta;
+} mcpu_layer_cfg;
+
+/* Layer parameters: device pointers owned by the caller. Matrices are
+ * row-major with the reduction dimension contiguous, in the layer dtype
+ * ("T") unless stated. Vectors are fp32.
+ *  g1, g2 [H]            RMSNorm gains before attention and before the MoE
+ *  w_qkv [(Hq+2Hkv)d, H] T   rows: all Q heads, then K heads, then V heads
+ *  b_qkv [(Hq+2Hkv)d]
+ *  w_o [H, Hq d] T, b_o [H]
+ *  w_r [E, H] T, b_r [E] router (logits are formed in fp32)
+ *  w_gu [E, 2I, H], b_gu [E, 2I]  row 2j is gate_j, row 2j+1 is up_j
+ *  w_d [E, H, I], b_d [E, H]
+ *    dense experts: w_gu/w_d in T, s_gu = s_d = NULL.
+ *    MXFP4 experts: w_gu/w_d hold E2M1 codes, [E, rows, cols/2] bytes, low
+ *    nibble = even column; s_gu/s_d hold E8M0 block scales [E, rows, cols/32].
+ *  sinks [Hq]            one attention-sink logit per query head
+ *  rope_cos, rope_sin [rope_max_pos, d/2]  rotation of the pair (j, j + d/2) */
+typedef struct mcpu_layer_weights {
+  const float* g1;
+  const void* w_qkv;
+  const float* b_qkv;
+  const void* w_o;
+  const float* b_o;
+  const float* g2;
+  const void* w_r;
+  const float* b_r;
+  const void* w_gu;
+  const float* b_gu;
+  const void* w_d;
+  const float* b_d;
+  const uint8_t* s_gu;
+  const uint8_t* s_d;
+  const float* sinks;
+  const float* rope_cos;
+  const float* rope_sin;
+  int32_t rope_max_pos;
+} mcpu_layer_weights;
+
+/* Opaque page pool: host-side free list over a caller-owned pair of device
+ * pools (K and V, each n_pages * Hkv * 16 * d elements of the layer dtype). */
+typedef struct mcpu_kv_pool mcpu_kv_pool;
+
+/* Thread-local description of the last non-OK return of this thread. */
+const char* mcpu_last_error(void);
+
+/* Create a pool handle over device buffers k_pool / v_pool. All pages start
+ * free. The handle does not own the buffers. */
+int kv_pool_create(const mcpu_layer_cfg* cfg, int32_t n_pages, void* k_pool, void* v_pool,
+                   mcpu_kv_pool** out);
+int kv_pool_destroy(mcpu_kv_pool* pool);
+/* Number of free pages. */
+int32_t kv_pool_free_pages(const mcpu_kv_pool* pool);
+
+/* Allocate n pages, all or nothing, writing their ids to host array out_ids.
+ * MCPU_ENOMEM (nothing allocated) when fewer than n are free. Ids come out in
+ * ascending order of the free list, lowest first. */
+int kv_pages_alloc(mcpu_kv_pool* pool, int32_t n, int32_t* out_ids);
+/* Return n pages (host array). MCPU_EINVAL, freeing nothing, if any id is out
+ * of range, not allocated, or repeated. */
+int kv_pages_free(mcpu_kv_pool* pool, int32_t n, const int32_t* ids);
+
+/* Write new keys and values into the cache (the append of a step).
+ *  batch sequences; page_table [batch, max_pages], seq_lens [batch] and cu_q
+ *  [batch+1] are device int32; new token row r in [cu_q[b], cu_q[b+1]) of
+ *  sequence b goes to position seq_lens[b] + r - cu_q[b]. cu_q == NULL means
+ *  one token per sequence (row b). n_tokens = total rows.
+ *  k_new, v_new: [n_tokens, Hkv, d] device arrays in the layer dtype, stored
+ *  bit-exactly. Missing pages set MCPU_DEVERR_PAGE and skip that token.
+ *  workspace: at least 256 bytes (error word). */
+int kv_pages_append(mcpu_kv_pool* pool, int32_t batch, const int32_t* page_table,
+                    int32_t max_pages, const int32_t* seq_lens, const int32_t* cu_q,
+                    int32_t n_tokens, const void* k_new, const void* v_new, void* workspace,
+                    size_t ws_bytes, hipStream_t stream);
+
+/* Attention of already-appended queries over the paged cache, with sinks.
+ *  q [n_tokens, Hq, d] (layer dtype, rotated), o [n_tokens, Hq * d] (layer dtype).
+ *  Token row r of sequence b sits at position p = seq_lens[b] + (r - cu_q[b])
+ *  and attends keys [lo, p] (lo = 0, or max(0, p - window + 1)):
+ *    o_h = sum_j e^{z_j - M} v_j / (e^{s_h - M} + sum_j e^{z_j - M}),
+ *    z_j = q_h . k_j / sqrt(d), M = max(s_h, max_j z_j), s_h = sinks[h],
+ *  with query head h reading KV head h / (Hq / Hkv). sinks may be NULL (no sink).
+ *  host_seq_lens / host_cu_q: host copies of the same arrays, used only to
+ *  plan the launch (no device-to-host traffic). */
+size_t paged_attention_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_batch,
+                                      int32_t max_tokens);
+int paged_attention(const mcpu_layer_cfg* cfg, const float* sinks, mcpu_kv_pool* pool,
+                    int32_t batch, const int32_t* page_table, int32_t max_pages,
+                    const int32_t* seq_lens, const int32_t* cu_q, const int32_t* host_seq_lens,
+                    const int32_t* host_cu_q, const void* q, void* o, void* workspace,
+                    size_t ws_bytes, hipStream_t stream);
+
+/* MoE sub-block on the residual stream: h, out [n_tokens, H] fp32 (may alias).
+ *  hn = RMSNorm(h; g2); logits = hn . w_r^T + b_r (fp32); S = the top_k
+ *  experts by logit (ties to the lower index); w_e = softmax over S;
+ *  out = h + sum_{e in S} w_e * (SwiGLU(hn . w_gu[e]^T + b_gu[e]) . w_d[e]^T + b_d[e]).
+ *  topk_idx [n_tokens, k] int32 and topk_w [n_tokens, k] fp32 (device,
+ *  nullable) receive the selection in descending logit order.
+ *  force_idx (device, nullable, [n_tokens, k]): use these experts instead of
+ *  the router's choice (weights still softmax of their logits). */
+size_t moe_forward_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_tokens);
+int moe_forward(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, int32_t n_tokens,
+                const float* h, float* out, int32_t* topk_idx, float* topk_w,
+                const int32_t* force_idx, void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* Optional copies of intermediates of decode_layer (each nullable):
+ *  q [T, Hq, d] layer dtype (after rotation), o [T, Hq * d] layer dtype
+ *  (attention output), h1 [T, H] fp32 (residual after attention). */
+typedef struct mcpu_taps {
+  void* q;
+  void* o;
+  float* h1;
+} mcpu_taps;
+
+/* One decoder-layer step for a batch of sequences:
+ *  xn = RMSNorm(x_in; g1); [q|k|v] = xn . w_qkv^T + b_qkv; q, k rotated at
+ *  their positions; k, v appended to the cache; o = paged_attention(q);
+ *  h1 = x_in + o . w_o^T + b_o; x_out = moe_forward(h1).
+ *  x_in, x_out [T, H] fp32 (must not alias); T = batch, or host_cu_q[batch].
+ *  Arrays as in kv_pages_append / paged_attention / moe_forward. */
+size_t decode_layer_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_batch,
+                                   int32_t max_tokens);
+int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv_pool* pool,
+                 int32_t batch, const int32_t* page_table, int32_t max_pages,
+                 const int32_t* seq_lens, const int32_t* cu_q, const int32_t* host_seq_lens,
+                 const int32_t* host_cu_q, const float* x_in, float* x_out, int32_t* topk_idx,
+                 float* topk_w, const mcpu_taps* taps, void* workspace, size_t ws_bytes,
+                 hipStream_t stream);
+
+/* Synchronise the stream, read the workspace's device error word, clear it.
+ * Returns MCPU_OK, MCPU_EDEVICE (bits in *bits if non-NULL) or MCPU_EHIP. */
+int mcpu_check_device_errors(void* workspace, hipStream_t stream, int32_t* bits);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MCPU_H */

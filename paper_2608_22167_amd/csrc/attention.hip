@@ -1,0 +1,313 @@
+// Paged GQA attention with per-head sinks for gfx950.
+//
+// The step's attention (every new token attends to its sequence's cached keys,
+// plus the sink logit of its head) is split three ways:
+//   plan    one workgroup maps tokens to (sequence, position) and cuts each
+//           token's visible page range into splits of `pps` pages;
+//   split   one wavefront per (split, KV head) streams the split's K and V
+//           pages and keeps a running max / sum / weighted value sum for the
+//           G = Hq / Hkv query heads that share the KV head;
+//   combine one workgroup per token merges the splits and adds the sink to
+//           the normaliser.
+// The score and value products run on the matrix cores: with keys as rows
+// and the G query heads as columns (padded to 16), S^T = K q^T is one 16x16
+// tile per page, and O^T += V^T P^T consumes it without any lane shuffle
+// because the score tile's lane layout is exactly the value product's B
+// operand layout. The page format (include/mcpu.h) makes every K and V
+// fragment load a contiguous 512 B - 1 KiB segment per wavefront.
+#include "device.h"
+#include "kernels.h"
+
+namespace mcpu {
+
+constexpr float LOG2E = 1.4426950408889634f;
+
+// ---------------------------------------------------------------------------
+// plan
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ int token_splits(int pos, int window, int pps) {
+  int lo = window > 0 ? max(0, pos - window + 1) : 0;
+  int pages = pos / PAGE - lo / PAGE + 1;
+  return (pages + pps - 1) / pps;
+}
+
+__device__ __forceinline__ int seq_of_token(const int32_t* cu_q, int batch, int t) {
+  // last b with cu_q[b] <= t
+  int lo = 0, hi = batch - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (cu_q[mid] <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__global__ __launch_bounds__(1024) void attn_plan_kernel(AttnPlan P) {
+  __shared__ int sums[1024];
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int per = (P.n_tokens + nt - 1) / nt;
+  const int t0 = min(P.n_tokens, tid * per), t1 = min(P.n_tokens, t0 + per);
+  int local = 0;
+  for (int t = t0; t < t1; ++t) {
+    int b = P.cu_q ? seq_of_token(P.cu_q, P.batch, t) : t;
+    int pos = P.seq_lens[b] + (P.cu_q ? t - P.cu_q[b] : 0);
+    local += token_splits(pos, P.window, P.pps);
+  }
+  sums[tid] = local;
+  __syncthreads();
+  // Hillis-Steele inclusive scan over the per-thread sums
+  for (int o = 1; o < nt; o <<= 1) {
+    int v = tid >= o ? sums[tid - o] : 0;
+    __syncthreads();
+    sums[tid] += v;
+    __syncthreads();
+  }
+  int run = sums[tid] - local;
+  for (int t = t0; t < t1; ++t) {
+    int b = P.cu_q ? seq_of_token(P.cu_q, P.batch, t) : t;
+    int pos = P.seq_lens[b] + (P.cu_q ? t - P.cu_q[b] : 0);
+    P.tok_seq[t] = b;
+    P.tok_pos[t] = pos;
+    P.split_start[t] = run;
+    run += token_splits(pos, P.window, P.pps);
+  }
+  if (tid == nt - 1) {
+    P.split_start[P.n_tokens] = sums[nt - 1];
+    if (sums[nt - 1] != P.host_total_splits) set_error(P.err, 8);
+  }
+}
+
+hipError_t launch_attn_plan(const AttnPlan& p, hipStream_t s) {
+  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, s, p);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// split: one wavefront per (split, KV head)
+// ---------------------------------------------------------------------------
+
+template <typename T, int D>
+struct PageFrags {
+  Frag<T> k[D / 32];   // chunk c holds dims 32c + 8 * (lane / 16) .. +7 of key lane % 16
+  Frag4<T> v[D / 16];  // block n holds V[4 * (lane / 16) + r][16n + lane % 16]
+  __device__ __forceinline__ void load(const T* kp, const T* vp, int lane) {
+#pragma unroll
+    for (int c = 0; c < D / 32; ++c) k[c].load(kp + (64 * c + lane) * 8);
+#pragma unroll
+    for (int n = 0; n < D / 16; ++n) v[n].load(vp + (64 * n + lane) * 4);
+  }
+};
+
+template <typename T, int D, int WAVES>
+__global__ __launch_bounds__(64 * WAVES) void attn_split_kernel(AttnSplit P) {
+  const int lane = lane_id();
+  const int item = blockIdx.x * WAVES + uniform(threadIdx.x >> 6);
+  const int s = item / P.hkv, g = item - (item / P.hkv) * P.hkv;
+  if (s >= P.n_splits) return;
+
+  // token owning split s: last t with split_start[t] <= s
+  int lo_t = 0, hi_t = P.n_tokens - 1;
+  while (lo_t < hi_t) {
+    int mid = (lo_t + hi_t + 1) >> 1;
+    if (P.split_start[mid] <= s) lo_t = mid; else hi_t = mid - 1;
+  }
+  const int t = uniform(lo_t);
+  const int b = uniform(P.tok_seq[t]), p = uniform(P.tok_pos[t]);
+  const int lo = P.window > 0 ? max(0, p - P.window + 1) : 0;
+  int pg0 = lo / PAGE + (s - uniform(P.split_start[t])) * P.pps;
+  int pg1 = min(pg0 + P.pps, p / PAGE + 1);
+  const int G = P.hq / P.hkv;
+  const int hl = lane & 15, grp = lane >> 4;
+  if (p < 0 || p / PAGE >= P.max_pages || pg0 < 0 || pg0 >= pg1) {
+    // positions outside the page table (device arrays disagree with the plan)
+    if (lane == 0) set_error(P.err, 1);
+    pg0 = pg1 = 0;
+  }
+
+  Frag<T> qf[D / 32];
+  const T* qb = reinterpret_cast<const T*>(P.q) + ((int64_t)t * P.hq + g * G + hl) * D + 8 * grp;
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c) {
+    if (hl < G) qf[c].load(qb + 32 * c); else qf[c].zero();
+  }
+
+  const T* kpool = reinterpret_cast<const T*>(P.k_pool);
+  const T* vpool = reinterpret_cast<const T*>(P.v_pool);
+  const int32_t* ptab = P.page_table + (int64_t)b * P.max_pages;
+  const int64_t head_off = (int64_t)g * PAGE * D, page_elems = (int64_t)P.hkv * PAGE * D;
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 acc[D / 16];
+#pragma unroll
+  for (int n = 0; n < D / 16; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto page_ok = [&](int pg) -> int {
+    int id = uniform(ptab[pg]);
+    if (id < 0 || id >= P.n_pages) {
+      if (lane == 0) set_error(P.err, 1);
+      return -1;
+    }
+    return id;
+  };
+
+  PageFrags<T, D> cur, nxt;
+  int id_cur = pg0 < pg1 ? page_ok(pg0) : -1;
+  if (id_cur >= 0) cur.load(kpool + id_cur * page_elems + head_off, vpool + id_cur * page_elems + head_off, lane);
+  for (int pg = pg0; pg < pg1; ++pg) {
+    int id_nxt = -1;
+    if (pg + 1 < pg1) {
+      id_nxt = page_ok(pg + 1);
+      if (id_nxt >= 0)
+        nxt.load(kpool + id_nxt * page_elems + head_off, vpool + id_nxt * page_elems + head_off, lane);
+    }
+    if (id_cur >= 0) {
+      f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < D / 32; ++c) sc = mma32(cur.k[c], qf[c], sc);
+      // sc[r] = score of key slot 4 * grp + r for query head hl
+      const int key0 = pg * PAGE + 4 * grp;
+      float x[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        int pos = key0 + r;
+        x[r] = (pos >= lo && pos <= p) ? sc[r] * P.scale_log2 : -INFINITY;
+      }
+      float mloc = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      // every page in [pg0, pg1) holds at least one visible key, so mloc is finite
+      const float m_new = fmaxf(m_run, mloc);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      float pr[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) pr[r] = __builtin_amdgcn_exp2f(x[r] - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int n = 0; n < D / 16; ++n) {
+        acc[n] *= alpha;
+        acc[n] = mma16_p(cur.v[n], pr, acc[n], n == 0 ? &l_run : nullptr);
+      }
+      m_run = m_new;
+    }
+    cur = nxt;
+    id_cur = id_nxt;
+  }
+
+  float l_tot = l_run + __shfl_xor(l_run, 16, 64);
+  l_tot += __shfl_xor(l_tot, 32, 64);
+  if (hl < G) {
+    const int64_t row = (int64_t)s * P.hq + g * G + hl;
+    if (grp == 0) {
+      P.part_ml[row * 2 + 0] = m_run;
+      P.part_ml[row * 2 + 1] = l_tot;
+    }
+    float* pa = P.part_acc + row * D + 4 * grp;
+#pragma unroll
+    for (int n = 0; n < D / 16; ++n)
+      *reinterpret_cast<float4*>(pa + 16 * n) = make_float4(acc[n][0], acc[n][1], acc[n][2], acc[n][3]);
+  }
+}
+
+template <typename T, int D>
+static hipError_t split_impl(const AttnSplit& p, hipStream_t s) {
+  constexpr int WAVES = 4;
+  int64_t items = (int64_t)p.n_splits * p.hkv;
+  int blocks = (int)((items + WAVES - 1) / WAVES);
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL((attn_split_kernel<T, D, WAVES>), dim3(blocks), dim3(64 * WAVES), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_split(int dtype, int head_dim, const AttnSplit& p, hipStream_t s) {
+  if (dtype == 0) return head_dim == 32 ? split_impl<float, 32>(p, s) : split_impl<float, 64>(p, s);
+  return head_dim == 32 ? split_impl<bf16, 32>(p, s) : split_impl<bf16, 64>(p, s);
+}
+
+// ---------------------------------------------------------------------------
+// combine: o_h = sum_s 2^{m_s - M} acc_s / (2^{sink_h log2e - M} + sum_s 2^{m_s - M} l_s)
+// ---------------------------------------------------------------------------
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnCombine P) {
+  const int t = blockIdx.x;
+  const int s0 = min(P.split_start[t], P.n_splits), s1 = min(P.split_start[t + 1], P.n_splits);
+  T* o = reinterpret_cast<T*>(P.o) + (int64_t)t * P.hq * D;
+  for (int w = threadIdx.x; w < P.hq * (D / 4); w += blockDim.x) {
+    const int h = w / (D / 4), c = w - h * (D / 4);
+    const float sink = P.sinks ? P.sinks[h] * LOG2E : -INFINITY;
+    float M = sink;
+    for (int s = s0; s < s1; ++s) M = fmaxf(M, P.part_ml[((int64_t)s * P.hq + h) * 2]);
+    float L = P.sinks ? __builtin_amdgcn_exp2f(sink - M) : 0.f;
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (M != -INFINITY) {
+      for (int s = s0; s < s1; ++s) {
+        const int64_t row = (int64_t)s * P.hq + h;
+        const float f = __builtin_amdgcn_exp2f(P.part_ml[row * 2] - M);
+        L += f * P.part_ml[row * 2 + 1];
+        float4 v = *reinterpret_cast<const float4*>(P.part_acc + row * D + 4 * c);
+        a.x += f * v.x; a.y += f * v.y; a.z += f * v.z; a.w += f * v.w;
+      }
+    }
+    const float inv = L > 0.f ? 1.0f / L : 0.f;
+    const int64_t base = (int64_t)h * D + 4 * c;
+    Elem<T>::store(o, base + 0, a.x * inv);
+    Elem<T>::store(o, base + 1, a.y * inv);
+    Elem<T>::store(o, base + 2, a.z * inv);
+    Elem<T>::store(o, base + 3, a.w * inv);
+  }
+}
+
+hipError_t launch_attn_combine(int dtype, int head_dim, const AttnCombine& p, hipStream_t s) {
+  if (p.n_tokens == 0) return hipSuccess;
+  dim3 grid(p.n_tokens), block(256);
+  if (dtype == 0) {
+    if (head_dim == 32) hipLaunchKernelGGL((attn_combine_kernel<float, 32>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((attn_combine_kernel<float, 64>), grid, block, 0, s, p);
+  } else {
+    if (head_dim == 32) hipLaunchKernelGGL((attn_combine_kernel<bf16, 32>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((attn_combine_kernel<bf16, 64>), grid, block, 0, s, p);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// KV append: copy new keys / values into their pages, bit for bit
+// ---------------------------------------------------------------------------
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void kv_append_kernel(KvAppend P) {
+  const int t = blockIdx.x;
+  const int b = P.cu_q ? seq_of_token(P.cu_q, P.batch, t) : t;
+  const int pos = P.seq_lens[b] + (P.cu_q ? t - P.cu_q[b] : 0);
+  const int lp = pos >= 0 ? pos / PAGE : -1;
+  int page = (lp >= 0 && lp < P.max_pages) ? P.page_table[(int64_t)b * P.max_pages + lp] : -1;
+  if (page < 0 || page >= P.n_pages) {
+    if (threadIdx.x == 0) set_error(P.err, 1);
+    return;
+  }
+  const int slot = pos % PAGE;
+  const T* kn = reinterpret_cast<const T*>(P.k_new) + (int64_t)t * P.hkv * D;
+  const T* vn = reinterpret_cast<const T*>(P.v_new) + (int64_t)t * P.hkv * D;
+  T* kp = reinterpret_cast<T*>(P.k_pool) + (int64_t)page * P.hkv * PAGE * D;
+  T* vp = reinterpret_cast<T*>(P.v_pool) + (int64_t)page * P.hkv * PAGE * D;
+  for (int e = threadIdx.x; e < P.hkv * D; e += blockDim.x) {
+    const int g = e / D, i = e - g * D;
+    kp[(int64_t)g * PAGE * D + k_off(slot, i)] = kn[e];
+    vp[(int64_t)g * PAGE * D + v_off(slot, i)] = vn[e];
+  }
+}
+
+hipError_t launch_kv_append(int dtype, int head_dim, const KvAppend& p, hipStream_t s) {
+  if (p.n_tokens == 0) return hipSuccess;
+  dim3 grid(p.n_tokens), block(256);
+  if (dtype == 0) {
+    if (head_dim == 32) hipLaunchKernelGGL((kv_append_kernel<float, 32>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((kv_append_kernel<float, 64>), grid, block, 0, s, p);
+  } else {
+    if (head_dim == 32) hipLaunchKernelGGL((kv_append_kernel<bf16, 32>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((kv_append_kernel<bf16, 64>), grid, block, 0, s, p);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mcpu

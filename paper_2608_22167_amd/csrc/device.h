@@ -1,0 +1,158 @@
+// Device-side helpers shared by the gfx950 kernels: storage types, bfloat16
+// conversion, wavefront reductions and the matrix-core (MFMA) fragment
+// operations the kernels are built on.
+//
+// Fragment convention. Every matrix-core product here is D[16][16] += A[16][K] * B[K][16]
+// with K a multiple of 32. A wavefront lane l (0..63) supplies row (or column)
+// l % 16 and the 8 consecutive reduction indices 8 * (l / 16) .. +7 of each
+// 32-wide reduction chunk, for both A and B. The accumulator lane l holds
+// D[4 * (l / 16) + r][l % 16], r = 0..3.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mcpu {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+
+struct bf16 {  // storage-only bfloat16 (raw bits)
+  uint16_t bits;
+};
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// round to nearest, ties to even; NaN stays NaN
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)((u >> 16) | ((u & 0xFFFFu) ? 0x40u : 0u));
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  static __device__ __forceinline__ float load(const float* p, int64_t i) { return p[i]; }
+  static __device__ __forceinline__ void store(float* p, int64_t i, float v) { p[i] = v; }
+};
+template <> struct Elem<bf16> {
+  static __device__ __forceinline__ float load(const bf16* p, int64_t i) { return bf16_to_f32(p[i].bits); }
+  static __device__ __forceinline__ void store(bf16* p, int64_t i, float v) { p[i].bits = f32_to_bf16(v); }
+};
+
+// ---------------------------------------------------------------------------
+// wavefront helpers (64 lanes)
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+// inclusive prefix sum over the 64 lanes
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int t = __shfl_up(v, o, 64);
+    if (l >= o) v += t;
+  }
+  return v;
+}
+
+// ---------------------------------------------------------------------------
+// 8-element fragments: one lane's 8 consecutive reduction indices
+// ---------------------------------------------------------------------------
+
+template <typename T> struct Frag;
+
+template <> struct Frag<bf16> {
+  uint4 v;  // 8 x bf16
+  __device__ __forceinline__ void load(const bf16* p) { v = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ void zero() { v = make_uint4(0, 0, 0, 0); }
+};
+template <> struct Frag<float> {
+  float4 a, b;  // 8 x fp32
+  __device__ __forceinline__ void load(const float* p) {
+    a = reinterpret_cast<const float4*>(p)[0];
+    b = reinterpret_cast<const float4*>(p)[1];
+  }
+  __device__ __forceinline__ void zero() { a = b = make_float4(0.f, 0.f, 0.f, 0.f); }
+};
+
+// acc += A-fragment x B-fragment over one 32-wide reduction chunk
+__device__ __forceinline__ f32x4 mma32(const Frag<bf16>& A, const Frag<bf16>& B, f32x4 acc) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, A.v),
+                                                  __builtin_bit_cast(bf16x8_t, B.v), acc, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma32(const Frag<float>& A, const Frag<float>& B, f32x4 acc) {
+  // eight K=4 products; product e pairs element e of every lane group
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.a.x, B.a.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.a.y, B.a.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.a.z, B.a.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.a.w, B.a.w, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.b.x, B.b.x, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.b.y, B.b.y, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.b.z, B.b.z, acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.b.w, B.b.w, acc, 0, 0, 0);
+  return acc;
+}
+
+// ---------------------------------------------------------------------------
+// 4-element fragments for the value product: lane l supplies reduction
+// indices 4 * (l / 16) .. +3 of a 16-wide chunk (one 16-token page).
+// ---------------------------------------------------------------------------
+
+template <typename T> struct Frag4;
+template <> struct Frag4<bf16> {
+  uint2 v;
+  __device__ __forceinline__ void load(const bf16* p) { v = *reinterpret_cast<const uint2*>(p); }
+};
+template <> struct Frag4<float> {
+  float4 v;
+  __device__ __forceinline__ void load(const float* p) { v = *reinterpret_cast<const float4*>(p); }
+};
+
+// acc += A(16 x 16 chunk) * B(16 x 16) where B's lane values are 4 fp32 p[r]
+// (converted to the operand type here).
+__device__ __forceinline__ f32x4 mma16_p(const Frag4<bf16>& A, const float p[4], f32x4 acc, float* psum) {
+  uint16_t b0 = f32_to_bf16(p[0]), b1 = f32_to_bf16(p[1]), b2 = f32_to_bf16(p[2]), b3 = f32_to_bf16(p[3]);
+  if (psum) *psum += bf16_to_f32(b0) + bf16_to_f32(b1) + bf16_to_f32(b2) + bf16_to_f32(b3);
+  uint2 bv = make_uint2((uint32_t)b0 | ((uint32_t)b1 << 16), (uint32_t)b2 | ((uint32_t)b3 << 16));
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, A.v),
+                                                    __builtin_bit_cast(i16x4_t, bv), acc, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma16_p(const Frag4<float>& A, const float p[4], f32x4 acc, float* psum) {
+  if (psum) *psum += p[0] + p[1] + p[2] + p[3];
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v.x, p[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v.y, p[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v.z, p[2], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.v.w, p[3], acc, 0, 0, 0);
+  return acc;
+}
+
+// ---------------------------------------------------------------------------
+// page format (see include/mcpu.h)
+// ---------------------------------------------------------------------------
+
+constexpr int PAGE = 16;
+
+__device__ __forceinline__ int k_off(int s, int i) { return ((i >> 3) * PAGE + s) * 8 + (i & 7); }
+__device__ __forceinline__ int v_off(int s, int i) {
+  return (((i >> 4) * (PAGE / 4) + (s >> 2)) * 16 + (i & 15)) * 4 + (s & 3);
+}
+
+__device__ __forceinline__ void set_error(int32_t* err, int bit) {
+  if (err) atomicOr(err, bit);
+}
+
+}  // namespace mcpu

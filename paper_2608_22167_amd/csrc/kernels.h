@@ -1,0 +1,152 @@
+// Internal launch interface between the host library (mcpu.cpp) and the
+// gfx950 kernels. Not part of the public ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mcpu {
+
+// ---- attention -----------------------------------------------------------
+
+struct AttnPlan {
+  const int32_t* seq_lens;  // [batch]
+  const int32_t* cu_q;      // [batch+1] or nullptr (one token per sequence)
+  int batch, n_tokens, window, pps;
+  int host_total_splits;    // what the host planned; checked on the device
+  int32_t* tok_seq;         // [n_tokens] out
+  int32_t* tok_pos;         // [n_tokens] out
+  int32_t* split_start;     // [n_tokens + 1] out
+  int32_t* err;
+};
+
+struct AttnSplit {
+  const void* q;  // [T][Hq][D]
+  const void* k_pool;
+  const void* v_pool;
+  const int32_t* page_table;
+  int max_pages, n_pages;
+  const int32_t* tok_seq;
+  const int32_t* tok_pos;
+  const int32_t* split_start;
+  int n_tokens, n_splits, hq, hkv, window, pps;
+  float scale_log2;  // log2(e) / sqrt(D)
+  float* part_ml;    // [S][Hq][2] running max (log2 units) and sum
+  float* part_acc;   // [S][Hq][D]
+  int32_t* err;
+};
+
+struct AttnCombine {
+  const float* part_ml;
+  const float* part_acc;
+  const int32_t* split_start;
+  const float* sinks;  // [Hq] or nullptr
+  int n_tokens, n_splits, hq;
+  void* o;             // [T][Hq * D]
+};
+
+hipError_t launch_attn_plan(const AttnPlan& p, hipStream_t s);
+hipError_t launch_attn_split(int dtype, int head_dim, const AttnSplit& p, hipStream_t s);
+hipError_t launch_attn_combine(int dtype, int head_dim, const AttnCombine& p, hipStream_t s);
+
+// ---- KV append -------------------------------------------------------------
+
+struct KvAppend {
+  const void* k_new;  // [T][Hkv][D]
+  const void* v_new;
+  void* k_pool;
+  void* v_pool;
+  const int32_t* page_table;
+  int max_pages, n_pages;
+  const int32_t* seq_lens;  // [batch]
+  const int32_t* cu_q;      // [batch+1] or nullptr
+  int batch, n_tokens, hkv;
+  int32_t* err;
+};
+hipError_t launch_kv_append(int dtype, int head_dim, const KvAppend& p, hipStream_t s);
+
+// ---- weight-streaming GEMMs with fused epilogues -------------------------
+
+enum EpiKind { EPI_QKV = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_BIAS = 3 };
+
+struct Gemm {
+  // Y[row][n] = sum_k X[src(row)][k] * W[group][n][k], rows of a group are
+  // group_off[g] .. group_off[g+1] (or 0 .. n_rows for one group).
+  const void* w;
+  const uint8_t* w_scales;  // MXFP4 block scales or nullptr
+  int64_t w_group_stride;   // elements (or bytes for MXFP4 codes) per group
+  int n, k;
+  const void* x;            // [*, k] layer dtype
+  const int32_t* row_src;   // nullptr = identity
+  const int32_t* group_off; // nullptr = one group of n_rows rows
+  int n_rows, n_groups;
+  int epi;
+  // epilogue operands
+  const float* bias;        // [groups][n]
+  int64_t bias_group_stride;
+  const float* residual;    // EPI_RESIDUAL: [rows][n] fp32
+  void* out;                // EPI_RESIDUAL/EPI_BIAS: fp32 [rows][n]; EPI_SWIGLU: dtype [rows][n/2]
+  float swiglu_alpha, swiglu_limit, swiglu_beta;
+  // EPI_QKV
+  int hq, hkv, head_dim;
+  void* q_out;              // [rows][Hq][D]
+  void* k_pool;
+  void* v_pool;
+  const int32_t* page_table;
+  int max_pages, n_pages;
+  const int32_t* tok_seq;
+  const int32_t* tok_pos;
+  const float* rope_cos;
+  const float* rope_sin;
+  int rope_max_pos;
+  int32_t* err;
+  int max_rows_per_group;   // upper bound used to pick the m-tiling
+};
+hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s);
+
+// ---- norms, router, permutation, combine --------------------------------
+
+struct RmsNorm {
+  const float* x;  // [T][H]
+  const float* g;
+  int n_tokens, hidden;
+  float eps;
+  void* out;       // [T][H] layer dtype
+};
+hipError_t launch_rmsnorm(int dtype, const RmsNorm& p, hipStream_t s);
+
+struct Router {
+  const float* h;      // [T][H] residual stream
+  const float* g2;
+  const void* w_r;     // [E][H] layer dtype
+  const float* b_r;
+  const int32_t* force_idx;
+  int n_tokens, hidden, n_experts, top_k;
+  float eps;
+  void* hn_out;        // [T][H] layer dtype (expert GEMM input)
+  int32_t* idx_out;    // [T][k]
+  float* w_out;        // [T][k]
+  int32_t* err;
+};
+hipError_t launch_router(int dtype, const Router& p, hipStream_t s);
+
+struct Permute {
+  const int32_t* idx;  // [T][k]
+  int n_tokens, top_k, n_experts;
+  int32_t* group_off;  // [E+1]
+  int32_t* pos_of;     // [T*k] sorted position of assignment t*k+s
+  int32_t* src_tok;    // [T*k] token of sorted row
+  int32_t* err;
+};
+hipError_t launch_permute(const Permute& p, hipStream_t s);
+
+struct MoeCombine {
+  const float* h;        // [T][H]
+  const float* y;        // [T*k][H] sorted rows
+  const float* w;        // [T][k]
+  const int32_t* pos_of; // [T*k]
+  int n_tokens, hidden, top_k;
+  float* out;            // [T][H]
+};
+hipError_t launch_moe_combine(const MoeCombine& p, hipStream_t s);
+
+}  // namespace mcpu

@@ -1,0 +1,500 @@
+// Host side of the C ABI (include/mcpu.h): argument checks, the page
+// allocator, launch planning from the caller's host copies of the sequence
+// lengths, workspace carving and the launch order of each entry point.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <set>
+#include <string>
+#include <vector>
+
+#include "../../include/mcpu.h"
+#include "kernels.h"
+
+using namespace mcpu;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                              \
+  do {                                                                             \
+    hipError_t e_ = (expr);                                                        \
+    if (e_ != hipSuccess) return fail(MCPU_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int PAGE_SIZE = 16;
+constexpr int SPLIT_EXTRA = 4096;   // splits beyond one per token that the workspace holds
+constexpr int PPS_MIN = 16;         // minimum pages per attention split
+constexpr int TARGET_WAVES = 8192;  // (split, KV head) wavefronts the planner aims for
+
+size_t dtype_bytes(const mcpu_layer_cfg* c) { return c->dtype == MCPU_F32 ? 4 : 2; }
+
+int check_cfg(const mcpu_layer_cfg* c) {
+  if (!c) return fail(MCPU_EINVAL, "cfg is NULL");
+  if (c->page_size != PAGE_SIZE) return fail(MCPU_EINVAL, "page_size must be 16 (got %d)", c->page_size);
+  if (c->dtype != MCPU_F32 && c->dtype != MCPU_BF16) return fail(MCPU_EINVAL, "dtype %d", c->dtype);
+  if (c->head_dim != 32 && c->head_dim != 64)
+    return fail(MCPU_EUNSUPPORTED, "head_dim %d (supported: 32, 64)", c->head_dim);
+  if (c->n_kv_heads <= 0 || c->n_q_heads <= 0 || c->n_q_heads % c->n_kv_heads)
+    return fail(MCPU_EINVAL, "n_q_heads %d must be a positive multiple of n_kv_heads %d", c->n_q_heads,
+                c->n_kv_heads);
+  if (c->n_q_heads / c->n_kv_heads > 16)
+    return fail(MCPU_EUNSUPPORTED, "more than 16 query heads per KV head");
+  if (c->hidden <= 0 || c->hidden % 32 || c->hidden > 8192)
+    return fail(MCPU_EINVAL, "hidden %d must be a multiple of 32 in (0, 8192]", c->hidden);
+  if (c->ffn_dim <= 0 || c->ffn_dim % 32) return fail(MCPU_EINVAL, "ffn_dim %d must be a multiple of 32", c->ffn_dim);
+  if ((c->n_q_heads * c->head_dim) % 32) return fail(MCPU_EINVAL, "n_q_heads * head_dim must be a multiple of 32");
+  if (c->n_experts <= 0 || c->n_experts > 64) return fail(MCPU_EINVAL, "n_experts %d not in [1, 64]", c->n_experts);
+  if (c->top_k <= 0 || c->top_k > std::min(8, c->n_experts)) return fail(MCPU_EINVAL, "top_k %d", c->top_k);
+  if (c->window < 0) return fail(MCPU_EINVAL, "window %d", c->window);
+  if (c->expert_fmt != MCPU_EXPERT_DENSE && c->expert_fmt != MCPU_EXPERT_MXFP4)
+    return fail(MCPU_EINVAL, "expert_fmt %d", c->expert_fmt);
+  if (c->expert_fmt == MCPU_EXPERT_MXFP4) return fail(MCPU_EUNSUPPORTED, "MXFP4 experts are not built yet");
+  if (!(c->rms_eps >= 0.f)) return fail(MCPU_EINVAL, "rms_eps");
+  return MCPU_OK;
+}
+
+// bump allocator over the workspace; a null base computes the size only
+struct Carve {
+  char* base;
+  size_t off = 256;  // bytes 0..255: device error word
+  explicit Carve(void* b) : base((char*)b) {}
+  template <typename T> T* take(size_t count) {
+    off = (off + 255) & ~size_t(255);
+    T* p = base ? (T*)(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+  void* take_bytes(size_t n) { return take<char>(n); }
+};
+
+int32_t* err_word(void* ws) { return (int32_t*)ws; }
+
+// per-token visible page count
+int token_pages(int pos, int window) {
+  int lo = window > 0 ? std::max(0, pos - window + 1) : 0;
+  return pos / PAGE_SIZE - lo / PAGE_SIZE + 1;
+}
+
+struct AttnPlanHost {
+  int n_tokens = 0, pps = PPS_MIN, n_splits = 0, max_pos = 0;
+};
+
+// Validate host positions and choose pages-per-split so that the split count
+// fits the workspace (<= n_tokens + SPLIT_EXTRA) and fills the GPU.
+int plan_attention(const mcpu_layer_cfg* c, int batch, int max_pages, const int32_t* hsl,
+                   const int32_t* hcu, AttnPlanHost* out) {
+  if (!hsl) return fail(MCPU_EINVAL, "host_seq_lens is NULL");
+  int T = hcu ? hcu[batch] : batch;
+  if (hcu && hcu[0] != 0) return fail(MCPU_EINVAL, "host_cu_q[0] must be 0");
+  std::vector<int> pages;
+  pages.reserve(T);
+  long long total_pages = 0;
+  int max_pos = 0;
+  for (int b = 0; b < batch; ++b) {
+    int q = hcu ? hcu[b + 1] - hcu[b] : 1;
+    if (q < 0) return fail(MCPU_EINVAL, "host_cu_q is not non-decreasing at %d", b);
+    if (hsl[b] < 0) return fail(MCPU_EINVAL, "seq_lens[%d] = %d < 0", b, hsl[b]);
+    for (int i = 0; i < q; ++i) {
+      int pos = hsl[b] + i;
+      if (pos / PAGE_SIZE >= max_pages)
+        return fail(MCPU_EINVAL, "sequence %d position %d beyond page table width %d", b, pos, max_pages);
+      int np = token_pages(pos, c->window);
+      pages.push_back(np);
+      total_pages += np;
+      max_pos = std::max(max_pos, pos);
+    }
+  }
+  long long target = std::max<long long>(1, (long long)TARGET_WAVES / c->n_kv_heads);
+  long long pps = std::max<long long>(PPS_MIN, (total_pages + target - 1) / target);
+  pps = std::max<long long>(pps, (total_pages + SPLIT_EXTRA - 1) / SPLIT_EXTRA);
+  long long splits = 0;
+  for (int np : pages) splits += (np + pps - 1) / pps;
+  out->n_tokens = T;
+  out->pps = (int)pps;
+  out->n_splits = (int)splits;
+  out->max_pos = max_pos;
+  return MCPU_OK;
+}
+
+struct AttnBufs {
+  int32_t *tok_seq, *tok_pos, *split_start;
+  float *part_ml, *part_acc;
+};
+
+AttnBufs carve_attention(Carve& cv, const mcpu_layer_cfg* c, int max_tokens) {
+  AttnBufs b;
+  size_t S = (size_t)max_tokens + SPLIT_EXTRA;
+  b.tok_seq = cv.take<int32_t>(max_tokens);
+  b.tok_pos = cv.take<int32_t>(max_tokens);
+  b.split_start = cv.take<int32_t>(max_tokens + 1);
+  b.part_ml = cv.take<float>(S * c->n_q_heads * 2);
+  b.part_acc = cv.take<float>(S * c->n_q_heads * c->head_dim);
+  return b;
+}
+
+struct MoeBufs {
+  void* hn;
+  int32_t* idx;
+  float* w;
+  int32_t *group_off, *pos_of, *src_tok;
+  void* act;
+  float* y;
+};
+
+MoeBufs carve_moe(Carve& cv, const mcpu_layer_cfg* c, int max_tokens) {
+  MoeBufs m;
+  size_t T = max_tokens, K = c->top_k, db = dtype_bytes(c);
+  m.hn = cv.take_bytes(T * c->hidden * db);
+  m.idx = cv.take<int32_t>(T * K);
+  m.w = cv.take<float>(T * K);
+  m.group_off = cv.take<int32_t>(c->n_experts + 1);
+  m.pos_of = cv.take<int32_t>(T * K);
+  m.src_tok = cv.take<int32_t>(T * K);
+  m.act = cv.take_bytes(T * K * c->ffn_dim * db);
+  m.y = cv.take<float>(T * K * c->hidden);
+  return m;
+}
+
+int check_weights(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, bool attn) {
+  if (!w) return fail(MCPU_EINVAL, "weights is NULL");
+  if (!w->g2 || !w->w_r || !w->b_r || !w->w_gu || !w->b_gu || !w->w_d || !w->b_d)
+    return fail(MCPU_EINVAL, "a MoE weight pointer is NULL");
+  if (attn && (!w->g1 || !w->w_qkv || !w->b_qkv || !w->w_o || !w->b_o || !w->rope_cos || !w->rope_sin))
+    return fail(MCPU_EINVAL, "an attention weight pointer is NULL");
+  return MCPU_OK;
+}
+
+// MoE sub-block launches (router, permute, two grouped GEMMs, combine)
+int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const float* h, float* out,
+            int32_t* idx_user, float* w_user, const int32_t* force_idx, const MoeBufs& m, int32_t* err,
+            hipStream_t st) {
+  if (T == 0) return MCPU_OK;
+  const int H = c->hidden, I = c->ffn_dim, E = c->n_experts, K = c->top_k;
+  int32_t* idx = idx_user ? idx_user : m.idx;
+  float* wt = w_user ? w_user : m.w;
+
+  Router r{};
+  r.h = h; r.g2 = w->g2; r.w_r = w->w_r; r.b_r = w->b_r; r.force_idx = force_idx;
+  r.n_tokens = T; r.hidden = H; r.n_experts = E; r.top_k = K; r.eps = c->rms_eps;
+  r.hn_out = m.hn; r.idx_out = idx; r.w_out = wt; r.err = err;
+  HIP_TRY(launch_router(c->dtype, r, st));
+
+  Permute p{};
+  p.idx = idx; p.n_tokens = T; p.top_k = K; p.n_experts = E;
+  p.group_off = m.group_off; p.pos_of = m.pos_of; p.src_tok = m.src_tok; p.err = err;
+  HIP_TRY(launch_permute(p, st));
+
+  const int max_rows = force_idx ? T * K : T;  // a token picks each expert at most once
+  Gemm g1{};
+  g1.w = w->w_gu; g1.w_group_stride = (int64_t)2 * I * H; g1.n = 2 * I; g1.k = H;
+  g1.x = m.hn; g1.row_src = m.src_tok; g1.group_off = m.group_off; g1.n_groups = E;
+  g1.epi = EPI_SWIGLU; g1.bias = w->b_gu; g1.bias_group_stride = 2 * I; g1.out = m.act;
+  g1.swiglu_alpha = c->swiglu_alpha; g1.swiglu_limit = c->swiglu_limit; g1.swiglu_beta = c->swiglu_beta;
+  g1.err = err; g1.max_rows_per_group = max_rows;
+  HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g1, st));
+
+  Gemm g2{};
+  g2.w = w->w_d; g2.w_group_stride = (int64_t)H * I; g2.n = H; g2.k = I;
+  g2.x = m.act; g2.group_off = m.group_off; g2.n_groups = E;
+  g2.epi = EPI_BIAS; g2.bias = w->b_d; g2.bias_group_stride = H; g2.out = m.y;
+  g2.err = err; g2.max_rows_per_group = max_rows;
+  HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g2, st));
+
+  MoeCombine mc{};
+  mc.h = h; mc.y = m.y; mc.w = wt; mc.pos_of = m.pos_of; mc.n_tokens = T; mc.hidden = H; mc.top_k = K;
+  mc.out = out;
+  HIP_TRY(launch_moe_combine(mc, st));
+  return MCPU_OK;
+}
+
+int run_attention(const mcpu_layer_cfg* c, const float* sinks, mcpu_kv_pool* pool, int batch,
+                  const int32_t* page_table, int max_pages, const int32_t* seq_lens, const int32_t* cu_q,
+                  const AttnPlanHost& ph, const void* q, void* o, const AttnBufs& ab, int32_t* err,
+                  hipStream_t st, bool plan_done);
+
+}  // namespace
+
+struct mcpu_kv_pool {
+  mcpu_layer_cfg cfg;
+  int32_t n_pages;
+  void* k;
+  void* v;
+  std::set<int32_t> free_ids;
+  std::vector<uint8_t> in_use;
+};
+
+namespace {
+int run_attention(const mcpu_layer_cfg* c, const float* sinks, mcpu_kv_pool* pool, int batch,
+                  const int32_t* page_table, int max_pages, const int32_t* seq_lens, const int32_t* cu_q,
+                  const AttnPlanHost& ph, const void* q, void* o, const AttnBufs& ab, int32_t* err,
+                  hipStream_t st, bool plan_done) {
+  if (!plan_done) {
+    AttnPlan pl{};
+    pl.seq_lens = seq_lens; pl.cu_q = cu_q; pl.batch = batch; pl.n_tokens = ph.n_tokens;
+    pl.window = c->window; pl.pps = ph.pps; pl.host_total_splits = ph.n_splits;
+    pl.tok_seq = ab.tok_seq; pl.tok_pos = ab.tok_pos; pl.split_start = ab.split_start; pl.err = err;
+    HIP_TRY(launch_attn_plan(pl, st));
+  }
+  AttnSplit sp{};
+  sp.q = q; sp.k_pool = pool->k; sp.v_pool = pool->v; sp.page_table = page_table;
+  sp.max_pages = max_pages; sp.n_pages = pool->n_pages;
+  sp.tok_seq = ab.tok_seq; sp.tok_pos = ab.tok_pos; sp.split_start = ab.split_start;
+  sp.n_tokens = ph.n_tokens; sp.n_splits = ph.n_splits; sp.hq = c->n_q_heads; sp.hkv = c->n_kv_heads;
+  sp.window = c->window; sp.pps = ph.pps;
+  sp.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->head_dim));
+  sp.part_ml = ab.part_ml; sp.part_acc = ab.part_acc; sp.err = err;
+  HIP_TRY(launch_attn_split(c->dtype, c->head_dim, sp, st));
+  AttnCombine cb{};
+  cb.part_ml = ab.part_ml; cb.part_acc = ab.part_acc; cb.split_start = ab.split_start; cb.sinks = sinks;
+  cb.n_tokens = ph.n_tokens; cb.n_splits = ph.n_splits; cb.hq = c->n_q_heads; cb.o = o;
+  HIP_TRY(launch_attn_combine(c->dtype, c->head_dim, cb, st));
+  return MCPU_OK;
+}
+
+bool same_shape(const mcpu_layer_cfg* a, const mcpu_layer_cfg* b) {
+  return a->n_kv_heads == b->n_kv_heads && a->head_dim == b->head_dim && a->dtype == b->dtype;
+}
+}  // namespace
+
+extern "C" {
+
+const char* mcpu_last_error(void) { return g_err.c_str(); }
+
+int kv_pool_create(const mcpu_layer_cfg* cfg, int32_t n_pages, void* k_pool, void* v_pool, mcpu_kv_pool** out) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!out || !k_pool || !v_pool) return fail(MCPU_EINVAL, "NULL pointer");
+  if (n_pages <= 0) return fail(MCPU_EINVAL, "n_pages %d", n_pages);
+  mcpu_kv_pool* p = new (std::nothrow) mcpu_kv_pool();
+  if (!p) return fail(MCPU_ENOMEM, "host allocation failed");
+  p->cfg = *cfg;
+  p->n_pages = n_pages;
+  p->k = k_pool;
+  p->v = v_pool;
+  p->in_use.assign(n_pages, 0);
+  for (int32_t i = 0; i < n_pages; ++i) p->free_ids.insert(p->free_ids.end(), i);
+  *out = p;
+  return MCPU_OK;
+}
+
+int kv_pool_destroy(mcpu_kv_pool* pool) {
+  delete pool;
+  return MCPU_OK;
+}
+
+int32_t kv_pool_free_pages(const mcpu_kv_pool* pool) { return pool ? (int32_t)pool->free_ids.size() : 0; }
+
+int kv_pages_alloc(mcpu_kv_pool* pool, int32_t n, int32_t* out_ids) {
+  if (!pool || (n > 0 && !out_ids) || n < 0) return fail(MCPU_EINVAL, "kv_pages_alloc: bad arguments");
+  if ((size_t)n > pool->free_ids.size())
+    return fail(MCPU_ENOMEM, "kv_pages_alloc: %d pages requested, %zu free", n, pool->free_ids.size());
+  auto it = pool->free_ids.begin();
+  for (int32_t i = 0; i < n; ++i) {
+    out_ids[i] = *it;
+    pool->in_use[*it] = 1;
+    it = pool->free_ids.erase(it);
+  }
+  return MCPU_OK;
+}
+
+int kv_pages_free(mcpu_kv_pool* pool, int32_t n, const int32_t* ids) {
+  if (!pool || (n > 0 && !ids) || n < 0) return fail(MCPU_EINVAL, "kv_pages_free: bad arguments");
+  std::vector<uint8_t> seen;
+  for (int32_t i = 0; i < n; ++i) {
+    int32_t id = ids[i];
+    if (id < 0 || id >= pool->n_pages) return fail(MCPU_EINVAL, "kv_pages_free: id %d out of range", id);
+    if (!pool->in_use[id]) return fail(MCPU_EINVAL, "kv_pages_free: page %d is not allocated", id);
+    if (seen.empty()) seen.assign(pool->n_pages, 0);
+    if (seen[id]) return fail(MCPU_EINVAL, "kv_pages_free: page %d repeated", id);
+    seen[id] = 1;
+  }
+  for (int32_t i = 0; i < n; ++i) {
+    pool->in_use[ids[i]] = 0;
+    pool->free_ids.insert(ids[i]);
+  }
+  return MCPU_OK;
+}
+
+int kv_pages_append(mcpu_kv_pool* pool, int32_t batch, const int32_t* page_table, int32_t max_pages,
+                    const int32_t* seq_lens, const int32_t* cu_q, int32_t n_tokens, const void* k_new,
+                    const void* v_new, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (!pool) return fail(MCPU_EINVAL, "pool is NULL");
+  if (batch < 0 || n_tokens < 0 || max_pages <= 0) return fail(MCPU_EINVAL, "bad sizes");
+  if (!cu_q && n_tokens != batch) return fail(MCPU_EINVAL, "n_tokens must equal batch when cu_q is NULL");
+  if (n_tokens == 0) return MCPU_OK;
+  if (!page_table || !seq_lens || !k_new || !v_new || !workspace) return fail(MCPU_EINVAL, "NULL pointer");
+  if (ws_bytes < 256) return fail(MCPU_ENOMEM, "workspace smaller than 256 bytes");
+  KvAppend a{};
+  a.k_new = k_new; a.v_new = v_new; a.k_pool = pool->k; a.v_pool = pool->v;
+  a.page_table = page_table; a.max_pages = max_pages; a.n_pages = pool->n_pages;
+  a.seq_lens = seq_lens; a.cu_q = cu_q; a.batch = batch; a.n_tokens = n_tokens;
+  a.hkv = pool->cfg.n_kv_heads; a.err = err_word(workspace);
+  HIP_TRY(launch_kv_append(pool->cfg.dtype, pool->cfg.head_dim, a, stream));
+  return MCPU_OK;
+}
+
+size_t paged_attention_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_batch, int32_t max_tokens) {
+  if (check_cfg(cfg)) return 0;
+  Carve cv(nullptr);
+  carve_attention(cv, cfg, std::max(max_tokens, max_batch));
+  return (cv.off + 255) & ~size_t(255);
+}
+
+int paged_attention(const mcpu_layer_cfg* cfg, const float* sinks, mcpu_kv_pool* pool, int32_t batch,
+                    const int32_t* page_table, int32_t max_pages, const int32_t* seq_lens, const int32_t* cu_q,
+                    const int32_t* host_seq_lens, const int32_t* host_cu_q, const void* q, void* o,
+                    void* workspace, size_t ws_bytes, hipStream_t stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!pool || !same_shape(cfg, &pool->cfg)) return fail(MCPU_EINVAL, "pool missing or of another shape");
+  if (batch <= 0 || max_pages <= 0) return fail(MCPU_EINVAL, "batch %d, max_pages %d", batch, max_pages);
+  if (!page_table || !seq_lens || !q || !o || !workspace) return fail(MCPU_EINVAL, "NULL pointer");
+  if ((cu_q == nullptr) != (host_cu_q == nullptr)) return fail(MCPU_EINVAL, "cu_q and host_cu_q must both be given or both NULL");
+  AttnPlanHost ph;
+  if ((rc = plan_attention(cfg, batch, max_pages, host_seq_lens, host_cu_q, &ph))) return rc;
+  if (ph.n_tokens == 0) return MCPU_OK;
+  size_t need = paged_attention_workspace_size(cfg, batch, ph.n_tokens);
+  if (ws_bytes < need) return fail(MCPU_ENOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Carve cv(workspace);
+  AttnBufs ab = carve_attention(cv, cfg, std::max(ph.n_tokens, batch));
+  return run_attention(cfg, sinks, pool, batch, page_table, max_pages, seq_lens, cu_q, ph, q, o, ab,
+                       err_word(workspace), stream, false);
+}
+
+size_t moe_forward_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_tokens) {
+  if (check_cfg(cfg)) return 0;
+  Carve cv(nullptr);
+  carve_moe(cv, cfg, max_tokens);
+  return (cv.off + 255) & ~size_t(255);
+}
+
+int moe_forward(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, int32_t n_tokens, const float* h,
+                float* out, int32_t* topk_idx, float* topk_w, const int32_t* force_idx, void* workspace,
+                size_t ws_bytes, hipStream_t stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if ((rc = check_weights(cfg, w, false))) return rc;
+  if (n_tokens < 0) return fail(MCPU_EINVAL, "n_tokens %d", n_tokens);
+  if (n_tokens == 0) return MCPU_OK;
+  if (!h || !out || !workspace) return fail(MCPU_EINVAL, "NULL pointer");
+  size_t need = moe_forward_workspace_size(cfg, n_tokens);
+  if (ws_bytes < need) return fail(MCPU_ENOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Carve cv(workspace);
+  MoeBufs m = carve_moe(cv, cfg, n_tokens);
+  return run_moe(cfg, w, n_tokens, h, out, topk_idx, topk_w, force_idx, m, err_word(workspace), stream);
+}
+
+size_t decode_layer_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_batch, int32_t max_tokens) {
+  if (check_cfg(cfg)) return 0;
+  int T = std::max(max_tokens, max_batch);
+  Carve cv(nullptr);
+  carve_attention(cv, cfg, T);
+  size_t db = dtype_bytes(cfg);
+  cv.take_bytes((size_t)T * cfg->hidden * db);                        // xn
+  cv.take_bytes((size_t)T * cfg->n_q_heads * cfg->head_dim * db);     // q
+  cv.take_bytes((size_t)T * cfg->n_q_heads * cfg->head_dim * db);     // o
+  cv.take<float>((size_t)T * cfg->hidden);                            // h1
+  carve_moe(cv, cfg, T);
+  return (cv.off + 255) & ~size_t(255);
+}
+
+int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv_pool* pool, int32_t batch,
+                 const int32_t* page_table, int32_t max_pages, const int32_t* seq_lens, const int32_t* cu_q,
+                 const int32_t* host_seq_lens, const int32_t* host_cu_q, const float* x_in, float* x_out,
+                 int32_t* topk_idx, float* topk_w, const mcpu_taps* taps, void* workspace, size_t ws_bytes,
+                 hipStream_t stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if ((rc = check_weights(cfg, w, true))) return rc;
+  if (!pool || !same_shape(cfg, &pool->cfg)) return fail(MCPU_EINVAL, "pool missing or of another shape");
+  if (batch <= 0 || max_pages <= 0) return fail(MCPU_EINVAL, "batch %d, max_pages %d", batch, max_pages);
+  if (!page_table || !seq_lens || !x_in || !x_out || !workspace) return fail(MCPU_EINVAL, "NULL pointer");
+  if (x_in == x_out) return fail(MCPU_EINVAL, "x_in and x_out must not alias");
+  if ((cu_q == nullptr) != (host_cu_q == nullptr)) return fail(MCPU_EINVAL, "cu_q and host_cu_q must both be given or both NULL");
+  AttnPlanHost ph;
+  if ((rc = plan_attention(cfg, batch, max_pages, host_seq_lens, host_cu_q, &ph))) return rc;
+  const int T = ph.n_tokens;
+  if (T == 0) return MCPU_OK;
+  if (ph.max_pos >= w->rope_max_pos)
+    return fail(MCPU_EINVAL, "position %d beyond the RoPE table (%d rows)", ph.max_pos, w->rope_max_pos);
+  size_t need = decode_layer_workspace_size(cfg, batch, T);
+  if (ws_bytes < need) return fail(MCPU_ENOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+
+  const int H = cfg->hidden, D = cfg->head_dim, Hq = cfg->n_q_heads, Hkv = cfg->n_kv_heads;
+  const size_t db = dtype_bytes(cfg);
+  Carve cv(workspace);
+  const int Tc = std::max(T, batch);
+  AttnBufs ab = carve_attention(cv, cfg, Tc);
+  void* xn = cv.take_bytes((size_t)Tc * H * db);
+  void* q = cv.take_bytes((size_t)Tc * Hq * D * db);
+  void* o = cv.take_bytes((size_t)Tc * Hq * D * db);
+  float* h1 = cv.take<float>((size_t)Tc * H);
+  MoeBufs mb = carve_moe(cv, cfg, Tc);
+  int32_t* err = err_word(workspace);
+
+  AttnPlan pl{};
+  pl.seq_lens = seq_lens; pl.cu_q = cu_q; pl.batch = batch; pl.n_tokens = T; pl.window = cfg->window;
+  pl.pps = ph.pps; pl.host_total_splits = ph.n_splits; pl.tok_seq = ab.tok_seq; pl.tok_pos = ab.tok_pos;
+  pl.split_start = ab.split_start; pl.err = err;
+  HIP_TRY(launch_attn_plan(pl, stream));
+
+  RmsNorm rn{};
+  rn.x = x_in; rn.g = w->g1; rn.n_tokens = T; rn.hidden = H; rn.eps = cfg->rms_eps; rn.out = xn;
+  HIP_TRY(launch_rmsnorm(cfg->dtype, rn, stream));
+
+  Gemm gq{};
+  gq.w = w->w_qkv; gq.n = (Hq + 2 * Hkv) * D; gq.k = H; gq.x = xn; gq.n_rows = T; gq.n_groups = 1;
+  gq.epi = EPI_QKV; gq.bias = w->b_qkv; gq.hq = Hq; gq.hkv = Hkv; gq.head_dim = D; gq.q_out = q;
+  gq.k_pool = pool->k; gq.v_pool = pool->v; gq.page_table = page_table; gq.max_pages = max_pages;
+  gq.n_pages = pool->n_pages; gq.tok_seq = ab.tok_seq; gq.tok_pos = ab.tok_pos; gq.rope_cos = w->rope_cos;
+  gq.rope_sin = w->rope_sin; gq.rope_max_pos = w->rope_max_pos; gq.err = err; gq.max_rows_per_group = T;
+  HIP_TRY(launch_gemm(cfg->dtype, MCPU_EXPERT_DENSE, gq, stream));
+
+  if ((rc = run_attention(cfg, w->sinks, pool, batch, page_table, max_pages, seq_lens, cu_q, ph, q, o, ab, err,
+                          stream, true)))
+    return rc;
+
+  Gemm go{};
+  go.w = w->w_o; go.n = H; go.k = Hq * D; go.x = o; go.n_rows = T; go.n_groups = 1; go.epi = EPI_RESIDUAL;
+  go.bias = w->b_o; go.residual = x_in; go.out = h1; go.err = err; go.max_rows_per_group = T;
+  HIP_TRY(launch_gemm(cfg->dtype, MCPU_EXPERT_DENSE, go, stream));
+
+  if ((rc = run_moe(cfg, w, T, h1, x_out, topk_idx, topk_w, nullptr, mb, err, stream))) return rc;
+
+  if (taps) {
+    if (taps->q) HIP_TRY(hipMemcpyAsync(taps->q, q, (size_t)T * Hq * D * db, hipMemcpyDeviceToDevice, stream));
+    if (taps->o) HIP_TRY(hipMemcpyAsync(taps->o, o, (size_t)T * Hq * D * db, hipMemcpyDeviceToDevice, stream));
+    if (taps->h1) HIP_TRY(hipMemcpyAsync(taps->h1, h1, (size_t)T * H * 4, hipMemcpyDeviceToDevice, stream));
+  }
+  return MCPU_OK;
+}
+
+int mcpu_check_device_errors(void* workspace, hipStream_t stream, int32_t* bits) {
+  if (!workspace) return fail(MCPU_EINVAL, "workspace is NULL");
+  int32_t v = 0;
+  HIP_TRY(hipStreamSynchronize(stream));
+  HIP_TRY(hipMemcpy(&v, workspace, sizeof v, hipMemcpyDeviceToHost));
+  if (bits) *bits = v;
+  if (v) {
+    HIP_TRY(hipMemset(workspace, 0, sizeof v));
+    return fail(MCPU_EDEVICE, "device error bits 0x%x", v);
+  }
+  return MCPU_OK;
+}
+
+}  // extern "C"

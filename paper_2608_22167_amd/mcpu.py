@@ -1,0 +1,302 @@
+"""Python binding of the C ABI in include/mcpu.h (argument marshalling only).
+
+Every function keeps the C name and forwards device pointers of torch
+tensors plus the current HIP stream; all arithmetic runs in libmcpu.so's
+gfx950 kernels. There is no fallback: if the library is missing or a call
+fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmcpu.so")
+
+MCPU_OK, MCPU_EINVAL, MCPU_ENOMEM, MCPU_EHIP, MCPU_EUNSUPPORTED, MCPU_EDEVICE = 0, -1, -2, -3, -4, -5
+MCPU_F32, MCPU_BF16 = 0, 1
+MCPU_EXPERT_DENSE, MCPU_EXPERT_MXFP4 = 0, 1
+DEVERR_PAGE, DEVERR_ROPE, DEVERR_EXPERT, DEVERR_PLAN = 1, 2, 4, 8
+
+EXPORTED = ("mcpu_last_error", "kv_pool_create", "kv_pool_destroy", "kv_pool_free_pages",
+            "kv_pages_alloc", "kv_pages_free", "kv_pages_append", "paged_attention_workspace_size",
+            "paged_attention", "moe_forward_workspace_size", "moe_forward",
+            "decode_layer_workspace_size", "decode_layer", "mcpu_check_device_errors")
+
+
+class McpuError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"mcpu status {code}: {msg}")
+        self.code = code
+
+
+class LayerCfg(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "hidden", "n_q_heads", "n_kv_heads", "head_dim", "n_experts", "top_k", "ffn_dim",
+        "page_size", "window", "dtype", "expert_fmt")] + [
+        (n, ctypes.c_float) for n in ("rms_eps", "swiglu_alpha", "swiglu_limit", "swiglu_beta")]
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "g1", "w_qkv", "b_qkv", "w_o", "b_o", "g2", "w_r", "b_r", "w_gu", "b_gu", "w_d", "b_d",
+        "s_gu", "s_d", "sinks", "rope_cos", "rope_sin")] + [("rope_max_pos", ctypes.c_int32)]
+
+
+class Taps(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_void_p), ("o", ctypes.c_void_p), ("h1", ctypes.c_void_p)]
+
+
+_LIB = None
+
+
+def lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        i32p = ctypes.POINTER(ctypes.c_int32)
+        L.mcpu_last_error.restype = ctypes.c_char_p
+        L.kv_pool_create.argtypes = [vp, i32, vp, vp, ctypes.POINTER(vp)]
+        L.kv_pool_destroy.argtypes = [vp]
+        L.kv_pool_free_pages.argtypes = [vp]
+        L.kv_pool_free_pages.restype = i32
+        L.kv_pages_alloc.argtypes = [vp, i32, vp]
+        L.kv_pages_free.argtypes = [vp, i32, vp]
+        L.kv_pages_append.argtypes = [vp, i32, vp, i32, vp, vp, i32, vp, vp, vp, sz, vp]
+        L.paged_attention_workspace_size.argtypes = [vp, i32, i32]
+        L.paged_attention_workspace_size.restype = sz
+        L.paged_attention.argtypes = [vp, vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.moe_forward_workspace_size.argtypes = [vp, i32]
+        L.moe_forward_workspace_size.restype = sz
+        L.moe_forward.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.decode_layer_workspace_size.argtypes = [vp, i32, i32]
+        L.decode_layer_workspace_size.restype = sz
+        L.decode_layer.argtypes = [vp, vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                   vp, sz, vp]
+        L.mcpu_check_device_errors.argtypes = [vp, vp, i32p]
+        _LIB = L
+    return _LIB
+
+
+def _check(rc):
+    if rc != MCPU_OK:
+        raise McpuError(rc, lib().mcpu_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, np.ndarray):
+        assert t.flags["C_CONTIGUOUS"]
+        return t.ctypes.data
+    assert t.is_contiguous()
+    return t.data_ptr()
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _host_i32(a) -> Optional[np.ndarray]:
+    if a is None:
+        return None
+    if isinstance(a, torch.Tensor):
+        a = a.cpu().numpy()
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+# ---------------------------------------------------------------------------
+# config / weights
+# ---------------------------------------------------------------------------
+
+
+def make_cfg(shape) -> LayerCfg:
+    return LayerCfg(hidden=shape.hidden, n_q_heads=shape.n_q_heads, n_kv_heads=shape.n_kv_heads,
+                    head_dim=shape.head_dim, n_experts=shape.n_experts, top_k=shape.top_k,
+                    ffn_dim=shape.ffn_dim, page_size=shape.page_size, window=shape.window,
+                    dtype=MCPU_F32 if shape.dtype == "f32" else MCPU_BF16,
+                    expert_fmt=MCPU_EXPERT_DENSE if shape.expert_fmt == "dense" else MCPU_EXPERT_MXFP4,
+                    rms_eps=shape.rms_eps, swiglu_alpha=shape.swiglu_alpha,
+                    swiglu_limit=shape.swiglu_limit, swiglu_beta=shape.swiglu_beta)
+
+
+class DeviceWeights:
+    """Layer parameters copied to the GPU, with the mcpu_layer_weights struct."""
+
+    def __init__(self, shape, W, device="cuda"):
+        self.t = {k: v.to(device).contiguous() for k, v in W.items()}
+        t = self.t
+        p = lambda k: _ptr(t[k]) if k in t else None
+        mx = shape.expert_fmt == "mxfp4"
+        self.struct = LayerWeights(
+            g1=p("g1"), w_qkv=p("w_qkv"), b_qkv=p("b_qkv"), w_o=p("w_o"), b_o=p("b_o"), g2=p("g2"),
+            w_r=p("w_r"), b_r=p("b_r"),
+            w_gu=p("w_gu_codes") if mx else p("w_gu"), b_gu=p("b_gu"),
+            w_d=p("w_d_codes") if mx else p("w_d"), b_d=p("b_d"),
+            s_gu=p("w_gu_scales") if mx else None, s_d=p("w_d_scales") if mx else None,
+            sinks=p("sinks"), rope_cos=p("rope_cos"), rope_sin=p("rope_sin"),
+            rope_max_pos=int(t["rope_cos"].shape[0]) if "rope_cos" in t else 0)
+
+
+# ---------------------------------------------------------------------------
+# page pool
+# ---------------------------------------------------------------------------
+
+
+class KVPool:
+    """mcpu_kv_pool over caller-owned device K/V pools (kept alive here)."""
+
+    def __init__(self, shape, k_pool: torch.Tensor, v_pool: torch.Tensor):
+        self.shape = shape
+        self.cfg = make_cfg(shape)
+        self.k, self.v = k_pool, v_pool
+        self.n_pages = int(k_pool.shape[0])
+        h = ctypes.c_void_p()
+        _check(lib().kv_pool_create(ctypes.byref(self.cfg), self.n_pages, _ptr(k_pool), _ptr(v_pool),
+                                    ctypes.byref(h)))
+        self.handle = h
+
+    def free_pages(self) -> int:
+        return lib().kv_pool_free_pages(self.handle)
+
+    def close(self):
+        if self.handle:
+            lib().kv_pool_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def kv_pool_create(shape, k_pool, v_pool) -> KVPool:
+    return KVPool(shape, k_pool, v_pool)
+
+
+def kv_pages_alloc(pool: KVPool, n: int) -> np.ndarray:
+    out = np.empty(max(n, 1), dtype=np.int32)
+    _check(lib().kv_pages_alloc(pool.handle, n, _ptr(out)))
+    return out[:n]
+
+
+def kv_pages_free(pool: KVPool, ids) -> None:
+    ids = _host_i32(ids)
+    _check(lib().kv_pages_free(pool.handle, len(ids), _ptr(ids) if len(ids) else None))
+
+
+def kv_pages_append(pool: KVPool, page_table, seq_lens, cu_q, k_new, v_new, workspace, stream=None):
+    batch = int(seq_lens.shape[0])
+    n_tokens = int(k_new.shape[0])
+    _check(lib().kv_pages_append(pool.handle, batch, _ptr(page_table), int(page_table.shape[1]),
+                                 _ptr(seq_lens), _ptr(cu_q), n_tokens, _ptr(k_new), _ptr(v_new),
+                                 _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                 _stream(stream)))
+
+
+def workspace(nbytes: int, device="cuda") -> torch.Tensor:
+    """Zero-filled, 256-byte aligned device workspace."""
+    return torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def paged_attention_workspace_size(shape, max_batch, max_tokens) -> int:
+    cfg = make_cfg(shape)
+    return lib().paged_attention_workspace_size(ctypes.byref(cfg), max_batch, max_tokens)
+
+
+def paged_attention(shape, sinks, pool: KVPool, page_table, seq_lens, cu_q, host_seq_lens, host_cu_q,
+                    q, o, workspace, stream=None):
+    cfg = make_cfg(shape)
+    hs, hc = _host_i32(host_seq_lens), _host_i32(host_cu_q)
+    _check(lib().paged_attention(ctypes.byref(cfg), _ptr(sinks), pool.handle, int(seq_lens.shape[0]),
+                                 _ptr(page_table), int(page_table.shape[1]), _ptr(seq_lens), _ptr(cu_q),
+                                 _ptr(hs), _ptr(hc), _ptr(q), _ptr(o), _ptr(workspace),
+                                 workspace.numel(), _stream(stream)))
+
+
+def moe_forward_workspace_size(shape, max_tokens) -> int:
+    cfg = make_cfg(shape)
+    return lib().moe_forward_workspace_size(ctypes.byref(cfg), max_tokens)
+
+
+def moe_forward(shape, weights: DeviceWeights, h, out, topk_idx=None, topk_w=None, force_idx=None,
+                workspace=None, stream=None):
+    cfg = make_cfg(shape)
+    _check(lib().moe_forward(ctypes.byref(cfg), ctypes.byref(weights.struct), int(h.shape[0]), _ptr(h),
+                             _ptr(out), _ptr(topk_idx), _ptr(topk_w), _ptr(force_idx),
+                             _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def decode_layer_workspace_size(shape, max_batch, max_tokens) -> int:
+    cfg = make_cfg(shape)
+    return lib().decode_layer_workspace_size(ctypes.byref(cfg), max_batch, max_tokens)
+
+
+def decode_layer(shape, weights: DeviceWeights, pool: KVPool, page_table, seq_lens, cu_q, host_seq_lens,
+                 host_cu_q, x_in, x_out, topk_idx=None, topk_w=None, taps: Optional[Taps] = None,
+                 workspace=None, stream=None):
+    cfg = make_cfg(shape)
+    hs, hc = _host_i32(host_seq_lens), _host_i32(host_cu_q)
+    _check(lib().decode_layer(ctypes.byref(cfg), ctypes.byref(weights.struct), pool.handle,
+                              int(seq_lens.shape[0]), _ptr(page_table), int(page_table.shape[1]),
+                              _ptr(seq_lens), _ptr(cu_q), _ptr(hs), _ptr(hc), _ptr(x_in), _ptr(x_out),
+                              _ptr(topk_idx), _ptr(topk_w),
+                              ctypes.byref(taps) if taps is not None else None,
+                              _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def mcpu_check_device_errors(workspace, stream=None) -> int:
+    bits = ctypes.c_int32(0)
+    rc = lib().mcpu_check_device_errors(_ptr(workspace), _stream(stream), ctypes.byref(bits))
+    if rc not in (MCPU_OK, MCPU_EDEVICE):
+        _check(rc)
+    return bits.value
+
+
+# ---------------------------------------------------------------------------
+# a workload resident on the GPU
+# ---------------------------------------------------------------------------
+
+
+class DeviceStep:
+    """Uploads a workload (weights, pools, tables, inputs) and runs decode_layer on it."""
+
+    def __init__(self, wl, device="cuda"):
+        s = wl.shape
+        self.wl = wl
+        self.shape = s
+        self.weights = DeviceWeights(s, wl.weights, device)
+        self.k_pool = wl.k_pool.to(device)
+        self.v_pool = wl.v_pool.to(device)
+        self.pool = KVPool(s, self.k_pool, self.v_pool)
+        self.page_table = torch.from_numpy(np.ascontiguousarray(wl.page_table)).to(device)
+        self.seq_lens = torch.from_numpy(np.ascontiguousarray(wl.seq_lens)).to(device)
+        self.host_seq_lens = np.ascontiguousarray(wl.seq_lens, dtype=np.int32)
+        if wl.is_decode:
+            self.cu_q, self.host_cu_q = None, None
+        else:
+            self.host_cu_q = np.ascontiguousarray(wl.cu_q, dtype=np.int32)
+            self.cu_q = torch.from_numpy(self.host_cu_q).to(device)
+        T = wl.n_tokens
+        self.x_in = wl.x_in.to(device)
+        self.x_out = torch.empty_like(self.x_in)
+        self.topk_idx = torch.empty((T, s.top_k), dtype=torch.int32, device=device)
+        self.topk_w = torch.empty((T, s.top_k), dtype=torch.float32, device=device)
+        self.ws = workspace(decode_layer_workspace_size(s, wl.batch, T), device)
+
+    def run(self, taps: Optional[Taps] = None, stream=None):
+        decode_layer(self.shape, self.weights, self.pool, self.page_table, self.seq_lens, self.cu_q,
+                     self.host_seq_lens, self.host_cu_q, self.x_in, self.x_out, self.topk_idx,
+                     self.topk_w, taps, self.ws, stream)
+
+    def device_errors(self) -> int:
+        return mcpu_check_device_errors(self.ws)
