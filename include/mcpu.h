@@ -216,6 +216,30 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
                  float* topk_w, const mcpu_taps* taps, void* workspace, size_t ws_bytes,
                  hipStream_t stream);
 
+/* Kernel timing, a profiling aid. mcpu_timing_start(kernel, n) arms the
+ * library to record a HIP event pair on the launching stream around each of
+ * the next n launches of that kernel (n = 0 disarms it); mcpu_timing_read
+ * waits for the recorded events and writes up to n durations in milliseconds
+ * to host array ms, setting *n_recorded. Process-wide state: not thread-safe,
+ * and recording adds two event records per timed launch. */
+enum {
+  MCPU_KERNEL_ATTN_PLAN = 0,
+  MCPU_KERNEL_RMSNORM = 1,
+  MCPU_KERNEL_QKV = 2,         /* QKV projection + RoPE + KV append */
+  MCPU_KERNEL_ATTN_SPLIT = 3,  /* paged attention partials */
+  MCPU_KERNEL_ATTN_COMBINE = 4,
+  MCPU_KERNEL_OPROJ = 5,
+  MCPU_KERNEL_ROUTER = 6,
+  MCPU_KERNEL_PERMUTE = 7,
+  MCPU_KERNEL_EXPERT_GU = 8,   /* expert gate/up GEMM + SwiGLU */
+  MCPU_KERNEL_EXPERT_DOWN = 9,
+  MCPU_KERNEL_MOE_COMBINE = 10,
+  MCPU_KERNEL_KV_APPEND = 11,
+  MCPU_KERNEL_COUNT = 12
+};
+int mcpu_timing_start(int kernel, int n);
+int mcpu_timing_read(int kernel, float* ms, int n, int* n_recorded);
+
 /* Synchronise the stream, read the workspace's device error word, clear it.
  * Returns MCPU_OK, MCPU_EDEVICE (bits in *bits if non-NULL) or MCPU_EHIP. */
 int mcpu_check_device_errors(void* workspace, hipStream_t stream, int32_t* bits);

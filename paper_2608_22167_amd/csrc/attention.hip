@@ -53,16 +53,19 @@ __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnPlan P) {
     int pos = P.seq_lens[b] + (P.cu_q ? t - P.cu_q[b] : 0);
     local += token_splits(pos, P.window, P.pps);
   }
-  sums[tid] = local;
+  // block-wide exclusive scan: wavefront scans, then a scan of the 16 totals
+  const int incl = wave_incl_scan(local);
+  const int wave = tid >> 6, lane = tid & 63;
+  if (lane == 63) sums[wave] = incl;
   __syncthreads();
-  // Hillis-Steele inclusive scan over the per-thread sums
-  for (int o = 1; o < nt; o <<= 1) {
-    int v = tid >= o ? sums[tid - o] : 0;
-    __syncthreads();
-    sums[tid] += v;
-    __syncthreads();
+  if (wave == 0) {
+    const int w = lane < (nt >> 6) ? sums[lane] : 0;
+    const int wi = wave_incl_scan(w);
+    if (lane < (nt >> 6)) sums[64 + lane] = wi - w;  // exclusive prefix of wave totals
+    if (lane == (nt >> 6) - 1) sums[128] = wi;       // grand total
   }
-  int run = sums[tid] - local;
+  __syncthreads();
+  int run = sums[64 + wave] + incl - local;
   for (int t = t0; t < t1; ++t) {
     int b = P.cu_q ? seq_of_token(P.cu_q, P.batch, t) : t;
     int pos = P.seq_lens[b] + (P.cu_q ? t - P.cu_q[b] : 0);
@@ -71,9 +74,9 @@ __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnPlan P) {
     P.split_start[t] = run;
     run += token_splits(pos, P.window, P.pps);
   }
-  if (tid == nt - 1) {
-    P.split_start[P.n_tokens] = sums[nt - 1];
-    if (sums[nt - 1] != P.host_total_splits) set_error(P.err, 8);
+  if (tid == 0) {
+    P.split_start[P.n_tokens] = sums[128];
+    if (P.host_total_splits >= 0 && sums[128] != P.host_total_splits) set_error(P.err, 8);
   }
 }
 
@@ -98,7 +101,7 @@ struct PageFrags {
   }
 };
 
-template <typename T, int D, int WAVES>
+template <typename T, int D, int WAVES, int PF>
 __global__ __launch_bounds__(64 * WAVES) void attn_split_kernel(AttnSplit P) {
   const int lane = lane_id();
   const int item = blockIdx.x * WAVES + uniform(threadIdx.x >> 6);
@@ -114,8 +117,12 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_kernel(AttnSplit P) {
   const int t = uniform(lo_t);
   const int b = uniform(P.tok_seq[t]), p = uniform(P.tok_pos[t]);
   const int lo = P.window > 0 ? max(0, p - P.window + 1) : 0;
-  int pg0 = lo / PAGE + (s - uniform(P.split_start[t])) * P.pps;
-  int pg1 = min(pg0 + P.pps, p / PAGE + 1);
+  // the token's ns splits share its np pages evenly (sizes differ by at most one)
+  const int first = lo / PAGE, np = p / PAGE - first + 1;
+  const int ns = uniform(P.split_start[t + 1]) - uniform(P.split_start[t]);
+  const int k = s - uniform(P.split_start[t]);
+  int pg0 = ns > 0 ? first + (int)((int64_t)k * np / ns) : 0;
+  int pg1 = ns > 0 ? first + (int)((int64_t)(k + 1) * np / ns) : 0;
   const int G = P.hq / P.hkv;
   const int hl = lane & 15, grp = lane >> 4;
   if (p < 0 || p / PAGE >= P.max_pages || pg0 < 0 || pg0 >= pg1) {
@@ -141,56 +148,67 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_kernel(AttnSplit P) {
 #pragma unroll
   for (int n = 0; n < D / 16; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto page_ok = [&](int pg) -> int {
+  // PF-deep ring of pages: while page i is consumed, pages i+1 .. i+PF-1 are
+  // in flight and page i+PF is issued into its slot. Loads are branch-free: a
+  // slot past the split re-reads the last page, a missing page reads page 0,
+  // and both are masked out of the softmax instead of skipped.
+  const int npg = pg1 - pg0;
+  PageFrags<T, D> ring[PF];
+  bool ok[PF];
+  auto fetch = [&](int slot, int i) {
+    const int pg = pg0 + min(i, npg - 1);
     int id = uniform(ptab[pg]);
-    if (id < 0 || id >= P.n_pages) {
-      if (lane == 0) set_error(P.err, 1);
-      return -1;
-    }
-    return id;
+    const bool good = id >= 0 && id < P.n_pages;
+    if (!good && lane == 0 && i < npg) set_error(P.err, 1);
+    id = good ? id : 0;
+    ok[slot] = good && i < npg;
+    ring[slot].load(kpool + id * page_elems + head_off, vpool + id * page_elems + head_off, lane);
   };
-
-  PageFrags<T, D> cur, nxt;
-  int id_cur = pg0 < pg1 ? page_ok(pg0) : -1;
-  if (id_cur >= 0) cur.load(kpool + id_cur * page_elems + head_off, vpool + id_cur * page_elems + head_off, lane);
-  for (int pg = pg0; pg < pg1; ++pg) {
-    int id_nxt = -1;
-    if (pg + 1 < pg1) {
-      id_nxt = page_ok(pg + 1);
-      if (id_nxt >= 0)
-        nxt.load(kpool + id_nxt * page_elems + head_off, vpool + id_nxt * page_elems + head_off, lane);
+  auto consume = [&](int slot, int i) {
+    const PageFrags<T, D>& cur = ring[slot];
+    f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < D / 32; ++c) sc = mma32(cur.k[c], qf[c], sc);
+    // sc[r] = score of key slot 4 * grp + r for query head hl
+    const int key0 = (pg0 + i) * PAGE + 4 * grp;
+    float x[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int pos = key0 + r;
+      x[r] = (ok[slot] && pos >= lo && pos <= p) ? sc[r] * P.scale_log2 : -INFINITY;
     }
-    if (id_cur >= 0) {
-      f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+    float mloc = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float m_new = fmaxf(m_run, mloc);
+    // m_new is -inf only while every key so far was masked (missing pages)
+    const bool live = m_new != -INFINITY;
+    const float alpha = live ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
+    float pr[4];
 #pragma unroll
-      for (int c = 0; c < D / 32; ++c) sc = mma32(cur.k[c], qf[c], sc);
-      // sc[r] = score of key slot 4 * grp + r for query head hl
-      const int key0 = pg * PAGE + 4 * grp;
-      float x[4];
+    for (int r = 0; r < 4; ++r) pr[r] = live ? __builtin_amdgcn_exp2f(x[r] - m_new) : 0.f;
+    l_run *= alpha;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        int pos = key0 + r;
-        x[r] = (pos >= lo && pos <= p) ? sc[r] * P.scale_log2 : -INFINITY;
-      }
-      float mloc = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      // every page in [pg0, pg1) holds at least one visible key, so mloc is finite
-      const float m_new = fmaxf(m_run, mloc);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      float pr[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) pr[r] = __builtin_amdgcn_exp2f(x[r] - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int n = 0; n < D / 16; ++n) {
-        acc[n] *= alpha;
-        acc[n] = mma16_p(cur.v[n], pr, acc[n], n == 0 ? &l_run : nullptr);
-      }
-      m_run = m_new;
+    for (int n = 0; n < D / 16; ++n) {
+      acc[n] *= alpha;
+      acc[n] = mma16_p(cur.v[n], pr, acc[n], n == 0 ? &l_run : nullptr);
     }
-    cur = nxt;
-    id_cur = id_nxt;
+    m_run = m_new;
+  };
+  if (npg > 0) {
+#pragma unroll
+    for (int u = 0; u < PF; ++u) fetch(u, u);
+    int i = 0;
+    for (; i + PF <= npg; i += PF) {
+#pragma unroll
+      for (int u = 0; u < PF; ++u) {
+        consume(u, i + u);
+        fetch(u, i + u + PF);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < PF; ++u)
+      if (i + u < npg) consume(u, i + u);
   }
 
   float l_tot = l_run + __shfl_xor(l_run, 16, 64);
@@ -208,13 +226,12 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_kernel(AttnSplit P) {
   }
 }
 
-template <typename T, int D>
-static hipError_t split_impl(const AttnSplit& p, hipStream_t s) {
-  constexpr int WAVES = 4;
+template <typename T, int D, int WAVES = 1, int PF = 2>
+hipError_t split_impl(const AttnSplit& p, hipStream_t s) {
   int64_t items = (int64_t)p.n_splits * p.hkv;
   int blocks = (int)((items + WAVES - 1) / WAVES);
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_split_kernel<T, D, WAVES>), dim3(blocks), dim3(64 * WAVES), 0, s, p);
+  hipLaunchKernelGGL((attn_split_kernel<T, D, WAVES, PF>), dim3(blocks), dim3(64 * WAVES), 0, s, p);
   return hipGetLastError();
 }
 
@@ -227,39 +244,68 @@ hipError_t launch_attn_split(int dtype, int head_dim, const AttnSplit& p, hipStr
 // combine: o_h = sum_s 2^{m_s - M} acc_s / (2^{sink_h log2e - M} + sum_s 2^{m_s - M} l_s)
 // ---------------------------------------------------------------------------
 
+// One wavefront per (token, query head); lane i owns dim i. The splits are
+// merged in order with a running maximum, so one pass reads each partial once.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void attn_combine_kernel(AttnCombine P) {
-  const int t = blockIdx.x;
-  const int s0 = min(P.split_start[t], P.n_splits), s1 = min(P.split_start[t + 1], P.n_splits);
-  T* o = reinterpret_cast<T*>(P.o) + (int64_t)t * P.hq * D;
-  for (int w = threadIdx.x; w < P.hq * (D / 4); w += blockDim.x) {
-    const int h = w / (D / 4), c = w - h * (D / 4);
-    const float sink = P.sinks ? P.sinks[h] * LOG2E : -INFINITY;
-    float M = sink;
-    for (int s = s0; s < s1; ++s) M = fmaxf(M, P.part_ml[((int64_t)s * P.hq + h) * 2]);
-    float L = P.sinks ? __builtin_amdgcn_exp2f(sink - M) : 0.f;
-    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (M != -INFINITY) {
-      for (int s = s0; s < s1; ++s) {
-        const int64_t row = (int64_t)s * P.hq + h;
-        const float f = __builtin_amdgcn_exp2f(P.part_ml[row * 2] - M);
-        L += f * P.part_ml[row * 2 + 1];
-        float4 v = *reinterpret_cast<const float4*>(P.part_acc + row * D + 4 * c);
-        a.x += f * v.x; a.y += f * v.y; a.z += f * v.z; a.w += f * v.w;
-      }
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = lane_id();
+  if (item >= P.n_tokens * P.hq) return;
+  const int t = uniform(item / P.hq), h = uniform(item - (item / P.hq) * P.hq);
+  const int s0 = min(uniform(P.split_start[t]), P.n_splits);
+  const int s1 = min(uniform(P.split_start[t + 1]), P.n_splits);
+  float M = P.sinks ? P.sinks[h] * LOG2E : -INFINITY;
+  float L = P.sinks ? 1.0f : 0.0f;  // the sink's own term, 2^(sink - M)
+  float a = 0.f;
+  const bool act = lane < D;
+  constexpr int U = 4;
+  int s = s0;
+  for (; s + U <= s1; s += U) {
+    float m[U], l[U], v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t row = (int64_t)(s + u) * P.hq + h;
+      m[u] = P.part_ml[row * 2];
+      l[u] = P.part_ml[row * 2 + 1];
+      v[u] = act ? P.part_acc[row * D + lane] : 0.f;
     }
-    const float inv = L > 0.f ? 1.0f / L : 0.f;
-    const int64_t base = (int64_t)h * D + 4 * c;
-    Elem<T>::store(o, base + 0, a.x * inv);
-    Elem<T>::store(o, base + 1, a.y * inv);
-    Elem<T>::store(o, base + 2, a.z * inv);
-    Elem<T>::store(o, base + 3, a.w * inv);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (m[u] == -INFINITY) continue;  // a split whose pages were all missing
+      if (m[u] > M) {
+        const float r = __builtin_amdgcn_exp2f(M - m[u]);
+        L *= r;
+        a *= r;
+        M = m[u];
+      }
+      const float f = __builtin_amdgcn_exp2f(m[u] - M);
+      L += f * l[u];
+      a += f * v[u];
+    }
+  }
+  for (; s < s1; ++s) {
+    const int64_t row = (int64_t)s * P.hq + h;
+    const float m = P.part_ml[row * 2];
+    if (m == -INFINITY) continue;
+    if (m > M) {
+      const float r = __builtin_amdgcn_exp2f(M - m);
+      L *= r;
+      a *= r;
+      M = m;
+    }
+    const float f = __builtin_amdgcn_exp2f(m - M);
+    L += f * P.part_ml[row * 2 + 1];
+    a += f * (act ? P.part_acc[row * D + lane] : 0.f);
+  }
+  if (act) {
+    T* o = reinterpret_cast<T*>(P.o) + ((int64_t)t * P.hq + h) * D;
+    Elem<T>::store(o, lane, L > 0.f ? a / L : 0.f);
   }
 }
 
 hipError_t launch_attn_combine(int dtype, int head_dim, const AttnCombine& p, hipStream_t s) {
   if (p.n_tokens == 0) return hipSuccess;
-  dim3 grid(p.n_tokens), block(256);
+  dim3 grid((p.n_tokens * p.hq + 3) / 4), block(256);
   if (dtype == 0) {
     if (head_dim == 32) hipLaunchKernelGGL((attn_combine_kernel<float, 32>), grid, block, 0, s, p);
     else hipLaunchKernelGGL((attn_combine_kernel<float, 64>), grid, block, 0, s, p);

@@ -79,6 +79,9 @@ template <> struct Frag<bf16> {
   uint4 v;  // 8 x bf16
   __device__ __forceinline__ void load(const bf16* p) { v = *reinterpret_cast<const uint4*>(p); }
   __device__ __forceinline__ void zero() { v = make_uint4(0, 0, 0, 0); }
+  __device__ __forceinline__ void keep_if(bool k) {  // zero unless k, without a branch
+    v.x = k ? v.x : 0u; v.y = k ? v.y : 0u; v.z = k ? v.z : 0u; v.w = k ? v.w : 0u;
+  }
 };
 template <> struct Frag<float> {
   float4 a, b;  // 8 x fp32
@@ -87,6 +90,10 @@ template <> struct Frag<float> {
     b = reinterpret_cast<const float4*>(p)[1];
   }
   __device__ __forceinline__ void zero() { a = b = make_float4(0.f, 0.f, 0.f, 0.f); }
+  __device__ __forceinline__ void keep_if(bool k) {
+    a.x = k ? a.x : 0.f; a.y = k ? a.y : 0.f; a.z = k ? a.z : 0.f; a.w = k ? a.w : 0.f;
+    b.x = k ? b.x : 0.f; b.y = k ? b.y : 0.f; b.z = k ? b.z : 0.f; b.w = k ? b.w : 0.f;
+  }
 };
 
 // acc += A-fragment x B-fragment over one 32-wide reduction chunk

@@ -2,12 +2,14 @@
 //
 // At decode every projection of the layer is skinny: a few to a few hundred
 // token rows against a weight matrix that is read exactly once, so the kernels
-// are bound by streaming the weights from HBM. One workgroup owns a 16-row
-// slab of one group's weight matrix (one expert, or the single dense matrix)
-// and all token rows of that group; its KW wavefronts split the reduction
-// dimension, each streaming a contiguous K range with one 16x16x32 matrix-core
-// product per 32-wide chunk and token block, then the partial tiles are summed
-// through LDS in a fixed order and a fused epilogue finishes the slab:
+// are bound by streaming the weights from HBM. A workgroup owns a slab of
+// 16 * WN * NB consecutive weight rows of one group (one expert, or the single
+// dense matrix) and all token rows of that group. Its WN x WK wavefronts split
+// the slab along N (WN) and the reduction dimension along K (WK); each
+// wavefront keeps an NB x MB grid of 16x16 accumulators, so every token
+// fragment it loads feeds NB matrix-core products and every weight fragment
+// feeds MB. Partial tiles of the WK wavefronts are summed into LDS in a fixed
+// order, and a fused epilogue finishes the slab:
 //   EPI_QKV      + bias, rotary embedding of q and k, q to the q buffer and
 //                k / v straight into their KV-cache pages (the append)
 //   EPI_RESIDUAL + bias + residual (fp32), e.g. h1 = x + o W_o^T + b_o
@@ -20,17 +22,17 @@
 
 namespace mcpu {
 
-// W row (output feature) that lane-row nl of slab `tile` multiplies. For the
-// QKV projection a slab holds dims 8t..8t+7 and d/2+8t..d/2+8t+7 of one head,
-// so both members of every rotary pair land in the same workgroup.
+// W row (output feature) that lane-row nl of 16-row block `blk` multiplies. For
+// the QKV projection a block holds dims 8t..8t+7 and d/2+8t..d/2+8t+7 of one
+// head, so both members of every rotary pair land in the same block.
 template <int EPI>
-__device__ __forceinline__ int slab_row(const Gemm& P, int tile, int nl) {
+__device__ __forceinline__ int block_row(const Gemm& P, int blk, int nl) {
   if (EPI == EPI_QKV) {
     const int D = P.head_dim, tph = D / 16;
-    const int head = tile / tph, ti = tile - head * tph;
+    const int head = blk / tph, ti = blk - head * tph;
     return head * D + (nl < 8 ? 8 * ti + nl : D / 2 + 8 * ti + nl - 8);
   }
-  return tile * 16 + nl;
+  return blk * 16 + nl;
 }
 
 __device__ __forceinline__ float swiglu(float gate, float up, float alpha, float limit, float beta) {
@@ -39,19 +41,22 @@ __device__ __forceinline__ float swiglu(float gate, float up, float alpha, float
   return gate / (1.0f + expf(-alpha * gate)) * (up + beta);
 }
 
+// cr[m * ld + n]: the finished fp32 tile for token rows m0 .. m0 + mrows - 1 and
+// the nblk 16-row weight blocks starting at blk0.
 template <typename T, int EPI>
-__device__ void epilogue(const Gemm& P, const float* cr, int m0, int mrows, int tile, int grp) {
+__device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mrows, int blk0, int nblk,
+                         int grp) {
   const int tid = threadIdx.x, nt = blockDim.x;
   const float* bias = P.bias + (int64_t)grp * P.bias_group_stride;
   if constexpr (EPI == EPI_QKV) {
     const int D = P.head_dim, tph = D / 16, half = D / 2;
-    const int head = tile / tph, ti = tile - head * tph;
-    for (int idx = tid; idx < mrows * 8; idx += nt) {
-      const int m = idx >> 3, i = idx & 7, t = m0 + m;
+    for (int idx = tid; idx < mrows * nblk * 8; idx += nt) {
+      const int i = idx & 7, b = (idx >> 3) % nblk, m = (idx >> 3) / nblk, t = m0 + m;
+      const int blk = blk0 + b, head = blk / tph, ti = blk - head * tph;
       const int j = 8 * ti + i;  // dim within the head, < D/2
       const int f_lo = head * D + j, f_hi = f_lo + half;
-      float lo = cr[m * 17 + i] + bias[f_lo];
-      float hi = cr[m * 17 + 8 + i] + bias[f_hi];
+      float lo = cr[m * ld + 16 * b + i] + bias[f_lo];
+      float hi = cr[m * ld + 16 * b + 8 + i] + bias[f_hi];
       const int pos = P.tok_pos[t];
       if (head < P.hq + P.hkv) {  // q or k: rotate the pair (j, j + d/2)
         if (pos < 0 || pos >= P.rope_max_pos) {
@@ -59,9 +64,9 @@ __device__ void epilogue(const Gemm& P, const float* cr, int m0, int mrows, int 
           continue;
         }
         const float c = P.rope_cos[(int64_t)pos * half + j], s = P.rope_sin[(int64_t)pos * half + j];
-        const float a = lo, b = hi;
-        lo = a * c - b * s;
-        hi = a * s + b * c;
+        const float a = lo, bb = hi;
+        lo = a * c - bb * s;
+        hi = a * s + bb * c;
       }
       if (head < P.hq) {
         T* q = reinterpret_cast<T*>(P.q_out) + ((int64_t)t * P.hq + head) * D;
@@ -78,48 +83,61 @@ __device__ void epilogue(const Gemm& P, const float* cr, int m0, int mrows, int 
       }
       const int slot = pos & 15;
       if (head < P.hq + P.hkv) {
-        const int g = head - P.hq;
-        T* kp = reinterpret_cast<T*>(P.k_pool) + ((int64_t)page * P.hkv + g) * PAGE * D;
+        T* kp = reinterpret_cast<T*>(P.k_pool) + ((int64_t)page * P.hkv + (head - P.hq)) * PAGE * D;
         Elem<T>::store(kp, k_off(slot, j), lo);
         Elem<T>::store(kp, k_off(slot, j + half), hi);
       } else {
-        const int g = head - P.hq - P.hkv;
-        T* vp = reinterpret_cast<T*>(P.v_pool) + ((int64_t)page * P.hkv + g) * PAGE * D;
+        T* vp = reinterpret_cast<T*>(P.v_pool) + ((int64_t)page * P.hkv + (head - P.hq - P.hkv)) * PAGE * D;
         Elem<T>::store(vp, v_off(slot, j), lo);
         Elem<T>::store(vp, v_off(slot, j + half), hi);
       }
     }
-  } else if constexpr (EPI == EPI_RESIDUAL) {
-    float* out = reinterpret_cast<float*>(P.out);
-    for (int idx = tid; idx < mrows * 16; idx += nt) {
-      const int m = idx >> 4, n = idx & 15;
-      const int64_t o = (int64_t)(m0 + m) * P.n + tile * 16 + n;
-      out[o] = cr[m * 17 + n] + bias[tile * 16 + n] + P.residual[o];
-    }
   } else if constexpr (EPI == EPI_SWIGLU) {
     T* out = reinterpret_cast<T*>(P.out);
     const int half_n = P.n / 2;
-    for (int idx = tid; idx < mrows * 8; idx += nt) {
-      const int m = idx >> 3, j = idx & 7;
-      const float gate = cr[m * 17 + 2 * j] + bias[tile * 16 + 2 * j];
-      const float up = cr[m * 17 + 2 * j + 1] + bias[tile * 16 + 2 * j + 1];
-      Elem<T>::store(out, (int64_t)(m0 + m) * half_n + tile * 8 + j,
+    for (int idx = tid; idx < mrows * nblk * 8; idx += nt) {
+      const int j = idx & 7, b = (idx >> 3) % nblk, m = (idx >> 3) / nblk;
+      const int col = (blk0 + b) * 16 + 2 * j;
+      const float gate = cr[m * ld + 16 * b + 2 * j] + bias[col];
+      const float up = cr[m * ld + 16 * b + 2 * j + 1] + bias[col + 1];
+      Elem<T>::store(out, (int64_t)(m0 + m) * half_n + (blk0 + b) * 8 + j,
                      swiglu(gate, up, P.swiglu_alpha, P.swiglu_limit, P.swiglu_beta));
     }
-  } else {  // EPI_BIAS
+  } else {  // EPI_RESIDUAL, EPI_BIAS: fp32 rows, 4 consecutive features per thread
     float* out = reinterpret_cast<float*>(P.out);
-    for (int idx = tid; idx < mrows * 16; idx += nt) {
-      const int m = idx >> 4, n = idx & 15;
-      out[(int64_t)(m0 + m) * P.n + tile * 16 + n] = cr[m * 17 + n] + bias[tile * 16 + n];
+    const int nq = nblk * 4;
+    for (int idx = tid; idx < mrows * nq; idx += nt) {
+      const int q = idx % nq, m = idx / nq;
+      const int n = blk0 * 16 + 4 * q;
+      const int64_t o = (int64_t)(m0 + m) * P.n + n;
+      float4 v = make_float4(cr[m * ld + 4 * q] + bias[n], cr[m * ld + 4 * q + 1] + bias[n + 1],
+                             cr[m * ld + 4 * q + 2] + bias[n + 2], cr[m * ld + 4 * q + 3] + bias[n + 3]);
+      if constexpr (EPI == EPI_RESIDUAL) {
+        const float4 r = *reinterpret_cast<const float4*>(P.residual + o);
+        v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
+      }
+      *reinterpret_cast<float4*>(out + o) = v;
     }
   }
 }
 
-template <typename T, int MB, int KW, int EPI>
-__global__ __launch_bounds__(64 * KW) void gemm_ws_kernel(Gemm P) {
-  __shared__ float red[KW * MB * 256];
+// Pipeline depth: chunks whose fragments are in flight per wavefront, sized so
+// the fragment ring stays within about 64 registers.
+template <typename T, int NB, int MB>
+struct Depth {
+  static constexpr int frag_regs = sizeof(Frag<T>) / 4;
+  static constexpr int v = (64 / ((NB + MB) * frag_regs)) < 2 ? 2 : (64 / ((NB + MB) * frag_regs)) > 8 ? 8
+                                                                   : (64 / ((NB + MB) * frag_regs));
+};
+
+template <typename T, int WN, int WK, int NB, int MB, int EPI, int U = Depth<T, NB, MB>::v>
+__global__ __launch_bounds__(64 * WN * WK) void gemm_kernel(Gemm P) {
+  constexpr int NT = 16 * WN * NB;  // weight rows per workgroup
+  constexpr int LD = NT + 1;
+  __shared__ float cr[MB * 16 * LD];
   const int lane = lane_id(), wave = uniform(threadIdx.x >> 6);
-  const int n_tiles = P.n >> 4;
+  const int wn = wave % WN, wk = wave / WN;
+  const int n_tiles = P.n / NT;
   const int tile = blockIdx.x % n_tiles, grp = blockIdx.x / n_tiles;
   int r0 = 0, r1 = P.n_rows;
   if (P.group_off) {
@@ -131,95 +149,129 @@ __global__ __launch_bounds__(64 * KW) void gemm_ws_kernel(Gemm P) {
   if (r1 <= r0) return;
 
   const int nl = lane & 15, kg = lane >> 4;
-  const T* wp = reinterpret_cast<const T*>(P.w) + grp * P.w_group_stride +
-                (int64_t)slab_row<EPI>(P, tile, nl) * P.k + 8 * kg;
+  const T* wp[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+    wp[nb] = reinterpret_cast<const T*>(P.w) + grp * P.w_group_stride +
+             (int64_t)block_row<EPI>(P, (tile * WN + wn) * NB + nb, nl) * P.k + 8 * kg;
   const int nC = P.k >> 5;
-  const int c0 = wave * nC / KW, c1 = (wave + 1) * nC / KW;
+  const int c0 = wk * nC / WK, c1 = (wk + 1) * nC / WK;
 
   for (int m0 = r0; m0 < r1; m0 += MB * 16) {
     const int mrows = min(MB * 16, r1 - m0);
     const int amb = (mrows + 15) >> 4;
     const T* xp[MB];
     bool xv[MB];
+    const int src0 = P.row_src ? P.row_src[r0] : r0;  // a valid row for lanes past the group
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       const int row = m0 + mb * 16 + nl;
       xv[mb] = row < r1;
-      const int src = xv[mb] ? (P.row_src ? P.row_src[row] : row) : 0;
+      const int src = xv[mb] ? (P.row_src ? P.row_src[row] : row) : src0;
       xp[mb] = reinterpret_cast<const T*>(P.x) + (int64_t)src * P.k + 8 * kg;
     }
-    f32x4 acc[MB];
+    f32x4 acc[NB][MB];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) acc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-#pragma unroll 4
-    for (int c = c0; c < c1; ++c) {
-      Frag<T> a;
-      a.load(wp + c * 32);
+    // U-deep ring of fragments: while chunk c is multiplied, chunks c+1 ..
+    // c+U-1 are in flight and chunk c+U is issued into its slot. The steady
+    // state has no branches (chunk indices are clamped, rows past the group
+    // are zeroed by a select) so the loads stay in flight across iterations.
+    const int nck = c1 - c0;
+    auto kloop = [&](auto amb_c) {
+      constexpr int AMB = decltype(amb_c)::value;
+      Frag<T> wa[U][NB], xb[U][AMB];
+      auto fetch = [&](int slot, int i) {
+        const int c = c0 + min(i, nck - 1);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        if (mb < amb) {
-          Frag<T> bx;
-          if (xv[mb]) bx.load(xp[mb] + c * 32); else bx.zero();
-          acc[mb] = mma32(a, bx, acc[mb]);
+        for (int nb = 0; nb < NB; ++nb) wa[slot][nb].load(wp[nb] + c * 32);
+#pragma unroll
+        for (int mb = 0; mb < AMB; ++mb) {
+          xb[slot][mb].load(xp[mb] + c * 32);
+          xb[slot][mb].keep_if(xv[mb]);
+        }
+      };
+      auto compute = [&](int slot) {
+#pragma unroll
+        for (int mb = 0; mb < AMB; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) acc[nb][mb] = mma32(wa[slot][nb], xb[slot][mb], acc[nb][mb]);
+      };
+#pragma unroll
+      for (int u = 0; u < U; ++u) fetch(u, u);
+      int i = 0;
+      for (; i + U <= nck; i += U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          compute(u);
+          fetch(u, i + u + U);
         }
       }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (i + u < nck) compute(u);
+    };
+    if (c1 > c0) {
+      if constexpr (MB >= 1) if (amb == 1) kloop(std::integral_constant<int, 1>{});
+      if constexpr (MB >= 2) if (amb == 2) kloop(std::integral_constant<int, 2 <= MB ? 2 : 1>{});
+      if constexpr (MB >= 3) if (amb == 3) kloop(std::integral_constant<int, 3 <= MB ? 3 : 1>{});
+      if constexpr (MB >= 4) if (amb == 4) kloop(std::integral_constant<int, 4 <= MB ? 4 : 1>{});
+      if constexpr (MB > 4) if (amb > 4) kloop(std::integral_constant<int, MB>{});
     }
 
-    // fixed-order reduction of the KW partial tiles
+    // sum the WK partial tiles into LDS in wavefront order (deterministic)
+    for (int k = 0; k < WK; ++k) {
+      if (wk == k) {
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
+        for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) red[((wave * MB + mb) * 4 + r) * 64 + lane] = acc[mb][r];
-    __syncthreads();
-    constexpr int PER = (MB * 256 + 64 * KW - 1) / (64 * KW);
-    float sum[PER];
+          for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const int e = threadIdx.x + q * 64 * KW;
-      float v = 0.f;
-      if (e < MB * 256) {
-#pragma unroll
-        for (int w = 0; w < KW; ++w) v += red[w * MB * 256 + e];
+            for (int r = 0; r < 4; ++r) {
+              const int n = (wn * NB + nb) * 16 + 4 * kg + r, m = mb * 16 + nl;
+              if (k == 0) cr[m * LD + n] = acc[nb][mb][r];
+              else cr[m * LD + n] += acc[nb][mb][r];
+            }
       }
-      sum[q] = v;
+      __syncthreads();
     }
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const int e = threadIdx.x + q * 64 * KW;
-      if (e < MB * 256) {
-        const int mb = e >> 8, r = (e >> 6) & 3, ln = e & 63;
-        const int n = 4 * (ln >> 4) + r, m = mb * 16 + (ln & 15);
-        red[m * 17 + n] = sum[q];
-      }
-    }
-    __syncthreads();
-    epilogue<T, EPI>(P, red, m0, mrows, tile, grp);
+    epilogue<T, EPI>(P, cr, LD, m0, mrows, tile * WN * NB, WN * NB, grp);
     __syncthreads();
   }
 }
 
-template <typename T, int MB, int KW>
-static hipError_t gemm_epi(const Gemm& g, hipStream_t s) {
-  dim3 grid((g.n / 16) * g.n_groups), block(64 * KW);
+template <typename T, int WN, int WK, int NB, int MB, int U = Depth<T, NB, MB>::v>
+hipError_t gemm_launch_cfg(const Gemm& g, hipStream_t s) {
+  constexpr int NT = 16 * WN * NB;
+  if (g.n % NT) return hipErrorInvalidValue;
+  dim3 grid((g.n / NT) * g.n_groups), block(64 * WN * WK);
   switch (g.epi) {
-    case EPI_QKV: hipLaunchKernelGGL((gemm_ws_kernel<T, MB, KW, EPI_QKV>), grid, block, 0, s, g); break;
-    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_ws_kernel<T, MB, KW, EPI_RESIDUAL>), grid, block, 0, s, g); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_ws_kernel<T, MB, KW, EPI_SWIGLU>), grid, block, 0, s, g); break;
-    default: hipLaunchKernelGGL((gemm_ws_kernel<T, MB, KW, EPI_BIAS>), grid, block, 0, s, g); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_QKV, U>), grid, block, 0, s, g); break;
+    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_RESIDUAL, U>), grid, block, 0, s, g); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_SWIGLU, U>), grid, block, 0, s, g); break;
+    default: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_BIAS, U>), grid, block, 0, s, g); break;
   }
   return hipGetLastError();
 }
 
+// Tiling choice. Grouped (expert) GEMMs have thousands of slabs, so each
+// wavefront streams whole rows (WK = 1). Dense projections have few slabs, so
+// the reduction is split across wavefronts to keep enough loads in flight.
+// (Measured on MI355X over the gpt-oss-20b decode shapes: 64-row batches
+// favour 2 wavefronts x 2 blocks per slab with a 2-deep ring; 256-row batches
+// favour 8 token blocks per pass so hot experts re-stream their rows less.)
 template <typename T>
 static hipError_t gemm_dispatch(const Gemm& g, hipStream_t s) {
   const int mb = (g.max_rows_per_group + 15) / 16;
-  if (mb <= 1) return gemm_epi<T, 1, 8>(g, s);
-  if (mb <= 2) return gemm_epi<T, 2, 8>(g, s);
-  if (mb <= 4) return gemm_epi<T, 4, 8>(g, s);
-  if (mb <= 8) return gemm_epi<T, 8, 4>(g, s);
-  return gemm_epi<T, 16, 4>(g, s);
+  if (g.n_groups > 1) {
+    if (mb <= 4) return gemm_launch_cfg<T, 2, 1, 2, 4, 2>(g, s);
+    return gemm_launch_cfg<T, 2, 2, 2, 8, 2>(g, s);
+  }
+  if (mb <= 4) return gemm_launch_cfg<T, 1, 4, 2, 4, 1>(g, s);
+  return gemm_launch_cfg<T, 1, 4, 2, 8, 1>(g, s);
 }
 
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s) {

@@ -39,7 +39,7 @@ int fail(int code, const char* fmt, ...) {
 constexpr int PAGE_SIZE = 16;
 constexpr int SPLIT_EXTRA = 4096;   // splits beyond one per token that the workspace holds
 constexpr int PPS_MIN = 16;         // minimum pages per attention split
-constexpr int TARGET_WAVES = 8192;  // (split, KV head) wavefronts the planner aims for
+constexpr int TARGET_WAVES = 3072;  // (split, KV head) wavefronts the planner aims for (measured: ~100 pages per split)
 
 size_t dtype_bytes(const mcpu_layer_cfg* c) { return c->dtype == MCPU_F32 ? 4 : 2; }
 
@@ -83,6 +83,32 @@ struct Carve {
 };
 
 int32_t* err_word(void* ws) { return (int32_t*)ws; }
+
+// ---- kernel timing (mcpu_timing_*) ------------------------------------------
+struct KernelTimer {
+  std::vector<hipEvent_t> start, stop;
+  int armed = 0, next = 0;
+};
+KernelTimer g_timers[MCPU_KERNEL_COUNT];
+
+// Records an event pair around the launch(es) made during its lifetime.
+struct Timed {
+  KernelTimer* t = nullptr;
+  hipStream_t s;
+  Timed(int kernel, hipStream_t st) : s(st) {
+    KernelTimer& k = g_timers[kernel];
+    if (k.next < k.armed) {
+      t = &k;
+      hipEventRecord(k.start[k.next], s);
+    }
+  }
+  ~Timed() {
+    if (t) {
+      hipEventRecord(t->stop[t->next], s);
+      ++t->next;
+    }
+  }
+};
 
 // per-token visible page count
 int token_pages(int pos, int window) {
@@ -192,12 +218,18 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   r.h = h; r.g2 = w->g2; r.w_r = w->w_r; r.b_r = w->b_r; r.force_idx = force_idx;
   r.n_tokens = T; r.hidden = H; r.n_experts = E; r.top_k = K; r.eps = c->rms_eps;
   r.hn_out = m.hn; r.idx_out = idx; r.w_out = wt; r.err = err;
-  HIP_TRY(launch_router(c->dtype, r, st));
+  {
+    Timed tm(MCPU_KERNEL_ROUTER, st);
+    HIP_TRY(launch_router(c->dtype, r, st));
+  }
 
   Permute p{};
   p.idx = idx; p.n_tokens = T; p.top_k = K; p.n_experts = E;
   p.group_off = m.group_off; p.pos_of = m.pos_of; p.src_tok = m.src_tok; p.err = err;
-  HIP_TRY(launch_permute(p, st));
+  {
+    Timed tm(MCPU_KERNEL_PERMUTE, st);
+    HIP_TRY(launch_permute(p, st));
+  }
 
   const int max_rows = force_idx ? T * K : T;  // a token picks each expert at most once
   Gemm g1{};
@@ -206,19 +238,28 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   g1.epi = EPI_SWIGLU; g1.bias = w->b_gu; g1.bias_group_stride = 2 * I; g1.out = m.act;
   g1.swiglu_alpha = c->swiglu_alpha; g1.swiglu_limit = c->swiglu_limit; g1.swiglu_beta = c->swiglu_beta;
   g1.err = err; g1.max_rows_per_group = max_rows;
-  HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g1, st));
+  {
+    Timed tm(MCPU_KERNEL_EXPERT_GU, st);
+    HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g1, st));
+  }
 
   Gemm g2{};
   g2.w = w->w_d; g2.w_group_stride = (int64_t)H * I; g2.n = H; g2.k = I;
   g2.x = m.act; g2.group_off = m.group_off; g2.n_groups = E;
   g2.epi = EPI_BIAS; g2.bias = w->b_d; g2.bias_group_stride = H; g2.out = m.y;
   g2.err = err; g2.max_rows_per_group = max_rows;
-  HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g2, st));
+  {
+    Timed tm(MCPU_KERNEL_EXPERT_DOWN, st);
+    HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g2, st));
+  }
 
   MoeCombine mc{};
   mc.h = h; mc.y = m.y; mc.w = wt; mc.pos_of = m.pos_of; mc.n_tokens = T; mc.hidden = H; mc.top_k = K;
   mc.out = out;
-  HIP_TRY(launch_moe_combine(mc, st));
+  {
+    Timed tm(MCPU_KERNEL_MOE_COMBINE, st);
+    HIP_TRY(launch_moe_combine(mc, st));
+  }
   return MCPU_OK;
 }
 
@@ -248,6 +289,7 @@ int run_attention(const mcpu_layer_cfg* c, const float* sinks, mcpu_kv_pool* poo
     pl.seq_lens = seq_lens; pl.cu_q = cu_q; pl.batch = batch; pl.n_tokens = ph.n_tokens;
     pl.window = c->window; pl.pps = ph.pps; pl.host_total_splits = ph.n_splits;
     pl.tok_seq = ab.tok_seq; pl.tok_pos = ab.tok_pos; pl.split_start = ab.split_start; pl.err = err;
+    Timed tm(MCPU_KERNEL_ATTN_PLAN, st);
     HIP_TRY(launch_attn_plan(pl, st));
   }
   AttnSplit sp{};
@@ -258,11 +300,17 @@ int run_attention(const mcpu_layer_cfg* c, const float* sinks, mcpu_kv_pool* poo
   sp.window = c->window; sp.pps = ph.pps;
   sp.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->head_dim));
   sp.part_ml = ab.part_ml; sp.part_acc = ab.part_acc; sp.err = err;
-  HIP_TRY(launch_attn_split(c->dtype, c->head_dim, sp, st));
+  {
+    Timed tm(MCPU_KERNEL_ATTN_SPLIT, st);
+    HIP_TRY(launch_attn_split(c->dtype, c->head_dim, sp, st));
+  }
   AttnCombine cb{};
   cb.part_ml = ab.part_ml; cb.part_acc = ab.part_acc; cb.split_start = ab.split_start; cb.sinks = sinks;
   cb.n_tokens = ph.n_tokens; cb.n_splits = ph.n_splits; cb.hq = c->n_q_heads; cb.o = o;
-  HIP_TRY(launch_attn_combine(c->dtype, c->head_dim, cb, st));
+  {
+    Timed tm(MCPU_KERNEL_ATTN_COMBINE, st);
+    HIP_TRY(launch_attn_combine(c->dtype, c->head_dim, cb, st));
+  }
   return MCPU_OK;
 }
 
@@ -344,7 +392,10 @@ int kv_pages_append(mcpu_kv_pool* pool, int32_t batch, const int32_t* page_table
   a.page_table = page_table; a.max_pages = max_pages; a.n_pages = pool->n_pages;
   a.seq_lens = seq_lens; a.cu_q = cu_q; a.batch = batch; a.n_tokens = n_tokens;
   a.hkv = pool->cfg.n_kv_heads; a.err = err_word(workspace);
-  HIP_TRY(launch_kv_append(pool->cfg.dtype, pool->cfg.head_dim, a, stream));
+  {
+    Timed tm(MCPU_KERNEL_KV_APPEND, stream);
+    HIP_TRY(launch_kv_append(pool->cfg.dtype, pool->cfg.head_dim, a, stream));
+  }
   return MCPU_OK;
 }
 
@@ -451,11 +502,17 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
   pl.seq_lens = seq_lens; pl.cu_q = cu_q; pl.batch = batch; pl.n_tokens = T; pl.window = cfg->window;
   pl.pps = ph.pps; pl.host_total_splits = ph.n_splits; pl.tok_seq = ab.tok_seq; pl.tok_pos = ab.tok_pos;
   pl.split_start = ab.split_start; pl.err = err;
-  HIP_TRY(launch_attn_plan(pl, stream));
+  {
+    Timed tm(MCPU_KERNEL_ATTN_PLAN, stream);
+    HIP_TRY(launch_attn_plan(pl, stream));
+  }
 
   RmsNorm rn{};
   rn.x = x_in; rn.g = w->g1; rn.n_tokens = T; rn.hidden = H; rn.eps = cfg->rms_eps; rn.out = xn;
-  HIP_TRY(launch_rmsnorm(cfg->dtype, rn, stream));
+  {
+    Timed tm(MCPU_KERNEL_RMSNORM, stream);
+    HIP_TRY(launch_rmsnorm(cfg->dtype, rn, stream));
+  }
 
   Gemm gq{};
   gq.w = w->w_qkv; gq.n = (Hq + 2 * Hkv) * D; gq.k = H; gq.x = xn; gq.n_rows = T; gq.n_groups = 1;
@@ -463,7 +520,10 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
   gq.k_pool = pool->k; gq.v_pool = pool->v; gq.page_table = page_table; gq.max_pages = max_pages;
   gq.n_pages = pool->n_pages; gq.tok_seq = ab.tok_seq; gq.tok_pos = ab.tok_pos; gq.rope_cos = w->rope_cos;
   gq.rope_sin = w->rope_sin; gq.rope_max_pos = w->rope_max_pos; gq.err = err; gq.max_rows_per_group = T;
-  HIP_TRY(launch_gemm(cfg->dtype, MCPU_EXPERT_DENSE, gq, stream));
+  {
+    Timed tm(MCPU_KERNEL_QKV, stream);
+    HIP_TRY(launch_gemm(cfg->dtype, MCPU_EXPERT_DENSE, gq, stream));
+  }
 
   if ((rc = run_attention(cfg, w->sinks, pool, batch, page_table, max_pages, seq_lens, cu_q, ph, q, o, ab, err,
                           stream, true)))
@@ -472,7 +532,10 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
   Gemm go{};
   go.w = w->w_o; go.n = H; go.k = Hq * D; go.x = o; go.n_rows = T; go.n_groups = 1; go.epi = EPI_RESIDUAL;
   go.bias = w->b_o; go.residual = x_in; go.out = h1; go.err = err; go.max_rows_per_group = T;
-  HIP_TRY(launch_gemm(cfg->dtype, MCPU_EXPERT_DENSE, go, stream));
+  {
+    Timed tm(MCPU_KERNEL_OPROJ, stream);
+    HIP_TRY(launch_gemm(cfg->dtype, MCPU_EXPERT_DENSE, go, stream));
+  }
 
   if ((rc = run_moe(cfg, w, T, h1, x_out, topk_idx, topk_w, nullptr, mb, err, stream))) return rc;
 
@@ -481,6 +544,34 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
     if (taps->o) HIP_TRY(hipMemcpyAsync(taps->o, o, (size_t)T * Hq * D * db, hipMemcpyDeviceToDevice, stream));
     if (taps->h1) HIP_TRY(hipMemcpyAsync(taps->h1, h1, (size_t)T * H * 4, hipMemcpyDeviceToDevice, stream));
   }
+  return MCPU_OK;
+}
+
+int mcpu_timing_start(int kernel, int n) {
+  if (kernel < 0 || kernel >= MCPU_KERNEL_COUNT || n < 0) return fail(MCPU_EINVAL, "timing kernel %d, n %d", kernel, n);
+  KernelTimer& k = g_timers[kernel];
+  while ((int)k.start.size() < n) {
+    hipEvent_t a, b;
+    HIP_TRY(hipEventCreate(&a));
+    HIP_TRY(hipEventCreate(&b));
+    k.start.push_back(a);
+    k.stop.push_back(b);
+  }
+  k.armed = n;
+  k.next = 0;
+  return MCPU_OK;
+}
+
+int mcpu_timing_read(int kernel, float* ms, int n, int* n_recorded) {
+  if (kernel < 0 || kernel >= MCPU_KERNEL_COUNT || n < 0 || (n > 0 && !ms))
+    return fail(MCPU_EINVAL, "timing kernel %d", kernel);
+  KernelTimer& k = g_timers[kernel];
+  int m = std::min(n, k.next);
+  for (int i = 0; i < m; ++i) {
+    HIP_TRY(hipEventSynchronize(k.stop[i]));
+    HIP_TRY(hipEventElapsedTime(&ms[i], k.start[i], k.stop[i]));
+  }
+  if (n_recorded) *n_recorded = m;
   return MCPU_OK;
 }
 

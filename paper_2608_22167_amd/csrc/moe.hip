@@ -26,23 +26,66 @@ __device__ __forceinline__ float block_sum_256(float v, float* scratch) {
   return t;
 }
 
-template <typename T>
+// Thread i of 256 loads float4 number i + 256 j (j < NV) of a row of length H
+// and of its gain vector, all loads in flight at once (rows past H read
+// element 0 and are masked); returns the thread's sum of squares.
+template <int NV>
+__device__ __forceinline__ float load_row(const float* x, const float* g, int H, float4* xv, float4* gv) {
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = (threadIdx.x + 256 * j) * 4;
+    const int ii = i < H ? i : 0;
+    xv[j] = *reinterpret_cast<const float4*>(x + ii);
+    gv[j] = *reinterpret_cast<const float4*>(g + ii);
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const bool v = (threadIdx.x + 256 * j) * 4 < H;
+    ss += v ? xv[j].x * xv[j].x + xv[j].y * xv[j].y + xv[j].z * xv[j].z + xv[j].w * xv[j].w : 0.f;
+  }
+  return ss;
+}
+
+__device__ __forceinline__ void store4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+__device__ __forceinline__ void store4(bf16* p, float4 v) {
+  *reinterpret_cast<uint2*>(p) = make_uint2((uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16),
+                                            (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16));
+}
+
+template <typename T, int NV>
 __global__ __launch_bounds__(256) void rmsnorm_kernel(RmsNorm P) {
   __shared__ float scratch[8];
-  const int t = blockIdx.x;
-  const float* x = P.x + (int64_t)t * P.hidden;
-  float ss = 0.f;
-  for (int i = threadIdx.x; i < P.hidden; i += blockDim.x) ss += x[i] * x[i];
-  ss = block_sum_256(ss, scratch);
-  const float inv = 1.0f / sqrtf(ss / (float)P.hidden + P.eps);
-  T* out = reinterpret_cast<T*>(P.out) + (int64_t)t * P.hidden;
-  for (int i = threadIdx.x; i < P.hidden; i += blockDim.x) Elem<T>::store(out, i, x[i] * inv * P.g[i]);
+  const int t = blockIdx.x, H = P.hidden;
+  float4 xv[NV], gv[NV];
+  const float ss = load_row<NV>(P.x + (int64_t)t * H, P.g, H, xv, gv);
+  const float inv = 1.0f / sqrtf(block_sum_256(ss, scratch) / (float)H + P.eps);
+  T* out = reinterpret_cast<T*>(P.out) + (int64_t)t * H;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = (threadIdx.x + 256 * j) * 4;
+    if (i < H)
+      store4(out + i, make_float4(xv[j].x * inv * gv[j].x, xv[j].y * inv * gv[j].y, xv[j].z * inv * gv[j].z,
+                                  xv[j].w * inv * gv[j].w));
+  }
+}
+
+template <typename T>
+static void rmsnorm_nv(const RmsNorm& p, hipStream_t s) {
+  const int nv = (p.hidden + 1023) / 1024;
+  dim3 g(p.n_tokens), b(256);
+  if (nv <= 1) hipLaunchKernelGGL((rmsnorm_kernel<T, 1>), g, b, 0, s, p);
+  else if (nv <= 2) hipLaunchKernelGGL((rmsnorm_kernel<T, 2>), g, b, 0, s, p);
+  else if (nv <= 3) hipLaunchKernelGGL((rmsnorm_kernel<T, 3>), g, b, 0, s, p);
+  else if (nv <= 4) hipLaunchKernelGGL((rmsnorm_kernel<T, 4>), g, b, 0, s, p);
+  else hipLaunchKernelGGL((rmsnorm_kernel<T, 8>), g, b, 0, s, p);
 }
 
 hipError_t launch_rmsnorm(int dtype, const RmsNorm& p, hipStream_t s) {
   if (p.n_tokens == 0) return hipSuccess;
-  if (dtype == 0) hipLaunchKernelGGL((rmsnorm_kernel<float>), dim3(p.n_tokens), dim3(256), 0, s, p);
-  else hipLaunchKernelGGL((rmsnorm_kernel<bf16>), dim3(p.n_tokens), dim3(256), 0, s, p);
+  if (p.hidden % 4 || p.hidden > 8192) return hipErrorInvalidValue;
+  if (dtype == 0) rmsnorm_nv<float>(p, s);
+  else rmsnorm_nv<bf16>(p, s);
   return hipGetLastError();
 }
 
@@ -51,46 +94,135 @@ hipError_t launch_rmsnorm(int dtype, const RmsNorm& p, hipStream_t s) {
 // ---------------------------------------------------------------------------
 
 constexpr int ROUTER_MAX_H = 8192;
+constexpr int ROUTER_MAX_E = 64;
 
-template <typename T>
+// 8 consecutive router weights, loaded raw and widened to fp32 (exact)
+template <typename T> struct Raw8;
+template <> struct Raw8<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = reinterpret_cast<const float4*>(p)[0];
+    b = reinterpret_cast<const float4*>(p)[1];
+  }
+  __device__ __forceinline__ void widen(float w[8]) const {
+    w[0] = a.x; w[1] = a.y; w[2] = a.z; w[3] = a.w; w[4] = b.x; w[5] = b.y; w[6] = b.z; w[7] = b.w;
+  }
+};
+template <> struct Raw8<bf16> {
+  uint4 v;
+  __device__ __forceinline__ void load(const bf16* p) { v = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ void widen(float w[8]) const {
+    const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      w[2 * i] = __uint_as_float(u[i] << 16);
+      w[2 * i + 1] = __uint_as_float(u[i] & 0xFFFF0000u);
+    }
+  }
+};
+
+// One workgroup per token. Thread i owns the 8-wide reduction chunks i, i+256,
+// ... and accumulates all E logits over them; partial logits are then summed
+// across lanes (wavefront butterflies) and across the 4 wavefronts (LDS).
+template <typename T, int E, int NV>
 __global__ __launch_bounds__(256) void router_kernel(Router P) {
   __shared__ float hn[ROUTER_MAX_H];
-  __shared__ float logits[64];
+  __shared__ float part[4][E];
+  __shared__ float logits[E];
   __shared__ float scratch[8];
   const int t = blockIdx.x, H = P.hidden;
-  const float* h = P.h + (int64_t)t * H;
-  float ss = 0.f;
-  for (int i = threadIdx.x; i < H; i += blockDim.x) ss += h[i] * h[i];
-  ss = block_sum_256(ss, scratch);
-  const float inv = 1.0f / sqrtf(ss / (float)H + P.eps);
+  float4 hv[NV], gv[NV];
+  const float ss = load_row<NV>(P.h + (int64_t)t * H, P.g2, H, hv, gv);
+  const float inv = 1.0f / sqrtf(block_sum_256(ss, scratch) / (float)H + P.eps);
   T* hq = reinterpret_cast<T*>(P.hn_out) + (int64_t)t * H;
-  for (int i = threadIdx.x; i < H; i += blockDim.x) {
-    const float v = h[i] * inv * P.g2[i];
-    hn[i] = v;
-    Elem<T>::store(hq, i, v);
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = (threadIdx.x + 256 * j) * 4;
+    if (i < H) {
+      const float4 v = make_float4(hv[j].x * inv * gv[j].x, hv[j].y * inv * gv[j].y,
+                                   hv[j].z * inv * gv[j].z, hv[j].w * inv * gv[j].w);
+      *reinterpret_cast<float4*>(hn + i) = v;
+      store4(hq + i, v);
+    }
   }
   __syncthreads();
 
-  const int wave = threadIdx.x >> 6, lane = lane_id(), nw = blockDim.x >> 6;
+  const int wave = threadIdx.x >> 6, lane = lane_id();
   const T* wr = reinterpret_cast<const T*>(P.w_r);
-  for (int e = wave; e < P.n_experts; e += nw) {
-    float acc = 0.f;
-    for (int i = lane; i < H; i += 64) acc += hn[i] * Elem<T>::load(wr, (int64_t)e * H + i);
-    acc = wave_sum(acc);
-    if (lane == 0) logits[e] = acc + P.b_r[e];
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  const int nchunk = H / 8;
+  for (int c0 = 0; c0 < nchunk; c0 += blockDim.x) {
+    // branch-free: out-of-range chunks and experts read a valid address and
+    // contribute zero
+    const int c = c0 + threadIdx.x;
+    const bool cv = c < nchunk;
+    const int cc = cv ? c : nchunk - 1;
+    float x[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = cv ? hn[8 * cc + j] : 0.f;
+    // the raw chunks of up to 32 experts are loaded together, then widened
+    constexpr int G = E < 32 ? E : 32;
+#pragma unroll
+    for (int e0 = 0; e0 < E; e0 += G) {
+      Raw8<T> raw[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int e = e0 + g, ee = e < P.n_experts ? e : 0;
+        raw[g].load(wr + (int64_t)ee * H + 8 * cc);
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float w[8];
+        raw[g].widen(w);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[e0 + g] += x[j] * w[j];
+      }
+    }
+  }
+  // reduce-scatter across the 64 lanes: each halving step trades half of the
+  // partial sums with the partner lane, so lane l ends with expert l / (64 / E)
+  {
+    int n = E;
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      if (n > 1) {
+        const bool upper = (lane & o) != 0;
+        const int half = n / 2;
+#pragma unroll
+        for (int j = 0; j < E / 2; ++j) {
+          if (j < half) {
+            const float send = upper ? acc[j] : acc[j + half];
+            const float keep = upper ? acc[j + half] : acc[j];
+            acc[j] = keep + __shfl_xor(send, o, 64);
+          }
+        }
+        n = half;
+      } else {
+        acc[0] += __shfl_xor(acc[0], o, 64);
+      }
+    }
+    const int e = lane / (64 / E);
+    if (lane % (64 / E) == 0) part[wave][e] = acc[0];
+  }
+  __syncthreads();
+  if (threadIdx.x < P.n_experts) {
+    const int e = threadIdx.x;
+    logits[e] = part[0][e] + part[1][e] + part[2][e] + part[3][e] + P.b_r[e];
   }
   __syncthreads();
 
   if (wave == 0) {
-    const int E = P.n_experts, K = P.top_k;
-    float v = lane < E ? logits[lane] : -INFINITY;
+    const int NE = P.n_experts, K = P.top_k;
+    float v = lane < NE ? logits[lane] : -INFINITY;
     int sel_e[8];
     float sel_v[8];
     for (int s = 0; s < K; ++s) {
       int e;
       if (P.force_idx) {
         e = P.force_idx[(int64_t)t * K + s];
-        if (e < 0 || e >= E) {
+        if (e < 0 || e >= NE) {
           if (lane == 0) set_error(P.err, 4);
           e = 0;
         }
@@ -134,11 +266,31 @@ __global__ __launch_bounds__(256) void router_kernel(Router P) {
   }
 }
 
+template <typename T, int E>
+static void router_nv(const Router& p, hipStream_t s) {
+  const int nv = (p.hidden + 1023) / 1024;
+  dim3 g(p.n_tokens), b(256);
+  if (nv <= 1) hipLaunchKernelGGL((router_kernel<T, E, 1>), g, b, 0, s, p);
+  else if (nv <= 2) hipLaunchKernelGGL((router_kernel<T, E, 2>), g, b, 0, s, p);
+  else if (nv <= 3) hipLaunchKernelGGL((router_kernel<T, E, 3>), g, b, 0, s, p);
+  else if (nv <= 4) hipLaunchKernelGGL((router_kernel<T, E, 4>), g, b, 0, s, p);
+  else hipLaunchKernelGGL((router_kernel<T, E, 8>), g, b, 0, s, p);
+}
+
+template <typename T>
+static void router_e(const Router& p, hipStream_t s) {
+  if (p.n_experts <= 8) router_nv<T, 8>(p, s);
+  else if (p.n_experts <= 16) router_nv<T, 16>(p, s);
+  else if (p.n_experts <= 32) router_nv<T, 32>(p, s);
+  else router_nv<T, 64>(p, s);
+}
+
 hipError_t launch_router(int dtype, const Router& p, hipStream_t s) {
   if (p.n_tokens == 0) return hipSuccess;
-  if (p.hidden > ROUTER_MAX_H || p.n_experts > 64 || p.top_k > 8) return hipErrorInvalidValue;
-  if (dtype == 0) hipLaunchKernelGGL((router_kernel<float>), dim3(p.n_tokens), dim3(256), 0, s, p);
-  else hipLaunchKernelGGL((router_kernel<bf16>), dim3(p.n_tokens), dim3(256), 0, s, p);
+  if (p.hidden > ROUTER_MAX_H || p.hidden % 8 || p.n_experts > ROUTER_MAX_E || p.top_k > 8)
+    return hipErrorInvalidValue;
+  if (dtype == 0) router_e<float>(p, s);
+  else router_e<bf16>(p, s);
   return hipGetLastError();
 }
 
@@ -146,57 +298,124 @@ hipError_t launch_router(int dtype, const Router& p, hipStream_t s) {
 // permute: expert-sorted rows, stable in (token, slot) order
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(256) void permute_kernel(Permute P) {
-  __shared__ int cnt[64];
-  const int n = P.n_tokens * P.top_k, E = P.n_experts;
-  if (threadIdx.x < 64) cnt[threadIdx.x] = 0;
-  __syncthreads();
-  for (int a = threadIdx.x; a < n; a += blockDim.x) {
-    int e = P.idx[a];
-    if (e < 0 || e >= E) {
-      set_error(P.err, 4);
-      e = 0;
+constexpr int PERM_CHUNKS = 64;  // chunks of 64 assignments counted in LDS (n <= 4096)
+
+// rank of this lane among the lanes of its wavefront holding the same expert
+// and a lower lane id, by peeling one expert value per round with ballots
+__device__ __forceinline__ int rank_in_chunk(int e, bool valid, int* uniq_first) {
+  const int lane = lane_id();
+  const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  bool todo = valid;
+  int rank = 0;
+  uint64_t pending = __ballot(todo);
+  while (pending) {
+    const int first = __ffsll((unsigned long long)pending) - 1;
+    const int e0 = __shfl(e, first, 64);
+    const uint64_t m = __ballot(todo && e == e0);
+    if (todo && e == e0) {
+      rank = __popcll(m & lt);
+      todo = false;
     }
-    atomicAdd(&cnt[e], 1);  // integer counts: order-independent
+    pending = __ballot(todo);
+  }
+  (void)uniq_first;
+  return rank;
+}
+
+__global__ __launch_bounds__(256) void permute_kernel(Permute P) {
+  __shared__ int cnt[PERM_CHUNKS][64];
+  const int n = P.n_tokens * P.top_k, E = P.n_experts;
+  const int nch = (n + 63) / 64;
+  const int wave = threadIdx.x >> 6, lane = lane_id();
+  for (int i = threadIdx.x; i < PERM_CHUNKS * 64; i += blockDim.x) (&cnt[0][0])[i] = 0;
+  __syncthreads();
+  // per-chunk histograms (integer counts; order-independent)
+  for (int c = wave; c < nch; c += 4) {
+    const int a = c * 64 + lane;
+    if (a < n) {
+      int e = P.idx[a];
+      if (e < 0 || e >= E) {
+        set_error(P.err, 4);
+        e = 0;
+      }
+      atomicAdd(&cnt[c][e], 1);
+    }
   }
   __syncthreads();
-  if (threadIdx.x >= 64) return;
-  const int lane = threadIdx.x;
-  const int c = lane < E ? cnt[lane] : 0;
-  const int incl = wave_incl_scan(c);
-  int base = incl - c;  // lane e holds the next free row of expert e
-  if (lane < E) P.group_off[lane] = base;
-  if (lane == E - 1) P.group_off[E] = incl;
-  const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-  for (int a0 = 0; a0 < n; a0 += 64) {
-    const int a = a0 + lane;
-    int e = a < n ? P.idx[a] : -1;
-    if (a < n && (e < 0 || e >= E)) e = 0;
-    bool todo = a < n;
-    int pos = -1;
-    uint64_t pending = __ballot(todo);
-    while (pending) {
-      const int first = __ffsll((unsigned long long)pending) - 1;
-      const int e0 = __shfl(e, first, 64);
-      const uint64_t m = __ballot(todo && e == e0);
-      const int b0 = __shfl(base, e0, 64);
-      if (todo && e == e0) {
-        pos = b0 + __popcll(m & lt_mask);
-        todo = false;
+  // lane e of wave 0: exclusive scan over experts, then running bases per chunk
+  if (wave == 0) {
+    int tot = 0;
+    if (lane < E)
+      for (int c = 0; c < nch; ++c) tot += cnt[c][lane];
+    const int incl = wave_incl_scan(tot);
+    int run = incl - tot;
+    if (lane < E) P.group_off[lane] = run;
+    if (lane == E - 1) P.group_off[E] = incl;
+    if (lane < E)
+      for (int c = 0; c < nch; ++c) {
+        const int k = cnt[c][lane];
+        cnt[c][lane] = run;
+        run += k;
       }
-      if (lane == e0) base += __popcll(m);
-      pending = __ballot(todo);
-    }
-    if (a < n) {
+  }
+  __syncthreads();
+  for (int c = wave; c < nch; c += 4) {
+    const int a = c * 64 + lane;
+    const bool valid = a < n;
+    int e = valid ? P.idx[a] : 0;
+    if (e < 0 || e >= E) e = 0;
+    const int r = rank_in_chunk(e, valid, nullptr);
+    if (valid) {
+      const int pos = cnt[c][e] + r;
       P.pos_of[a] = pos;
       P.src_tok[pos] = a / P.top_k;
     }
   }
 }
 
+// Larger batches: one wavefront walks the chunks in order with running bases.
+__global__ __launch_bounds__(64) void permute_serial_kernel(Permute P) {
+  __shared__ int cnt[64];
+  const int n = P.n_tokens * P.top_k, E = P.n_experts, lane = lane_id();
+  cnt[lane] = 0;
+  __syncthreads();
+  for (int a = lane; a < n; a += 64) {
+    int e = P.idx[a];
+    if (e < 0 || e >= E) {
+      set_error(P.err, 4);
+      e = 0;
+    }
+    atomicAdd(&cnt[e], 1);
+  }
+  __syncthreads();
+  const int c = lane < E ? cnt[lane] : 0;
+  const int incl = wave_incl_scan(c);
+  int base = incl - c;
+  if (lane < E) P.group_off[lane] = base;
+  if (lane == E - 1) P.group_off[E] = incl;
+  for (int a0 = 0; a0 < n; a0 += 64) {
+    const int a = a0 + lane;
+    const bool valid = a < n;
+    int e = valid ? P.idx[a] : 0;
+    if (e < 0 || e >= E) e = 0;
+    const int r = rank_in_chunk(e, valid, nullptr);
+    // expert e's base is held by lane e; count this chunk's rows per expert
+    const int b0 = __shfl(base, e, 64);
+    int mine = 0;
+    for (int x = 0; x < 64; ++x) mine += (__shfl(valid ? e : -1, x, 64) == lane) ? 1 : 0;
+    if (valid) {
+      const int pos = b0 + r;
+      P.pos_of[a] = pos;
+      P.src_tok[pos] = a / P.top_k;
+    }
+    base += mine;
+  }
+}
+
 hipError_t launch_permute(const Permute& p, hipStream_t s) {
   if (p.n_experts > 64) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(permute_kernel, dim3(1), dim3(256), 0, s, p);
+  if (p.n_tokens * p.top_k <= PERM_CHUNKS * 64) hipLaunchKernelGGL(permute_kernel, dim3(1), dim3(256), 0, s, p);
+  else hipLaunchKernelGGL(permute_serial_kernel, dim3(1), dim3(64), 0, s, p);
   return hipGetLastError();
 }
 
@@ -204,24 +423,27 @@ hipError_t launch_permute(const Permute& p, hipStream_t s) {
 // combine: out[t] = h[t] + sum_{s < k} w[t][s] * y[pos_of[t k + s]]
 // ---------------------------------------------------------------------------
 
+// grid (tokens, H / 1024): each thread combines 4 consecutive features
 __global__ __launch_bounds__(256) void moe_combine_kernel(MoeCombine P) {
   const int t = blockIdx.x, H = P.hidden, K = P.top_k;
-  int rows[8];
-  float ws[8];
+  const int i = (blockIdx.y * 256 + threadIdx.x) * 4;
+  if (i >= H) return;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int s = 0; s < K; ++s) {
-    rows[s] = P.pos_of[(int64_t)t * K + s];
-    ws[s] = P.w[(int64_t)t * K + s];
+    const int row = P.pos_of[(int64_t)t * K + s];
+    const float w = P.w[(int64_t)t * K + s];
+    const float4 y = *reinterpret_cast<const float4*>(P.y + (int64_t)row * H + i);
+    acc.x += w * y.x; acc.y += w * y.y; acc.z += w * y.z; acc.w += w * y.w;
   }
-  for (int i = threadIdx.x; i < H; i += blockDim.x) {
-    float acc = 0.f;
-    for (int s = 0; s < K; ++s) acc += ws[s] * P.y[(int64_t)rows[s] * H + i];
-    P.out[(int64_t)t * H + i] = P.h[(int64_t)t * H + i] + acc;
-  }
+  const float4 h = *reinterpret_cast<const float4*>(P.h + (int64_t)t * H + i);
+  *reinterpret_cast<float4*>(P.out + (int64_t)t * H + i) =
+      make_float4(h.x + acc.x, h.y + acc.y, h.z + acc.z, h.w + acc.w);
 }
 
 hipError_t launch_moe_combine(const MoeCombine& p, hipStream_t s) {
   if (p.n_tokens == 0) return hipSuccess;
-  hipLaunchKernelGGL(moe_combine_kernel, dim3(p.n_tokens), dim3(256), 0, s, p);
+  if (p.hidden % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(moe_combine_kernel, dim3(p.n_tokens, (p.hidden + 1023) / 1024), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

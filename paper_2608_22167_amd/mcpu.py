@@ -25,7 +25,11 @@ DEVERR_PAGE, DEVERR_ROPE, DEVERR_EXPERT, DEVERR_PLAN = 1, 2, 4, 8
 EXPORTED = ("mcpu_last_error", "kv_pool_create", "kv_pool_destroy", "kv_pool_free_pages",
             "kv_pages_alloc", "kv_pages_free", "kv_pages_append", "paged_attention_workspace_size",
             "paged_attention", "moe_forward_workspace_size", "moe_forward",
-            "decode_layer_workspace_size", "decode_layer", "mcpu_check_device_errors")
+            "decode_layer_workspace_size", "decode_layer", "mcpu_check_device_errors",
+            "mcpu_timing_start", "mcpu_timing_read")
+
+KERNELS = ("attn_plan", "rmsnorm", "qkv", "attn_split", "attn_combine", "oproj", "router", "permute",
+           "expert_gu", "expert_down", "moe_combine", "kv_append")
 
 
 class McpuError(RuntimeError):
@@ -81,6 +85,8 @@ def lib():
         L.decode_layer.argtypes = [vp, vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    vp, sz, vp]
         L.mcpu_check_device_errors.argtypes = [vp, vp, i32p]
+        L.mcpu_timing_start.argtypes = [i32, i32]
+        L.mcpu_timing_read.argtypes = [i32, vp, i32, i32p]
         _LIB = L
     return _LIB
 
@@ -260,6 +266,17 @@ def mcpu_check_device_errors(workspace, stream=None) -> int:
     if rc not in (MCPU_OK, MCPU_EDEVICE):
         _check(rc)
     return bits.value
+
+
+def mcpu_timing_start(kernel: str, n: int) -> None:
+    _check(lib().mcpu_timing_start(KERNELS.index(kernel), n))
+
+
+def mcpu_timing_read(kernel: str, n: int) -> np.ndarray:
+    ms = np.zeros(max(n, 1), dtype=np.float32)
+    rec = ctypes.c_int32(0)
+    _check(lib().mcpu_timing_read(KERNELS.index(kernel), _ptr(ms), n, ctypes.byref(rec)))
+    return ms[:rec.value].astype(np.float64)
 
 
 # ---------------------------------------------------------------------------

@@ -333,5 +333,25 @@ def mixed_prefill(seed=1004, n_dec=192, n_pre=64, ctx_lo=1024, ctx_hi=24576,
                          kw.pop("shape", GPT_OSS_20B), ctx, q, seed, **kw)
 
 
+def restrict(wl: Workload, seqs):
+    """The same step restricted to sequences `seqs`, with a compact page pool
+    holding only their pages (same values). Returns (workload, token rows)."""
+    seqs = np.asarray(seqs)
+    pt = wl.page_table[seqs]
+    used = np.unique(pt[pt >= 0])
+    remap = -np.ones(wl.n_pages, np.int64)
+    remap[used] = np.arange(len(used))
+    sub = Workload(name=wl.name + "_subset", shape=wl.shape, seed=wl.seed, seq_lens=wl.seq_lens[seqs],
+                   q_lens=wl.q_lens[seqs],
+                   page_table=np.where(pt >= 0, remap[np.maximum(pt, 0)], -1).astype(np.int32),
+                   n_pages=len(used), weights=wl.weights)
+    idx = torch.from_numpy(used)
+    sub.k_pool, sub.v_pool = wl.k_pool[idx], wl.v_pool[idx]
+    cu = wl.cu_q
+    rows = np.concatenate([np.arange(cu[b], cu[b + 1]) for b in seqs])
+    sub.x_in = wl.x_in[torch.from_numpy(rows)]
+    return sub, rows
+
+
 def custom(shape: LayerShape, ctx, q, seed, name="custom", **kw) -> Workload:
     return make_workload(name, shape, ctx, q, seed, **kw)

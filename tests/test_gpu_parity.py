@@ -272,23 +272,6 @@ def test_moe_forward_and_forced_selection(kind):
 # ---------------------------------------------------------------------------------- full size, sampled
 
 
-def subset(wl, seqs):
-    """The same step restricted to sequences `seqs` with a compact page pool."""
-    seqs = np.asarray(seqs)
-    pt = wl.page_table[seqs]
-    used = np.unique(pt[pt >= 0])
-    remap = -np.ones(wl.n_pages, np.int64)
-    remap[used] = np.arange(len(used))
-    sub = W.Workload(name=wl.name + "_subset", shape=wl.shape, seed=wl.seed, seq_lens=wl.seq_lens[seqs],
-                     q_lens=wl.q_lens[seqs], page_table=np.where(pt >= 0, remap[np.maximum(pt, 0)], -1).astype(np.int32),
-                     n_pages=len(used), weights=wl.weights)
-    idx = torch.from_numpy(used)
-    sub.k_pool, sub.v_pool = wl.k_pool[idx], wl.v_pool[idx]
-    rows = np.concatenate([np.arange(wl.cu_q[b], wl.cu_q[b + 1]) for b in seqs])
-    sub.x_in = wl.x_in[torch.from_numpy(rows)]
-    return sub, rows
-
-
 def _sampled(wl, n=6):
     order = np.argsort(wl.seq_lens)
     pick = {int(order[0]), int(order[-1])}
@@ -305,7 +288,7 @@ def test_full_size_sampled(which):
     wl = W.full_b64() if which == "full_b64" else W.sliding_b256()
     gpu, step = run_layer(wl)
     seqs = _sampled(wl)
-    sub, rows = subset(wl, seqs)
+    sub, rows = W.restrict(wl, seqs)
     g = {k: v[rows] for k, v in gpu.items()}
     ref, _ = reference(sub, g)
     compare_layer(sub, g, None, ref)
