@@ -75,7 +75,7 @@ def traffic_from_profile(kernel_src, workload_name):
     return float(t.group(1))
 
 
-def cpu_baseline(wl, n_seq=16):
+def cpu_baseline(wl, n_seq=64):
     """The CPU reference on `n_seq` seeded sequences of the same workload."""
     from oracle import oracle as O
     from paper_2608_22167_amd import workload as W
@@ -99,6 +99,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="full_b64")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="after the benchmark, run 5 device-to-device copies of MIB MiB, the "
+                         "reference kernel for scaling hardware byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this benchmark runs on one GPU; the decode step is not sharded "
@@ -165,6 +168,15 @@ def main():
                 "traffic": traffic, "avg_us": round(attn_us, 2),
                 "algorithmic_bytes": kb["attn_split"]}
     per_kernel_gbs = {k: round(kb[k] / (breakdown[k] * 1e-6) / 1e9, 1) for k in kb if k in breakdown}
+
+    if args.copy_calibration > 0:
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"copy calibration: 5 copies of {n} bytes")
 
     cpu = None
     if not args.no_cpu_baseline:
