@@ -71,7 +71,9 @@ enum {
   MCPU_DEVERR_PAGE = 1,  /* a needed page-table entry was -1 or >= n_pages; its keys were skipped */
   MCPU_DEVERR_ROPE = 2,  /* a position was >= rope_max_pos; that token's q/k were not written */
   MCPU_DEVERR_EXPERT = 4, /* a top-k expert id outside [0, n_experts) was passed in */
-  MCPU_DEVERR_PLAN = 8    /* device seq_lens / cu_q disagree with the host copies */
+  MCPU_DEVERR_PLAN = 8,   /* device seq_lens / cu_q disagree with the host copies */
+  MCPU_DEVERR_MXFP4 = 16  /* an MXFP4 block scale outside [2, 252]: scaled values would not be
+                             normal bfloat16; that block contributed zero */
 };
 
 /* Layer configuration (host struct, by value semantics).

@@ -420,13 +420,20 @@ double orc_e2m1(int code) {
 int orc_mxfp4_dequant(int64_t rows, int cols, const uint8_t* codes, const uint8_t* scales,
                       float* out) {
   if (cols % 32) return ORC_EINVAL;
+  double value[16];
+  for (int c = 0; c < 16; ++c) value[c] = orc_e2m1(c);
+  int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
   for (int64_t r = 0; r < rows; ++r)
-    for (int j = 0; j < cols; ++j) {
-      uint8_t byte = codes[r * (cols / 2) + j / 2];
-      int code = (j % 2 == 0) ? (byte & 0xF) : (byte >> 4);
-      uint8_t s = scales[r * (cols / 32) + j / 32];
-      if (s == 0xFF) return ORC_EINVAL; /* NaN scale is not a weight */
-      out[r * cols + j] = (float)ldexp(orc_e2m1(code), (int)s - 127);
+    for (int blk = 0; blk < cols / 32; ++blk) {
+      uint8_t s = scales[r * (cols / 32) + blk];
+      if (s == 0xFF) { bad = 1; continue; } /* NaN scale is not a weight */
+      double scale = ldexp(1.0, (int)s - 127);
+      for (int j = 32 * blk; j < 32 * blk + 32; ++j) {
+        uint8_t byte = codes[r * (cols / 2) + j / 2];
+        int code = (j % 2 == 0) ? (byte & 0xF) : (byte >> 4);
+        out[r * cols + j] = (float)(value[code] * scale);
+      }
     }
-  return ORC_OK;
+  return bad ? ORC_EINVAL : ORC_OK;
 }

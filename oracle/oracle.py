@@ -160,11 +160,15 @@ def e2m1(code: int) -> float:
     return lib().orc_e2m1(code)
 
 
-def mxfp4_dequant(codes, scales, rows_per_mat: int, cols: int) -> np.ndarray:
+def mxfp4_dequant(codes, scales, rows_per_mat: int, cols: int, out=None) -> np.ndarray:
+    """out, if given, is a C-contiguous float32 array of rows * cols elements."""
     c = _np(codes, np.uint8)
     s = _np(scales, np.uint8)
     rows = c.size // (cols // 2)
-    out = np.empty((rows, cols), dtype=np.float32)
+    if out is None:
+        out = np.empty((rows, cols), dtype=np.float32)
+    elif out.dtype != np.float32 or out.size != rows * cols or not out.flags.c_contiguous:
+        raise ValueError("mxfp4_dequant: out must be contiguous float32 of rows * cols elements")
     rc = lib().orc_mxfp4_dequant(rows, cols, _p(c), _p(s), _p(out))
     if rc:
         raise ValueError("invalid MXFP4 input")

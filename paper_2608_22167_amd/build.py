@@ -50,8 +50,17 @@ def build_hip(jobs: int = 4) -> str:
     return out
 
 
+def build_synth_device() -> str:
+    """Device twin of the input generator (bench and tests only; no layer arithmetic)."""
+    out = os.path.join(HERE, "libmcpu_synth_dev.so")
+    _run([HIPCC, *HIP_FLAGS, "-shared", "-o", out + ".tmp", os.path.join(CSRC, "synth_fill.hip")])
+    os.replace(out + ".tmp", out)
+    return out
+
+
 def build() -> None:
     build_synth()
+    build_synth_device()
     build_hip()
 
 

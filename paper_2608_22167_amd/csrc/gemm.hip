@@ -121,6 +121,66 @@ __device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mro
   }
 }
 
+// ---------------------------------------------------------------------------
+// weight sources: where a lane's 8 weights of a 32-wide chunk come from
+// ---------------------------------------------------------------------------
+
+// Dense weights in the layer dtype.
+template <typename T, int WF> struct WSrc {
+  using Raw = Frag<T>;
+  const T* p;
+  __device__ __forceinline__ void init(const Gemm& P, int grp, int row, int kg) {
+    p = reinterpret_cast<const T*>(P.w) + grp * P.w_group_stride + (int64_t)row * P.k + 8 * kg;
+  }
+  __device__ __forceinline__ void fetch(Raw& r, int c) const { r.load(p + c * 32); }
+  __device__ __forceinline__ Frag<T> frag(const Raw& r, bool&) const { return r; }
+};
+
+// One E2M1 element (4-bit code: sign, 2 exponent bits, 1 mantissa bit) times the
+// block scale, as bfloat16 bits. dexp = (scale - 127) << 7 adds the E8M0 power of
+// two to the bfloat16 exponent field; E2M1 magnitudes 0, .5, 1, 1.5, 2, 3, 4, 6
+// are 0 and bfloat16 0x3F00, 0x3F80 + 0x40 (m - 2) for m >= 2.
+__device__ __forceinline__ uint32_t e2m1_to_bf16(uint32_t nib, int32_t dexp) {
+  const uint32_t m = nib & 7u;
+  uint32_t b = m >= 2u ? 0x3F80u + (m - 2u) * 0x40u : (m == 1u ? 0x3F00u : 0u);
+  b = b ? (uint32_t)((int32_t)b + dexp) : 0u;
+  return b | ((nib & 8u) << 12);
+}
+
+// MXFP4 experts (OCP MX): per row, K/2 bytes of E2M1 codes (low nibble = even
+// column) and K/32 E8M0 scales; one 32-wide chunk is exactly one scale block.
+// Scales outside [2, 252] (results that are not normal bfloat16) raise
+// MCPU_DEVERR_MXFP4 and contribute zero.
+template <> struct WSrc<bf16, 1> {
+  struct Raw {
+    uint32_t codes, scale;
+  };
+  const uint32_t* cp;
+  const uint8_t* sp;
+  __device__ __forceinline__ void init(const Gemm& P, int grp, int row, int kg) {
+    cp = reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(P.w) + grp * P.w_group_stride +
+                                           (int64_t)row * (P.k / 2)) + kg;
+    sp = P.w_scales + grp * (P.w_group_stride / 16) + (int64_t)row * (P.k / 32);
+  }
+  __device__ __forceinline__ void fetch(Raw& r, int c) const {
+    r.codes = cp[c * 4];
+    r.scale = sp[c];
+  }
+  __device__ __forceinline__ Frag<bf16> frag(const Raw& r, bool& bad) const {
+    const bool ok = r.scale >= 2u && r.scale <= 252u;
+    bad = bad || !ok;
+    const uint32_t codes = ok ? r.codes : 0u;
+    const int32_t dexp = ((int32_t)r.scale - 127) * 128;
+    Frag<bf16> f;
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = e2m1_to_bf16((codes >> (8 * i)) & 0xFu, dexp) | (e2m1_to_bf16((codes >> (8 * i + 4)) & 0xFu, dexp) << 16);
+    f.v = make_uint4(w[0], w[1], w[2], w[3]);
+    return f;
+  }
+};
+
 // Pipeline depth: chunks whose fragments are in flight per wavefront, sized so
 // the fragment ring stays within about 64 registers.
 template <typename T, int NB, int MB>
@@ -130,7 +190,7 @@ struct Depth {
                                                                    : (64 / ((NB + MB) * frag_regs));
 };
 
-template <typename T, int WN, int WK, int NB, int MB, int EPI, int U = Depth<T, NB, MB>::v>
+template <typename T, int WN, int WK, int NB, int MB, int EPI, int U = Depth<T, NB, MB>::v, int WF = 0>
 __global__ __launch_bounds__(64 * WN * WK) void gemm_kernel(Gemm P) {
   constexpr int NT = 16 * WN * NB;  // weight rows per workgroup
   constexpr int LD = NT + 1;
@@ -149,11 +209,11 @@ __global__ __launch_bounds__(64 * WN * WK) void gemm_kernel(Gemm P) {
   if (r1 <= r0) return;
 
   const int nl = lane & 15, kg = lane >> 4;
-  const T* wp[NB];
+  using Src = WSrc<T, WF>;
+  Src ws[NB];
 #pragma unroll
-  for (int nb = 0; nb < NB; ++nb)
-    wp[nb] = reinterpret_cast<const T*>(P.w) + grp * P.w_group_stride +
-             (int64_t)block_row<EPI>(P, (tile * WN + wn) * NB + nb, nl) * P.k + 8 * kg;
+  for (int nb = 0; nb < NB; ++nb) ws[nb].init(P, grp, block_row<EPI>(P, (tile * WN + wn) * NB + nb, nl), kg);
+  bool bad_scale = false;
   const int nC = P.k >> 5;
   const int c0 = wk * nC / WK, c1 = (wk + 1) * nC / WK;
 
@@ -183,11 +243,12 @@ __global__ __launch_bounds__(64 * WN * WK) void gemm_kernel(Gemm P) {
     const int nck = c1 - c0;
     auto kloop = [&](auto amb_c) {
       constexpr int AMB = decltype(amb_c)::value;
-      Frag<T> wa[U][NB], xb[U][AMB];
+      typename Src::Raw wa[U][NB];
+      Frag<T> xb[U][AMB];
       auto fetch = [&](int slot, int i) {
         const int c = c0 + min(i, nck - 1);
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) wa[slot][nb].load(wp[nb] + c * 32);
+        for (int nb = 0; nb < NB; ++nb) ws[nb].fetch(wa[slot][nb], c);
 #pragma unroll
         for (int mb = 0; mb < AMB; ++mb) {
           xb[slot][mb].load(xp[mb] + c * 32);
@@ -195,10 +256,13 @@ __global__ __launch_bounds__(64 * WN * WK) void gemm_kernel(Gemm P) {
         }
       };
       auto compute = [&](int slot) {
+        Frag<T> a[NB];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) a[nb] = ws[nb].frag(wa[slot][nb], bad_scale);
 #pragma unroll
         for (int mb = 0; mb < AMB; ++mb)
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) acc[nb][mb] = mma32(wa[slot][nb], xb[slot][mb], acc[nb][mb]);
+          for (int nb = 0; nb < NB; ++nb) acc[nb][mb] = mma32(a[nb], xb[slot][mb], acc[nb][mb]);
       };
 #pragma unroll
       for (int u = 0; u < U; ++u) fetch(u, u);
@@ -222,6 +286,8 @@ __global__ __launch_bounds__(64 * WN * WK) void gemm_kernel(Gemm P) {
       if constexpr (MB > 4) if (amb > 4) kloop(std::integral_constant<int, MB>{});
     }
 
+    if (bad_scale) set_error(P.err, 16);
+
     // sum the WK partial tiles into LDS in wavefront order (deterministic)
     for (int k = 0; k < WK; ++k) {
       if (wk == k) {
@@ -243,16 +309,16 @@ __global__ __launch_bounds__(64 * WN * WK) void gemm_kernel(Gemm P) {
   }
 }
 
-template <typename T, int WN, int WK, int NB, int MB, int U = Depth<T, NB, MB>::v>
+template <typename T, int WN, int WK, int NB, int MB, int U = Depth<T, NB, MB>::v, int WF = 0>
 hipError_t gemm_launch_cfg(const Gemm& g, hipStream_t s) {
   constexpr int NT = 16 * WN * NB;
   if (g.n % NT) return hipErrorInvalidValue;
   dim3 grid((g.n / NT) * g.n_groups), block(64 * WN * WK);
   switch (g.epi) {
-    case EPI_QKV: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_QKV, U>), grid, block, 0, s, g); break;
-    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_RESIDUAL, U>), grid, block, 0, s, g); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_SWIGLU, U>), grid, block, 0, s, g); break;
-    default: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_BIAS, U>), grid, block, 0, s, g); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_QKV, U, WF>), grid, block, 0, s, g); break;
+    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_RESIDUAL, U, WF>), grid, block, 0, s, g); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_SWIGLU, U, WF>), grid, block, 0, s, g); break;
+    default: hipLaunchKernelGGL((gemm_kernel<T, WN, WK, NB, MB, EPI_BIAS, U, WF>), grid, block, 0, s, g); break;
   }
   return hipGetLastError();
 }
@@ -274,9 +340,18 @@ static hipError_t gemm_dispatch(const Gemm& g, hipStream_t s) {
   return gemm_launch_cfg<T, 1, 4, 2, 8, 1>(g, s);
 }
 
+// MXFP4 expert weights (bf16 activations): the fragment ring holds raw codes
+// (2 registers per chunk), decoded to bfloat16 right before each product.
+static hipError_t gemm_dispatch_mxfp4(const Gemm& g, hipStream_t s) {
+  const int mb = (g.max_rows_per_group + 15) / 16;
+  if (g.k % 32 || !g.w_scales) return hipErrorInvalidValue;
+  if (mb <= 4) return gemm_launch_cfg<bf16, 2, 1, 2, 4, 4, 1>(g, s);
+  return gemm_launch_cfg<bf16, 2, 2, 2, 8, 2, 1>(g, s);
+}
+
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s) {
-  if (expert_fmt != 0) return hipErrorNotSupported;
   if (g.n_groups == 0 || g.n == 0) return hipSuccess;
+  if (expert_fmt != 0) return dtype == 1 ? gemm_dispatch_mxfp4(g, s) : hipErrorNotSupported;
   return dtype == 0 ? gemm_dispatch<float>(g, s) : gemm_dispatch<bf16>(g, s);
 }
 

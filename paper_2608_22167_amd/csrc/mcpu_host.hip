@@ -63,7 +63,8 @@ int check_cfg(const mcpu_layer_cfg* c) {
   if (c->window < 0) return fail(MCPU_EINVAL, "window %d", c->window);
   if (c->expert_fmt != MCPU_EXPERT_DENSE && c->expert_fmt != MCPU_EXPERT_MXFP4)
     return fail(MCPU_EINVAL, "expert_fmt %d", c->expert_fmt);
-  if (c->expert_fmt == MCPU_EXPERT_MXFP4) return fail(MCPU_EUNSUPPORTED, "MXFP4 experts are not built yet");
+  if (c->expert_fmt == MCPU_EXPERT_MXFP4 && c->dtype != MCPU_BF16)
+    return fail(MCPU_EUNSUPPORTED, "MXFP4 experts need a bf16 layer");
   if (!(c->rms_eps >= 0.f)) return fail(MCPU_EINVAL, "rms_eps");
   return MCPU_OK;
 }
@@ -200,6 +201,8 @@ int check_weights(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, bool att
   if (!w) return fail(MCPU_EINVAL, "weights is NULL");
   if (!w->g2 || !w->w_r || !w->b_r || !w->w_gu || !w->b_gu || !w->w_d || !w->b_d)
     return fail(MCPU_EINVAL, "a MoE weight pointer is NULL");
+  if (c->expert_fmt == MCPU_EXPERT_MXFP4 && (!w->s_gu || !w->s_d))
+    return fail(MCPU_EINVAL, "MXFP4 experts need the scale arrays s_gu and s_d");
   if (attn && (!w->g1 || !w->w_qkv || !w->b_qkv || !w->w_o || !w->b_o || !w->rope_cos || !w->rope_sin))
     return fail(MCPU_EINVAL, "an attention weight pointer is NULL");
   return MCPU_OK;
@@ -232,8 +235,10 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   }
 
   const int max_rows = force_idx ? T * K : T;  // a token picks each expert at most once
+  // per-expert stride: elements for dense experts, bytes of E2M1 codes for MXFP4
+  const int64_t fdiv = c->expert_fmt == MCPU_EXPERT_MXFP4 ? 2 : 1;
   Gemm g1{};
-  g1.w = w->w_gu; g1.w_group_stride = (int64_t)2 * I * H; g1.n = 2 * I; g1.k = H;
+  g1.w = w->w_gu; g1.w_scales = w->s_gu; g1.w_group_stride = (int64_t)2 * I * H / fdiv; g1.n = 2 * I; g1.k = H;
   g1.x = m.hn; g1.row_src = m.src_tok; g1.group_off = m.group_off; g1.n_groups = E;
   g1.epi = EPI_SWIGLU; g1.bias = w->b_gu; g1.bias_group_stride = 2 * I; g1.out = m.act;
   g1.swiglu_alpha = c->swiglu_alpha; g1.swiglu_limit = c->swiglu_limit; g1.swiglu_beta = c->swiglu_beta;
@@ -244,7 +249,7 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   }
 
   Gemm g2{};
-  g2.w = w->w_d; g2.w_group_stride = (int64_t)H * I; g2.n = H; g2.k = I;
+  g2.w = w->w_d; g2.w_scales = w->s_d; g2.w_group_stride = (int64_t)H * I / fdiv; g2.n = H; g2.k = I;
   g2.x = m.act; g2.group_off = m.group_off; g2.n_groups = E;
   g2.epi = EPI_BIAS; g2.bias = w->b_d; g2.bias_group_stride = H; g2.out = m.y;
   g2.err = err; g2.max_rows_per_group = max_rows;

@@ -69,6 +69,34 @@ void synth_fill_bf16(uint64_t seed, uint64_t tensor_id, uint64_t offset, int64_t
   for (int64_t j = 0; j < n; ++j) out[j] = to_bf16_rne(draw(key, offset + (uint64_t)j, c, bias));
 }
 
+/*
+ * Bulk variant for very large KV pools (indices below 2^32):
+ *   g(i) = fmix32(key32 + i * 0x9E3779B9)   (murmur3 32-bit finaliser, a bijection)
+ *   S(i) = sum of the four bytes of g(i)     (0..1020), Irwin-Hall(4)
+ *   value = fp32(fp32((float)(S - 510) * c) + bias) -> bfloat16, c = fp32(std / sqrt(21845))
+ * with key32 = low 32 bits of mix(mix(seed) ^ tensor_id).
+ */
+static inline uint32_t fmix32(uint32_t h) {
+  h ^= h >> 16;
+  h *= 0x85EBCA6Bu;
+  h ^= h >> 13;
+  h *= 0xC2B2AE35u;
+  h ^= h >> 16;
+  return h;
+}
+
+void synth_fill_fast_bf16(uint64_t seed, uint64_t tensor_id, uint32_t offset, int64_t n, float c, float bias,
+                          uint16_t* out) {
+  uint32_t key = (uint32_t)synth_stream_key(seed, tensor_id);
+#pragma omp parallel for schedule(static)
+  for (int64_t j = 0; j < n; ++j) {
+    uint32_t g = fmix32(key + (offset + (uint32_t)j) * 0x9E3779B9u);
+    int s = (int)(g & 0xFF) + (int)((g >> 8) & 0xFF) + (int)((g >> 16) & 0xFF) + (int)(g >> 24);
+    float z = (float)(s - 510) * c;
+    out[j] = to_bf16_rne(z + bias);
+  }
+}
+
 /* Uniform bytes: out[j] = low byte of h(offset + j). Used for MXFP4 codes and scales. */
 void synth_fill_u8(uint64_t seed, uint64_t tensor_id, uint64_t offset, int64_t n, uint8_t* out) {
   uint64_t key = synth_stream_key(seed, tensor_id);

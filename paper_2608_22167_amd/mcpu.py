@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libmcpu.so")
 MCPU_OK, MCPU_EINVAL, MCPU_ENOMEM, MCPU_EHIP, MCPU_EUNSUPPORTED, MCPU_EDEVICE = 0, -1, -2, -3, -4, -5
 MCPU_F32, MCPU_BF16 = 0, 1
 MCPU_EXPERT_DENSE, MCPU_EXPERT_MXFP4 = 0, 1
-DEVERR_PAGE, DEVERR_ROPE, DEVERR_EXPERT, DEVERR_PLAN = 1, 2, 4, 8
+DEVERR_PAGE, DEVERR_ROPE, DEVERR_EXPERT, DEVERR_PLAN, DEVERR_MXFP4 = 1, 2, 4, 8, 16
 
 EXPORTED = ("mcpu_last_error", "kv_pool_create", "kv_pool_destroy", "kv_pool_free_pages",
             "kv_pages_alloc", "kv_pages_free", "kv_pages_append", "paged_attention_workspace_size",
@@ -314,6 +314,48 @@ class DeviceStep:
         decode_layer(self.shape, self.weights, self.pool, self.page_table, self.seq_lens, self.cu_q,
                      self.host_seq_lens, self.host_cu_q, self.x_in, self.x_out, self.topk_idx,
                      self.topk_w, taps, self.ws, stream)
+
+    def device_errors(self) -> int:
+        return mcpu_check_device_errors(self.ws)
+
+
+class DeviceStack:
+    """A stack of decoder layers resident on the GPU (per-layer weights and KV
+    pools, one page table per attention kind), stepped by calling decode_layer
+    once per layer. The residual stream ping-pongs between two buffers so the
+    step's input x_in is left intact and the step can be re-run."""
+
+    def __init__(self, spec, device="cuda", n_layers=None):
+        from paper_2608_22167_amd import workload as W
+        self.spec = spec
+        self.n_layers = spec.n_layers if n_layers is None else n_layers
+        self.weights, self.k, self.v, self.pools = [], [], [], []
+        for i in range(self.n_layers):
+            s = spec.shape(i)
+            self.weights.append(DeviceWeights(s, W.stack_weights_device(spec, i, device), device))
+            self.k.append(W.stack_pool_device(spec, i, "k", device))
+            self.v.append(W.stack_pool_device(spec, i, "v", device))
+            self.pools.append(KVPool(s, self.k[i], self.v[i]))
+        self.pt_full = torch.from_numpy(np.ascontiguousarray(spec.page_table_full)).to(device)
+        self.pt_sw = torch.from_numpy(np.ascontiguousarray(spec.page_table_sw)).to(device)
+        self.seq_lens = torch.from_numpy(np.ascontiguousarray(spec.seq_lens)).to(device)
+        self.host_seq_lens = np.ascontiguousarray(spec.seq_lens, dtype=np.int32)
+        B, H, K = spec.batch, spec.shape_full.hidden, spec.shape_full.top_k
+        self.x_in = W.stack_x_in(spec).to(device)
+        self.buf = [torch.empty_like(self.x_in), torch.empty_like(self.x_in)]
+        self.topk_idx = torch.empty((self.n_layers, B, K), dtype=torch.int32, device=device)
+        ws = max(decode_layer_workspace_size(spec.shape(i), B, B) for i in range(min(2, self.n_layers)))
+        self.ws = workspace(ws, device)
+
+    def run(self, stream=None) -> torch.Tensor:
+        x = self.x_in
+        for i in range(self.n_layers):
+            y = self.buf[i % 2]
+            pt = self.pt_sw if self.spec.is_sw(i) else self.pt_full
+            decode_layer(self.spec.shape(i), self.weights[i], self.pools[i], pt, self.seq_lens, None,
+                         self.host_seq_lens, None, x, y, self.topk_idx[i], None, None, self.ws, stream)
+            x = y
+        return x
 
     def device_errors(self) -> int:
         return mcpu_check_device_errors(self.ws)

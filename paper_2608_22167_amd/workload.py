@@ -87,6 +87,7 @@ def _synth():
         lib.synth_fill_f32.argtypes = [u64, u64, u64, i64, f32, f32, vp]
         lib.synth_fill_bf16.argtypes = [u64, u64, u64, i64, f32, f32, vp]
         lib.synth_fill_u8.argtypes = [u64, u64, u64, i64, vp]
+        lib.synth_fill_fast_bf16.argtypes = [u64, u64, ctypes.c_uint32, i64, f32, f32, vp]
         _SYNTH = lib
     return _SYNTH
 
@@ -108,6 +109,70 @@ def synth_normal(seed: int, tid: int, shape, std: float = 1.0, mean: float = 0.0
     else:
         raise ValueError(dtype)
     return out.view(*shape)
+
+
+IH4_STD = math.sqrt(4 * (256 * 256 - 1) / 12.0)  # std of a sum of four uniform bytes
+
+
+def synth_fast_normal(seed: int, tid: int, n: int, std: float = 1.0, offset: int = 0) -> torch.Tensor:
+    """Bulk Irwin-Hall(4) bf16 values for KV pools (indices below 2^32)."""
+    out = torch.empty(n, dtype=torch.bfloat16)
+    _synth().synth_fill_fast_bf16(seed, tid, offset, n, float(np.float32(std / IH4_STD)), 0.0, out.data_ptr())
+    return out
+
+
+# --- device twin (csrc/synth_fill.hip): the same values, generated in HBM ----------
+
+_SYNTH_DEV = None
+
+
+def _synth_dev():
+    global _SYNTH_DEV
+    if _SYNTH_DEV is None:
+        path = os.path.join(_HERE, "libmcpu_synth_dev.so")
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is not built; run __graft_entry__.build()")
+        lib = ctypes.CDLL(path)
+        u64, i64, f32, vp = ctypes.c_uint64, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
+        lib.synth_fill_device_bf16.argtypes = [u64, u64, u64, i64, f32, f32, vp, vp]
+        lib.synth_fill_device_fast_bf16.argtypes = [u64, u64, ctypes.c_uint32, i64, f32, f32, vp, vp]
+        lib.synth_fill_device_u8.argtypes = [u64, u64, u64, i64, vp, vp]
+        _SYNTH_DEV = lib
+    return _SYNTH_DEV
+
+
+def _stream_ptr():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def fill_normal_device(out: torch.Tensor, seed: int, tid: int, std: float = 1.0, mean: float = 0.0,
+                       offset: int = 0) -> torch.Tensor:
+    """Device twin of synth_normal (bf16 only)."""
+    assert out.dtype == torch.bfloat16 and out.is_contiguous()
+    c = float(np.float32(std / IH_STD))
+    rc = _synth_dev().synth_fill_device_bf16(seed, tid, offset, out.numel(), c, float(np.float32(mean)),
+                                             out.data_ptr(), _stream_ptr())
+    if rc:
+        raise RuntimeError(f"device fill failed ({rc})")
+    return out
+
+
+def fill_fast_normal_device(out: torch.Tensor, seed: int, tid: int, std: float = 1.0, offset: int = 0):
+    """Device twin of synth_fast_normal."""
+    assert out.dtype == torch.bfloat16 and out.is_contiguous() and offset + out.numel() <= 2 ** 32
+    rc = _synth_dev().synth_fill_device_fast_bf16(seed, tid, offset, out.numel(), float(np.float32(std / IH4_STD)),
+                                                  0.0, out.data_ptr(), _stream_ptr())
+    if rc:
+        raise RuntimeError(f"device fill failed ({rc})")
+    return out
+
+
+def fill_bytes_device(out: torch.Tensor, seed: int, tid: int, offset: int = 0) -> torch.Tensor:
+    assert out.dtype == torch.uint8 and out.is_contiguous()
+    rc = _synth_dev().synth_fill_device_u8(seed, tid, offset, out.numel(), out.data_ptr(), _stream_ptr())
+    if rc:
+        raise RuntimeError(f"device fill failed ({rc})")
+    return out
 
 
 def synth_bytes(seed: int, tid: int, shape, offset: int = 0) -> torch.Tensor:
@@ -355,3 +420,149 @@ def restrict(wl: Workload, seqs):
 
 def custom(shape: LayerShape, ctx, q, seed, name="custom", **kw) -> Workload:
     return make_workload(name, shape, ctx, q, seed, **kw)
+
+
+# --------------------------------------------------------------------------
+# the 24-layer stack: alternating sliding-window (even layers) and full (odd)
+# attention, MXFP4 experts, 512 sequences, log-normal contexts (median 8192,
+# sigma 1, cap 65536). Large tensors are generated in HBM by the device twin
+# of the generator; the host regenerates exactly the slices it needs.
+# --------------------------------------------------------------------------
+
+
+@dataclass
+class StackSpec:
+    name: str
+    seed: int
+    n_layers: int
+    shape_full: LayerShape
+    shape_sw: LayerShape
+    seq_lens: np.ndarray
+    page_table_full: np.ndarray
+    n_pages_full: int
+    page_table_sw: np.ndarray
+    n_pages_sw: int
+    rope_max_pos: int
+
+    @property
+    def batch(self) -> int:
+        return int(self.seq_lens.shape[0])
+
+    def is_sw(self, layer: int) -> bool:
+        return layer % 2 == 0
+
+    def shape(self, layer: int) -> LayerShape:
+        return self.shape_sw if self.is_sw(layer) else self.shape_full
+
+    def page_table(self, layer: int) -> np.ndarray:
+        return self.page_table_sw if self.is_sw(layer) else self.page_table_full
+
+    def n_pages(self, layer: int) -> int:
+        return self.n_pages_sw if self.is_sw(layer) else self.n_pages_full
+
+    def tid(self, layer: int, key: str) -> int:
+        return 100 * (layer + 1) + TID[key]
+
+    def kv_bytes_read(self) -> int:
+        """K/V bytes the step's attention reads over all layers (2 KiB per visible key per layer)."""
+        s = self.shape_full
+        per_key = s.n_kv_heads * s.head_dim * 2 * 2
+        full = int((self.seq_lens.astype(np.int64) + 1).sum())
+        sw = int(np.minimum(self.seq_lens.astype(np.int64) + 1, self.shape_sw.window).sum())
+        n_full = sum(0 if self.is_sw(i) else 1 for i in range(self.n_layers))
+        return per_key * (n_full * full + (self.n_layers - n_full) * sw)
+
+
+def stack24(seed=1005, batch=512, median=8192, cap=65536, n_layers=24, slack=1.05) -> StackSpec:
+    """24-layer gpt-oss-20b-shaped stack, bf16 attention and router, MXFP4 experts."""
+    rng = np.random.default_rng(seed + 1)
+    ctx = lognormal_lengths(rng, batch, median, 1.0, cap)
+    q = np.ones(batch, dtype=np.int32)
+    full = replace(GPT_OSS_20B, expert_fmt="mxfp4")
+    sw = replace(full, window=128)
+    pt_f, np_f = _pages(ctx, q, 0, np.random.default_rng(seed + 2), slack)
+    pt_s, np_s = _pages(ctx, q, 128, np.random.default_rng(seed + 3), slack)
+    return StackSpec(name="stack%d_mxfp4_b%d_lognormal%d" % (n_layers, batch, median), seed=seed,
+                     n_layers=n_layers, shape_full=full, shape_sw=sw, seq_lens=ctx,
+                     page_table_full=pt_f, n_pages_full=np_f, page_table_sw=pt_s, n_pages_sw=np_s,
+                     rope_max_pos=int(ctx.max()) + 2)
+
+
+def stack_small_weights(spec: StackSpec, layer: int) -> Dict[str, torch.Tensor]:
+    """Gains, biases, sinks and the RoPE table of one layer (host, fp32)."""
+    s = spec.shape(layer)
+    nrm = lambda key, shp, std=0.02, mean=0.0: synth_normal(spec.seed, spec.tid(layer, key), shp, std=std, mean=mean)
+    W = dict(g1=nrm("g1", (s.hidden,), mean=1.0), b_qkv=nrm("b_qkv", (s.qkv_dim,)), b_o=nrm("b_o", (s.hidden,)),
+             g2=nrm("g2", (s.hidden,), mean=1.0), b_r=nrm("b_r", (s.n_experts,)),
+             b_gu=nrm("b_gu", (s.n_experts, 2 * s.ffn_dim)), b_d=nrm("b_d", (s.n_experts, s.hidden)),
+             sinks=nrm("sinks", (s.n_q_heads,)))
+    W["rope_cos"], W["rope_sin"] = rope_table(spec.rope_max_pos, s.head_dim)
+    return W
+
+
+def _mx_dims(s: LayerShape):
+    E, I, H = s.n_experts, s.ffn_dim, s.hidden
+    return {"w_gu": (E, 2 * I, H), "w_d": (E, H, I)}
+
+
+def stack_weights_host(spec: StackSpec, layer: int, experts=None) -> Dict[str, torch.Tensor]:
+    """All of a layer's parameters on the host. MXFP4 experts not in `experts`
+    (when given) are left zero-filled, so only the experts a sample uses are drawn."""
+    s = spec.shape(layer)
+    W = stack_small_weights(spec, layer)
+    nb = lambda key, shp: synth_normal(spec.seed, spec.tid(layer, key), shp, std=0.02, dtype=torch.bfloat16)
+    W["w_qkv"] = nb("w_qkv", (s.qkv_dim, s.hidden))
+    W["w_o"] = nb("w_o", (s.hidden, s.attn_dim))
+    W["w_r"] = nb("w_r", (s.n_experts, s.hidden))
+    if experts is not None and len(experts) == 0:
+        return W  # no expert tensors wanted
+    for key, (E, rows, cols) in _mx_dims(s).items():
+        codes = torch.zeros((E, rows, cols // 2), dtype=torch.uint8)
+        scales = torch.zeros((E, rows, cols // 32), dtype=torch.uint8)
+        for e in (range(E) if experts is None else experts):
+            codes[e] = synth_bytes(spec.seed, spec.tid(layer, key + "_codes"), (rows, cols // 2),
+                                   offset=e * rows * (cols // 2))
+            raw = synth_bytes(spec.seed, spec.tid(layer, key + "_scales"), (rows, cols // 32),
+                              offset=e * rows * (cols // 32))
+            scales[e] = 117 + raw % 3
+        W[key + "_codes"], W[key + "_scales"] = codes, scales
+    return W
+
+
+def stack_weights_device(spec: StackSpec, layer: int, device="cuda") -> Dict[str, torch.Tensor]:
+    """The same parameters generated in HBM (the large tensors never touch the host)."""
+    s = spec.shape(layer)
+    W = {k: v.to(device) for k, v in stack_small_weights(spec, layer).items()}
+    for key, shp in (("w_qkv", (s.qkv_dim, s.hidden)), ("w_o", (s.hidden, s.attn_dim)),
+                     ("w_r", (s.n_experts, s.hidden))):
+        W[key] = fill_normal_device(torch.empty(shp, dtype=torch.bfloat16, device=device), spec.seed,
+                                    spec.tid(layer, key), std=0.02)
+    for key, (E, rows, cols) in _mx_dims(s).items():
+        W[key + "_codes"] = fill_bytes_device(torch.empty((E, rows, cols // 2), dtype=torch.uint8, device=device),
+                                              spec.seed, spec.tid(layer, key + "_codes"))
+        raw = fill_bytes_device(torch.empty((E, rows, cols // 32), dtype=torch.uint8, device=device), spec.seed,
+                                spec.tid(layer, key + "_scales"))
+        W[key + "_scales"] = (117 + raw % 3).to(torch.uint8)
+    return W
+
+
+def stack_pool_device(spec: StackSpec, layer: int, which: str, device="cuda") -> torch.Tensor:
+    """K or V pool of one layer, [n_pages, Hkv, 16, d] bf16, bulk generator, N(0, 1)."""
+    s = spec.shape(layer)
+    pool = torch.empty((spec.n_pages(layer), s.n_kv_heads, PAGE, s.head_dim), dtype=torch.bfloat16, device=device)
+    return fill_fast_normal_device(pool.view(-1), spec.seed, spec.tid(layer, which + "_pool")).view(pool.shape)
+
+
+def stack_pages_host(spec: StackSpec, layer: int, which: str, pages) -> torch.Tensor:
+    """The listed pages of a layer's K or V pool, regenerated on the host."""
+    s = spec.shape(layer)
+    per = s.n_kv_heads * PAGE * s.head_dim
+    out = torch.empty((len(pages), s.n_kv_heads, PAGE, s.head_dim), dtype=torch.bfloat16)
+    for i, p in enumerate(pages):
+        out[i] = synth_fast_normal(spec.seed, spec.tid(layer, which + "_pool"), per, offset=int(p) * per).view(
+            s.n_kv_heads, PAGE, s.head_dim)
+    return out
+
+
+def stack_x_in(spec: StackSpec) -> torch.Tensor:
+    return synth_normal(spec.seed, TID["x_in"], (spec.batch, spec.shape_full.hidden))

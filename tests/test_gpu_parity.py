@@ -295,3 +295,35 @@ def test_full_size_sampled(which):
     # every token: finite output and weights summing to one
     assert np.isfinite(gpu["out"]).all()
     np.testing.assert_allclose(gpu["w"].sum(1), 1.0, rtol=1e-5)
+
+
+# ---------------------------------------------------------------------------------- MXFP4 experts
+
+
+def _mxfp4_shape(small=True):
+    if small:
+        return replace(W.GPT_OSS_20B, hidden=256, n_q_heads=8, n_kv_heads=2, head_dim=64, n_experts=8,
+                       top_k=2, ffn_dim=256, expert_fmt="mxfp4")
+    return replace(W.GPT_OSS_20B, expert_fmt="mxfp4")
+
+
+@pytest.mark.parametrize("small", [True, False])
+def test_mxfp4_experts_layer(small):
+    shape = _mxfp4_shape(small)
+    ctx = [0, 15, 16, 200, 1100] if small else [3, 129, 700, 2049]
+    wl = W.custom(shape, ctx, np.ones(len(ctx)), 1061, sink_std=0.5)
+    gpu, step = run_layer(wl)
+    compare_layer(wl, gpu, step)
+
+
+def test_mxfp4_bad_scale_sets_device_error():
+    shape = _mxfp4_shape(True)
+    wl = W.custom(shape, [10, 20], np.ones(2), 1062)
+    wl.weights["w_gu_scales"] = wl.weights["w_gu_scales"].clone()
+    wl.weights["w_gu_scales"][:, 0, 0] = 255  # NaN scale in every expert's first row
+    dw = mcpu.DeviceWeights(shape, wl.weights)
+    h = W.synth_normal(3, 4, (2, shape.hidden)).cuda()
+    out = torch.empty_like(h)
+    ws = mcpu.workspace(mcpu.moe_forward_workspace_size(shape, 2))
+    mcpu.moe_forward(shape, dw, h, out, None, None, None, ws)
+    assert mcpu.mcpu_check_device_errors(ws) & mcpu.DEVERR_MXFP4
