@@ -3,13 +3,23 @@
 Each sampled sequence is independent of the others given its own cache pages,
 so the reference restricts the step to the sample: it regenerates on the host
 exactly the pages those sequences read (the generator is counter based) and
-chains the per-layer reference from the step's input through every layer.
-Each layer is evaluated twice: once to learn the routing (which does not
-depend on the expert weights), then, after drawing and dequantising only the
-experts that routing uses, with that selection forced. Wherever the
-reference's k-th and (k+1)-th fp32 router logits lie within 1e-3 of each other,
-the selection of the GPU run (if given) is used instead, because both sets are
-then correct; everywhere else the two selections must agree exactly.
+evaluates the per-layer reference layer by layer. Each layer is evaluated
+twice: once to learn the routing (which does not depend on the expert
+weights), then, after drawing and dequantising only the experts that routing
+uses, with that selection forced.
+
+Three ways to chain the layers:
+  free running      the reference's own output feeds the next layer; wherever
+                    its k-th and (k+1)-th fp32 router logits lie within 1e-3,
+                    the GPU's selection (if given) is used, since both are then
+                    correct; elsewhere the selections must agree exactly;
+  teacher forced    every layer takes the GPU's own input to that layer
+                    (`inputs`), so each layer is checked at the single-layer
+                    bar however deep it sits;
+  following the GPU the reference adopts the GPU's selection at every layer
+                    (`follow_gpu`), which isolates the numerical drift of a
+                    deep chain once teacher forcing has shown every selection
+                    correct.
 """
 from __future__ import annotations
 
@@ -26,20 +36,28 @@ def _near_ties(logits, k):
     return (lf[:, k - 1] - lf[:, k]).astype(np.float64) <= TIE_GAP
 
 
-def reference_stack(spec, seqs, n_layers=None, gpu_idx=None):
-    """Returns (final residual [n, H] float64, per-layer dict(idx, ties, mismatch))."""
+def reference_stack(spec, seqs, n_layers=None, gpu_idx=None, inputs=None, follow_gpu=False):
+    """seqs: sampled sequence ids; gpu_idx: [L][B][k] selections of the GPU run;
+    inputs: per-layer input rows [n, H] of the sampled sequences (teacher forcing).
+    Returns (final residual [n, H] float64, per-layer dicts with the layer's
+    output `out`, selection `idx`, near-tie mask `ties` and `mismatch`, the rows
+    whose GPU selection differs from the reference's outside a near tie)."""
     from paper_2608_22167_amd import workload as W
     seqs = np.asarray(sorted(int(s) for s in seqs))
     L = spec.n_layers if n_layers is None else n_layers
+    if follow_gpu and gpu_idx is None:
+        raise ValueError("follow_gpu needs the GPU's selections")
     x = W.stack_x_in(spec)[torch.from_numpy(seqs)].double().numpy()
     info = []
     s0 = spec.shape(0)
     E, I, H = s0.n_experts, s0.ffn_dim, s0.hidden
-    # dense fp32 expert arrays reused by every layer: pass A never reads them,
-    # pass B reads only the experts re-drawn for the current layer
+    # dense fp32 expert arrays reused by every layer: the routing pass never
+    # reads them, the second pass reads only the experts re-drawn for the layer
     w_gu = np.zeros((E, 2 * I, H), np.float32)
     w_d = np.zeros((E, H, I), np.float32)
     for layer in range(L):
+        if inputs is not None:
+            x = np.asarray(inputs[layer], np.float64)
         s = spec.shape(layer)
         pt = spec.page_table(layer)[seqs]
         used = np.unique(pt[pt >= 0])
@@ -55,15 +73,18 @@ def reference_stack(spec, seqs, n_layers=None, gpu_idx=None):
         sub.v_pool = W.stack_pages_host(spec, layer, "v", used)
         sub.x_in = torch.from_numpy(x)
         weights = O.Weights(s, Wd)
-        # pass A: routing only (expert weights still zero)
-        ra = O.decode_layer(sub, weights)
-        sel = ra["idx"].copy()
-        ties = _near_ties(ra["logits"], s.top_k)
-        mismatch = np.zeros(len(seqs), bool)
-        if gpu_idx is not None:
-            g = np.asarray(gpu_idx[layer])[seqs]
-            mismatch = (~ties) & (np.sort(g, 1) != np.sort(sel, 1)).any(1)
-            sel[ties] = g[ties]
+        g = None if gpu_idx is None else np.asarray(gpu_idx[layer])[seqs]
+        if follow_gpu:
+            sel, ties, mismatch = g.copy(), np.zeros(len(seqs), bool), np.zeros(len(seqs), bool)
+        else:
+            # routing pass (expert weights are still zero)
+            ra = O.decode_layer(sub, weights)
+            sel = ra["idx"].copy()
+            ties = _near_ties(ra["logits"], s.top_k)
+            mismatch = np.zeros(len(seqs), bool)
+            if g is not None:
+                mismatch = (~ties) & (np.sort(g, 1) != np.sort(sel, 1)).any(1)
+                sel[ties] = g[ties]
         # draw and dequantise only the experts the sample uses
         for e in np.unique(sel):
             e = int(e)
@@ -74,6 +95,6 @@ def reference_stack(spec, seqs, n_layers=None, gpu_idx=None):
                                     offset=e * rows * (cols // 32))
                 O.mxfp4_dequant(codes, 117 + raw % 3, rows, cols, out=arr[e])
         rb = O.decode_layer(sub, weights, force_idx=sel)
-        info.append(dict(idx=sel, ties=ties, mismatch=mismatch))
         x = rb["out"]
+        info.append(dict(out=x, idx=sel, ties=ties, mismatch=mismatch))
     return x, info

@@ -347,15 +347,21 @@ class DeviceStack:
         ws = max(decode_layer_workspace_size(spec.shape(i), B, B) for i in range(min(2, self.n_layers)))
         self.ws = workspace(ws, device)
 
-    def run(self, stream=None) -> torch.Tensor:
+    def run(self, stream=None, capture_rows=None):
+        """One step through every layer; returns the final residual stream. With
+        `capture_rows` (a device index tensor) it also returns the residual rows
+        entering each layer plus the final ones (n_layers + 1 tensors)."""
         x = self.x_in
+        caps = None if capture_rows is None else [x.index_select(0, capture_rows)]
         for i in range(self.n_layers):
             y = self.buf[i % 2]
             pt = self.pt_sw if self.spec.is_sw(i) else self.pt_full
             decode_layer(self.spec.shape(i), self.weights[i], self.pools[i], pt, self.seq_lens, None,
                          self.host_seq_lens, None, x, y, self.topk_idx[i], None, None, self.ws, stream)
+            if caps is not None:
+                caps.append(y.index_select(0, capture_rows))
             x = y
-        return x
+        return x if caps is None else (x, caps)
 
     def device_errors(self) -> int:
         return mcpu_check_device_errors(self.ws)

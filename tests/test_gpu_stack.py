@@ -65,31 +65,52 @@ def _sample(spec, extra, seed):
     return sorted(pick)
 
 
-def _run_and_compare(spec, n_layers, seqs):
+def _run(spec, n_layers, seqs):
     st = mcpu.DeviceStack(spec, n_layers=n_layers)
-    out = st.run()
+    rows = torch.tensor(seqs, device="cuda")
+    out, caps = st.run(capture_rows=rows)
     torch.cuda.synchronize()
     assert st.device_errors() == 0
-    got = out[torch.tensor(seqs, device="cuda")].double().cpu().numpy()
+    xs = [c.double().cpu().numpy() for c in caps]
     idx = st.topk_idx.cpu().numpy()
     again = st.run()
     torch.cuda.synchronize()
     assert torch.equal(out, again), "stack step is not repeatable"
-    del st, out, again
+    del st, out, again, caps
     torch.cuda.empty_cache()
-    ref, info = OS.reference_stack(spec, seqs, n_layers=n_layers, gpu_idx=idx)
+    return xs, idx
+
+
+def _no_mismatch(info):
     for layer, d in enumerate(info):
-        assert not d["mismatch"].any(), f"layer {layer}: router sets differ at sampled rows {np.nonzero(d['mismatch'])[0]}"
-    return PT.check(f"stack{n_layers}", got, ref, "bf16", scale=n_layers)
+        assert not d["mismatch"].any(), \
+            f"layer {layer}: router sets differ at sampled rows {np.nonzero(d['mismatch'])[0]}"
 
 
 def test_stack_depth4_small_batch():
+    """Free-running chain: the reference's own output feeds its next layer."""
     spec = W.stack24(seed=1006, batch=16, median=1024, cap=8192, n_layers=4)
-    _run_and_compare(spec, 4, _sample(spec, 4, 11))
+    seqs = _sample(spec, 4, 11)
+    xs, idx = _run(spec, 4, seqs)
+    ref, info = OS.reference_stack(spec, seqs, n_layers=4, gpu_idx=idx)
+    _no_mismatch(info)
+    PT.check("stack4", xs[-1], ref, "bf16", scale=4)
 
 
 @pytest.mark.timeout(900)
 def test_stack24_full_size_sampled():
-    """The 24-layer, 512-sequence stack the benchmark times, on sampled sequences."""
+    """The 24-layer, 512-sequence stack the benchmark times, on sampled sequences.
+
+    Teacher forced: every layer, given the GPU's own input to it, matches the
+    reference at the single-layer bar, routing included. Then the reference
+    chain that follows the GPU's (thereby validated) routing bounds the
+    accumulated drift of the whole stack at 24 times that bar."""
     spec = W.stack24()
-    _run_and_compare(spec, spec.n_layers, _sample(spec, 1, 12))
+    seqs = _sample(spec, 1, 12)
+    xs, idx = _run(spec, spec.n_layers, seqs)
+    _, info = OS.reference_stack(spec, seqs, gpu_idx=idx, inputs=xs[:-1])
+    _no_mismatch(info)
+    for layer, d in enumerate(info):
+        PT.check(f"layer {layer}", xs[layer + 1], d["out"], "bf16")
+    ref, _ = OS.reference_stack(spec, seqs, gpu_idx=idx, follow_gpu=True)
+    PT.check("stack24", xs[-1], ref, "bf16", scale=spec.n_layers)
