@@ -15,7 +15,10 @@ HIP_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I" + os.path.join(ROOT, "include"),
 ]
-SOURCES = ["attention.hip", "gemm.hip", "moe.hip", "mcpu_host.hip"]
+SOURCES = ["attention.hip", "gemm.hip", "gemm_tiled.hip", "moe.hip", "mcpu_host.hip"]
+# per-source code generation: the tiled GEMM keeps its matrix-core accumulators
+# in ordinary VGPRs (the AGPR form shuffles them between loop iterations)
+SOURCE_FLAGS = {"gemm_tiled.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def _run(cmd):
@@ -39,7 +42,7 @@ def build_hip(jobs: int = 4) -> str:
 
     def one(src):
         obj = os.path.join(BUILD, src.replace(".hip", ".o"))
-        _run([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        _run([HIPCC, *HIP_FLAGS, *SOURCE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj])
         return obj
 
     with ThreadPoolExecutor(jobs) as ex:

@@ -18,108 +18,10 @@
 // Token rows may be gathered through row_src (the expert-sorted order), so the
 // permuted activations are never materialised.
 #include "device.h"
+#include "gemm_epilogue.h"
 #include "kernels.h"
 
 namespace mcpu {
-
-// W row (output feature) that lane-row nl of 16-row block `blk` multiplies. For
-// the QKV projection a block holds dims 8t..8t+7 and d/2+8t..d/2+8t+7 of one
-// head, so both members of every rotary pair land in the same block.
-template <int EPI>
-__device__ __forceinline__ int block_row(const Gemm& P, int blk, int nl) {
-  if (EPI == EPI_QKV) {
-    const int D = P.head_dim, tph = D / 16;
-    const int head = blk / tph, ti = blk - head * tph;
-    return head * D + (nl < 8 ? 8 * ti + nl : D / 2 + 8 * ti + nl - 8);
-  }
-  return blk * 16 + nl;
-}
-
-__device__ __forceinline__ float swiglu(float gate, float up, float alpha, float limit, float beta) {
-  gate = fminf(gate, limit);
-  up = fminf(fmaxf(up, -limit), limit);
-  return gate / (1.0f + expf(-alpha * gate)) * (up + beta);
-}
-
-// cr[m * ld + n]: the finished fp32 tile for token rows m0 .. m0 + mrows - 1 and
-// the nblk 16-row weight blocks starting at blk0.
-template <typename T, int EPI>
-__device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mrows, int blk0, int nblk,
-                         int grp) {
-  const int tid = threadIdx.x, nt = blockDim.x;
-  const float* bias = P.bias + (int64_t)grp * P.bias_group_stride;
-  if constexpr (EPI == EPI_QKV) {
-    const int D = P.head_dim, tph = D / 16, half = D / 2;
-    for (int idx = tid; idx < mrows * nblk * 8; idx += nt) {
-      const int i = idx & 7, b = (idx >> 3) % nblk, m = (idx >> 3) / nblk, t = m0 + m;
-      const int blk = blk0 + b, head = blk / tph, ti = blk - head * tph;
-      const int j = 8 * ti + i;  // dim within the head, < D/2
-      const int f_lo = head * D + j, f_hi = f_lo + half;
-      float lo = cr[m * ld + 16 * b + i] + bias[f_lo];
-      float hi = cr[m * ld + 16 * b + 8 + i] + bias[f_hi];
-      const int pos = P.tok_pos[t];
-      if (head < P.hq + P.hkv) {  // q or k: rotate the pair (j, j + d/2)
-        if (pos < 0 || pos >= P.rope_max_pos) {
-          set_error(P.err, 2);
-          continue;
-        }
-        const float c = P.rope_cos[(int64_t)pos * half + j], s = P.rope_sin[(int64_t)pos * half + j];
-        const float a = lo, bb = hi;
-        lo = a * c - bb * s;
-        hi = a * s + bb * c;
-      }
-      if (head < P.hq) {
-        T* q = reinterpret_cast<T*>(P.q_out) + ((int64_t)t * P.hq + head) * D;
-        Elem<T>::store(q, j, lo);
-        Elem<T>::store(q, j + half, hi);
-        continue;
-      }
-      const int lp = pos >> 4;
-      const int seq = P.tok_seq[t];
-      const int page = (pos >= 0 && lp < P.max_pages) ? P.page_table[(int64_t)seq * P.max_pages + lp] : -1;
-      if (page < 0 || page >= P.n_pages) {
-        set_error(P.err, 1);
-        continue;
-      }
-      const int slot = pos & 15;
-      if (head < P.hq + P.hkv) {
-        T* kp = reinterpret_cast<T*>(P.k_pool) + ((int64_t)page * P.hkv + (head - P.hq)) * PAGE * D;
-        Elem<T>::store(kp, k_off(slot, j), lo);
-        Elem<T>::store(kp, k_off(slot, j + half), hi);
-      } else {
-        T* vp = reinterpret_cast<T*>(P.v_pool) + ((int64_t)page * P.hkv + (head - P.hq - P.hkv)) * PAGE * D;
-        Elem<T>::store(vp, v_off(slot, j), lo);
-        Elem<T>::store(vp, v_off(slot, j + half), hi);
-      }
-    }
-  } else if constexpr (EPI == EPI_SWIGLU) {
-    T* out = reinterpret_cast<T*>(P.out);
-    const int half_n = P.n / 2;
-    for (int idx = tid; idx < mrows * nblk * 8; idx += nt) {
-      const int j = idx & 7, b = (idx >> 3) % nblk, m = (idx >> 3) / nblk;
-      const int col = (blk0 + b) * 16 + 2 * j;
-      const float gate = cr[m * ld + 16 * b + 2 * j] + bias[col];
-      const float up = cr[m * ld + 16 * b + 2 * j + 1] + bias[col + 1];
-      Elem<T>::store(out, (int64_t)(m0 + m) * half_n + (blk0 + b) * 8 + j,
-                     swiglu(gate, up, P.swiglu_alpha, P.swiglu_limit, P.swiglu_beta));
-    }
-  } else {  // EPI_RESIDUAL, EPI_BIAS: fp32 rows, 4 consecutive features per thread
-    float* out = reinterpret_cast<float*>(P.out);
-    const int nq = nblk * 4;
-    for (int idx = tid; idx < mrows * nq; idx += nt) {
-      const int q = idx % nq, m = idx / nq;
-      const int n = blk0 * 16 + 4 * q;
-      const int64_t o = (int64_t)(m0 + m) * P.n + n;
-      float4 v = make_float4(cr[m * ld + 4 * q] + bias[n], cr[m * ld + 4 * q + 1] + bias[n + 1],
-                             cr[m * ld + 4 * q + 2] + bias[n + 2], cr[m * ld + 4 * q + 3] + bias[n + 3]);
-      if constexpr (EPI == EPI_RESIDUAL) {
-        const float4 r = *reinterpret_cast<const float4*>(P.residual + o);
-        v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
-      }
-      *reinterpret_cast<float4*>(out + o) = v;
-    }
-  }
-}
 
 // ---------------------------------------------------------------------------
 // weight sources: where a lane's 8 weights of a 32-wide chunk come from
@@ -351,6 +253,7 @@ static hipError_t gemm_dispatch_mxfp4(const Gemm& g, hipStream_t s) {
 
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s) {
   if (g.n_groups == 0 || g.n == 0) return hipSuccess;
+  if (tiled_gemm_applies(dtype, g)) return launch_gemm_tiled(expert_fmt, g, s);
   if (expert_fmt != 0) return dtype == 1 ? gemm_dispatch_mxfp4(g, s) : hipErrorNotSupported;
   return dtype == 0 ? gemm_dispatch<float>(g, s) : gemm_dispatch<bf16>(g, s);
 }

@@ -1,0 +1,345 @@
+// LDS-tiled grouped GEMM for many token rows per weight matrix (gfx950, bf16).
+//
+// Once a weight matrix meets tens of token rows or more, streaming it through
+// every wavefront (gemm.hip) re-reads the activations from L2 once per weight
+// slab and runs out of matrix-core work per byte. Here a workgroup of four
+// wavefronts owns one BM x BN output tile: token rows m0 .. m0 + BM - 1 of one
+// group against weight rows n0 .. n0 + BN - 1 of that group's matrix. Per
+// 64-wide slice of the reduction the workgroup stages the BM activation rows
+// (gathered through row_src) and the BN weight rows in LDS, double buffered,
+// and each wavefront multiplies a (BM/2) x (BN/2) quadrant out of LDS with the
+// 16x16x32 bf16 matrix-core product while the next R slices are in flight
+// in a ring of R register sets (deep rings for weight-streaming shapes, whose
+// time goes into HBM latency). MXFP4 weights are decoded once, while they are staged, with the
+// packed e2m1 -> bf16 conversion that applies the block scale (exact: every
+// product of an e2m1 value and a scale in [2^-125, 2^125] is a normal
+// bfloat16).
+//
+// Work items are (m-tile, n-tile) pairs over all groups; the per-group m-tile
+// counts come from group_off on the device, so the host only bounds the grid.
+// Within a group the items go in bands of GM m-tiles: a band walks the
+// n-tiles, and each n-tile visits the band's m-tiles back to back, so a weight
+// tile is fetched once per band and the band's activation tiles stay in L2.
+// The item sequence is cut into eight contiguous ranges, one per XCD
+// (workgroups are dealt to the XCDs round robin), so that reuse happens within
+// one XCD's L2. The finished fp32 tile goes through LDS to the fused epilogue.
+#include "device.h"
+#include "gemm_epilogue.h"
+#include "kernels.h"
+
+namespace mcpu {
+
+constexpr int TBK = 64;        // reduction slice per stage
+constexpr int TLDK = TBK + 8;  // LDS row stride in bf16: rows 144 B apart spread fragment reads over all banks
+constexpr int TMAXG = 256;     // groups (experts) one launch supports
+
+// 16-byte staging registers as a native vector type: copies of HIP's uint4
+// struct become memcpy calls that keep the register sets in scratch memory.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+
+template <int BM, int BN>
+struct TiledSmem {
+  static constexpr int stage = (BM + BN) * TLDK;  // bf16 elements per stage
+  static constexpr int ab_bytes = 2 * stage * 2;
+  static constexpr int c_ld = BN + 4;             // fp32 tile row stride
+  static constexpr int c_bytes = BM * c_ld * 4;
+  static constexpr int bytes = ab_bytes > c_bytes ? ab_bytes : c_bytes;
+};
+
+// Staged weight rows: dense bf16 (16-byte chunks, 8 per row and slice) ...
+template <int BN, int WF>
+struct TiledW {
+  static constexpr int J = BN / 32;
+  struct Regs {
+    u32x4 r[J];
+  };
+  const bf16* src[J];
+  static __device__ __forceinline__ int row(int tid, int j) { return (tid >> 3) + 32 * j; }
+  __device__ __forceinline__ void init(const Gemm& P, int grp, const int* wrow, int tid) {
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+      src[j] = reinterpret_cast<const bf16*>(P.w) + grp * P.w_group_stride + (int64_t)wrow[j] * P.k + (tid & 7) * 8;
+  }
+  __device__ __forceinline__ void fetch(Regs& g, int ks) const {
+#pragma unroll
+    for (int j = 0; j < J; ++j) g.r[j] = ld16(src[j] + ks * TBK);
+  }
+  static __device__ __forceinline__ void store(const Regs& g, bf16* ws, int tid, bool&) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) st16(ws + row(tid, j) * TLDK + (tid & 7) * 8, g.r[j]);
+  }
+};
+
+// ... or MXFP4: per row and slice 32 code bytes (two scale blocks) and two
+// E8M0 scales; a thread stages one block of 32 weights per chunk.
+template <int BN>
+struct TiledW<BN, 1> {
+  static constexpr int J = BN / 128;
+  struct Regs {
+    u32x4 r[J];
+    uint32_t s[J];
+  };
+  const uint8_t* csrc[J];
+  const uint8_t* ssrc[J];
+  static __device__ __forceinline__ int row(int tid, int j) { return (tid + 256 * j) >> 1; }
+  __device__ __forceinline__ void init(const Gemm& P, int grp, const int* wrow, int tid) {
+    const int half = tid & 1;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      csrc[j] = reinterpret_cast<const uint8_t*>(P.w) + grp * P.w_group_stride + (int64_t)wrow[j] * (P.k / 2) +
+                16 * half;
+      ssrc[j] = P.w_scales + grp * (P.w_group_stride / 16) + (int64_t)wrow[j] * (P.k / 32) + half;
+    }
+  }
+  __device__ __forceinline__ void fetch(Regs& g, int ks) const {
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      g.r[j] = ld16(csrc[j] + ks * (TBK / 2));
+      g.s[j] = ssrc[j][ks * (TBK / 32)];
+    }
+  }
+  static __device__ __forceinline__ void store(const Regs& g, bf16* ws, int tid, bool& bad) {
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const bool ok = g.s[j] >= 2u && g.s[j] <= 252u;
+      bad = bad || !ok;
+      const float scale = __uint_as_float(ok ? g.s[j] << 23 : 127u << 23);
+      const uint32_t w4[4] = {ok ? g.r[j][0] : 0u, ok ? g.r[j][1] : 0u, ok ? g.r[j][2] : 0u, ok ? g.r[j][3] : 0u};
+      uint32_t o[16];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        // byte b of word i holds weights 8i + 2b (low nibble) and 8i + 2b + 1
+        o[4 * i + 0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w4[i], scale, 0));
+        o[4 * i + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w4[i], scale, 1));
+        o[4 * i + 2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w4[i], scale, 2));
+        o[4 * i + 3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w4[i], scale, 3));
+      }
+      bf16* d = ws + row(tid, j) * TLDK + 32 * (tid & 1);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) st16(d + 8 * q, u32x4{o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]});
+    }
+  }
+};
+
+// Position of local item L of a group with mt_g m-tiles and n_tn n-tiles, in
+// bands of GM m-tiles (the last band may be shorter).
+template <int GM>
+__device__ __forceinline__ void band_order(int L, int mt_g, int n_tn, int& mt, int& tn) {
+  const int full = mt_g / GM;
+  if (L < full * GM * n_tn) {
+    const int b = L / (GM * n_tn), r = L - b * (GM * n_tn);
+    tn = r / GM;
+    mt = b * GM + (r - tn * GM);
+  } else {
+    const int rem = mt_g - full * GM, r = L - full * GM * n_tn;
+    tn = r / rem;
+    mt = full * GM + (r - tn * rem);
+  }
+}
+
+template <int BM, int BN, int R, int EPI, int WF>
+__global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
+  static_assert(R % 2 == 0, "the unrolled ring must cover both LDS buffers");
+  using S = TiledSmem<BM, BN>;
+  constexpr int GM = BM == 64 ? 8 : 4;  // m-tiles per band: about 3 MB of activations
+  __shared__ __align__(16) unsigned char smem_raw[S::bytes];
+  __shared__ int mt_start[TMAXG + 1];
+  bf16* smem = reinterpret_cast<bf16*>(smem_raw);
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  const int G = P.n_groups;
+
+  // exclusive prefix of m-tiles per group (one wavefront, 64 groups per pass)
+  if (wave == 0) {
+    int carry = 0;
+    for (int g0 = 0; g0 < G; g0 += 64) {
+      const int g = g0 + lane;
+      int cnt = 0;
+      if (g < G) {
+        const int r0 = P.group_off ? P.group_off[g] : 0;
+        const int r1 = P.group_off ? P.group_off[g + 1] : P.n_rows;
+        cnt = (max(r1 - r0, 0) + BM - 1) / BM;
+      }
+      const int incl = wave_incl_scan(cnt);
+      if (g < G) mt_start[g] = carry + incl - cnt;
+      carry += __shfl(incl, 63, 64);
+    }
+    if (lane == 0) mt_start[G] = carry;
+  }
+  __syncthreads();
+
+  const int n_tn = (P.n + BN - 1) / BN;
+  const int total = mt_start[G] * n_tn;
+  const int chunk = (total + 7) >> 3;
+  const int local = blockIdx.x >> 3;
+  const int item = (blockIdx.x & 7) * chunk + local;
+  if (local >= chunk || item >= total) return;
+  // group of the item: last g with mt_start[g] * n_tn <= item (each group owns mt_g * n_tn items)
+  int lo = 0, hi = G - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (mt_start[mid] * n_tn <= item) lo = mid; else hi = mid - 1;
+  }
+  const int grp = uniform(lo);
+  int mt, tn;
+  band_order<GM>(item - mt_start[grp] * n_tn, mt_start[grp + 1] - mt_start[grp], n_tn, mt, tn);
+  const int gr0 = P.group_off ? P.group_off[grp] : 0;
+  const int gr1 = P.group_off ? P.group_off[grp + 1] : P.n_rows;
+  const int m0 = uniform(gr0 + mt * BM);
+  const int mrows = min(BM, gr1 - m0);
+  const int n0 = uniform(tn * BN), nrows = min(BN, P.n - n0);
+
+  // activation rows this thread stages: (tid >> 3) + 32 j, chunk tid & 7;
+  // rows past the tile's end repeat its last row (their results are dropped)
+  constexpr int XJ = BM / 32;
+  const bf16* xsrc[XJ];
+#pragma unroll
+  for (int j = 0; j < XJ; ++j) {
+    const int row = m0 + min((tid >> 3) + 32 * j, mrows - 1);
+    const int src = P.row_src ? P.row_src[row] : row;
+    xsrc[j] = reinterpret_cast<const bf16*>(P.x) + (int64_t)src * P.k + (tid & 7) * 8;
+  }
+  using WL = TiledW<BN, WF>;
+  WL wl;
+  {
+    int wrow[WL::J];
+#pragma unroll
+    for (int j = 0; j < WL::J; ++j) {
+      const int rr = min(WL::row(tid, j), nrows - 1);
+      wrow[j] = block_row<EPI>(P, (n0 + rr) >> 4, rr & 15);
+    }
+    wl.init(P, grp, wrow, tid);
+  }
+  struct Regs {
+    u32x4 x[XJ];
+    typename WL::Regs w;
+  };
+  const int nk = P.k / TBK;
+  // slices past the end re-read the last one (branch-free; never staged for use)
+  auto fetch = [&](Regs& g, int ks) __attribute__((always_inline)) {
+    ks = min(ks, nk - 1);
+#pragma unroll
+    for (int j = 0; j < XJ; ++j) g.x[j] = ld16(xsrc[j] + ks * TBK);
+    wl.fetch(g.w, ks);
+  };
+  bool bad_scale = false;
+  auto stage = [&](const Regs& g, int buf) __attribute__((always_inline)) {
+    bf16* xs = smem + buf * S::stage;
+#pragma unroll
+    for (int j = 0; j < XJ; ++j)
+      st16(xs + ((tid >> 3) + 32 * j) * TLDK + (tid & 7) * 8, g.x[j]);
+    WL::store(g.w, xs + BM * TLDK, tid, bad_scale);
+  };
+
+  const int wm = wave & 1, wn = wave >> 1;
+  constexpr int MT = BM / 32, NT = BN / 32;  // 16-row tiles per wavefront quadrant
+  f32x4 acc[NT][MT];
+#pragma unroll
+  for (int nb = 0; nb < NT; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MT; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int fr = lane & 15, fk = 8 * (lane >> 4);
+  auto compute = [&](int buf) __attribute__((always_inline)) {
+    const bf16* xs = smem + buf * S::stage + (wm * (BM / 2) + fr) * TLDK + fk;
+    const bf16* ws = smem + buf * S::stage + (BM + wn * (BN / 2) + fr) * TLDK + fk;
+#pragma unroll
+    for (int c = 0; c < TBK / 32; ++c) {
+      Frag<bf16> a[NT], b[MT];
+#pragma unroll
+      for (int nb = 0; nb < NT; ++nb) a[nb].load(ws + nb * 16 * TLDK + 32 * c);
+#pragma unroll
+      for (int mb = 0; mb < MT; ++mb) b[mb].load(xs + mb * 16 * TLDK + 32 * c);
+#pragma unroll
+      for (int nb = 0; nb < NT; ++nb)
+#pragma unroll
+        for (int mb = 0; mb < MT; ++mb) acc[nb][mb] = mma32(a[nb], b[mb], acc[nb][mb]);
+    }
+  };
+
+  // Slice j is loaded into register set j % R and staged into LDS buffer j & 1.
+  // While slice ks is multiplied out of LDS, slices ks + 1 .. ks + R are in
+  // flight; afterwards slice ks + 1 is staged and its set refilled with slice
+  // ks + 1 + R. The loop is unrolled R times so every set index is a
+  // constant, and only the products are conditional (past the last slice the
+  // loads are clamped and the staged copies never read), so the wait counts
+  // at the loop head see one load order on every path. The scheduling
+  // barriers keep the loads ahead of the products and the LDS writes, which
+  // wait for their loads, behind them.
+  Regs rs[R];
+#pragma unroll
+  for (int u = 0; u < R; ++u) {
+    fetch(rs[u], u);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  stage(rs[0], 0);
+  fetch(rs[0], R);
+  __builtin_amdgcn_sched_barrier(0);
+  __syncthreads();
+  for (int ks = 0; ks < nk; ks += R) {
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      if (ks + u < nk) compute(u & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      stage(rs[(u + 1) % R], (u + 1) & 1);
+      fetch(rs[(u + 1) % R], ks + u + 1 + R);
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+    }
+  }
+  __syncthreads();  // the fp32 tile below reuses the operand buffers
+  if (bad_scale) set_error(P.err, 16);
+
+  // acc[nb][mb][r] = C[m = wm*BM/2 + 16 mb + fr][n = wn*BN/2 + 16 nb + 4 (lane/16) + r]
+  float* cr = reinterpret_cast<float*>(smem_raw);
+#pragma unroll
+  for (int nb = 0; nb < NT; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < MT; ++mb) {
+      const int m = wm * (BM / 2) + mb * 16 + fr, n = wn * (BN / 2) + nb * 16 + 4 * (lane >> 4);
+      *reinterpret_cast<float4*>(cr + m * S::c_ld + n) =
+          make_float4(acc[nb][mb][0], acc[nb][mb][1], acc[nb][mb][2], acc[nb][mb][3]);
+    }
+  __syncthreads();
+  epilogue<bf16, EPI>(P, cr, S::c_ld, m0, mrows, n0 >> 4, nrows >> 4, grp);
+}
+
+template <int BM, int BN, int R, int WF>
+static hipError_t tiled_launch(const Gemm& g, hipStream_t s) {
+  // bound on the m-tiles of all groups: sum_g ceil(rows_g / BM) <= rows / BM + groups
+  const int64_t mt_bound = g.group_off ? (int64_t)g.n_rows / BM + g.n_groups : ((int64_t)g.n_rows + BM - 1) / BM;
+  const int64_t items = mt_bound * ((g.n + BN - 1) / BN);
+  const int64_t grid = (items + 7) / 8 * 8;
+  if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
+  dim3 gd((unsigned)grid), bd(256);
+  switch (g.epi) {
+    case EPI_QKV: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, R, EPI_QKV, WF>), gd, bd, 0, s, g); break;
+    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, R, EPI_RESIDUAL, WF>), gd, bd, 0, s, g); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, R, EPI_SWIGLU, WF>), gd, bd, 0, s, g); break;
+    default: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, R, EPI_BIAS, WF>), gd, bd, 0, s, g); break;
+  }
+  return hipGetLastError();
+}
+
+bool tiled_gemm_applies(int dtype, const Gemm& g) {
+  if (dtype != 1 || g.k % TBK || g.n % 16 || g.n_groups > TMAXG || g.n_rows < TILED_MIN_TOTAL_ROWS) return false;
+  return (int64_t)g.n_rows >= (int64_t)TILED_MIN_ROWS * g.n_groups;
+}
+
+// 128 x 128 tiles once groups average 128 rows and the launch still has a few
+// tiles per compute unit; 64-row tiles otherwise (less padding per group), and
+// 64 x 64 tiles for a single dense matrix that would not fill the chip.
+hipError_t launch_gemm_tiled(int expert_fmt, const Gemm& g, hipStream_t s) {
+  const int64_t n_tn = (g.n + 127) / 128;
+  const int64_t groups = g.group_off ? g.n_groups : 1;
+  const bool big = (int64_t)g.n_rows >= 128LL * g.n_groups && ((int64_t)g.n_rows / 128 + groups) * n_tn >= 1024;
+  if (expert_fmt != 0) {
+    if (!g.w_scales) return hipErrorInvalidValue;
+    return big ? tiled_launch<128, 128, 2, 1>(g, s) : tiled_launch<64, 128, 4, 1>(g, s);
+  }
+  if (big) return tiled_launch<128, 128, 2, 0>(g, s);
+  if (((int64_t)g.n_rows / 64 + groups) * n_tn < 512) return tiled_launch<64, 64, 4, 0>(g, s);
+  return tiled_launch<64, 128, 4, 0>(g, s);
+}
+
+}  // namespace mcpu

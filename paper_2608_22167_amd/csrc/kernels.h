@@ -102,6 +102,13 @@ struct Gemm {
   int max_rows_per_group;   // upper bound used to pick the m-tiling
 };
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s);
+// LDS-tiled path (gemm_tiled.hip): bf16, k a multiple of 64, at least
+// TILED_MIN_TOTAL_ROWS rows in all and groups averaging TILED_MIN_ROWS rows;
+// n_rows must then hold the total row count.
+constexpr int TILED_MIN_ROWS = 16;
+constexpr int TILED_MIN_TOTAL_ROWS = 128;
+bool tiled_gemm_applies(int dtype, const Gemm& g);
+hipError_t launch_gemm_tiled(int expert_fmt, const Gemm& g, hipStream_t s);
 
 // ---- norms, router, permutation, combine --------------------------------
 

@@ -239,7 +239,7 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   const int64_t fdiv = c->expert_fmt == MCPU_EXPERT_MXFP4 ? 2 : 1;
   Gemm g1{};
   g1.w = w->w_gu; g1.w_scales = w->s_gu; g1.w_group_stride = (int64_t)2 * I * H / fdiv; g1.n = 2 * I; g1.k = H;
-  g1.x = m.hn; g1.row_src = m.src_tok; g1.group_off = m.group_off; g1.n_groups = E;
+  g1.x = m.hn; g1.row_src = m.src_tok; g1.group_off = m.group_off; g1.n_rows = T * K; g1.n_groups = E;
   g1.epi = EPI_SWIGLU; g1.bias = w->b_gu; g1.bias_group_stride = 2 * I; g1.out = m.act;
   g1.swiglu_alpha = c->swiglu_alpha; g1.swiglu_limit = c->swiglu_limit; g1.swiglu_beta = c->swiglu_beta;
   g1.err = err; g1.max_rows_per_group = max_rows;
@@ -250,7 +250,7 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
 
   Gemm g2{};
   g2.w = w->w_d; g2.w_scales = w->s_d; g2.w_group_stride = (int64_t)H * I / fdiv; g2.n = H; g2.k = I;
-  g2.x = m.act; g2.group_off = m.group_off; g2.n_groups = E;
+  g2.x = m.act; g2.group_off = m.group_off; g2.n_rows = T * K; g2.n_groups = E;
   g2.epi = EPI_BIAS; g2.bias = w->b_d; g2.bias_group_stride = H; g2.out = m.y;
   g2.err = err; g2.max_rows_per_group = max_rows;
   {

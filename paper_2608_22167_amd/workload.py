@@ -49,6 +49,10 @@ class LayerShape:
     swiglu_limit: float = 7.0
     swiglu_beta: float = 1.0
 
+    def __post_init__(self):
+        if self.dtype not in ("f32", "bf16") or self.expert_fmt not in ("dense", "mxfp4"):
+            raise ValueError(f"dtype {self.dtype!r} / expert_fmt {self.expert_fmt!r}")
+
     @property
     def qkv_dim(self) -> int:
         return (self.n_q_heads + 2 * self.n_kv_heads) * self.head_dim

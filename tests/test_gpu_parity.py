@@ -327,3 +327,51 @@ def test_mxfp4_bad_scale_sets_device_error():
     ws = mcpu.workspace(mcpu.moe_forward_workspace_size(shape, 2))
     mcpu.moe_forward(shape, dw, h, out, None, None, None, ws)
     assert mcpu.mcpu_check_device_errors(ws) & mcpu.DEVERR_MXFP4
+
+
+# ---------------------------------------------------------------------------------- many rows per matrix
+
+
+def _moe_shape(hidden, ffn, fmt):
+    return replace(W.GPT_OSS_20B, hidden=hidden, n_q_heads=8, n_kv_heads=2, head_dim=64, n_experts=8, top_k=2,
+                   ffn_dim=ffn, expert_fmt=fmt)
+
+
+@pytest.mark.parametrize("fmt", ["dense", "mxfp4"])
+@pytest.mark.parametrize("hidden,ffn,T", [(512, 512, 1000), (1024, 1024, 3600)])
+def test_moe_forward_many_rows(fmt, hidden, ffn, T):
+    """Expert GEMMs with hundreds of rows per expert (64- and 128-row tiles,
+    ragged last tiles in every group)."""
+    s = _moe_shape(hidden, ffn, fmt)
+    wl = W.custom(s, [4], [1], 1071 + hidden)
+    dw = mcpu.DeviceWeights(s, wl.weights)
+    h = W.synth_normal(9, 4, (T, s.hidden))
+    out = torch.empty((T, s.hidden), device="cuda")
+    idx = torch.empty((T, s.top_k), dtype=torch.int32, device="cuda")
+    wt = torch.empty((T, s.top_k), device="cuda")
+    ws = mcpu.workspace(mcpu.moe_forward_workspace_size(s, T))
+    mcpu.moe_forward(s, dw, h.cuda(), out, idx, wt, None, ws)
+    torch.cuda.synchronize()
+    assert mcpu.mcpu_check_device_errors(ws) == 0
+    weights = O.Weights(s, wl.weights)
+    ref = O.moe(s, weights, h)
+    tie = PT.check_router(idx.cpu().numpy(), ref["idx"], ref["logits"], s.top_k)
+    if tie.any():
+        f = ref["idx"].copy()
+        f[tie] = idx.cpu().numpy()[tie]
+        ref = O.moe(s, weights, h, force_idx=f)
+    PT.check("moe out", _np(out), ref["out"], "bf16")
+
+
+def test_dense_projections_ragged_rows_sampled():
+    """300 decode tokens: the dense projections take 64-row tiles with a ragged
+    last tile; compared on sampled sequences."""
+    rng = np.random.default_rng(1081)
+    ctx = rng.integers(1, 400, size=300)
+    wl = W.custom(W.GPT_OSS_20B, ctx, np.ones(300), 1081)
+    gpu, step = run_layer(wl)
+    seqs = sorted({0, 63, 64, 255, 256, 299} | {int(b) for b in rng.choice(300, 4, replace=False)})
+    sub, rows = W.restrict(wl, seqs)
+    g = {k: v[rows] for k, v in gpu.items()}
+    ref, _ = reference(sub, g)
+    compare_layer(sub, g, None, ref)
