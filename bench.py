@@ -2,12 +2,15 @@
 
 One step = one decoder-layer step (RMSNorm, QKV + RoPE + KV append, paged
 attention with sinks, O-projection, router, expert permutation, expert
-GEMMs, combine) for every sequence of the batch, through the C ABI. Inputs
-are seeded synthetic tensors already resident in HBM when timing starts.
-Prints one JSON line: decode tokens/s, the roofline of the dominant kernel
-(paged attention) measured with HIP events over the timed region, a
-per-kernel breakdown from a separate pass, and the CPU reference timed on a
-bounded sample of the same workload.
+GEMMs, combine) for every sequence of the batch, through the C ABI; for the
+stack workload, that step through all 24 layers. Inputs are seeded synthetic
+tensors already resident in HBM when timing starts.
+
+Prints one JSON line: tokens/s, the roofline of the dominant kernel (the one
+with the most time per step in an untimed breakdown pass), whose launch
+durations are measured with HIP events on its own stream inside the timed
+region, a per-kernel breakdown, and the CPU reference timed on a bounded
+sample of the same workload.
 """
 import argparse
 import hashlib
@@ -23,57 +26,87 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-BF16_PEAK_TFLOPS = 2500.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 METRIC = "decode tokens/s on 1 MI355X (gpt-oss-20b-shape layer); % of HBM / MFMA peak"
+PREFILL_MIN_Q = 16  # chunks of this many new tokens or more go to the prefill kernel
+
+STACK_WORKLOADS = ("stack24",)
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-STACK_WORKLOADS = ("stack24",)
-
-
 def make_workload(name):
     from paper_2608_22167_amd import workload as W
-    if name == "full_b64":
-        return W.full_b64()
-    if name == "sliding_b256":
-        return W.sliding_b256()
-    if name == "tiny_f32":
-        return W.tiny_f32()
-    if name == "stack24":
-        return W.stack24()
-    raise SystemExit(f"unknown workload {name}")
+    makers = {"full_b64": W.full_b64, "sliding_b256": W.sliding_b256, "tiny_f32": W.tiny_f32,
+              "mixed_prefill": W.mixed_prefill, "stack24": W.stack24}
+    if name not in makers:
+        raise SystemExit(f"unknown workload {name}; one of {sorted(makers)}")
+    return makers[name]()
 
 
-def kernel_bytes(s, T, visible_keys, idx):
-    """Algorithmic HBM bytes per launch of each kernel of one layer (weights
-    read once, the visible K/V once, activations in and out). MXFP4 experts
-    count their codes (half a byte per weight) and scales (one byte per 32)."""
+def _visible_sum(L0, q, window):
+    """Sum over a sequence's new tokens (positions L0 .. L0+q-1) of the keys each sees."""
+    p = np.arange(L0, L0 + q, dtype=np.int64)
+    return int(np.minimum(p + 1, window).sum() if window else (p + 1).sum())
+
+
+def layer_work(s, seq_lens, q_lens, idx):
+    """Algorithmic (HBM bytes, flops) of each kernel of one layer step: weights
+    read once, the visible K/V once per sequence, activations in and out; MXFP4
+    experts count their codes (half a byte per weight) and scales (one byte per
+    32). Attention flops are 4 Hq d per (query, visible key) pair."""
     eb = 4 if s.dtype == "f32" else 2
-    H, D, Hq, Hkv, I = s.hidden, s.head_dim, s.n_q_heads, s.n_kv_heads, s.ffn_dim
+    H, D, Hq, Hkv, I, k = s.hidden, s.head_dim, s.n_q_heads, s.n_kv_heads, s.ffn_dim, s.top_k
+    A = Hq * D
+    T = int(np.sum(q_lens))
+    kvb = Hkv * D * 2 * eb
+    dec_pairs = pre_pairs = pre_keys = 0
+    t_dec = t_pre = 0
+    for L0, q in zip(np.asarray(seq_lens, np.int64), np.asarray(q_lens, np.int64)):
+        vis = _visible_sum(int(L0), int(q), s.window)
+        if q >= PREFILL_MIN_Q:
+            pre_pairs += vis
+            t_pre += int(q)
+            last = int(L0 + q - 1)
+            lo = max(0, int(L0) - s.window + 1) if s.window else 0
+            pre_keys += last - lo + 1
+        else:
+            dec_pairs += vis
+            t_dec += int(q)
+    rows = T * k
     touched = len(np.unique(idx))
     wb = (lambda r, c: r * c // 2 + r * c // 32) if s.expert_fmt == "mxfp4" else (lambda r, c: r * c * eb)
-    kv = visible_keys * Hkv * D * 2 * eb
-    return {
-        "attn_split": kv + T * Hq * D * eb,
-        "qkv": s.qkv_dim * H * eb + T * H * eb + T * s.qkv_dim * eb,
-        "oproj": H * Hq * D * eb + T * Hq * D * eb + 2 * T * H * 4,
-        "expert_gu": touched * wb(2 * I, H) + T * s.top_k * (H + I) * eb,
-        "expert_down": touched * wb(H, I) + T * s.top_k * (I * eb + H * 4),
+    work = {
+        "attn_split": (dec_pairs * kvb + t_dec * A * eb, 4 * A * dec_pairs),
+        "qkv": (s.qkv_dim * H * eb + T * H * eb + T * s.qkv_dim * eb, 2 * T * s.qkv_dim * H),
+        "oproj": (H * A * eb + T * A * eb + 2 * T * H * 4, 2 * T * H * A),
+        "expert_gu": (touched * wb(2 * I, H) + rows * (H + I) * eb, 2 * rows * 2 * I * H),
+        "expert_down": (touched * wb(H, I) + rows * (I * eb + H * 4), 2 * rows * H * I),
     }
+    if t_pre:
+        work["attn_prefill"] = (pre_keys * kvb + 2 * t_pre * A * eb, 4 * A * pre_pairs)
+    return work, t_dec, t_pre
 
 
-def stack_visible_keys(spec, layer):
-    lens = spec.seq_lens.astype(np.int64) + 1
-    return int(np.minimum(lens, spec.shape_sw.window).sum() if spec.is_sw(layer) else lens.sum())
+def roofline_of(work_bytes, work_flops, seconds, dtype):
+    """The binding resource of a kernel: HBM below the ridge point, MFMA above."""
+    peak_tf = MFMA_PEAK_TFLOPS[dtype]
+    ridge = peak_tf * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if work_flops > ridge * work_bytes:
+        a = work_flops / seconds / 1e12
+        return {"bound": "mfma", "achieved": round(a, 1), "peak": peak_tf, "unit": "TFLOP/s",
+                "frac": round(a / peak_tf, 4)}
+    a = work_bytes / seconds / 1e9
+    return {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(a / HBM_PEAK_GBS, 4)}
 
 
-def traffic_from_profile(kernel_src, workload_name):
+def traffic_from_profile(kernel, kernel_src, workload_name):
     """HBM bytes per launch from a committed rocprofv3 counter summary, if it
     was taken on the current source of the kernel; else None."""
-    path = os.path.join(ROOT, "profiles", f"attn_split_{workload_name}_counters.md")
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_name}_counters.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -85,36 +118,12 @@ def traffic_from_profile(kernel_src, workload_name):
     return float(t.group(1))
 
 
-def cpu_baseline(wl, n_seq=64):
-    """The CPU reference on `n_seq` seeded sequences of the same workload."""
-    from oracle import oracle as O
-    from paper_2608_22167_amd import workload as W
-    rng = np.random.default_rng(wl.seed + 99)
-    seqs = np.sort(rng.choice(wl.batch, size=min(n_seq, wl.batch), replace=False))
-    sub, _ = W.restrict(wl, seqs)
-    weights = O.Weights(sub.shape, sub.weights)
-    t0 = time.perf_counter()
-    O.decode_layer(sub, weights)
-    dt = time.perf_counter() - t0
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": round(sub.n_tokens / dt, 3), "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{len(seqs)} of {wl.batch} sequences (seeded), one full layer step, "
-                      f"{dt:.2f} s wall"}
+KERNEL_SOURCES = {"attn_split": "attention.hip", "attn_prefill": "attention.hip", "qkv": "gemm_tiled.hip",
+                  "oproj": "gemm_tiled.hip", "expert_gu": "gemm_tiled.hip", "expert_down": "gemm_tiled.hip"}
 
 
-def cpu_baseline_stack(spec, n_seq=2):
-    """The CPU reference of the layer stack on `n_seq` seeded sequences, all layers."""
-    from oracle import stack as OS
-    rng = np.random.default_rng(spec.seed + 99)
-    seqs = np.sort(rng.choice(spec.batch, size=min(n_seq, spec.batch), replace=False))
-    t0 = time.perf_counter()
-    OS.reference_stack(spec, seqs)
-    dt = time.perf_counter() - t0
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": round(len(seqs) / dt, 4), "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{len(seqs)} of {spec.batch} sequences (seeded, contexts "
-                      f"{', '.join(str(int(spec.seq_lens[i])) for i in seqs)}) through all {spec.n_layers} "
-                      f"layers, pages and used experts regenerated on the host, {dt:.2f} s wall"}
+def cpu_cores():
+    return int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
 
 
 class LayerBench:
@@ -125,7 +134,7 @@ class LayerBench:
         self.wl, self.shape = wl, wl.shape
         self.step = mcpu.DeviceStep(wl)
         self.tokens = wl.n_tokens
-        self.attn_per_step = 1
+        self.launches = 1
 
     def run(self):
         self.step.run()
@@ -133,23 +142,50 @@ class LayerBench:
     def errors(self):
         return self.step.device_errors()
 
-    def bytes(self):
-        """(per-step bytes of each kernel, bytes of each attn_split launch in a step)."""
-        kb = kernel_bytes(self.shape, self.tokens, self.wl.visible_keys(), self.step.topk_idx.cpu().numpy())
-        return kb, [kb["attn_split"]]
+    def work(self):
+        """[launch in a step] -> {kernel: (bytes, flops)}; decode and prefill token counts."""
+        w, t_dec, t_pre = layer_work(self.shape, self.wl.seq_lens, self.wl.q_lens,
+                                     self.step.topk_idx.cpu().numpy())
+        return [w], t_dec, t_pre
+
+    def dominant_launches(self, kernel):
+        return [0]
 
     def config(self):
         wl, s = self.wl, self.shape
-        return {"workload": wl.name, "batch": wl.batch, "tokens": wl.n_tokens,
-                "context": f"{int(wl.seq_lens.min())}..{int(wl.seq_lens.max())} "
-                           f"(mean {float(wl.seq_lens.mean()):.0f})",
-                "layer": f"hidden {s.hidden}, {s.n_q_heads}/{s.n_kv_heads} heads, d {s.head_dim}, "
-                         f"{s.n_experts} experts top-{s.top_k}, ffn {s.ffn_dim}",
-                "attention": "sliding window %d + sinks" % s.window if s.window else "full + sinks",
-                "parallelism": "single GPU"}
+        c = {"workload": wl.name, "batch": wl.batch, "tokens": wl.n_tokens,
+             "context": f"{int(wl.seq_lens.min())}..{int(wl.seq_lens.max())} (mean {float(wl.seq_lens.mean()):.0f})",
+             "layer": f"hidden {s.hidden}, {s.n_q_heads}/{s.n_kv_heads} heads, d {s.head_dim}, "
+                      f"{s.n_experts} experts top-{s.top_k}, ffn {s.ffn_dim}",
+             "attention": "sliding window %d + sinks" % s.window if s.window else "full + sinks",
+             "parallelism": "single GPU"}
+        if wl.q_lens.max() > 1:
+            pre = wl.q_lens[wl.q_lens > 1]
+            c["prefill_chunks"] = f"{len(pre)} chunks of {int(pre.min())}..{int(pre.max())} tokens"
+        return c
 
-    def cpu_baseline(self):
-        return cpu_baseline(self.wl)
+    def cpu_baseline(self, n_seq=64):
+        """The CPU reference on n_seq seeded sequences (decode steps) or on the
+        decode sequences plus the shortest prefill chunk (mixed steps)."""
+        from oracle import oracle as O
+        from paper_2608_22167_amd import workload as W
+        wl = self.wl
+        rng = np.random.default_rng(wl.seed + 99)
+        dec = np.nonzero(wl.q_lens == 1)[0]
+        seqs = rng.choice(dec, size=min(n_seq if len(dec) == wl.batch else 8, len(dec)), replace=False)
+        if len(dec) < wl.batch:
+            pre = np.nonzero(wl.q_lens > 1)[0]
+            seqs = np.append(seqs, pre[np.argmin(wl.q_lens[pre])])
+        seqs = np.sort(seqs)
+        sub, _ = W.restrict(wl, seqs)
+        weights = O.Weights(sub.shape, sub.weights)
+        t0 = time.perf_counter()
+        O.decode_layer(sub, weights)
+        dt = time.perf_counter() - t0
+        return {"value": round(sub.n_tokens / dt, 3), "unit": "tokens/s (all tokens of the sample)",
+                "cores": cpu_cores(), "kind": "oracle",
+                "sample": f"{len(seqs)} of {wl.batch} sequences (seeded), {sub.n_tokens} tokens, one layer step, "
+                          f"{dt:.2f} s wall"}
 
 
 class StackBench:
@@ -160,7 +196,7 @@ class StackBench:
         self.spec, self.shape = spec, spec.shape_full
         self.stack = mcpu.DeviceStack(spec)
         self.tokens = spec.batch
-        self.attn_per_step = spec.n_layers
+        self.launches = spec.n_layers
 
     def run(self):
         self.stack.run()
@@ -168,15 +204,17 @@ class StackBench:
     def errors(self):
         return self.stack.device_errors()
 
-    def bytes(self):
+    def work(self):
         idx = self.stack.topk_idx.cpu().numpy()
-        total, attn = {}, []
-        for layer in range(self.spec.n_layers):
-            kb = kernel_bytes(self.spec.shape(layer), self.tokens, stack_visible_keys(self.spec, layer), idx[layer])
-            for k, v in kb.items():
-                total[k] = total.get(k, 0) + v
-            attn.append(kb["attn_split"])
-        return total, attn
+        q = np.ones(self.spec.batch, np.int64)
+        per = [layer_work(self.spec.shape(i), self.spec.seq_lens, q, idx[i])[0] for i in range(self.spec.n_layers)]
+        return per, self.spec.batch, 0
+
+    def dominant_launches(self, kernel):
+        # the full-attention layers read over 99% of the stack's K/V
+        if kernel == "attn_split":
+            return [i for i in range(self.spec.n_layers) if not self.spec.is_sw(i)]
+        return list(range(self.spec.n_layers))
 
     def config(self):
         sp, s = self.spec, self.shape
@@ -189,15 +227,26 @@ class StackBench:
                 "kv_resident_gb": round(sum(p.numel() * 2 for p in self.stack.k + self.stack.v) / 1e9, 1),
                 "parallelism": "single GPU"}
 
-    def cpu_baseline(self):
-        return cpu_baseline_stack(self.spec)
+    def cpu_baseline(self, n_seq=2):
+        """The CPU reference of the layer stack on n_seq seeded sequences, all layers."""
+        from oracle import stack as OS
+        spec = self.spec
+        rng = np.random.default_rng(spec.seed + 99)
+        seqs = np.sort(rng.choice(spec.batch, size=min(n_seq, spec.batch), replace=False))
+        t0 = time.perf_counter()
+        OS.reference_stack(spec, seqs)
+        dt = time.perf_counter() - t0
+        return {"value": round(len(seqs) / dt, 4), "unit": "tokens/s", "cores": cpu_cores(), "kind": "oracle",
+                "sample": f"{len(seqs)} of {spec.batch} sequences (seeded, contexts "
+                          f"{', '.join(str(int(spec.seq_lens[i])) for i in seqs)}) through all {spec.n_layers} "
+                          f"layers, pages and used experts regenerated on the host, {dt:.2f} s wall"}
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 50; 5 for a stack)")
-    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 10; 2 for a stack)")
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 50; 5 for a stack or mixed step)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 10; 2 for a stack or mixed step)")
     ap.add_argument("--workload", default="full_b64")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -208,9 +257,9 @@ def main():
         print(json.dumps({"error": "this benchmark runs on one GPU; the decode step is not sharded "
                                    "across GPUs in this build", "n_gpus": args.gpus}))
         raise SystemExit(2)
-    is_stack = args.workload in STACK_WORKLOADS
-    K = args.steps if args.steps is not None else (5 if is_stack else 50)
-    warmup = args.warmup if args.warmup is not None else (2 if is_stack else 10)
+    heavy = args.workload in STACK_WORKLOADS or args.workload == "mixed_prefill"
+    K = args.steps if args.steps is not None else (5 if heavy else 50)
+    warmup = args.warmup if args.warmup is not None else (2 if heavy else 10)
 
     import torch
     from paper_2608_22167_amd import mcpu
@@ -218,7 +267,7 @@ def main():
     torch.cuda.set_device(0)
     log(f"generating workload {args.workload}")
     wl = make_workload(args.workload)
-    bench = StackBench(wl) if is_stack else LayerBench(wl)
+    bench = StackBench(wl) if args.workload in STACK_WORKLOADS else LayerBench(wl)
     torch.cuda.synchronize()
     log(f"resident: {torch.cuda.memory_allocated() / 1e9:.1f} GB; {bench.tokens} tokens per step")
 
@@ -228,8 +277,31 @@ def main():
     if bench.errors():
         raise SystemExit("device error during warm-up")
 
-    n_attn = K * bench.attn_per_step
-    mcpu.mcpu_timing_start("attn_split", n_attn)
+    # per-kernel breakdown (microseconds per step, all launches), untimed pass
+    nb = min(K, 20)
+    cap = 4 * nb * bench.launches
+    for k in mcpu.KERNELS:
+        mcpu.mcpu_timing_start(k, cap)
+    for _ in range(nb):
+        bench.run()
+    torch.cuda.synchronize()
+    breakdown = {}
+    for k in mcpu.KERNELS:
+        ms = mcpu.mcpu_timing_read(k, cap)
+        mcpu.mcpu_timing_start(k, 0)
+        if len(ms):
+            breakdown[k] = round(float(np.sum(ms)) / nb * 1e3, 2)
+    per_launch, t_dec, t_pre = bench.work()
+    work = {}
+    for w in per_launch:
+        for k, (b, f) in w.items():
+            work[k] = (work.get(k, (0, 0))[0] + b, work.get(k, (0, 0))[1] + f)
+    dominant = max((k for k in breakdown if k in work), key=lambda k: breakdown[k])
+    log(f"dominant kernel {dominant} ({breakdown[dominant]} us per step)")
+
+    # timed region: HIP events around the dominant kernel's launches
+    n_launch = K * bench.launches
+    mcpu.mcpu_timing_start(dominant, n_launch)
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -241,54 +313,33 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_step = ev0.elapsed_time(ev1) / K
-    attn_ms = mcpu.mcpu_timing_read("attn_split", n_attn)
-    mcpu.mcpu_timing_start("attn_split", 0)
-    log(f"timed {K} steps: {ms_step * 1e3:.1f} us/step (wall {wall / K * 1e6:.1f} us/step)")
-
-    # per-kernel breakdown (microseconds per step, all launches), separate pass
-    nb = min(K, 20)
-    n_launch = nb * bench.attn_per_step
-    for k in mcpu.KERNELS:
-        mcpu.mcpu_timing_start(k, 4 * n_launch)
-    for _ in range(nb):
-        bench.run()
-    torch.cuda.synchronize()
-    breakdown = {}
-    for k in mcpu.KERNELS:
-        ms = mcpu.mcpu_timing_read(k, 4 * n_launch)
-        mcpu.mcpu_timing_start(k, 0)
-        if len(ms):
-            breakdown[k] = round(float(np.sum(ms)) / nb * 1e3, 2)
+    dom_ms = np.asarray(mcpu.mcpu_timing_read(dominant, n_launch), np.float64)
+    mcpu.mcpu_timing_start(dominant, 0)
     if bench.errors():
         raise SystemExit("device error during timing")
+    log(f"timed {K} steps: {ms_step * 1e3:.1f} us/step (wall {wall / K * 1e6:.1f} us/step)")
 
-    kb, attn_launch_bytes = bench.bytes()
-    # dominant kernel: attention over the full-context layers (every launch for a
-    # single layer; the full-attention layers of a stack, which read >99% of its K/V)
-    per = np.asarray(attn_ms, np.float64).reshape(K, bench.attn_per_step)
-    if is_stack:
-        cols = [i for i in range(bench.attn_per_step) if not wl.is_sw(i)]
-        kernel_label = "attn_split (full-attention layers)"
-    else:
-        cols = [0]
-        kernel_label = "attn_split"
-    launch_bytes = float(np.mean([attn_launch_bytes[c] for c in cols]))
-    attn_us = float(per[:, cols].mean()) * 1e3
-    achieved = launch_bytes / (attn_us * 1e-6) / 1e9
-    traffic = traffic_from_profile(os.path.join(ROOT, "paper_2608_22167_amd", "csrc", "attention.hip"),
-                                   args.workload)
-    roofline = {"kernel": kernel_label, "bound": "hbm", "achieved": round(achieved, 1),
-                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic, "avg_us": round(attn_us, 2), "algorithmic_bytes": round(launch_bytes)}
-    per_kernel_gbs = {k: round(kb[k] / (breakdown[k] * 1e-6) / 1e9, 1) for k in kb if k in breakdown}
-    step_bytes = sum(kb.values())
+    cols = bench.dominant_launches(dominant)
+    per = dom_ms.reshape(K, -1)[:, cols]
+    launch_bytes = float(np.mean([per_launch[c][dominant][0] for c in cols]))
+    launch_flops = float(np.mean([per_launch[c][dominant][1] for c in cols]))
+    dom_us = float(per.mean()) * 1e3
+    roofline = {"kernel": dominant + (" (full-attention layers)" if cols != list(range(bench.launches)) else "")}
+    roofline.update(roofline_of(launch_bytes, launch_flops, dom_us * 1e-6, bench.shape.dtype))
+    src = os.path.join(ROOT, "paper_2608_22167_amd", "csrc", KERNEL_SOURCES.get(dominant, "attention.hip"))
+    roofline.update({"traffic": traffic_from_profile(dominant, src, args.workload), "avg_us": round(dom_us, 2),
+                     "algorithmic_bytes": round(launch_bytes), "algorithmic_flops": round(launch_flops)})
+    kernels_util = {k: roofline_of(b, f, breakdown[k] * 1e-6, bench.shape.dtype)
+                    for k, (b, f) in work.items() if breakdown.get(k)}
+    kernels_util = {k: f"{v['achieved']} {v['unit']} ({100 * v['frac']:.1f}% {v['bound']})"
+                    for k, v in kernels_util.items()}
 
     if args.copy_calibration > 0:
         n = args.copy_calibration << 20
-        src = torch.ones(n, dtype=torch.uint8, device="cuda")
-        dst = torch.empty_like(src)
+        src_t = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src_t)
         for _ in range(5):
-            dst.copy_(src)
+            dst.copy_(src_t)
         torch.cuda.synchronize()
         log(f"copy calibration: 5 copies of {n} bytes")
 
@@ -297,18 +348,20 @@ def main():
         log("timing the CPU reference on a sample")
         cpu = bench.cpu_baseline()
 
-    value = bench.tokens / (ms_step * 1e-3)
+    decode_tokens = t_dec if t_pre else bench.tokens
     out = {
-        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
-        "warmup": warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "metric": METRIC, "value": round(decode_tokens / (ms_step * 1e-3), 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": bench.shape.dtype, "data": "synthetic",
         "config": bench.config(),
         "roofline": roofline,
-        "step_hbm_gbs": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
         "cpu_baseline": cpu,
         "kernels_us": breakdown,
-        "kernels_gbs": per_kernel_gbs,
+        "kernels_roofline": kernels_util,
     }
+    if t_pre:
+        out["prefill_tokens_per_s"] = round(t_pre / (ms_step * 1e-3), 1)
+        out["all_tokens_per_s"] = round((t_dec + t_pre) / (ms_step * 1e-3), 1)
     print(json.dumps(out), flush=True)
 
 

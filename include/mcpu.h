@@ -172,7 +172,10 @@ int kv_pages_append(mcpu_kv_pool* pool, int32_t batch, const int32_t* page_table
  *    z_j = q_h . k_j / sqrt(d), M = max(s_h, max_j z_j), s_h = sinks[h],
  *  with query head h reading KV head h / (Hq / Hkv). sinks may be NULL (no sink).
  *  host_seq_lens / host_cu_q: host copies of the same arrays, used only to
- *  plan the launch (no device-to-host traffic). */
+ *  plan the launch (no device-to-host traffic). A sequence that adds 16 or
+ *  more rows in the step (a tool observation appended as a prefill chunk,
+ *  paper Section 1) is served by the chunked-prefill kernel, the other rows
+ *  by split-K decode attention; the result is the same formula either way. */
 size_t paged_attention_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_batch,
                                       int32_t max_tokens);
 int paged_attention(const mcpu_layer_cfg* cfg, const float* sinks, mcpu_kv_pool* pool,
@@ -196,11 +199,13 @@ int moe_forward(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, int32_t 
 
 /* Optional copies of intermediates of decode_layer (each nullable):
  *  q [T, Hq, d] layer dtype (after rotation), o [T, Hq * d] layer dtype
- *  (attention output), h1 [T, H] fp32 (residual after attention). */
+ *  (attention output), h1 [T, H] fp32 (residual after attention), logits
+ *  [T, E] fp32 (router logits the top-k selection is made on). */
 typedef struct mcpu_taps {
   void* q;
   void* o;
   float* h1;
+  float* logits;
 } mcpu_taps;
 
 /* One decoder-layer step for a batch of sequences:
@@ -237,7 +242,8 @@ enum {
   MCPU_KERNEL_EXPERT_DOWN = 9,
   MCPU_KERNEL_MOE_COMBINE = 10,
   MCPU_KERNEL_KV_APPEND = 11,
-  MCPU_KERNEL_COUNT = 12
+  MCPU_KERNEL_ATTN_PREFILL = 12, /* chunked-prefill attention */
+  MCPU_KERNEL_COUNT = 13
 };
 int mcpu_timing_start(int kernel, int n);
 int mcpu_timing_read(int kernel, float* ms, int n, int* n_recorded);

@@ -12,8 +12,12 @@
  * the public gpt-oss conventions, each stated where it is used. Everything is
  * computed in float64 with plain loops, in the order the definition gives, with
  * no blocking, splitting or reordering. Values are rounded only where the
- * layer stores them: new keys and values are rounded to the cache dtype
- * (bfloat16 for bf16 layers) when written to the paged cache.
+ * layer stores them, to the layer's dtype (bfloat16 for bf16 layers, binary32
+ * for fp32 layers): the normalised input of the QKV product, the rotated
+ * queries, the new keys and values written to the paged cache, the attention
+ * output, the normalised rows the experts read and the SwiGLU activations.
+ * Everything between two such points (the products' sums, the softmax, the
+ * residual stream, the router logits) stays in float64.
  *
  * Only the tests, the smoke check and the benchmark's CPU-baseline leg use
  * this file. It shares no code, header or table with the GPU library.
@@ -39,7 +43,7 @@ typedef struct {
   int32_t hidden, n_q_heads, n_kv_heads, head_dim, n_experts, top_k, ffn_dim;
   int32_t page_size; /* must be 16 */
   int32_t window;    /* 0: full attention; else keys p-window+1 .. p */
-  int32_t kv_bf16;   /* 1: the cache stores bfloat16 */
+  int32_t kv_bf16;   /* 1: the layer (cache and stored activations) is bfloat16 */
   double rms_eps, swiglu_alpha, swiglu_limit, swiglu_beta;
 } orc_cfg;
 
@@ -69,6 +73,12 @@ double orc_round_bf16(double v) {
 
 void orc_round_bf16_array(int64_t n, const double* in, double* out) {
   for (int64_t i = 0; i < n; ++i) out[i] = orc_round_bf16(in[i]);
+}
+
+/* a value as the layer stores it: bfloat16 or binary32 */
+static double stored(const orc_cfg* c, double v) { return c->kv_bf16 ? orc_round_bf16(v) : (double)(float)v; }
+static void stored_array(const orc_cfg* c, int64_t n, double* v) {
+  for (int64_t i = 0; i < n; ++i) v[i] = stored(c, v[i]);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -181,7 +191,8 @@ int orc_kv_append(const orc_cfg* c, int T, const int32_t* tok_seq, const int32_t
       for (int i = 0; i < d; ++i) {
         double kv = k_new[((int64_t)t * G + g) * d + i];
         double vv = v_new[((int64_t)t * G + g) * d + i];
-        if (c->kv_bf16) { kv = orc_round_bf16(kv); vv = orc_round_bf16(vv); }
+        kv = stored(c, kv);
+        vv = stored(c, vv);
         k_pool[k_index(c, page, g, s, i)] = (float)kv;
         v_pool[v_index(c, page, g, s, i)] = (float)vv;
       }
@@ -277,18 +288,19 @@ void orc_topk(int E, int k, const double* logits, int32_t* idx) {
 }
 
 /* One token through one expert: gu = hn . W_gu[e]^T + b_gu[e], rows 2j/2j+1  */
-/* are gate_j/up_j; a_j = swiglu(gate_j, up_j); y = a . W_d[e]^T + b_d[e].    */
+/* are gate_j/up_j; a_j = swiglu(gate_j, up_j) (stored); y = a . W_d[e]^T +   */
+/* b_d[e]. hn here is the stored copy of the normalised row.                  */
 static void expert_ffn(const orc_cfg* c, const orc_weights* w, int e, const double* hn, double* y,
                        double* gu, double* act) {
   int H = c->hidden, I = c->ffn_dim;
   linear(1, H, 2 * I, hn, w->w_gu + (int64_t)e * 2 * I * H, w->b_gu + (int64_t)e * 2 * I, gu);
   for (int j = 0; j < I; ++j)
-    act[j] = orc_swiglu(gu[2 * j], gu[2 * j + 1], c->swiglu_alpha, c->swiglu_limit, c->swiglu_beta);
+    act[j] = stored(c, orc_swiglu(gu[2 * j], gu[2 * j + 1], c->swiglu_alpha, c->swiglu_limit, c->swiglu_beta));
   linear(1, I, H, act, w->w_d + (int64_t)e * H * I, w->b_d + (int64_t)e * H, y);
 }
 
 /* MoE sub-block on the residual stream h [T][H]:                             */
-/*   hn = RMSNorm(h; g2); logits = hn . W_r^T + b_r;                          */
+/*   hn = RMSNorm(h; g2); logits = hn . W_r^T + b_r (hn unrounded);           */
 /*   S = top-k set; w_e = softmax over {logits_e : e in S};                   */
 /*   out = h + sum_{e in S} w_e * FFN_e(hn).                                  */
 /* force_idx (optional [T][k]) replaces the selected set (used where the      */
@@ -310,6 +322,7 @@ int orc_moe(const orc_cfg* c, const orc_weights* w, int T, const double* h, doub
     double wt[256];
     orc_rmsnorm(1, H, h + (int64_t)t * H, w->g2, c->rms_eps, hn);
     linear(1, H, E, hn, w->w_r, w->b_r, lg);
+    stored_array(c, H, hn);  /* the router reads hn as computed; the experts its stored copy */
     if (force_idx) memcpy(sel, force_idx + (int64_t)t * k, sizeof(int32_t) * (size_t)k);
     else orc_topk(E, k, lg, sel);
     double mx = -INFINITY, den = 0.0;
@@ -335,7 +348,8 @@ int orc_moe(const orc_cfg* c, const orc_weights* w, int T, const double* h, doub
 /*   seq_lens[b]: tokens already cached; cu_q (optional, [B+1]): token b's    */
 /*   new tokens are rows cu_q[b] .. cu_q[b+1]-1 of x_in, at positions         */
 /*   seq_lens[b] + i. cu_q = NULL means one new token per sequence.           */
-/* Per token at position p:                                                  */
+/* Per token at position p (xn, q, k, v and o are stored, i.e. rounded to    */
+/* the layer dtype):                                                         */
 /*   xn = RMSNorm(x; g1); [q | k | v] = xn . W_qkv^T + b_qkv;                 */
 /*   q, k rotated at p; k, v stored in the cache;                            */
 /*   o = attention with sink (after every new k, v is stored);               */
@@ -368,6 +382,7 @@ int orc_decode_layer(const orc_cfg* c, const orc_weights* w, int B, const int32_
   int rc = ORC_OK;
 
   orc_rmsnorm(T, H, x_in, w->g1, c->rms_eps, xn);
+  stored_array(c, (int64_t)T * H, xn);
 #pragma omp parallel for schedule(static)
   for (int t = 0; t < T; ++t) linear(1, H, QKV, xn + (int64_t)t * H, w->w_qkv, w->b_qkv, qkv + (int64_t)t * QKV);
   for (int t = 0; t < T; ++t) {
@@ -376,6 +391,7 @@ int orc_decode_layer(const orc_cfg* c, const orc_weights* w, int B, const int32_
       double* qh = q + ((int64_t)t * Hq + h) * d;
       memcpy(qh, qkv + (int64_t)t * QKV + h * d, sizeof(double) * (size_t)d);
       orc_rope(d, tok_pos[t], w->rope_cos, w->rope_sin, qh);
+      stored_array(c, d, qh);
     }
     for (int g = 0; g < Hkv; ++g) {
       double* kh = kn + ((int64_t)t * Hkv + g) * d;
@@ -390,6 +406,7 @@ int orc_decode_layer(const orc_cfg* c, const orc_weights* w, int B, const int32_
   rc = orc_attention(c, T, tok_seq, tok_pos, q, k_pool, v_pool, page_table, max_pages, n_pages,
                      w->sinks, o);
   if (rc) goto done;
+  stored_array(c, (int64_t)T * A, o);
 #pragma omp parallel for schedule(static)
   for (int t = 0; t < T; ++t) {
     linear(1, A, H, o + (int64_t)t * A, w->w_o, w->b_o, h1 + (int64_t)t * H);

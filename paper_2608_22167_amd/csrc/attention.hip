@@ -42,18 +42,13 @@ __device__ __forceinline__ int seq_of_token(const int32_t* cu_q, int batch, int 
   return lo;
 }
 
-__global__ __launch_bounds__(1024) void attn_plan_kernel(AttnPlan P) {
-  __shared__ int sums[1024];
+__device__ __forceinline__ bool is_prefill(const AttnPlan& P, int b) {
+  return P.cu_q && P.prefill_min_q > 0 && P.cu_q[b + 1] - P.cu_q[b] >= P.prefill_min_q;
+}
+
+// Exclusive prefix of `local` over the 1024 threads of the block, and the total.
+__device__ int block_exclusive_scan(int local, int* sums, int& total) {
   const int tid = threadIdx.x, nt = blockDim.x;
-  const int per = (P.n_tokens + nt - 1) / nt;
-  const int t0 = min(P.n_tokens, tid * per), t1 = min(P.n_tokens, t0 + per);
-  int local = 0;
-  for (int t = t0; t < t1; ++t) {
-    int b = P.cu_q ? seq_of_token(P.cu_q, P.batch, t) : t;
-    int pos = P.seq_lens[b] + (P.cu_q ? t - P.cu_q[b] : 0);
-    local += token_splits(pos, P.window, P.pps);
-  }
-  // block-wide exclusive scan: wavefront scans, then a scan of the 16 totals
   const int incl = wave_incl_scan(local);
   const int wave = tid >> 6, lane = tid & 63;
   if (lane == 63) sums[wave] = incl;
@@ -65,18 +60,53 @@ __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnPlan P) {
     if (lane == (nt >> 6) - 1) sums[128] = wi;       // grand total
   }
   __syncthreads();
-  int run = sums[64 + wave] + incl - local;
+  const int excl = sums[64 + wave] + incl - local;
+  total = sums[128];
+  __syncthreads();  // sums is reused by the next scan
+  return excl;
+}
+
+__global__ __launch_bounds__(1024) void attn_plan_kernel(AttnPlan P) {
+  __shared__ int sums[160];
+  const int tid = threadIdx.x, nt = blockDim.x;
+  // tokens: positions and split counts (no splits for prefill sequences)
+  const int per = (P.n_tokens + nt - 1) / nt;
+  const int t0 = min(P.n_tokens, tid * per), t1 = min(P.n_tokens, t0 + per);
+  int local = 0;
+  for (int t = t0; t < t1; ++t) {
+    int b = P.cu_q ? seq_of_token(P.cu_q, P.batch, t) : t;
+    int pos = P.seq_lens[b] + (P.cu_q ? t - P.cu_q[b] : 0);
+    local += is_prefill(P, b) ? 0 : token_splits(pos, P.window, P.pps);
+  }
+  int total = 0;
+  int run = block_exclusive_scan(local, sums, total);
   for (int t = t0; t < t1; ++t) {
     int b = P.cu_q ? seq_of_token(P.cu_q, P.batch, t) : t;
     int pos = P.seq_lens[b] + (P.cu_q ? t - P.cu_q[b] : 0);
     P.tok_seq[t] = b;
     P.tok_pos[t] = pos;
     P.split_start[t] = run;
-    run += token_splits(pos, P.window, P.pps);
+    run += is_prefill(P, b) ? 0 : token_splits(pos, P.window, P.pps);
   }
   if (tid == 0) {
-    P.split_start[P.n_tokens] = sums[128];
-    if (P.host_total_splits >= 0 && sums[128] != P.host_total_splits) set_error(P.err, 8);
+    P.split_start[P.n_tokens] = total;
+    if (P.host_total_splits >= 0 && total != P.host_total_splits) set_error(P.err, 8);
+  }
+  if (!P.blk_start) return;
+  // sequences: prefill blocks of prefill_qb tokens
+  const int perb = (P.batch + nt - 1) / nt;
+  const int b0 = min(P.batch, tid * perb), b1 = min(P.batch, b0 + perb);
+  local = 0;
+  for (int b = b0; b < b1; ++b)
+    if (is_prefill(P, b)) local += (P.cu_q[b + 1] - P.cu_q[b] + P.prefill_qb - 1) / P.prefill_qb;
+  run = block_exclusive_scan(local, sums, total);
+  for (int b = b0; b < b1; ++b) {
+    P.blk_start[b] = run;
+    if (is_prefill(P, b)) run += (P.cu_q[b + 1] - P.cu_q[b] + P.prefill_qb - 1) / P.prefill_qb;
+  }
+  if (tid == 0) {
+    P.blk_start[P.batch] = total;
+    if (total != P.host_total_blocks) set_error(P.err, 8);
   }
 }
 
@@ -254,6 +284,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnCombine P) {
   const int t = uniform(item / P.hq), h = uniform(item - (item / P.hq) * P.hq);
   const int s0 = min(uniform(P.split_start[t]), P.n_splits);
   const int s1 = min(uniform(P.split_start[t + 1]), P.n_splits);
+  if (s0 == s1) return;  // a prefill token: its row comes from the prefill kernel
   float M = P.sinks ? P.sinks[h] * LOG2E : -INFINITY;
   float L = P.sinks ? 1.0f : 0.0f;  // the sink's own term, 2^(sink - M)
   float a = 0.f;
@@ -314,6 +345,249 @@ hipError_t launch_attn_combine(int dtype, int head_dim, const AttnCombine& p, hi
     else hipLaunchKernelGGL((attn_combine_kernel<bf16, 64>), grid, block, 0, s, p);
   }
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// prefill: a chunk of new tokens attending causally to its sequence's pages
+// ---------------------------------------------------------------------------
+
+// A workgroup of four wavefronts owns QB consecutive new tokens of one
+// sequence and one KV head. The matrix-core columns are (token, query head)
+// pairs, 64 per wavefront: 64 / G tokens times the G query heads that share
+// the KV head. The workgroup walks the pages from the first key any of its
+// tokens sees to its last token's page, two pages (32 keys) per step, staged
+// through LDS (double buffered) for all four wavefronts. Per step a wavefront
+// forms S^T = K Q^T for both pages and its four 16-column tiles, masks keys
+// outside each column's causal (and window) range, updates the running
+// maximum and normaliser per column, and accumulates O^T += V^T P^T with one
+// 16x16x32 product per tile that consumes both pages' scores as they sit in
+// the lanes. The sink enters the normaliser at the end.
+template <int G>
+struct PrefillShape {
+  static constexpr int TPW = 64 / G;    // tokens per wavefront
+  static constexpr int QB = 4 * TPW;    // tokens per workgroup
+};
+
+int prefill_block_tokens(int group) {
+  switch (group) {
+    case 1: return PrefillShape<1>::QB;
+    case 2: return PrefillShape<2>::QB;
+    case 4: return PrefillShape<4>::QB;
+    case 8: return PrefillShape<8>::QB;
+    case 16: return PrefillShape<16>::QB;
+    default: return 0;
+  }
+}
+
+template <typename T, int D, int G>
+__global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
+  using SH = PrefillShape<G>;
+  constexpr int PE = PAGE * D;                          // elements of one page of one KV head
+  constexpr int CH = 16 / sizeof(T);                    // elements per 16-byte chunk
+  constexpr int NCH = 4 * PE / CH;                      // chunks per step (K and V of two pages)
+  constexpr int PT = NCH / 256;                         // chunks per thread
+  static_assert(NCH % 256 == 0, "a step's pages must split evenly over the workgroup");
+  __shared__ __align__(16) T kv[2][4][PE];              // [buffer][K page a, K page b, V page a, V page b]
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  const int g = blockIdx.x % P.hkv;
+  const int blk = P.n_blocks - 1 - (int)(blockIdx.x / P.hkv);  // latest (heaviest) blocks first
+  int lo_b = 0, hi_b = P.batch - 1;                            // sequence: last b with blk_start[b] <= blk
+  while (lo_b < hi_b) {
+    const int mid = (lo_b + hi_b + 1) >> 1;
+    if (P.blk_start[mid] <= blk) lo_b = mid; else hi_b = mid - 1;
+  }
+  const int b = uniform(lo_b);
+  const int q0 = P.cu_q[b], q1 = P.cu_q[b + 1];
+  const int t0 = uniform(q0 + (blk - P.blk_start[b]) * SH::QB);
+  const int ntok = min(SH::QB, q1 - t0);
+  const int p_first = uniform(P.seq_lens[b] + (t0 - q0)), p_last = p_first + ntok - 1;
+  const int lo = P.window > 0 ? max(0, p_first - P.window + 1) : 0;
+  const int pg_lo = lo / PAGE;
+  int n_steps = (p_last / PAGE - pg_lo + 2) / 2;
+  if (ntok <= 0 || p_first < 0 || p_last / PAGE >= P.max_pages) {
+    if (tid == 0) set_error(P.err, 1);
+    n_steps = 0;
+  }
+  const int32_t* ptab = P.page_table + (int64_t)b * P.max_pages;
+  const int64_t page_elems = (int64_t)P.hkv * PE;
+
+  // this lane's column in each of the wavefront's four 16-column tiles
+  const int fr = lane & 15, grp = lane >> 4;
+  int pos[4], head[4];
+  bool valid[4];
+  Frag<T> qf[4][D / 32];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int c = 16 * j + fr;
+    const int ti = wave * SH::TPW + c / G;
+    valid[j] = ti < ntok;
+    pos[j] = p_first + ti;
+    head[j] = g * G + c % G;
+    const int trow = min(max(t0 + ti, 0), P.n_tokens - 1);  // in range even if the tables disagree
+    const T* qp = reinterpret_cast<const T*>(P.q) + ((int64_t)trow * P.hq + head[j]) * D + 8 * grp;
+#pragma unroll
+    for (int cc = 0; cc < D / 32; ++cc) {
+      qf[j][cc].load(qp + 32 * cc);
+      qf[j][cc].keep_if(valid[j]);
+    }
+  }
+
+  // staging: chunk i of a step is piece i / (PE / CH) (K a, K b, V a, V b) at
+  // element offset (i % (PE / CH)) * CH; pages past the range repeat the last
+  // one and missing pages read page 0 (both masked below)
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 st[PT];
+  auto page_id = [&](int step, int which, bool& ok) {
+    const int pg = min(pg_lo + 2 * step + which, p_last / PAGE);
+    int id = ptab[pg];
+    ok = id >= 0 && id < P.n_pages;
+    return ok ? id : 0;
+  };
+  auto fetch = [&](int step) __attribute__((always_inline)) {
+    step = min(step, max(n_steps - 1, 0));
+    bool oka, okb;
+    const int ida = page_id(step, 0, oka), idb = page_id(step, 1, okb);
+#pragma unroll
+    for (int u = 0; u < PT; ++u) {
+      const int i = tid + 256 * u, piece = i / (PE / CH), off = (i % (PE / CH)) * CH;
+      const T* pool = reinterpret_cast<const T*>(piece < 2 ? P.k_pool : P.v_pool);
+      const int id = (piece & 1) ? idb : ida;
+      st[u] = *reinterpret_cast<const u32x4*>(pool + id * page_elems + (int64_t)g * PE + off);
+    }
+  };
+  auto stage = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < PT; ++u) {
+      const int i = tid + 256 * u, piece = i / (PE / CH), off = (i % (PE / CH)) * CH;
+      *reinterpret_cast<u32x4*>(&kv[buf][piece][off]) = st[u];
+    }
+  };
+
+  float m_run[4], l_run[4];
+  f32x4 acc[D / 16][4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    m_run[j] = -INFINITY;
+    l_run[j] = 0.f;
+#pragma unroll
+    for (int n = 0; n < D / 16; ++n) acc[n][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  auto compute = [&](int step, int buf) __attribute__((always_inline)) {
+    bool ok[2];
+    page_id(step, 0, ok[0]);
+    page_id(step, 1, ok[1]);
+    const int pg0 = pg_lo + 2 * step;
+    // scores: sc[pg][j][r] = q(column j) . k(key 4 grp + r of page pg)
+    f32x4 sc[2][4];
+#pragma unroll
+    for (int pg = 0; pg < 2; ++pg) {
+      Frag<T> kf[D / 32];
+#pragma unroll
+      for (int cc = 0; cc < D / 32; ++cc) kf[cc].load(&kv[buf][pg][(64 * cc + lane) * 8]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        sc[pg][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int cc = 0; cc < D / 32; ++cc) sc[pg][j] = mma32(kf[cc], qf[j][cc], sc[pg][j]);
+      }
+    }
+    Frag4<T> va[D / 16], vb[D / 16];
+#pragma unroll
+    for (int n = 0; n < D / 16; ++n) {
+      va[n].load(&kv[buf][2][(64 * n + lane) * 4]);
+      vb[n].load(&kv[buf][3][(64 * n + lane) * 4]);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int hi = pos[j], lo_c = P.window > 0 ? pos[j] - P.window + 1 : 0;
+      float x[2][4];
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int pg = 0; pg < 2; ++pg)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int kp = (pg0 + pg) * PAGE + 4 * grp + r;
+          const bool in = valid[j] && ok[pg] && pg0 + pg <= p_last / PAGE && kp >= lo_c && kp <= hi;
+          x[pg][r] = in ? sc[pg][j][r] * P.scale_log2 : -INFINITY;
+          mloc = fmaxf(mloc, x[pg][r]);
+        }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      const float m_new = fmaxf(m_run[j], mloc);
+      const bool live = m_new != -INFINITY;  // -inf only while no key of the column was visible
+      const float alpha = live ? __builtin_amdgcn_exp2f(m_run[j] - m_new) : 1.0f;
+      float pa[4], pb[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        pa[r] = live ? __builtin_amdgcn_exp2f(x[0][r] - m_new) : 0.f;
+        pb[r] = live ? __builtin_amdgcn_exp2f(x[1][r] - m_new) : 0.f;
+      }
+      l_run[j] *= alpha;
+#pragma unroll
+      for (int n = 0; n < D / 16; ++n) {
+        acc[n][j] *= alpha;
+        float dummy = 0.f;
+        acc[n][j] = mma32_p(va[n], vb[n], pa, pb, acc[n][j], n == 0 ? &l_run[j] : &dummy);
+      }
+      m_run[j] = m_new;
+    }
+  };
+
+  if (n_steps > 0) {
+    fetch(0);
+    stage(0);
+    __syncthreads();
+    for (int step = 0; step < n_steps; ++step) {
+      fetch(step + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(step, step & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      stage((step & 1) ^ 1);
+      __syncthreads();
+    }
+  }
+
+  // normalise with the sink and store this lane's 4 dims of each column
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float l_tot = l_run[j] + __shfl_xor(l_run[j], 16, 64);
+    l_tot += __shfl_xor(l_tot, 32, 64);
+    float M = m_run[j], scale = 1.0f;
+    if (P.sinks) {
+      const float sk = P.sinks[head[j]] * LOG2E;
+      const float Mt = fmaxf(M, sk);
+      const float f = M == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(M - Mt);
+      l_tot = l_tot * f + __builtin_amdgcn_exp2f(sk - Mt);
+      scale = f;
+    }
+    const float inv = l_tot > 0.f ? scale / l_tot : 0.f;
+    if (valid[j]) {
+      T* o = reinterpret_cast<T*>(P.o) + ((int64_t)(t0 + wave * SH::TPW + (16 * j + fr) / G) * P.hq + head[j]) * D +
+             4 * grp;
+#pragma unroll
+      for (int n = 0; n < D / 16; ++n)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Elem<T>::store(o, 16 * n + r, acc[n][j][r] * inv);
+    }
+  }
+}
+
+template <typename T, int D>
+static hipError_t prefill_impl(int group, const AttnPrefill& p, hipStream_t s) {
+  dim3 grid((unsigned)(p.n_blocks * p.hkv)), block(256);
+  switch (group) {
+    case 4: hipLaunchKernelGGL((attn_prefill_kernel<T, D, 4>), grid, block, 0, s, p); break;
+    case 8: hipLaunchKernelGGL((attn_prefill_kernel<T, D, 8>), grid, block, 0, s, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_prefill(int dtype, int head_dim, int group, const AttnPrefill& p, hipStream_t s) {
+  if (p.n_blocks == 0) return hipSuccess;
+  if (dtype == 0) return head_dim == 32 ? prefill_impl<float, 32>(group, p, s) : prefill_impl<float, 64>(group, p, s);
+  return head_dim == 32 ? prefill_impl<bf16, 32>(group, p, s) : prefill_impl<bf16, 64>(group, p, s);
 }
 
 // ---------------------------------------------------------------------------

@@ -147,6 +147,35 @@ __device__ __forceinline__ f32x4 mma16_p(const Frag4<float>& A, const float p[4]
   return acc;
 }
 
+// acc += A * B over 32 keys taken from two 16-key pages: the reduction slots
+// of lane l are keys 4 (l / 16) .. +3 of page a, then the same keys of page b,
+// in both operands, so the score tiles of two pages feed one 16x16x32 product.
+// Lane values pa[r], pb[r] are rounded to the operand type; their rounded sum
+// is added to *psum.
+__device__ __forceinline__ f32x4 mma32_p(const Frag4<bf16>& Va, const Frag4<bf16>& Vb, const float pa[4],
+                                         const float pb[4], f32x4 acc, float* psum) {
+  uint16_t b[8];
+  float s = 0.f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    b[r] = f32_to_bf16(pa[r]);
+    b[4 + r] = f32_to_bf16(pb[r]);
+  }
+#pragma unroll
+  for (int r = 0; r < 8; ++r) s += bf16_to_f32(b[r]);
+  *psum += s;
+  const uint4 bv = make_uint4((uint32_t)b[0] | ((uint32_t)b[1] << 16), (uint32_t)b[2] | ((uint32_t)b[3] << 16),
+                              (uint32_t)b[4] | ((uint32_t)b[5] << 16), (uint32_t)b[6] | ((uint32_t)b[7] << 16));
+  const uint4 av = make_uint4(Va.v.x, Va.v.y, Vb.v.x, Vb.v.y);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv),
+                                                  acc, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma32_p(const Frag4<float>& Va, const Frag4<float>& Vb, const float pa[4],
+                                         const float pb[4], f32x4 acc, float* psum) {
+  acc = mma16_p(Va, pa, acc, psum);
+  return mma16_p(Vb, pb, acc, psum);
+}
+
 // ---------------------------------------------------------------------------
 // page format (see include/mcpu.h)
 // ---------------------------------------------------------------------------

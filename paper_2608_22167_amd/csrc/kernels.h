@@ -13,9 +13,31 @@ struct AttnPlan {
   const int32_t* cu_q;      // [batch+1] or nullptr (one token per sequence)
   int batch, n_tokens, window, pps;
   int host_total_splits;    // what the host planned; checked on the device
+  // sequences adding prefill_min_q or more tokens go to the prefill kernel in
+  // blocks of prefill_qb tokens; their tokens get no splits
+  int prefill_min_q, prefill_qb, host_total_blocks;
   int32_t* tok_seq;         // [n_tokens] out
   int32_t* tok_pos;         // [n_tokens] out
   int32_t* split_start;     // [n_tokens + 1] out
+  int32_t* blk_start;       // [batch + 1] out: first prefill block of each sequence
+  int32_t* err;
+};
+
+// Chunked prefill: the new tokens of a sequence attend causally to its pages
+// (the cached keys and the chunk's own, already appended).
+struct AttnPrefill {
+  const void* q;  // [T][Hq][D]
+  const void* k_pool;
+  const void* v_pool;
+  const int32_t* page_table;
+  int max_pages, n_pages;
+  const int32_t* seq_lens;
+  const int32_t* cu_q;
+  const int32_t* blk_start;
+  int batch, n_tokens, n_blocks, hq, hkv, window;
+  float scale_log2;     // log2(e) / sqrt(D)
+  const float* sinks;   // [Hq] or nullptr
+  void* o;              // [T][Hq * D]
   int32_t* err;
 };
 
@@ -47,6 +69,9 @@ struct AttnCombine {
 hipError_t launch_attn_plan(const AttnPlan& p, hipStream_t s);
 hipError_t launch_attn_split(int dtype, int head_dim, const AttnSplit& p, hipStream_t s);
 hipError_t launch_attn_combine(int dtype, int head_dim, const AttnCombine& p, hipStream_t s);
+// tokens per prefill workgroup for G = Hq / Hkv query heads per KV head (0 if unsupported)
+int prefill_block_tokens(int group);
+hipError_t launch_attn_prefill(int dtype, int head_dim, int group, const AttnPrefill& p, hipStream_t s);
 
 // ---- KV append -------------------------------------------------------------
 
@@ -132,6 +157,7 @@ struct Router {
   void* hn_out;        // [T][H] layer dtype (expert GEMM input)
   int32_t* idx_out;    // [T][k]
   float* w_out;        // [T][k]
+  float* logits_out;   // [T][E] fp32 router logits, or nullptr
   int32_t* err;
 };
 hipError_t launch_router(int dtype, const Router& p, hipStream_t s);

@@ -40,6 +40,7 @@ constexpr int PAGE_SIZE = 16;
 constexpr int SPLIT_EXTRA = 4096;   // splits beyond one per token that the workspace holds
 constexpr int PPS_MIN = 16;         // minimum pages per attention split
 constexpr int TARGET_WAVES = 3072;  // (split, KV head) wavefronts the planner aims for (measured: ~100 pages per split)
+constexpr int PREFILL_MIN_Q = 16;   // sequences adding this many tokens or more use the prefill kernel
 
 size_t dtype_bytes(const mcpu_layer_cfg* c) { return c->dtype == MCPU_F32 ? 4 : 2; }
 
@@ -119,6 +120,7 @@ int token_pages(int pos, int window) {
 
 struct AttnPlanHost {
   int n_tokens = 0, pps = PPS_MIN, n_splits = 0, max_pos = 0;
+  int prefill_min_q = 0, prefill_qb = 0, n_blocks = 0;  // chunked-prefill work (0 blocks: none)
 };
 
 // Validate host positions and choose pages-per-split so that the split count
@@ -130,22 +132,33 @@ int plan_attention(const mcpu_layer_cfg* c, int batch, int max_pages, const int3
   if (hcu && hcu[0] != 0) return fail(MCPU_EINVAL, "host_cu_q[0] must be 0");
   std::vector<int> pages;
   pages.reserve(T);
-  long long total_pages = 0;
+  long long total_pages = 0, blocks = 0;
   int max_pos = 0;
+  // chunks of PREFILL_MIN_Q or more tokens go to the prefill kernel when it
+  // supports the head grouping; everything else is split per token
+  const int qb = hcu ? prefill_block_tokens(c->n_q_heads / c->n_kv_heads) : 0;
+  const int min_q = qb > 0 ? PREFILL_MIN_Q : 0;
   for (int b = 0; b < batch; ++b) {
     int q = hcu ? hcu[b + 1] - hcu[b] : 1;
     if (q < 0) return fail(MCPU_EINVAL, "host_cu_q is not non-decreasing at %d", b);
     if (hsl[b] < 0) return fail(MCPU_EINVAL, "seq_lens[%d] = %d < 0", b, hsl[b]);
+    const bool pre = min_q > 0 && q >= min_q;
+    if (pre) blocks += (q + qb - 1) / qb;
     for (int i = 0; i < q; ++i) {
       int pos = hsl[b] + i;
       if (pos / PAGE_SIZE >= max_pages)
         return fail(MCPU_EINVAL, "sequence %d position %d beyond page table width %d", b, pos, max_pages);
+      max_pos = std::max(max_pos, pos);
+      if (pre) continue;
       int np = token_pages(pos, c->window);
       pages.push_back(np);
       total_pages += np;
-      max_pos = std::max(max_pos, pos);
     }
   }
+  if (blocks * c->n_kv_heads > 0x7FFFFFFFLL) return fail(MCPU_EINVAL, "too many prefill blocks");
+  out->prefill_min_q = min_q;
+  out->prefill_qb = qb;
+  out->n_blocks = (int)blocks;
   long long target = std::max<long long>(1, (long long)TARGET_WAVES / c->n_kv_heads);
   long long pps = std::max<long long>(PPS_MIN, (total_pages + target - 1) / target);
   pps = std::max<long long>(pps, (total_pages + SPLIT_EXTRA - 1) / SPLIT_EXTRA);
@@ -159,7 +172,7 @@ int plan_attention(const mcpu_layer_cfg* c, int batch, int max_pages, const int3
 }
 
 struct AttnBufs {
-  int32_t *tok_seq, *tok_pos, *split_start;
+  int32_t *tok_seq, *tok_pos, *split_start, *blk_start;
   float *part_ml, *part_acc;
 };
 
@@ -169,9 +182,22 @@ AttnBufs carve_attention(Carve& cv, const mcpu_layer_cfg* c, int max_tokens) {
   b.tok_seq = cv.take<int32_t>(max_tokens);
   b.tok_pos = cv.take<int32_t>(max_tokens);
   b.split_start = cv.take<int32_t>(max_tokens + 1);
+  b.blk_start = cv.take<int32_t>(max_tokens + 1);  // max_tokens >= batch here
   b.part_ml = cv.take<float>(S * c->n_q_heads * 2);
   b.part_acc = cv.take<float>(S * c->n_q_heads * c->head_dim);
   return b;
+}
+
+// The plan kernel's arguments (one place for both launch sites).
+AttnPlan make_plan(const mcpu_layer_cfg* c, int batch, const int32_t* seq_lens, const int32_t* cu_q,
+                   const AttnPlanHost& ph, const AttnBufs& ab, int32_t* err) {
+  AttnPlan pl{};
+  pl.seq_lens = seq_lens; pl.cu_q = cu_q; pl.batch = batch; pl.n_tokens = ph.n_tokens;
+  pl.window = c->window; pl.pps = ph.pps; pl.host_total_splits = ph.n_splits;
+  pl.prefill_min_q = ph.prefill_min_q; pl.prefill_qb = ph.prefill_qb; pl.host_total_blocks = ph.n_blocks;
+  pl.tok_seq = ab.tok_seq; pl.tok_pos = ab.tok_pos; pl.split_start = ab.split_start;
+  pl.blk_start = ab.blk_start; pl.err = err;
+  return pl;
 }
 
 struct MoeBufs {
@@ -211,7 +237,7 @@ int check_weights(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, bool att
 // MoE sub-block launches (router, permute, two grouped GEMMs, combine)
 int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const float* h, float* out,
             int32_t* idx_user, float* w_user, const int32_t* force_idx, const MoeBufs& m, int32_t* err,
-            hipStream_t st) {
+            hipStream_t st, float* logits_out = nullptr) {
   if (T == 0) return MCPU_OK;
   const int H = c->hidden, I = c->ffn_dim, E = c->n_experts, K = c->top_k;
   int32_t* idx = idx_user ? idx_user : m.idx;
@@ -220,7 +246,7 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   Router r{};
   r.h = h; r.g2 = w->g2; r.w_r = w->w_r; r.b_r = w->b_r; r.force_idx = force_idx;
   r.n_tokens = T; r.hidden = H; r.n_experts = E; r.top_k = K; r.eps = c->rms_eps;
-  r.hn_out = m.hn; r.idx_out = idx; r.w_out = wt; r.err = err;
+  r.hn_out = m.hn; r.idx_out = idx; r.w_out = wt; r.logits_out = logits_out; r.err = err;
   {
     Timed tm(MCPU_KERNEL_ROUTER, st);
     HIP_TRY(launch_router(c->dtype, r, st));
@@ -290,12 +316,8 @@ int run_attention(const mcpu_layer_cfg* c, const float* sinks, mcpu_kv_pool* poo
                   const AttnPlanHost& ph, const void* q, void* o, const AttnBufs& ab, int32_t* err,
                   hipStream_t st, bool plan_done) {
   if (!plan_done) {
-    AttnPlan pl{};
-    pl.seq_lens = seq_lens; pl.cu_q = cu_q; pl.batch = batch; pl.n_tokens = ph.n_tokens;
-    pl.window = c->window; pl.pps = ph.pps; pl.host_total_splits = ph.n_splits;
-    pl.tok_seq = ab.tok_seq; pl.tok_pos = ab.tok_pos; pl.split_start = ab.split_start; pl.err = err;
     Timed tm(MCPU_KERNEL_ATTN_PLAN, st);
-    HIP_TRY(launch_attn_plan(pl, st));
+    HIP_TRY(launch_attn_plan(make_plan(c, batch, seq_lens, cu_q, ph, ab, err), st));
   }
   AttnSplit sp{};
   sp.q = q; sp.k_pool = pool->k; sp.v_pool = pool->v; sp.page_table = page_table;
@@ -315,6 +337,16 @@ int run_attention(const mcpu_layer_cfg* c, const float* sinks, mcpu_kv_pool* poo
   {
     Timed tm(MCPU_KERNEL_ATTN_COMBINE, st);
     HIP_TRY(launch_attn_combine(c->dtype, c->head_dim, cb, st));
+  }
+  if (ph.n_blocks > 0) {
+    AttnPrefill pf{};
+    pf.q = q; pf.k_pool = pool->k; pf.v_pool = pool->v; pf.page_table = page_table;
+    pf.max_pages = max_pages; pf.n_pages = pool->n_pages;
+    pf.seq_lens = seq_lens; pf.cu_q = cu_q; pf.blk_start = ab.blk_start;
+    pf.batch = batch; pf.n_tokens = ph.n_tokens; pf.n_blocks = ph.n_blocks; pf.hq = c->n_q_heads; pf.hkv = c->n_kv_heads;
+    pf.window = c->window; pf.scale_log2 = sp.scale_log2; pf.sinks = sinks; pf.o = o; pf.err = err;
+    Timed tm(MCPU_KERNEL_ATTN_PREFILL, st);
+    HIP_TRY(launch_attn_prefill(c->dtype, c->head_dim, c->n_q_heads / c->n_kv_heads, pf, st));
   }
   return MCPU_OK;
 }
@@ -503,13 +535,9 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
   MoeBufs mb = carve_moe(cv, cfg, Tc);
   int32_t* err = err_word(workspace);
 
-  AttnPlan pl{};
-  pl.seq_lens = seq_lens; pl.cu_q = cu_q; pl.batch = batch; pl.n_tokens = T; pl.window = cfg->window;
-  pl.pps = ph.pps; pl.host_total_splits = ph.n_splits; pl.tok_seq = ab.tok_seq; pl.tok_pos = ab.tok_pos;
-  pl.split_start = ab.split_start; pl.err = err;
   {
     Timed tm(MCPU_KERNEL_ATTN_PLAN, stream);
-    HIP_TRY(launch_attn_plan(pl, stream));
+    HIP_TRY(launch_attn_plan(make_plan(cfg, batch, seq_lens, cu_q, ph, ab, err), stream));
   }
 
   RmsNorm rn{};
@@ -542,7 +570,9 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
     HIP_TRY(launch_gemm(cfg->dtype, MCPU_EXPERT_DENSE, go, stream));
   }
 
-  if ((rc = run_moe(cfg, w, T, h1, x_out, topk_idx, topk_w, nullptr, mb, err, stream))) return rc;
+  if ((rc = run_moe(cfg, w, T, h1, x_out, topk_idx, topk_w, nullptr, mb, err, stream,
+                    taps ? taps->logits : nullptr)))
+    return rc;
 
   if (taps) {
     if (taps->q) HIP_TRY(hipMemcpyAsync(taps->q, q, (size_t)T * Hq * D * db, hipMemcpyDeviceToDevice, stream));

@@ -210,6 +210,7 @@ __global__ __launch_bounds__(256) void router_kernel(Router P) {
   if (threadIdx.x < P.n_experts) {
     const int e = threadIdx.x;
     logits[e] = part[0][e] + part[1][e] + part[2][e] + part[3][e] + P.b_r[e];
+    if (P.logits_out) P.logits_out[(int64_t)t * P.n_experts + e] = logits[e];
   }
   __syncthreads();
 

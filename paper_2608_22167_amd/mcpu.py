@@ -29,7 +29,7 @@ EXPORTED = ("mcpu_last_error", "kv_pool_create", "kv_pool_destroy", "kv_pool_fre
             "mcpu_timing_start", "mcpu_timing_read")
 
 KERNELS = ("attn_plan", "rmsnorm", "qkv", "attn_split", "attn_combine", "oproj", "router", "permute",
-           "expert_gu", "expert_down", "moe_combine", "kv_append")
+           "expert_gu", "expert_down", "moe_combine", "kv_append", "attn_prefill")
 
 
 class McpuError(RuntimeError):
@@ -52,7 +52,8 @@ class LayerWeights(ctypes.Structure):
 
 
 class Taps(ctypes.Structure):
-    _fields_ = [("q", ctypes.c_void_p), ("o", ctypes.c_void_p), ("h1", ctypes.c_void_p)]
+    _fields_ = [("q", ctypes.c_void_p), ("o", ctypes.c_void_p), ("h1", ctypes.c_void_p),
+                ("logits", ctypes.c_void_p)]
 
 
 _LIB = None
@@ -347,21 +348,18 @@ class DeviceStack:
         ws = max(decode_layer_workspace_size(spec.shape(i), B, B) for i in range(min(2, self.n_layers)))
         self.ws = workspace(ws, device)
 
-    def run(self, stream=None, capture_rows=None):
-        """One step through every layer; returns the final residual stream. With
-        `capture_rows` (a device index tensor) it also returns the residual rows
-        entering each layer plus the final ones (n_layers + 1 tensors)."""
+    def run(self, stream=None, logits: Optional[torch.Tensor] = None) -> torch.Tensor:
+        """One step through every layer; returns the final residual stream.
+        logits, if given ([n_layers, B, E] fp32), receives each layer's router logits."""
         x = self.x_in
-        caps = None if capture_rows is None else [x.index_select(0, capture_rows)]
         for i in range(self.n_layers):
             y = self.buf[i % 2]
             pt = self.pt_sw if self.spec.is_sw(i) else self.pt_full
+            taps = None if logits is None else Taps(logits=logits[i].data_ptr())
             decode_layer(self.spec.shape(i), self.weights[i], self.pools[i], pt, self.seq_lens, None,
-                         self.host_seq_lens, None, x, y, self.topk_idx[i], None, None, self.ws, stream)
-            if caps is not None:
-                caps.append(y.index_select(0, capture_rows))
+                         self.host_seq_lens, None, x, y, self.topk_idx[i], None, taps, self.ws, stream)
             x = y
-        return x if caps is None else (x, caps)
+        return x
 
     def device_errors(self) -> int:
         return mcpu_check_device_errors(self.ws)

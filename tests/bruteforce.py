@@ -92,9 +92,18 @@ def swiglu(gate, up, alpha, limit, beta):
     return gate * (1.0 / (1.0 + np.exp(-alpha * gate))) * (up + beta)
 
 
+def stored(x, dtype):
+    """A value as a layer of this dtype stores it (bfloat16 or binary32)."""
+    x = np.asarray(x, np.float64)
+    return bf16(x) if dtype == "bf16" else x.astype(np.float32).astype(np.float64)
+
+
 def moe_token(hn, W, shape, force=None):
+    """The router reads hn itself; the experts read its stored copy and store
+    their SwiGLU activations."""
     f = lambda k: np.asarray(W[k], dtype=np.float64)
     logits = f("w_r") @ hn + f("b_r")
+    hs = stored(hn, shape.dtype)
     lf = logits.astype(np.float32)
     order = np.argsort(-lf, kind="stable")
     sel = order[: shape.top_k] if force is None else np.asarray(force)
@@ -102,8 +111,9 @@ def moe_token(hn, W, shape, force=None):
     w /= w.sum()
     acc = np.zeros(shape.hidden)
     for e, we in zip(sel, w):
-        gu = f("w_gu")[e] @ hn + f("b_gu")[e]
-        a = swiglu(gu[0::2], gu[1::2], shape.swiglu_alpha, shape.swiglu_limit, shape.swiglu_beta)
+        gu = f("w_gu")[e] @ hs + f("b_gu")[e]
+        a = stored(swiglu(gu[0::2], gu[1::2], shape.swiglu_alpha, shape.swiglu_limit, shape.swiglu_beta),
+                   shape.dtype)
         acc += we * (f("w_d")[e] @ a + f("b_d")[e])
     return acc, sel, w, logits
 
@@ -124,7 +134,7 @@ def decode_layer(wl):
     kl, vl = pool_to_logical(wl.k_pool.float().numpy().astype(np.float64),
                              wl.v_pool.float().numpy().astype(np.float64))
     d, Hq, Hkv = s.head_dim, s.n_q_heads, s.n_kv_heads
-    xn = rmsnorm(x, W["g1"], s.rms_eps)
+    xn = stored(rmsnorm(x, W["g1"], s.rms_eps), s.dtype)
     qkv = xn @ W["w_qkv"].T + W["b_qkv"]
     A = Hq * d
     cu = wl.cu_q
@@ -145,19 +155,15 @@ def decode_layer(wl):
         for i, r in enumerate(range(r0, r1)):
             p = L0 + i
             row = qkv[r]
-            q = rope(row[:A].reshape(Hq, d), p, W["rope_cos"], W["rope_sin"])
-            k = rope(row[A:A + Hkv * d].reshape(Hkv, d), p, W["rope_cos"], W["rope_sin"])
-            v = row[A + Hkv * d:].reshape(Hkv, d)
-            if s.dtype == "bf16":
-                k, v = bf16(k), bf16(v)
-            else:  # an fp32 cache stores fp32
-                k, v = k.astype(np.float32).astype(np.float64), v.astype(np.float32).astype(np.float64)
+            q = stored(rope(row[:A].reshape(Hq, d), p, W["rope_cos"], W["rope_sin"]), s.dtype)
+            k = stored(rope(row[A:A + Hkv * d].reshape(Hkv, d), p, W["rope_cos"], W["rope_sin"]), s.dtype)
+            v = stored(row[A + Hkv * d:].reshape(Hkv, d), s.dtype)
             Kd[p], Vd[p] = k, v
             q_all[r] = q
         for i, r in enumerate(range(r0, r1)):
             p = L0 + i
-            o_all[r] = attention_dense(q_all[r], Kd, Vd, p, s.window, W["sinks"],
-                                       1.0 / np.sqrt(d)).reshape(-1)
+            o_all[r] = stored(attention_dense(q_all[r], Kd, Vd, p, s.window, W["sinks"],
+                                              1.0 / np.sqrt(d)).reshape(-1), s.dtype)
     h1 = x + o_all @ W["w_o"].T + W["b_o"]
     hn = rmsnorm(h1, W["g2"], s.rms_eps)
     out = np.zeros_like(h1)

@@ -23,9 +23,12 @@ def check(name, got, ref, dtype, scale=1.0):
     ref = np.asarray(ref, np.float64)
     assert got.shape == ref.shape, (name, got.shape, ref.shape)
     assert np.isfinite(got).all(), f"{name}: non-finite values"
-    mx = float(np.abs(got - ref).max()) if got.size else 0.0
+    err = np.abs(got - ref)
+    mx = float(err.max()) if got.size else 0.0
     rl = rel_l2(got, ref)
-    msg = f"{name}: max-abs {mx:.3e} (tol {atol * scale:.1e}), rel-L2 {rl:.3e} (tol {rtol * scale:.1e})"
+    where = np.unravel_index(int(err.argmax()), err.shape) if got.size else ()
+    msg = (f"{name}: max-abs {mx:.3e} (tol {atol * scale:.1e}) at {tuple(int(i) for i in where)} "
+           f"(ref {float(ref[where]) if got.size else 0.0:.4g}), rel-L2 {rl:.3e} (tol {rtol * scale:.1e})")
     assert mx <= atol * scale and rl <= rtol * scale, msg
     return mx, rl
 

@@ -334,9 +334,9 @@ def test_moe_identical_experts_is_dense_ffn():
     h = np.random.default_rng(2).standard_normal((5, wl.shape.hidden))
     r = O.moe(wl.shape, Wt, h)
     s = wl.shape
-    hn = BF.rmsnorm(h, Wd["g2"].double().numpy(), s.rms_eps)
+    hn = BF.stored(BF.rmsnorm(h, Wd["g2"].double().numpy(), s.rms_eps), s.dtype)
     gu = hn @ Wd["w_gu"][0].double().numpy().T + Wd["b_gu"][0].double().numpy()
-    a = BF.swiglu(gu[:, 0::2], gu[:, 1::2], s.swiglu_alpha, s.swiglu_limit, s.swiglu_beta)
+    a = BF.stored(BF.swiglu(gu[:, 0::2], gu[:, 1::2], s.swiglu_alpha, s.swiglu_limit, s.swiglu_beta), s.dtype)
     y = a @ Wd["w_d"][0].double().numpy().T + Wd["b_d"][0].double().numpy()
     np.testing.assert_allclose(r["out"], h + y, rtol=1e-11, atol=1e-12)
 
@@ -353,9 +353,9 @@ def test_moe_top1_is_the_argmax_expert_ffn():
         hn = BF.rmsnorm(h[t:t + 1], Wn["g2"], s.rms_eps)[0]
         e = int(np.argmax(Wn["w_r"] @ hn + Wn["b_r"]))
         assert r["idx"][t, 0] == e and r["w"][t, 0] == 1.0
-        gu = Wn["w_gu"][e] @ hn + Wn["b_gu"][e]
-        y = Wn["w_d"][e] @ BF.swiglu(gu[0::2], gu[1::2], s.swiglu_alpha, s.swiglu_limit,
-                                     s.swiglu_beta) + Wn["b_d"][e]
+        gu = Wn["w_gu"][e] @ BF.stored(hn, s.dtype) + Wn["b_gu"][e]
+        y = Wn["w_d"][e] @ BF.stored(BF.swiglu(gu[0::2], gu[1::2], s.swiglu_alpha, s.swiglu_limit,
+                                               s.swiglu_beta), s.dtype) + Wn["b_d"][e]
         np.testing.assert_allclose(r["out"][t], h[t] + y, rtol=1e-11, atol=1e-12)
 
 
