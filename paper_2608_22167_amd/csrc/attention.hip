@@ -463,21 +463,37 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
     }
   };
 
-  float m_run[4], l_run[4];
-  f32x4 acc[D / 16][4];
+  // Per column: running maximum m (log2 units) and the accumulators of
+  // O^T = V^T P^T, plus a tile against ones that sums the (rounded) weights.
+  // The maximum is raised lazily: a step rescales only when some column's
+  // scores exceed its m by more than RESCALE (weights then stay below
+  // 2^RESCALE); every weight uses the same m as its normaliser, so the result
+  // is the same quotient.
+  constexpr float RESCALE = 8.0f;
+  float m_run[4];
+  f32x4 acc[D / 16][4], accl[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     m_run[j] = -INFINITY;
-    l_run[j] = 0.f;
+    accl[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int n = 0; n < D / 16; ++n) acc[n][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  Frag4<T> one;
+  ones(one);
+  // keys a step may need to mask: past the wave's first token (causal), before
+  // its last token's window, or on a missing or out-of-range page
+  const int pos_lo_w = p_first + wave * SH::TPW;
+  const int pos_hi_w = min(pos_lo_w + SH::TPW - 1, p_last);
+  const int pg_last = p_last / PAGE;
 
   auto compute = [&](int step, int buf) __attribute__((always_inline)) {
     bool ok[2];
     page_id(step, 0, ok[0]);
     page_id(step, 1, ok[1]);
-    const int pg0 = pg_lo + 2 * step;
+    const int pg0 = pg_lo + 2 * step, k0 = pg0 * PAGE;
+    const bool edge = k0 + 2 * PAGE - 1 > pos_lo_w || (P.window > 0 && k0 < pos_hi_w - P.window + 1) ||
+                      !ok[0] || !ok[1] || pg0 + 1 > pg_last;
     // scores: sc[pg][j][r] = q(column j) . k(key 4 grp + r of page pg)
     f32x4 sc[2][4];
 #pragma unroll
@@ -492,6 +508,40 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
         for (int cc = 0; cc < D / 32; ++cc) sc[pg][j] = mma32(kf[cc], qf[j][cc], sc[pg][j]);
       }
     }
+    if (edge) {  // wave-uniform: mask keys outside each column's range
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int hi = pos[j], lo_c = P.window > 0 ? pos[j] - P.window + 1 : 0;
+#pragma unroll
+        for (int pg = 0; pg < 2; ++pg)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int kp = k0 + pg * PAGE + 4 * grp + r;
+            const bool in = ok[pg] && pg0 + pg <= pg_last && kp >= lo_c && kp <= hi;
+            sc[pg][j][r] = in ? sc[pg][j][r] : -INFINITY;
+          }
+      }
+    }
+    float mstep[4];
+    bool raise = false;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float mx = fmaxf(fmaxf(fmaxf(sc[0][j][0], sc[0][j][1]), fmaxf(sc[0][j][2], sc[0][j][3])),
+                       fmaxf(fmaxf(sc[1][j][0], sc[1][j][1]), fmaxf(sc[1][j][2], sc[1][j][3])));
+      mstep[j] = max_over_rows(mx) * P.scale_log2;
+      raise = raise || mstep[j] > m_run[j] + RESCALE;
+    }
+    if (__builtin_amdgcn_ballot_w64(raise)) {  // wave-uniform rescale
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float m_new = fmaxf(m_run[j], mstep[j]);
+        const float alpha = m_new == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f(m_run[j] - m_new);
+        accl[j] *= alpha;
+#pragma unroll
+        for (int n = 0; n < D / 16; ++n) acc[n][j] *= alpha;
+        m_run[j] = m_new;
+      }
+    }
     Frag4<T> va[D / 16], vb[D / 16];
 #pragma unroll
     for (int n = 0; n < D / 16; ++n) {
@@ -500,37 +550,16 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int hi = pos[j], lo_c = P.window > 0 ? pos[j] - P.window + 1 : 0;
-      float x[2][4];
-      float mloc = -INFINITY;
-#pragma unroll
-      for (int pg = 0; pg < 2; ++pg)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int kp = (pg0 + pg) * PAGE + 4 * grp + r;
-          const bool in = valid[j] && ok[pg] && pg0 + pg <= p_last / PAGE && kp >= lo_c && kp <= hi;
-          x[pg][r] = in ? sc[pg][j][r] * P.scale_log2 : -INFINITY;
-          mloc = fmaxf(mloc, x[pg][r]);
-        }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float m_new = fmaxf(m_run[j], mloc);
-      const bool live = m_new != -INFINITY;  // -inf only while no key of the column was visible
-      const float alpha = live ? __builtin_amdgcn_exp2f(m_run[j] - m_new) : 1.0f;
+      const float msub = m_run[j] == -INFINITY ? 0.f : m_run[j];  // masked scores give 2^-inf = 0
       float pa[4], pb[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        pa[r] = live ? __builtin_amdgcn_exp2f(x[0][r] - m_new) : 0.f;
-        pb[r] = live ? __builtin_amdgcn_exp2f(x[1][r] - m_new) : 0.f;
+        pa[r] = __builtin_amdgcn_exp2f(fmaf(sc[0][j][r], P.scale_log2, -msub));
+        pb[r] = __builtin_amdgcn_exp2f(fmaf(sc[1][j][r], P.scale_log2, -msub));
       }
-      l_run[j] *= alpha;
+      accl[j] = mma32_pv(one, one, pa, pb, accl[j]);
 #pragma unroll
-      for (int n = 0; n < D / 16; ++n) {
-        acc[n][j] *= alpha;
-        float dummy = 0.f;
-        acc[n][j] = mma32_p(va[n], vb[n], pa, pb, acc[n][j], n == 0 ? &l_run[j] : &dummy);
-      }
-      m_run[j] = m_new;
+      for (int n = 0; n < D / 16; ++n) acc[n][j] = mma32_pv(va[n], vb[n], pa, pb, acc[n][j]);
     }
   };
 
@@ -551,8 +580,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
   // normalise with the sink and store this lane's 4 dims of each column
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    float l_tot = l_run[j] + __shfl_xor(l_run[j], 16, 64);
-    l_tot += __shfl_xor(l_tot, 32, 64);
+    float l_tot = accl[j][0];  // every row of the ones tile holds the column's sum
     float M = m_run[j], scale = 1.0f;
     if (P.sinks) {
       const float sk = P.sinks[head[j]] * LOG2E;

@@ -176,6 +176,42 @@ __device__ __forceinline__ f32x4 mma32_p(const Frag4<float>& Va, const Frag4<flo
   return mma16_p(Vb, pb, acc, psum);
 }
 
+// Maximum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (the four 16-lane rows
+// holding one accumulator column), with the gfx950 row-swap permutes.
+__device__ __forceinline__ float max_over_rows(float v) {
+  uint32_t u = __float_as_uint(v);
+  auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);  // rows {0,1} vs {2,3}
+  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  u = __float_as_uint(v);
+  auto b = __builtin_amdgcn_permlane16_swap(u, u, false, false);  // rows {0,2} vs {1,3}
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+// two floats to packed bfloat16 (round to nearest even, in hardware)
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t));
+}
+
+// As mma32_p, without the running sum (the caller gets it from a product
+// against a fragment of ones).
+__device__ __forceinline__ f32x4 mma32_pv(const Frag4<bf16>& Va, const Frag4<bf16>& Vb, const float pa[4],
+                                          const float pb[4], f32x4 acc) {
+  const uint4 bv = make_uint4(pack_bf16(pa[0], pa[1]), pack_bf16(pa[2], pa[3]), pack_bf16(pb[0], pb[1]),
+                              pack_bf16(pb[2], pb[3]));
+  const uint4 av = make_uint4(Va.v.x, Va.v.y, Vb.v.x, Vb.v.y);
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv),
+                                                  acc, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma32_pv(const Frag4<float>& Va, const Frag4<float>& Vb, const float pa[4],
+                                          const float pb[4], f32x4 acc) {
+  acc = mma16_p(Va, pa, acc, nullptr);
+  return mma16_p(Vb, pb, acc, nullptr);
+}
+__device__ __forceinline__ void ones(Frag4<bf16>& f) { f.v = make_uint2(0x3F803F80u, 0x3F803F80u); }
+__device__ __forceinline__ void ones(Frag4<float>& f) { f.v = make_float4(1.f, 1.f, 1.f, 1.f); }
+
 // ---------------------------------------------------------------------------
 // page format (see include/mcpu.h)
 // ---------------------------------------------------------------------------

@@ -168,8 +168,10 @@ struct Permute {
   int32_t* group_off;  // [E+1]
   int32_t* pos_of;     // [T*k] sorted position of assignment t*k+s
   int32_t* src_tok;    // [T*k] token of sorted row
+  int32_t* chunk_cnt;  // workspace: [ceil(T*k / PERM_CHUNK)][E] (batches above PERM_CHUNK)
   int32_t* err;
 };
+constexpr int PERM_CHUNK = 4096;  // assignments one permute workgroup ranks
 hipError_t launch_permute(const Permute& p, hipStream_t s);
 
 struct MoeCombine {

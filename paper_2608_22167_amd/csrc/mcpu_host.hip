@@ -204,7 +204,7 @@ struct MoeBufs {
   void* hn;
   int32_t* idx;
   float* w;
-  int32_t *group_off, *pos_of, *src_tok;
+  int32_t *group_off, *pos_of, *src_tok, *chunk_cnt;
   void* act;
   float* y;
 };
@@ -218,6 +218,7 @@ MoeBufs carve_moe(Carve& cv, const mcpu_layer_cfg* c, int max_tokens) {
   m.group_off = cv.take<int32_t>(c->n_experts + 1);
   m.pos_of = cv.take<int32_t>(T * K);
   m.src_tok = cv.take<int32_t>(T * K);
+  m.chunk_cnt = cv.take<int32_t>((T * K + PERM_CHUNK - 1) / PERM_CHUNK * c->n_experts);
   m.act = cv.take_bytes(T * K * c->ffn_dim * db);
   m.y = cv.take<float>(T * K * c->hidden);
   return m;
@@ -254,7 +255,7 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
 
   Permute p{};
   p.idx = idx; p.n_tokens = T; p.top_k = K; p.n_experts = E;
-  p.group_off = m.group_off; p.pos_of = m.pos_of; p.src_tok = m.src_tok; p.err = err;
+  p.group_off = m.group_off; p.pos_of = m.pos_of; p.src_tok = m.src_tok; p.chunk_cnt = m.chunk_cnt; p.err = err;
   {
     Timed tm(MCPU_KERNEL_PERMUTE, st);
     HIP_TRY(launch_permute(p, st));

@@ -5,10 +5,12 @@
 //               fp32, fp32 router logits (bf16 router weights widened
 //               exactly), top-k by wavefront arg-max reductions (ties to the
 //               lower expert id), softmax over the selected logits
-//  permute      one workgroup: per-expert histogram, exclusive scan, and a
-//               stable placement of every (token, slot) assignment into
-//               expert-sorted rows using wavefront ballots; no atomics on the
-//               placement, so the order is deterministic
+//  permute      per-expert histogram, exclusive scan, and a stable placement
+//               of every (token, slot) assignment into expert-sorted rows
+//               using wavefront ballots; no atomics on the placement, so the
+//               order is deterministic. One workgroup up to 4096 assignments;
+//               beyond, per-chunk histograms, one scan over the chunks and a
+//               per-chunk placement
 //  moe_combine  one workgroup per token: out = h + sum_k w_k y_k in slot order
 #include "device.h"
 #include "kernels.h"
@@ -299,11 +301,11 @@ hipError_t launch_router(int dtype, const Router& p, hipStream_t s) {
 // permute: expert-sorted rows, stable in (token, slot) order
 // ---------------------------------------------------------------------------
 
-constexpr int PERM_CHUNKS = 64;  // chunks of 64 assignments counted in LDS (n <= 4096)
+constexpr int PERM_SUB = PERM_CHUNK / 64;  // 64-assignment sub-chunks per workgroup
 
 // rank of this lane among the lanes of its wavefront holding the same expert
 // and a lower lane id, by peeling one expert value per round with ballots
-__device__ __forceinline__ int rank_in_chunk(int e, bool valid, int* uniq_first) {
+__device__ __forceinline__ int rank_in_chunk(int e, bool valid) {
   const int lane = lane_id();
   const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
   bool todo = valid;
@@ -319,39 +321,49 @@ __device__ __forceinline__ int rank_in_chunk(int e, bool valid, int* uniq_first)
     }
     pending = __ballot(todo);
   }
-  (void)uniq_first;
   return rank;
 }
 
-__global__ __launch_bounds__(256) void permute_kernel(Permute P) {
-  __shared__ int cnt[PERM_CHUNKS][64];
-  const int n = P.n_tokens * P.top_k, E = P.n_experts;
-  const int nch = (n + 63) / 64;
+__device__ __forceinline__ int checked_expert(const Permute& P, int a) {
+  const int e = P.idx[a];
+  if (e < 0 || e >= P.n_experts) {
+    set_error(P.err, 4);
+    return 0;
+  }
+  return e;
+}
+
+// Ranks the assignments a0 .. a0 + nloc - 1 (at most PERM_CHUNK) stably by
+// expert and scatters them. base (per expert, the chunk's first row) comes
+// from the multi-chunk scan; without it the workgroup holds the whole batch
+// and writes group_off itself.
+__device__ void permute_chunk(const Permute& P, int a0, int nloc, const int32_t* base) {
+  __shared__ int cnt[PERM_SUB][64];
+  const int E = P.n_experts;
+  const int nch = (nloc + 63) / 64;
   const int wave = threadIdx.x >> 6, lane = lane_id();
-  for (int i = threadIdx.x; i < PERM_CHUNKS * 64; i += blockDim.x) (&cnt[0][0])[i] = 0;
+  for (int i = threadIdx.x; i < PERM_SUB * 64; i += blockDim.x) (&cnt[0][0])[i] = 0;
   __syncthreads();
-  // per-chunk histograms (integer counts; order-independent)
+  // per-sub-chunk histograms (integer counts; order-independent)
   for (int c = wave; c < nch; c += 4) {
     const int a = c * 64 + lane;
-    if (a < n) {
-      int e = P.idx[a];
-      if (e < 0 || e >= E) {
-        set_error(P.err, 4);
-        e = 0;
-      }
-      atomicAdd(&cnt[c][e], 1);
-    }
+    if (a < nloc) atomicAdd(&cnt[c][checked_expert(P, a0 + a)], 1);
   }
   __syncthreads();
-  // lane e of wave 0: exclusive scan over experts, then running bases per chunk
+  // lane e of wave 0: running first row of expert e in each sub-chunk
   if (wave == 0) {
-    int tot = 0;
-    if (lane < E)
-      for (int c = 0; c < nch; ++c) tot += cnt[c][lane];
-    const int incl = wave_incl_scan(tot);
-    int run = incl - tot;
-    if (lane < E) P.group_off[lane] = run;
-    if (lane == E - 1) P.group_off[E] = incl;
+    int run = 0;
+    if (base) {
+      run = lane < E ? base[lane] : 0;
+    } else {
+      int tot = 0;
+      if (lane < E)
+        for (int c = 0; c < nch; ++c) tot += cnt[c][lane];
+      const int incl = wave_incl_scan(tot);
+      run = incl - tot;
+      if (lane < E) P.group_off[lane] = run;
+      if (lane == E - 1) P.group_off[E] = incl;
+    }
     if (lane < E)
       for (int c = 0; c < nch; ++c) {
         const int k = cnt[c][lane];
@@ -362,61 +374,71 @@ __global__ __launch_bounds__(256) void permute_kernel(Permute P) {
   __syncthreads();
   for (int c = wave; c < nch; c += 4) {
     const int a = c * 64 + lane;
-    const bool valid = a < n;
-    int e = valid ? P.idx[a] : 0;
+    const bool valid = a < nloc;
+    int e = valid ? P.idx[a0 + a] : 0;
     if (e < 0 || e >= E) e = 0;
-    const int r = rank_in_chunk(e, valid, nullptr);
+    const int r = rank_in_chunk(e, valid);
     if (valid) {
       const int pos = cnt[c][e] + r;
-      P.pos_of[a] = pos;
-      P.src_tok[pos] = a / P.top_k;
+      P.pos_of[a0 + a] = pos;
+      P.src_tok[pos] = (a0 + a) / P.top_k;
     }
   }
 }
 
-// Larger batches: one wavefront walks the chunks in order with running bases.
-__global__ __launch_bounds__(64) void permute_serial_kernel(Permute P) {
+__global__ __launch_bounds__(256) void permute_kernel(Permute P) {
+  permute_chunk(P, 0, P.n_tokens * P.top_k, nullptr);
+}
+
+// Larger batches: per-chunk histograms, one scan over chunks, per-chunk scatter.
+__global__ __launch_bounds__(256) void perm_count_kernel(Permute P) {
   __shared__ int cnt[64];
-  const int n = P.n_tokens * P.top_k, E = P.n_experts, lane = lane_id();
-  cnt[lane] = 0;
+  const int n = P.n_tokens * P.top_k, E = P.n_experts;
+  if (threadIdx.x < 64) cnt[threadIdx.x] = 0;
   __syncthreads();
-  for (int a = lane; a < n; a += 64) {
-    int e = P.idx[a];
-    if (e < 0 || e >= E) {
-      set_error(P.err, 4);
-      e = 0;
-    }
-    atomicAdd(&cnt[e], 1);
-  }
+  const int a0 = blockIdx.x * PERM_CHUNK, a1 = min(n, a0 + PERM_CHUNK);
+  for (int a = a0 + (int)threadIdx.x; a < a1; a += blockDim.x) atomicAdd(&cnt[checked_expert(P, a)], 1);
   __syncthreads();
-  const int c = lane < E ? cnt[lane] : 0;
-  const int incl = wave_incl_scan(c);
-  int base = incl - c;
-  if (lane < E) P.group_off[lane] = base;
+  if ((int)threadIdx.x < E) P.chunk_cnt[(int64_t)blockIdx.x * E + threadIdx.x] = cnt[threadIdx.x];
+}
+
+// One wavefront, lane e = expert: totals -> group_off, and each chunk's count
+// replaced by the chunk's first row for that expert (stable in assignment order).
+__global__ __launch_bounds__(64) void perm_scan_kernel(Permute P, int n_chunks) {
+  const int lane = lane_id(), E = P.n_experts;
+  int tot = 0;
+  if (lane < E)
+    for (int c = 0; c < n_chunks; ++c) tot += P.chunk_cnt[(int64_t)c * E + lane];
+  const int incl = wave_incl_scan(tot);
+  int run = incl - tot;
+  if (lane < E) P.group_off[lane] = run;
   if (lane == E - 1) P.group_off[E] = incl;
-  for (int a0 = 0; a0 < n; a0 += 64) {
-    const int a = a0 + lane;
-    const bool valid = a < n;
-    int e = valid ? P.idx[a] : 0;
-    if (e < 0 || e >= E) e = 0;
-    const int r = rank_in_chunk(e, valid, nullptr);
-    // expert e's base is held by lane e; count this chunk's rows per expert
-    const int b0 = __shfl(base, e, 64);
-    int mine = 0;
-    for (int x = 0; x < 64; ++x) mine += (__shfl(valid ? e : -1, x, 64) == lane) ? 1 : 0;
-    if (valid) {
-      const int pos = b0 + r;
-      P.pos_of[a] = pos;
-      P.src_tok[pos] = a / P.top_k;
+  if (lane < E)
+    for (int c = 0; c < n_chunks; ++c) {
+      const int k = P.chunk_cnt[(int64_t)c * E + lane];
+      P.chunk_cnt[(int64_t)c * E + lane] = run;
+      run += k;
     }
-    base += mine;
-  }
+}
+
+__global__ __launch_bounds__(256) void perm_scatter_kernel(Permute P) {
+  const int n = P.n_tokens * P.top_k;
+  const int a0 = blockIdx.x * PERM_CHUNK;
+  permute_chunk(P, a0, min(PERM_CHUNK, n - a0), P.chunk_cnt + (int64_t)blockIdx.x * P.n_experts);
 }
 
 hipError_t launch_permute(const Permute& p, hipStream_t s) {
   if (p.n_experts > 64) return hipErrorInvalidValue;
-  if (p.n_tokens * p.top_k <= PERM_CHUNKS * 64) hipLaunchKernelGGL(permute_kernel, dim3(1), dim3(256), 0, s, p);
-  else hipLaunchKernelGGL(permute_serial_kernel, dim3(1), dim3(64), 0, s, p);
+  const int n = p.n_tokens * p.top_k;
+  if (n <= PERM_CHUNK) {
+    hipLaunchKernelGGL(permute_kernel, dim3(1), dim3(256), 0, s, p);
+    return hipGetLastError();
+  }
+  if (!p.chunk_cnt) return hipErrorInvalidValue;
+  const int chunks = (n + PERM_CHUNK - 1) / PERM_CHUNK;
+  hipLaunchKernelGGL(perm_count_kernel, dim3(chunks), dim3(256), 0, s, p);
+  hipLaunchKernelGGL(perm_scan_kernel, dim3(1), dim3(64), 0, s, p, chunks);
+  hipLaunchKernelGGL(perm_scatter_kernel, dim3(chunks), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 
