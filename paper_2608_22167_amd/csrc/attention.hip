@@ -436,14 +436,18 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
   // element offset (i % (PE / CH)) * CH; pages past the range repeat the last
   // one and missing pages read page 0 (both masked below)
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-  u32x4 st[PT];
-  auto page_id = [&](int step, int which, bool& ok) {
-    const int pg = min(pg_lo + 2 * step + which, p_last / PAGE);
-    int id = ptab[pg];
+  struct Regs {
+    u32x4 v[PT];
+  };
+  // page ids are wave-uniform: read them with scalar loads, whose wait counter
+  // is separate from the vector loads kept in flight below
+  auto page_id = [&](int step, int which, bool& ok) __attribute__((always_inline)) {
+    const int pg = uniform(min(pg_lo + 2 * step + which, p_last / PAGE));
+    const int id = load_uniform(ptab, pg);
     ok = id >= 0 && id < P.n_pages;
     return ok ? id : 0;
   };
-  auto fetch = [&](int step) __attribute__((always_inline)) {
+  auto fetch = [&](Regs& st, int step) __attribute__((always_inline)) {
     step = min(step, max(n_steps - 1, 0));
     bool oka, okb;
     const int ida = page_id(step, 0, oka), idb = page_id(step, 1, okb);
@@ -452,14 +456,14 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
       const int i = tid + 256 * u, piece = i / (PE / CH), off = (i % (PE / CH)) * CH;
       const T* pool = reinterpret_cast<const T*>(piece < 2 ? P.k_pool : P.v_pool);
       const int id = (piece & 1) ? idb : ida;
-      st[u] = *reinterpret_cast<const u32x4*>(pool + id * page_elems + (int64_t)g * PE + off);
+      st.v[u] = *reinterpret_cast<const u32x4*>(pool + id * page_elems + (int64_t)g * PE + off);
     }
   };
-  auto stage = [&](int buf) __attribute__((always_inline)) {
+  auto stage = [&](const Regs& st, int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < PT; ++u) {
       const int i = tid + 256 * u, piece = i / (PE / CH), off = (i % (PE / CH)) * CH;
-      *reinterpret_cast<u32x4*>(&kv[buf][piece][off]) = st[u];
+      *reinterpret_cast<u32x4*>(&kv[buf][piece][off]) = st.v[u];
     }
   };
 
@@ -563,17 +567,33 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
     }
   };
 
+  // Step j's pages are loaded into register set j % R and staged into LDS
+  // buffer j & 1: while step s is computed, steps s + 1 .. s + R are in flight
+  // (L2 latency exceeds one step's products). The loop is unrolled R times so
+  // set indices are constants; only the products are conditional (loads past
+  // the last step are clamped and their staged copies never read).
+  constexpr int R = 4;
   if (n_steps > 0) {
-    fetch(0);
-    stage(0);
+    Regs rs[R];
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      fetch(rs[u], u);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    stage(rs[0], 0);
+    fetch(rs[0], R);
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
-    for (int step = 0; step < n_steps; ++step) {
-      fetch(step + 1);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(step, step & 1);
-      __builtin_amdgcn_sched_barrier(0);
-      stage((step & 1) ^ 1);
-      __syncthreads();
+    for (int step = 0; step < n_steps; step += R) {
+#pragma unroll
+      for (int u = 0; u < R; ++u) {
+        if (step + u < n_steps) compute(step + u, u & 1);
+        __builtin_amdgcn_sched_barrier(0);
+        stage(rs[(u + 1) % R], (u + 1) & 1);
+        fetch(rs[(u + 1) % R], step + u + 1 + R);
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+      }
     }
   }
 

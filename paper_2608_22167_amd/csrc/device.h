@@ -48,6 +48,14 @@ template <> struct Elem<bf16> {
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Load of a wave-uniform element of memory the kernel only reads (a page
+// table), through the constant address space so that it becomes a scalar load:
+// its wait counter is separate from the vector loads a kernel keeps in flight.
+__device__ __forceinline__ int32_t load_uniform(const int32_t* p, int64_t i) {
+  typedef __attribute__((address_space(4))) const int32_t cint32;
+  return reinterpret_cast<cint32*>(reinterpret_cast<uintptr_t>(p))[i];
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
