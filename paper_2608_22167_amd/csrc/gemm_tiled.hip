@@ -29,9 +29,7 @@
 
 namespace mcpu {
 
-constexpr int TBK = 64;        // reduction slice per stage
-constexpr int TLDK = TBK + 8;  // LDS row stride in bf16: rows 144 B apart spread fragment reads over all banks
-constexpr int TMAXG = 256;     // groups (experts) one launch supports
+constexpr int TMAXG = 256;  // groups (experts) one launch supports
 
 // 16-byte staging registers as a native vector type: copies of HIP's uint4
 // struct become memcpy calls that keep the register sets in scratch memory.
@@ -39,65 +37,77 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 
-template <int BM, int BN>
+// LDS plan of a BM x BN tile with BK-wide reduction slices. Rows are padded by
+// 16 B (BK = 64: 144 B apart; BK = 32: 80 B apart), which spreads the eight
+// 16-byte fragment reads a cycle serves over all banks. The fp32 output tile
+// reuses the operand buffers, EP rows at a time.
+template <int BM, int BN, int BK>
 struct TiledSmem {
-  static constexpr int stage = (BM + BN) * TLDK;  // bf16 elements per stage
+  static constexpr int ldk = BK + 8;              // LDS row stride in bf16
+  static constexpr int stage = (BM + BN) * ldk;   // bf16 elements per stage
   static constexpr int ab_bytes = 2 * stage * 2;
   static constexpr int c_ld = BN + 4;             // fp32 tile row stride
-  static constexpr int c_bytes = BM * c_ld * 4;
-  static constexpr int bytes = ab_bytes > c_bytes ? ab_bytes : c_bytes;
+  static constexpr int EP = BM * c_ld * 4 <= ab_bytes ? BM : 64;  // output rows per epilogue pass
+  static_assert(EP * c_ld * 4 <= ab_bytes, "an epilogue pass must fit the operand buffers");
+  static constexpr int bytes = ab_bytes;
+  static constexpr int cpr = BK / 8;              // 16-byte chunks per staged row
+  static constexpr int rpp = 256 / cpr;           // rows one pass of the workgroup stages
 };
 
-// Staged weight rows: dense bf16 (16-byte chunks, 8 per row and slice) ...
-template <int BN, int WF>
+// Staged weight rows: dense bf16 (16-byte chunks, BK / 8 per row and slice) ...
+template <int BN, int BK, int WF>
 struct TiledW {
-  static constexpr int J = BN / 32;
+  static constexpr int cpr = BK / 8, rpp = 256 / cpr;
+  static constexpr int J = BN / rpp;
   struct Regs {
     u32x4 r[J];
   };
   const bf16* src[J];
-  static __device__ __forceinline__ int row(int tid, int j) { return (tid >> 3) + 32 * j; }
+  static __device__ __forceinline__ int row(int tid, int j) { return tid / cpr + rpp * j; }
   __device__ __forceinline__ void init(const Gemm& P, int grp, const int* wrow, int tid) {
 #pragma unroll
     for (int j = 0; j < J; ++j)
-      src[j] = reinterpret_cast<const bf16*>(P.w) + grp * P.w_group_stride + (int64_t)wrow[j] * P.k + (tid & 7) * 8;
+      src[j] = reinterpret_cast<const bf16*>(P.w) + grp * P.w_group_stride + (int64_t)wrow[j] * P.k +
+               (tid % cpr) * 8;
   }
   __device__ __forceinline__ void fetch(Regs& g, int ks) const {
 #pragma unroll
-    for (int j = 0; j < J; ++j) g.r[j] = ld16(src[j] + ks * TBK);
+    for (int j = 0; j < J; ++j) g.r[j] = ld16(src[j] + ks * BK);
   }
   static __device__ __forceinline__ void store(const Regs& g, bf16* ws, int tid, bool&) {
 #pragma unroll
-    for (int j = 0; j < J; ++j) st16(ws + row(tid, j) * TLDK + (tid & 7) * 8, g.r[j]);
+    for (int j = 0; j < J; ++j) st16(ws + row(tid, j) * (BK + 8) + (tid % cpr) * 8, g.r[j]);
   }
 };
 
-// ... or MXFP4: per row and slice 32 code bytes (two scale blocks) and two
-// E8M0 scales; a thread stages one block of 32 weights per chunk.
-template <int BN>
-struct TiledW<BN, 1> {
-  static constexpr int J = BN / 128;
+// ... or MXFP4: per row and slice BK / 2 code bytes (BK / 32 scale blocks)
+// and BK / 32 E8M0 scales; a thread stages one block of 32 weights per chunk.
+template <int BN, int BK>
+struct TiledW<BN, BK, 1> {
+  static constexpr int bpr = BK / 32;  // scale blocks per row and slice
+  static constexpr int J = BN * bpr / 256;
+  static_assert(J >= 1 && BN * bpr % 256 == 0, "whole scale blocks per thread");
   struct Regs {
     u32x4 r[J];
     uint32_t s[J];
   };
   const uint8_t* csrc[J];
   const uint8_t* ssrc[J];
-  static __device__ __forceinline__ int row(int tid, int j) { return (tid + 256 * j) >> 1; }
+  static __device__ __forceinline__ int row(int tid, int j) { return (tid + 256 * j) / bpr; }
+  static __device__ __forceinline__ int blk(int tid, int j) { return (tid + 256 * j) % bpr; }
   __device__ __forceinline__ void init(const Gemm& P, int grp, const int* wrow, int tid) {
-    const int half = tid & 1;
 #pragma unroll
     for (int j = 0; j < J; ++j) {
       csrc[j] = reinterpret_cast<const uint8_t*>(P.w) + grp * P.w_group_stride + (int64_t)wrow[j] * (P.k / 2) +
-                16 * half;
-      ssrc[j] = P.w_scales + grp * (P.w_group_stride / 16) + (int64_t)wrow[j] * (P.k / 32) + half;
+                16 * blk(tid, j);
+      ssrc[j] = P.w_scales + grp * (P.w_group_stride / 16) + (int64_t)wrow[j] * (P.k / 32) + blk(tid, j);
     }
   }
   __device__ __forceinline__ void fetch(Regs& g, int ks) const {
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-      g.r[j] = ld16(csrc[j] + ks * (TBK / 2));
-      g.s[j] = ssrc[j][ks * (TBK / 32)];
+      g.r[j] = ld16(csrc[j] + ks * (BK / 2));
+      g.s[j] = ssrc[j][ks * bpr];
     }
   }
   static __device__ __forceinline__ void store(const Regs& g, bf16* ws, int tid, bool& bad) {
@@ -116,7 +126,7 @@ struct TiledW<BN, 1> {
         o[4 * i + 2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w4[i], scale, 2));
         o[4 * i + 3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w4[i], scale, 3));
       }
-      bf16* d = ws + row(tid, j) * TLDK + 32 * (tid & 1);
+      bf16* d = ws + row(tid, j) * (BK + 8) + 32 * blk(tid, j);
 #pragma unroll
       for (int q = 0; q < 4; ++q) st16(d + 8 * q, u32x4{o[4 * q], o[4 * q + 1], o[4 * q + 2], o[4 * q + 3]});
     }
@@ -139,11 +149,13 @@ __device__ __forceinline__ void band_order(int L, int mt_g, int n_tn, int& mt, i
   }
 }
 
-template <int BM, int BN, int R, int EPI, int WF>
+template <int BM, int BN, int BK, int R, int EPI, int WF>
 __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
-  static_assert(R % 2 == 0, "the unrolled ring must cover both LDS buffers");
-  using S = TiledSmem<BM, BN>;
-  constexpr int GM = BM == 64 ? 8 : 4;  // m-tiles per band: about 3 MB of activations
+  static_assert(R == 1 || R % 2 == 0, "the unrolled ring must cover both LDS buffers");
+  constexpr int UN = R == 1 ? 2 : R;  // loop unroll: a multiple of the ring and of the two buffers
+  using S = TiledSmem<BM, BN, BK>;
+  constexpr int LDK = S::ldk;
+  constexpr int GM = BM == 64 ? 8 : BM == 128 ? 4 : 2;  // m-tiles per band: 2-3 MB of activations
   __shared__ __align__(16) unsigned char smem_raw[S::bytes];
   __shared__ int mt_start[TMAXG + 1];
   bf16* smem = reinterpret_cast<bf16*>(smem_raw);
@@ -190,17 +202,17 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
   const int mrows = min(BM, gr1 - m0);
   const int n0 = uniform(tn * BN), nrows = min(BN, P.n - n0);
 
-  // activation rows this thread stages: (tid >> 3) + 32 j, chunk tid & 7;
+  // activation rows this thread stages: tid / cpr + rpp j, chunk tid % cpr;
   // rows past the tile's end repeat its last row (their results are dropped)
-  constexpr int XJ = BM / 32;
+  constexpr int XJ = BM / S::rpp;
   const bf16* xsrc[XJ];
 #pragma unroll
   for (int j = 0; j < XJ; ++j) {
-    const int row = m0 + min((tid >> 3) + 32 * j, mrows - 1);
+    const int row = m0 + min(tid / S::cpr + S::rpp * j, mrows - 1);
     const int src = P.row_src ? P.row_src[row] : row;
-    xsrc[j] = reinterpret_cast<const bf16*>(P.x) + (int64_t)src * P.k + (tid & 7) * 8;
+    xsrc[j] = reinterpret_cast<const bf16*>(P.x) + (int64_t)src * P.k + (tid % S::cpr) * 8;
   }
-  using WL = TiledW<BN, WF>;
+  using WL = TiledW<BN, BK, WF>;
   WL wl;
   {
     int wrow[WL::J];
@@ -215,12 +227,12 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
     u32x4 x[XJ];
     typename WL::Regs w;
   };
-  const int nk = P.k / TBK;
+  const int nk = P.k / BK;
   // slices past the end re-read the last one (branch-free; never staged for use)
   auto fetch = [&](Regs& g, int ks) __attribute__((always_inline)) {
     ks = min(ks, nk - 1);
 #pragma unroll
-    for (int j = 0; j < XJ; ++j) g.x[j] = ld16(xsrc[j] + ks * TBK);
+    for (int j = 0; j < XJ; ++j) g.x[j] = ld16(xsrc[j] + ks * BK);
     wl.fetch(g.w, ks);
   };
   bool bad_scale = false;
@@ -228,8 +240,8 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
     bf16* xs = smem + buf * S::stage;
 #pragma unroll
     for (int j = 0; j < XJ; ++j)
-      st16(xs + ((tid >> 3) + 32 * j) * TLDK + (tid & 7) * 8, g.x[j]);
-    WL::store(g.w, xs + BM * TLDK, tid, bad_scale);
+      st16(xs + (tid / S::cpr + S::rpp * j) * LDK + (tid % S::cpr) * 8, g.x[j]);
+    WL::store(g.w, xs + BM * LDK, tid, bad_scale);
   };
 
   const int wm = wave & 1, wn = wave >> 1;
@@ -241,15 +253,15 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
     for (int mb = 0; mb < MT; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int fr = lane & 15, fk = 8 * (lane >> 4);
   auto compute = [&](int buf) __attribute__((always_inline)) {
-    const bf16* xs = smem + buf * S::stage + (wm * (BM / 2) + fr) * TLDK + fk;
-    const bf16* ws = smem + buf * S::stage + (BM + wn * (BN / 2) + fr) * TLDK + fk;
+    const bf16* xs = smem + buf * S::stage + (wm * (BM / 2) + fr) * LDK + fk;
+    const bf16* ws = smem + buf * S::stage + (BM + wn * (BN / 2) + fr) * LDK + fk;
 #pragma unroll
-    for (int c = 0; c < TBK / 32; ++c) {
+    for (int c = 0; c < BK / 32; ++c) {
       Frag<bf16> a[NT], b[MT];
 #pragma unroll
-      for (int nb = 0; nb < NT; ++nb) a[nb].load(ws + nb * 16 * TLDK + 32 * c);
+      for (int nb = 0; nb < NT; ++nb) a[nb].load(ws + nb * 16 * LDK + 32 * c);
 #pragma unroll
-      for (int mb = 0; mb < MT; ++mb) b[mb].load(xs + mb * 16 * TLDK + 32 * c);
+      for (int mb = 0; mb < MT; ++mb) b[mb].load(xs + mb * 16 * LDK + 32 * c);
 #pragma unroll
       for (int nb = 0; nb < NT; ++nb)
 #pragma unroll
@@ -276,9 +288,9 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
   fetch(rs[0], R);
   __builtin_amdgcn_sched_barrier(0);
   __syncthreads();
-  for (int ks = 0; ks < nk; ks += R) {
+  for (int ks = 0; ks < nk; ks += UN) {
 #pragma unroll
-    for (int u = 0; u < R; ++u) {
+    for (int u = 0; u < UN; ++u) {
       if (ks + u < nk) compute(u & 1);
       __builtin_amdgcn_sched_barrier(0);
       stage(rs[(u + 1) % R], (u + 1) & 1);
@@ -290,21 +302,28 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
   __syncthreads();  // the fp32 tile below reuses the operand buffers
   if (bad_scale) set_error(P.err, 16);
 
-  // acc[nb][mb][r] = C[m = wm*BM/2 + 16 mb + fr][n = wn*BN/2 + 16 nb + 4 (lane/16) + r]
+  // acc[nb][mb][r] = C[m = wm*BM/2 + 16 mb + fr][n = wn*BN/2 + 16 nb + 4 (lane/16) + r];
+  // the fp32 tile goes through LDS EP rows at a time
   float* cr = reinterpret_cast<float*>(smem_raw);
 #pragma unroll
-  for (int nb = 0; nb < NT; ++nb)
+  for (int e0 = 0; e0 < BM; e0 += S::EP) {
+    if (e0 >= mrows) break;  // uniform
 #pragma unroll
-    for (int mb = 0; mb < MT; ++mb) {
-      const int m = wm * (BM / 2) + mb * 16 + fr, n = wn * (BN / 2) + nb * 16 + 4 * (lane >> 4);
-      *reinterpret_cast<float4*>(cr + m * S::c_ld + n) =
-          make_float4(acc[nb][mb][0], acc[nb][mb][1], acc[nb][mb][2], acc[nb][mb][3]);
-    }
-  __syncthreads();
-  epilogue<bf16, EPI>(P, cr, S::c_ld, m0, mrows, n0 >> 4, nrows >> 4, grp);
+    for (int nb = 0; nb < NT; ++nb)
+#pragma unroll
+      for (int mb = 0; mb < MT; ++mb) {
+        const int m = wm * (BM / 2) + mb * 16 + fr, n = wn * (BN / 2) + nb * 16 + 4 * (lane >> 4);
+        if (m >= e0 && m < e0 + S::EP)  // the same for all lanes of a 16-row tile
+          *reinterpret_cast<float4*>(cr + (m - e0) * S::c_ld + n) =
+              make_float4(acc[nb][mb][0], acc[nb][mb][1], acc[nb][mb][2], acc[nb][mb][3]);
+      }
+    __syncthreads();
+    epilogue<bf16, EPI>(P, cr, S::c_ld, m0 + e0, min(S::EP, mrows - e0), n0 >> 4, nrows >> 4, grp);
+    __syncthreads();
+  }
 }
 
-template <int BM, int BN, int R, int WF>
+template <int BM, int BN, int BK, int R, int WF>
 static hipError_t tiled_launch(const Gemm& g, hipStream_t s) {
   // bound on the m-tiles of all groups: sum_g ceil(rows_g / BM) <= rows / BM + groups
   const int64_t mt_bound = g.group_off ? (int64_t)g.n_rows / BM + g.n_groups : ((int64_t)g.n_rows + BM - 1) / BM;
@@ -313,33 +332,36 @@ static hipError_t tiled_launch(const Gemm& g, hipStream_t s) {
   if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
   dim3 gd((unsigned)grid), bd(256);
   switch (g.epi) {
-    case EPI_QKV: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, R, EPI_QKV, WF>), gd, bd, 0, s, g); break;
-    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, R, EPI_RESIDUAL, WF>), gd, bd, 0, s, g); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, R, EPI_SWIGLU, WF>), gd, bd, 0, s, g); break;
-    default: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, R, EPI_BIAS, WF>), gd, bd, 0, s, g); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, EPI_QKV, WF>), gd, bd, 0, s, g); break;
+    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, EPI_RESIDUAL, WF>), gd, bd, 0, s, g); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, EPI_SWIGLU, WF>), gd, bd, 0, s, g); break;
+    default: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, EPI_BIAS, WF>), gd, bd, 0, s, g); break;
   }
   return hipGetLastError();
 }
 
 bool tiled_gemm_applies(int dtype, const Gemm& g) {
-  if (dtype != 1 || g.k % TBK || g.n % 16 || g.n_groups > TMAXG || g.n_rows < TILED_MIN_TOTAL_ROWS) return false;
+  if (dtype != 1 || g.k % 64 || g.n % 16 || g.n_groups > TMAXG || g.n_rows < TILED_MIN_TOTAL_ROWS) return false;
   return (int64_t)g.n_rows >= (int64_t)TILED_MIN_ROWS * g.n_groups;
 }
 
-// 128 x 128 tiles once groups average 128 rows and the launch still has a few
-// tiles per compute unit; 64-row tiles otherwise (less padding per group), and
-// 64 x 64 tiles for a single dense matrix that would not fill the chip.
+// Tile choice by rows per group and the number of tiles a launch has.
+// 128 x 128 tiles once groups average 128 rows with a few tiles per compute
+// unit; 64-row tiles otherwise (less padding per group), 64 x 64 for a single
+// dense matrix that would not fill the chip. (256 x 256 tiles with 128 x 128
+// wavefront quadrants measured slower: at one wavefront per SIMD the barrier
+// and LDS latencies of each slice are exposed.)
 hipError_t launch_gemm_tiled(int expert_fmt, const Gemm& g, hipStream_t s) {
-  const int64_t n_tn = (g.n + 127) / 128;
   const int64_t groups = g.group_off ? g.n_groups : 1;
-  const bool big = (int64_t)g.n_rows >= 128LL * g.n_groups && ((int64_t)g.n_rows / 128 + groups) * n_tn >= 1024;
+  auto tiles = [&](int bm, int bn) { return ((int64_t)g.n_rows / bm + groups) * ((g.n + bn - 1) / bn); };
+  const bool big = (int64_t)g.n_rows >= 128LL * g.n_groups && tiles(128, 128) >= 1024;
   if (expert_fmt != 0) {
     if (!g.w_scales) return hipErrorInvalidValue;
-    return big ? tiled_launch<128, 128, 2, 1>(g, s) : tiled_launch<64, 128, 4, 1>(g, s);
+    return big ? tiled_launch<128, 128, 64, 2, 1>(g, s) : tiled_launch<64, 128, 64, 4, 1>(g, s);
   }
-  if (big) return tiled_launch<128, 128, 2, 0>(g, s);
-  if (((int64_t)g.n_rows / 64 + groups) * n_tn < 512) return tiled_launch<64, 64, 4, 0>(g, s);
-  return tiled_launch<64, 128, 4, 0>(g, s);
+  if (big) return tiled_launch<128, 128, 64, 2, 0>(g, s);
+  if (tiles(64, 128) < 512) return tiled_launch<64, 64, 64, 4, 0>(g, s);
+  return tiled_launch<64, 128, 64, 4, 0>(g, s);
 }
 
 }  // namespace mcpu

@@ -375,3 +375,51 @@ def test_dense_projections_ragged_rows_sampled():
     g = {k: v[rows] for k, v in gpu.items()}
     ref, _ = reference(sub, g)
     compare_layer(sub, g, None, ref)
+
+
+@pytest.mark.parametrize("fmt", ["dense", "mxfp4"])
+def test_moe_forward_large_groups_sampled(fmt):
+    """16384 tokens routed over the experts (thousands of rows each): the
+    128 x 128-tile path with many tiles per group; tokens are independent given their routing, so a seeded sample of
+    rows is compared (the grouping still covers every token)."""
+    s = _moe_shape(1024, 1024, fmt)
+    T = 16384
+    wl = W.custom(s, [4], [1], 1091)
+    dw = mcpu.DeviceWeights(s, wl.weights)
+    h = W.synth_normal(9, 5, (T, s.hidden))
+    out = torch.empty((T, s.hidden), device="cuda")
+    idx = torch.empty((T, s.top_k), dtype=torch.int32, device="cuda")
+    wt = torch.empty((T, s.top_k), device="cuda")
+    ws = mcpu.workspace(mcpu.moe_forward_workspace_size(s, T))
+    mcpu.moe_forward(s, dw, h.cuda(), out, idx, wt, None, ws)
+    torch.cuda.synchronize()
+    assert mcpu.mcpu_check_device_errors(ws) == 0
+    rows = np.sort(np.random.default_rng(3).choice(T, 96, replace=False))
+    rows[0], rows[-1] = 0, T - 1
+    weights = O.Weights(s, wl.weights)
+    ref = O.moe(s, weights, h[torch.from_numpy(rows)])
+    g_idx = idx.cpu().numpy()[rows]
+    tie = PT.check_router(g_idx, ref["idx"], ref["logits"], s.top_k)
+    if tie.any():
+        f = ref["idx"].copy()
+        f[tie] = g_idx[tie]
+        ref = O.moe(s, weights, h[torch.from_numpy(rows)], force_idx=f)
+    PT.check("moe out", _np(out)[rows], ref["out"], "bf16")
+
+
+def test_dense_projections_large_rows_sampled():
+    """8200 decode tokens: the dense projections take 128 x 128 tiles with a
+    ragged last tile; compared on sampled sequences."""
+    rng = np.random.default_rng(1093)
+    ctx = rng.integers(1, 64, size=8200)
+    wl = W.custom(W.GPT_OSS_20B, ctx, np.ones(8200), 1093)
+    step = mcpu.DeviceStep(wl)
+    step.run()
+    torch.cuda.synchronize()
+    assert step.device_errors() == 0
+    seqs = sorted({0, 255, 256, 8191, 8199} | {int(b) for b in rng.choice(8200, 4, replace=False)})
+    sub, rows = W.restrict(wl, seqs)
+    r = torch.from_numpy(np.asarray(rows, np.int64)).cuda()
+    g = dict(out=_np(step.x_out.index_select(0, r)), idx=step.topk_idx.index_select(0, r).cpu().numpy())
+    ref, _ = reference(sub, g)
+    PT.check("out", g["out"], ref["out"], "bf16")
