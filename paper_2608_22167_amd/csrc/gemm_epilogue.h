@@ -1,5 +1,6 @@
-// Shared pieces of the GEMM kernels: the weight-row order of a 16-row block
-// and the fused epilogues that finish an fp32 output tile held in LDS.
+// Shared pieces of the GEMM kernels: the weight-row order of a 16-row block,
+// the work-item order of the LDS-tiled kernels and the fused epilogues that
+// finish an fp32 output tile held in LDS.
 //   EPI_QKV      + bias, rotary embedding of q and k, q to the q buffer and
 //                k / v straight into their KV-cache pages (the append)
 //   EPI_RESIDUAL + bias + residual (fp32), e.g. h1 = x + o W_o^T + b_o
@@ -22,6 +23,78 @@ __device__ __forceinline__ int block_row(const Gemm& P, int blk, int nl) {
     return head * D + (nl < 8 ? 8 * ti + nl : D / 2 + 8 * ti + nl - 8);
   }
   return blk * 16 + nl;
+}
+
+constexpr int TILE_MAXG = 256;  // groups (experts) one tiled launch supports
+
+// Position of local item L of a group with mt_g m-tiles and n_tn n-tiles, in
+// bands of GM m-tiles (the last band may be shorter).
+template <int GM>
+__device__ __forceinline__ void band_order(int L, int mt_g, int n_tn, int& mt, int& tn) {
+  const int full = mt_g / GM;
+  if (L < full * GM * n_tn) {
+    const int b = L / (GM * n_tn), r = L - b * (GM * n_tn);
+    tn = r / GM;
+    mt = b * GM + (r - tn * GM);
+  } else {
+    const int rem = mt_g - full * GM, r = L - full * GM * n_tn;
+    tn = r / rem;
+    mt = full * GM + (r - tn * rem);
+  }
+}
+
+// Work item of this workgroup in a tiled launch: (group, m-tile, n-tile) of a
+// BM x BN tiling of every group's rows against the n weight rows. mt_start
+// (LDS, TILE_MAXG + 1 ints) receives the exclusive prefix of m-tiles per group,
+// computed from group_off on the device so the host only bounds the grid.
+// Items are cut into eight contiguous ranges, one per XCD (workgroups are
+// dealt to the XCDs round robin), so that a band's reuse stays in one L2.
+// Returns false for a workgroup past the last item. Contains a barrier: every
+// thread of the workgroup calls it.
+template <int BM, int BN, int GM>
+__device__ bool tile_of_block(const Gemm& P, int* mt_start, int& grp, int& mt, int& tn) {
+  const int lane = threadIdx.x & 63, wave = uniform((int)threadIdx.x >> 6);
+  const int G = P.n_groups;
+  if (wave == 0) {  // one wavefront, 64 groups per pass
+    int carry = 0;
+    for (int g0 = 0; g0 < G; g0 += 64) {
+      const int g = g0 + lane;
+      int cnt = 0;
+      if (g < G) {
+        const int r0 = P.group_off ? P.group_off[g] : 0;
+        const int r1 = P.group_off ? P.group_off[g + 1] : P.n_rows;
+        cnt = (max(r1 - r0, 0) + BM - 1) / BM;
+      }
+      const int incl = wave_incl_scan(cnt);
+      if (g < G) mt_start[g] = carry + incl - cnt;
+      carry += __shfl(incl, 63, 64);
+    }
+    if (lane == 0) mt_start[G] = carry;
+  }
+  __syncthreads();
+  const int n_tn = (P.n + BN - 1) / BN;
+  const int total = mt_start[G] * n_tn;
+  const int chunk = (total + 7) >> 3;
+  const int local = blockIdx.x >> 3;
+  const int item = (blockIdx.x & 7) * chunk + local;
+  if (local >= chunk || item >= total) return false;
+  // group of the item: last g with mt_start[g] * n_tn <= item (each group owns mt_g * n_tn items)
+  int lo = 0, hi = G - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (mt_start[mid] * n_tn <= item) lo = mid; else hi = mid - 1;
+  }
+  grp = uniform(lo);
+  band_order<GM>(item - mt_start[grp] * n_tn, mt_start[grp + 1] - mt_start[grp], n_tn, mt, tn);
+  return true;
+}
+
+// Grid bound of a tiled launch: sum_g ceil(rows_g / BM) <= rows / BM + groups
+// m-tiles, rounded up to whole rounds of the eight XCDs.
+inline int64_t tile_grid(const Gemm& g, int bm, int bn) {
+  const int64_t mt_bound = g.group_off ? (int64_t)g.n_rows / bm + g.n_groups : ((int64_t)g.n_rows + bm - 1) / bm;
+  const int64_t items = mt_bound * ((g.n + bn - 1) / bn);
+  return (items + 7) / 8 * 8;
 }
 
 __device__ __forceinline__ float swiglu(float gate, float up, float alpha, float limit, float beta) {

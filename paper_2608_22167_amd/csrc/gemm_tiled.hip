@@ -29,8 +29,6 @@
 
 namespace mcpu {
 
-constexpr int TMAXG = 256;  // groups (experts) one launch supports
-
 // 16-byte staging registers as a native vector type: copies of HIP's uint4
 // struct become memcpy calls that keep the register sets in scratch memory.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -41,7 +39,7 @@ __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4
 // 16 B (BK = 64: 144 B apart; BK = 32: 80 B apart), which spreads the eight
 // 16-byte fragment reads a cycle serves over all banks. The fp32 output tile
 // reuses the operand buffers, EP rows at a time.
-template <int BM, int BN, int BK>
+template <int BM, int BN, int BK, int NTH>
 struct TiledSmem {
   static constexpr int ldk = BK + 8;              // LDS row stride in bf16
   static constexpr int stage = (BM + BN) * ldk;   // bf16 elements per stage
@@ -51,13 +49,13 @@ struct TiledSmem {
   static_assert(EP * c_ld * 4 <= ab_bytes, "an epilogue pass must fit the operand buffers");
   static constexpr int bytes = ab_bytes;
   static constexpr int cpr = BK / 8;              // 16-byte chunks per staged row
-  static constexpr int rpp = 256 / cpr;           // rows one pass of the workgroup stages
+  static constexpr int rpp = NTH / cpr;           // rows one pass of the workgroup stages
 };
 
 // Staged weight rows: dense bf16 (16-byte chunks, BK / 8 per row and slice) ...
-template <int BN, int BK, int WF>
+template <int BN, int BK, int WF, int NTH>
 struct TiledW {
-  static constexpr int cpr = BK / 8, rpp = 256 / cpr;
+  static constexpr int cpr = BK / 8, rpp = NTH / cpr;
   static constexpr int J = BN / rpp;
   struct Regs {
     u32x4 r[J];
@@ -82,19 +80,19 @@ struct TiledW {
 
 // ... or MXFP4: per row and slice BK / 2 code bytes (BK / 32 scale blocks)
 // and BK / 32 E8M0 scales; a thread stages one block of 32 weights per chunk.
-template <int BN, int BK>
-struct TiledW<BN, BK, 1> {
+template <int BN, int BK, int NTH>
+struct TiledW<BN, BK, 1, NTH> {
   static constexpr int bpr = BK / 32;  // scale blocks per row and slice
-  static constexpr int J = BN * bpr / 256;
-  static_assert(J >= 1 && BN * bpr % 256 == 0, "whole scale blocks per thread");
+  static constexpr int J = BN * bpr / NTH;
+  static_assert(J >= 1 && BN * bpr % NTH == 0, "whole scale blocks per thread");
   struct Regs {
     u32x4 r[J];
     uint32_t s[J];
   };
   const uint8_t* csrc[J];
   const uint8_t* ssrc[J];
-  static __device__ __forceinline__ int row(int tid, int j) { return (tid + 256 * j) / bpr; }
-  static __device__ __forceinline__ int blk(int tid, int j) { return (tid + 256 * j) % bpr; }
+  static __device__ __forceinline__ int row(int tid, int j) { return (tid + NTH * j) / bpr; }
+  static __device__ __forceinline__ int blk(int tid, int j) { return (tid + NTH * j) % bpr; }
   __device__ __forceinline__ void init(const Gemm& P, int grp, const int* wrow, int tid) {
 #pragma unroll
     for (int j = 0; j < J; ++j) {
@@ -133,69 +131,20 @@ struct TiledW<BN, BK, 1> {
   }
 };
 
-// Position of local item L of a group with mt_g m-tiles and n_tn n-tiles, in
-// bands of GM m-tiles (the last band may be shorter).
-template <int GM>
-__device__ __forceinline__ void band_order(int L, int mt_g, int n_tn, int& mt, int& tn) {
-  const int full = mt_g / GM;
-  if (L < full * GM * n_tn) {
-    const int b = L / (GM * n_tn), r = L - b * (GM * n_tn);
-    tn = r / GM;
-    mt = b * GM + (r - tn * GM);
-  } else {
-    const int rem = mt_g - full * GM, r = L - full * GM * n_tn;
-    tn = r / rem;
-    mt = full * GM + (r - tn * rem);
-  }
-}
-
-template <int BM, int BN, int BK, int R, int EPI, int WF>
-__global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
+template <int BM, int BN, int BK, int R, int NW, int EPI, int WF>
+__global__ __launch_bounds__(NW * 64) void gemm_tiled_kernel(Gemm P) {
   static_assert(R == 1 || R % 2 == 0, "the unrolled ring must cover both LDS buffers");
   constexpr int UN = R == 1 ? 2 : R;  // loop unroll: a multiple of the ring and of the two buffers
-  using S = TiledSmem<BM, BN, BK>;
+  constexpr int NTH = NW * 64;
+  using S = TiledSmem<BM, BN, BK, NTH>;
   constexpr int LDK = S::ldk;
   constexpr int GM = BM == 64 ? 8 : BM == 128 ? 4 : 2;  // m-tiles per band: 2-3 MB of activations
   __shared__ __align__(16) unsigned char smem_raw[S::bytes];
-  __shared__ int mt_start[TMAXG + 1];
+  __shared__ int mt_start[TILE_MAXG + 1];
   bf16* smem = reinterpret_cast<bf16*>(smem_raw);
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
-  const int G = P.n_groups;
-
-  // exclusive prefix of m-tiles per group (one wavefront, 64 groups per pass)
-  if (wave == 0) {
-    int carry = 0;
-    for (int g0 = 0; g0 < G; g0 += 64) {
-      const int g = g0 + lane;
-      int cnt = 0;
-      if (g < G) {
-        const int r0 = P.group_off ? P.group_off[g] : 0;
-        const int r1 = P.group_off ? P.group_off[g + 1] : P.n_rows;
-        cnt = (max(r1 - r0, 0) + BM - 1) / BM;
-      }
-      const int incl = wave_incl_scan(cnt);
-      if (g < G) mt_start[g] = carry + incl - cnt;
-      carry += __shfl(incl, 63, 64);
-    }
-    if (lane == 0) mt_start[G] = carry;
-  }
-  __syncthreads();
-
-  const int n_tn = (P.n + BN - 1) / BN;
-  const int total = mt_start[G] * n_tn;
-  const int chunk = (total + 7) >> 3;
-  const int local = blockIdx.x >> 3;
-  const int item = (blockIdx.x & 7) * chunk + local;
-  if (local >= chunk || item >= total) return;
-  // group of the item: last g with mt_start[g] * n_tn <= item (each group owns mt_g * n_tn items)
-  int lo = 0, hi = G - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (mt_start[mid] * n_tn <= item) lo = mid; else hi = mid - 1;
-  }
-  const int grp = uniform(lo);
-  int mt, tn;
-  band_order<GM>(item - mt_start[grp] * n_tn, mt_start[grp + 1] - mt_start[grp], n_tn, mt, tn);
+  int grp, mt, tn;
+  if (!tile_of_block<BM, BN, GM>(P, mt_start, grp, mt, tn)) return;
   const int gr0 = P.group_off ? P.group_off[grp] : 0;
   const int gr1 = P.group_off ? P.group_off[grp + 1] : P.n_rows;
   const int m0 = uniform(gr0 + mt * BM);
@@ -212,7 +161,7 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
     const int src = P.row_src ? P.row_src[row] : row;
     xsrc[j] = reinterpret_cast<const bf16*>(P.x) + (int64_t)src * P.k + (tid % S::cpr) * 8;
   }
-  using WL = TiledW<BN, BK, WF>;
+  using WL = TiledW<BN, BK, WF, NTH>;
   WL wl;
   {
     int wrow[WL::J];
@@ -244,8 +193,10 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
     WL::store(g.w, xs + BM * LDK, tid, bad_scale);
   };
 
+  // wavefronts in 2 x NW/2: each owns BM/2 token rows and BN/(NW/2) weight rows
+  constexpr int WN = BN / (NW / 2);
   const int wm = wave & 1, wn = wave >> 1;
-  constexpr int MT = BM / 32, NT = BN / 32;  // 16-row tiles per wavefront quadrant
+  constexpr int MT = BM / 32, NT = WN / 16;  // 16-row tiles per wavefront
   f32x4 acc[NT][MT];
 #pragma unroll
   for (int nb = 0; nb < NT; ++nb)
@@ -254,7 +205,7 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
   const int fr = lane & 15, fk = 8 * (lane >> 4);
   auto compute = [&](int buf) __attribute__((always_inline)) {
     const bf16* xs = smem + buf * S::stage + (wm * (BM / 2) + fr) * LDK + fk;
-    const bf16* ws = smem + buf * S::stage + (BM + wn * (BN / 2) + fr) * LDK + fk;
+    const bf16* ws = smem + buf * S::stage + (BM + wn * WN + fr) * LDK + fk;
 #pragma unroll
     for (int c = 0; c < BK / 32; ++c) {
       Frag<bf16> a[NT], b[MT];
@@ -312,7 +263,7 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
     for (int nb = 0; nb < NT; ++nb)
 #pragma unroll
       for (int mb = 0; mb < MT; ++mb) {
-        const int m = wm * (BM / 2) + mb * 16 + fr, n = wn * (BN / 2) + nb * 16 + 4 * (lane >> 4);
+        const int m = wm * (BM / 2) + mb * 16 + fr, n = wn * WN + nb * 16 + 4 * (lane >> 4);
         if (m >= e0 && m < e0 + S::EP)  // the same for all lanes of a 16-row tile
           *reinterpret_cast<float4*>(cr + (m - e0) * S::c_ld + n) =
               make_float4(acc[nb][mb][0], acc[nb][mb][1], acc[nb][mb][2], acc[nb][mb][3]);
@@ -323,45 +274,42 @@ __global__ __launch_bounds__(256) void gemm_tiled_kernel(Gemm P) {
   }
 }
 
-template <int BM, int BN, int BK, int R, int WF>
+template <int BM, int BN, int BK, int R, int NW, int WF>
 static hipError_t tiled_launch(const Gemm& g, hipStream_t s) {
-  // bound on the m-tiles of all groups: sum_g ceil(rows_g / BM) <= rows / BM + groups
-  const int64_t mt_bound = g.group_off ? (int64_t)g.n_rows / BM + g.n_groups : ((int64_t)g.n_rows + BM - 1) / BM;
-  const int64_t items = mt_bound * ((g.n + BN - 1) / BN);
-  const int64_t grid = (items + 7) / 8 * 8;
+  const int64_t grid = tile_grid(g, BM, BN);
   if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
-  dim3 gd((unsigned)grid), bd(256);
+  dim3 gd((unsigned)grid), bd(NW * 64);
   switch (g.epi) {
-    case EPI_QKV: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, EPI_QKV, WF>), gd, bd, 0, s, g); break;
-    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, EPI_RESIDUAL, WF>), gd, bd, 0, s, g); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, EPI_SWIGLU, WF>), gd, bd, 0, s, g); break;
-    default: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, EPI_BIAS, WF>), gd, bd, 0, s, g); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, NW, EPI_QKV, WF>), gd, bd, 0, s, g); break;
+    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, NW, EPI_RESIDUAL, WF>), gd, bd, 0, s, g); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, NW, EPI_SWIGLU, WF>), gd, bd, 0, s, g); break;
+    default: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, NW, EPI_BIAS, WF>), gd, bd, 0, s, g); break;
   }
   return hipGetLastError();
 }
 
 bool tiled_gemm_applies(int dtype, const Gemm& g) {
-  if (dtype != 1 || g.k % 64 || g.n % 16 || g.n_groups > TMAXG || g.n_rows < TILED_MIN_TOTAL_ROWS) return false;
+  if (dtype != 1 || g.k <= 0 || g.k % 64 || g.n % 16 || g.n_groups > TILE_MAXG || g.n_rows < TILED_MIN_TOTAL_ROWS) return false;
   return (int64_t)g.n_rows >= (int64_t)TILED_MIN_ROWS * g.n_groups;
 }
 
-// Tile choice by rows per group and the number of tiles a launch has.
-// 128 x 128 tiles once groups average 128 rows with a few tiles per compute
-// unit; 64-row tiles otherwise (less padding per group), 64 x 64 for a single
-// dense matrix that would not fill the chip. (256 x 256 tiles with 128 x 128
-// wavefront quadrants measured slower: at one wavefront per SIMD the barrier
-// and LDS latencies of each slice are exposed.)
+// Tile choice by rows per group and the number of tiles a launch has: the
+// pipelined 256 x 256 kernel (gemm_pipe.hip) once groups average 256 rows
+// with two tiles per compute unit; else 128 x 128 tiles once they average 128
+// rows with a few tiles per compute unit; 64-row tiles otherwise (less
+// padding per group), 64 x 64 for a single dense matrix that would not fill
+// the chip.
 hipError_t launch_gemm_tiled(int expert_fmt, const Gemm& g, hipStream_t s) {
+  if (expert_fmt != 0 && !g.w_scales) return hipErrorInvalidValue;
+  if (pipe_gemm_applies(1, g)) return launch_gemm_pipe(expert_fmt, g, s);
   const int64_t groups = g.group_off ? g.n_groups : 1;
   auto tiles = [&](int bm, int bn) { return ((int64_t)g.n_rows / bm + groups) * ((g.n + bn - 1) / bn); };
   const bool big = (int64_t)g.n_rows >= 128LL * g.n_groups && tiles(128, 128) >= 1024;
-  if (expert_fmt != 0) {
-    if (!g.w_scales) return hipErrorInvalidValue;
-    return big ? tiled_launch<128, 128, 64, 2, 1>(g, s) : tiled_launch<64, 128, 64, 4, 1>(g, s);
-  }
-  if (big) return tiled_launch<128, 128, 64, 2, 0>(g, s);
-  if (tiles(64, 128) < 512) return tiled_launch<64, 64, 64, 4, 0>(g, s);
-  return tiled_launch<64, 128, 64, 4, 0>(g, s);
+  if (expert_fmt != 0)
+    return big ? tiled_launch<128, 128, 64, 2, 4, 1>(g, s) : tiled_launch<64, 128, 64, 4, 4, 1>(g, s);
+  if (big) return tiled_launch<128, 128, 64, 2, 4, 0>(g, s);
+  if (tiles(64, 128) < 512) return tiled_launch<64, 64, 64, 4, 4, 0>(g, s);
+  return tiled_launch<64, 128, 64, 4, 4, 0>(g, s);
 }
 
 }  // namespace mcpu

@@ -134,6 +134,10 @@ constexpr int TILED_MIN_ROWS = 16;
 constexpr int TILED_MIN_TOTAL_ROWS = 128;
 bool tiled_gemm_applies(int dtype, const Gemm& g);
 hipError_t launch_gemm_tiled(int expert_fmt, const Gemm& g, hipStream_t s);
+// Software-pipelined 256 x 256 tiles once groups average 256 rows and the
+// launch has at least two tiles per compute unit (bf16 activations, k % 32 == 0).
+bool pipe_gemm_applies(int dtype, const Gemm& g);
+hipError_t launch_gemm_pipe(int expert_fmt, const Gemm& g, hipStream_t s);
 
 // ---- norms, router, permutation, combine --------------------------------
 
