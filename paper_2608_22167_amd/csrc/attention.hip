@@ -474,11 +474,14 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
   // 2^RESCALE); every weight uses the same m as its normaliser, so the result
   // is the same quotient.
   constexpr float RESCALE = 8.0f;
-  float m_run[4];
+  const float inv_scale = 1.0f / P.scale_log2;
+  float m_run[4], m_sub[4], thr[4];
   f32x4 acc[D / 16][4], accl[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     m_run[j] = -INFINITY;
+    m_sub[j] = 0.f;
+    thr[j] = -INFINITY;
     accl[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int n = 0; n < D / 16; ++n) acc[n][j] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -512,7 +515,11 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
         for (int cc = 0; cc < D / 32; ++cc) sc[pg][j] = mma32(kf[cc], qf[j][cc], sc[pg][j]);
       }
     }
-    if (edge) {  // wave-uniform: mask keys outside each column's range
+    // wave-uniform: mask keys outside each column's range. The empty asm
+    // keeps this a branch: if-converted, its compares and selects would run
+    // on every step.
+    if (__builtin_expect(edge, 0)) {
+      asm volatile("");
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int hi = pos[j], lo_c = P.window > 0 ? pos[j] - P.window + 1 : 0;
@@ -526,24 +533,31 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
           }
       }
     }
-    float mstep[4];
+    // Each lane takes the largest of its 8 raw scores per column; the step
+    // rescales only when one of them exceeds the column's threshold
+    // (m + RESCALE in raw score units), and only then forms the column
+    // maximum across the four row groups.
+    float mloc[4];
     bool raise = false;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      float mx = fmaxf(fmaxf(fmaxf(sc[0][j][0], sc[0][j][1]), fmaxf(sc[0][j][2], sc[0][j][3])),
-                       fmaxf(fmaxf(sc[1][j][0], sc[1][j][1]), fmaxf(sc[1][j][2], sc[1][j][3])));
-      mstep[j] = max_over_rows(mx) * P.scale_log2;
-      raise = raise || mstep[j] > m_run[j] + RESCALE;
+      mloc[j] = vmax(vmax(vmax(sc[0][j][0], sc[0][j][1]), vmax(sc[0][j][2], sc[0][j][3])),
+                     vmax(vmax(sc[1][j][0], sc[1][j][1]), vmax(sc[1][j][2], sc[1][j][3])));
+      raise = raise || mloc[j] > thr[j];
     }
-    if (__builtin_amdgcn_ballot_w64(raise)) {  // wave-uniform rescale
+    if (__builtin_expect(__builtin_amdgcn_ballot_w64(raise) != 0, 0)) {  // wave-uniform rescale (kept a branch)
+      asm volatile("");
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float m_new = fmaxf(m_run[j], mstep[j]);
+        const float mstep = max_over_rows(mloc[j]) * P.scale_log2;
+        const float m_new = fmaxf(m_run[j], mstep);
         const float alpha = m_new == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f(m_run[j] - m_new);
         accl[j] *= alpha;
 #pragma unroll
         for (int n = 0; n < D / 16; ++n) acc[n][j] *= alpha;
         m_run[j] = m_new;
+        m_sub[j] = m_new == -INFINITY ? 0.f : m_new;  // masked scores give 2^-inf = 0
+        thr[j] = (m_new + RESCALE) * inv_scale;
       }
     }
     Frag4<T> va[D / 16], vb[D / 16];
@@ -554,7 +568,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const float msub = m_run[j] == -INFINITY ? 0.f : m_run[j];  // masked scores give 2^-inf = 0
+      const float msub = m_sub[j];
       float pa[4], pb[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {

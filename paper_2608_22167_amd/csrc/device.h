@@ -186,13 +186,18 @@ __device__ __forceinline__ f32x4 mma32_p(const Frag4<float>& Va, const Frag4<flo
 
 // Maximum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (the four 16-lane rows
 // holding one accumulator column), with the gfx950 row-swap permutes.
+// Maximum that propagates NaN (IEEE 754-2019 maximum). Unlike fmaxf it needs
+// no quieting of its operands, so a max over products is one v_maximum3_f32
+// per two or three values instead of a canonicalising v_max per operand.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+
 __device__ __forceinline__ float max_over_rows(float v) {
   uint32_t u = __float_as_uint(v);
   auto a = __builtin_amdgcn_permlane32_swap(u, u, false, false);  // rows {0,1} vs {2,3}
-  v = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  v = vmax(__uint_as_float(a[0]), __uint_as_float(a[1]));
   u = __float_as_uint(v);
   auto b = __builtin_amdgcn_permlane16_swap(u, u, false, false);  // rows {0,2} vs {1,3}
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+  return vmax(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
