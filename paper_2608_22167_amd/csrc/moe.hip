@@ -1,10 +1,11 @@
 // Normalisation, router, token permutation and expert combine for gfx950.
 //
 //  rmsnorm      one workgroup per token: y = x / sqrt(mean(x^2) + eps) * g
-//  router       one workgroup per token: RMSNorm of the residual stream in
-//               fp32, fp32 router logits (bf16 router weights widened
-//               exactly), top-k by wavefront arg-max reductions (ties to the
-//               lower expert id), softmax over the selected logits
+//  router       RMSNorm of the residual stream in fp32, fp32 router logits
+//               (bf16 router weights widened exactly), top-k (ties to the
+//               lower expert id), softmax over the selected logits: one
+//               workgroup per token for small batches, 16 tokens per
+//               workgroup with fp32 matrix-core products for large ones
 //  permute      per-expert histogram, exclusive scan, and a stable placement
 //               of every (token, slot) assignment into expert-sorted rows
 //               using wavefront ballots; no atomics on the placement, so the
@@ -269,6 +270,171 @@ __global__ __launch_bounds__(256) void router_kernel(Router P) {
   }
 }
 
+// Router for many tokens: a workgroup owns 16 tokens, so the router weights
+// are read once per 16 tokens instead of once per token, and its four
+// wavefronts split the reduction into quarters. Pass 1 sums the squares of
+// each token's residual row; pass 2 normalises it (hn is written in the layer
+// dtype) and feeds the fp32 matrix-core product logits^T = W_r hn^T in
+// 16 x 16 x 4 tiles (16 experts x 16 tokens). A lane loads four consecutive
+// reduction indices of its expert row and token row and spends one per
+// product, so both operands see the same index order; RU independent
+// accumulator chains keep loads of later indices in flight. The quarters'
+// logits meet in LDS, and lanes 0-15 of wavefront 0 take one token each for
+// the top-k (ties to the lower expert id) and the softmax.
+constexpr int RT_TOK = 16;
+constexpr int ROUTER_TILED_MIN_TOKENS = 1024;
+
+template <typename T> struct Raw4;
+template <> struct Raw4<float> {
+  __device__ __forceinline__ static float4 load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+};
+template <> struct Raw4<bf16> {
+  __device__ __forceinline__ static float4 load(const bf16* p) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u), __uint_as_float(u.y << 16),
+                       __uint_as_float(u.y & 0xFFFF0000u));
+  }
+};
+
+template <typename T, int EB>
+__global__ __launch_bounds__(256) void router_tiled_kernel(Router P) {
+  constexpr int EMAX = 16 * EB, RU = 4;
+  __shared__ float lg[4][RT_TOK][EMAX + 1];
+  __shared__ float ssq[4][RT_TOK];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tok0 = blockIdx.x * RT_TOK;
+  const int H = P.hidden, E = P.n_experts, HQ = H / 4;
+  const int c = lane & 15, grp = lane >> 4;
+  const bool live = tok0 + c < P.n_tokens;
+  const int t = live ? tok0 + c : P.n_tokens - 1;  // rows past the end repeat the last (dropped)
+  const int k_begin = wave * HQ + 4 * grp, k_end = (wave + 1) * HQ;
+  const float* hrow = P.h + (int64_t)t * H;
+
+  float ssu[RU] = {};  // RU loads in flight
+  int k = k_begin;
+  for (; k + 16 * (RU - 1) < k_end; k += 16 * RU) {
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      const float4 v = *reinterpret_cast<const float4*>(hrow + k + 16 * u);
+      ssu[u] += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+    }
+  }
+  for (; k < k_end; k += 16) {
+    const float4 v = *reinterpret_cast<const float4*>(hrow + k);
+    ssu[0] += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < RU; ++u) ss += ssu[u];
+  ss += __shfl_xor(ss, 16, 64);
+  ss += __shfl_xor(ss, 32, 64);
+  if (grp == 0) ssq[wave][c] = ss;
+  __syncthreads();
+  const float inv = 1.0f / sqrtf((ssq[0][c] + ssq[1][c] + ssq[2][c] + ssq[3][c]) / (float)H + P.eps);
+
+  const T* wr = reinterpret_cast<const T*>(P.w_r);
+  const T* wrow[EB];
+#pragma unroll
+  for (int b = 0; b < EB; ++b) wrow[b] = wr + (int64_t)min(16 * b + c, E - 1) * H;  // rows past E: dropped
+  T* hq = reinterpret_cast<T*>(P.hn_out) + (int64_t)t * H;
+  f32x4 acc[RU][EB];
+#pragma unroll
+  for (int u = 0; u < RU; ++u)
+#pragma unroll
+    for (int b = 0; b < EB; ++b) acc[u][b] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // per group of RU indices: every load, then the products, then the hn
+  // stores (a store between loads would serialise them)
+  auto group = [&](int k0, int n) __attribute__((always_inline)) {
+    float4 v[RU], g[RU], w[RU][EB];
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      if (u < n) {
+        v[u] = *reinterpret_cast<const float4*>(hrow + k0 + 16 * u);
+        g[u] = *reinterpret_cast<const float4*>(P.g2 + k0 + 16 * u);
+#pragma unroll
+        for (int b = 0; b < EB; ++b) w[u][b] = Raw4<T>::load(wrow[b] + k0 + 16 * u);
+      }
+    }
+    float4 hn[RU];
+#pragma unroll
+    for (int u = 0; u < RU; ++u) {
+      if (u < n) {
+        hn[u] = make_float4(v[u].x * inv * g[u].x, v[u].y * inv * g[u].y, v[u].z * inv * g[u].z,
+                            v[u].w * inv * g[u].w);
+#pragma unroll
+        for (int b = 0; b < EB; ++b) {
+          acc[u][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[u][b].x, hn[u].x, acc[u][b], 0, 0, 0);
+          acc[u][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[u][b].y, hn[u].y, acc[u][b], 0, 0, 0);
+          acc[u][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[u][b].z, hn[u].z, acc[u][b], 0, 0, 0);
+          acc[u][b] = __builtin_amdgcn_mfma_f32_16x16x4f32(w[u][b].w, hn[u].w, acc[u][b], 0, 0, 0);
+        }
+      }
+    }
+    // rows past the end rewrite the last row's identical values
+#pragma unroll
+    for (int u = 0; u < RU; ++u)
+      if (u < n) store4(hq + k0 + 16 * u, hn[u]);
+  };
+  k = k_begin;
+  for (; k + 16 * (RU - 1) < k_end; k += 16 * RU) group(k, RU);
+  for (; k < k_end; k += 16) group(k, 1);
+  // acc[.][b][r] = partial logit of expert 16 b + 4 grp + r for token c
+#pragma unroll
+  for (int b = 0; b < EB; ++b)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float v = 0.f;
+#pragma unroll
+      for (int u = 0; u < RU; ++u) v += acc[u][b][r];
+      lg[wave][c][16 * b + 4 * grp + r] = v;
+    }
+  __syncthreads();
+  if (wave == 0 && lane < RT_TOK && tok0 + lane < P.n_tokens) {
+    const int tk = tok0 + lane, K = P.top_k;
+    float* L = lg[0][lane];
+    for (int e = 0; e < E; ++e) {
+      const float v = L[e] + lg[1][lane][e] + lg[2][lane][e] + lg[3][lane][e] + P.b_r[e];
+      L[e] = v;
+      if (P.logits_out) P.logits_out[(int64_t)tk * E + e] = v;
+    }
+    int sel_e[8];
+    float sel_v[8];
+    uint64_t taken = 0;
+    for (int s = 0; s < K; ++s) {
+      int e = 0;
+      if (P.force_idx) {
+        e = P.force_idx[(int64_t)tk * K + s];
+        if (e < 0 || e >= E) {
+          set_error(P.err, 4);
+          e = 0;
+        }
+      } else {
+        float bv = -INFINITY;
+        e = -1;
+        for (int x = 0; x < E; ++x)  // first maximum among the rest: ties to the lower id
+          if (!((taken >> x) & 1) && (e < 0 || L[x] > bv)) {
+            bv = L[x];
+            e = x;
+          }
+        taken |= 1ull << e;
+      }
+      sel_e[s] = e;
+      sel_v[s] = L[e];
+    }
+    float mx = sel_v[0];
+    for (int s = 1; s < K; ++s) mx = fmaxf(mx, sel_v[s]);
+    float den = 0.f, wv[8];
+    for (int s = 0; s < K; ++s) {
+      wv[s] = expf(sel_v[s] - mx);
+      den += wv[s];
+    }
+    for (int s = 0; s < K; ++s) {
+      P.idx_out[(int64_t)tk * K + s] = sel_e[s];
+      P.w_out[(int64_t)tk * K + s] = wv[s] / den;
+    }
+  }
+}
+
 template <typename T, int E>
 static void router_nv(const Router& p, hipStream_t s) {
   const int nv = (p.hidden + 1023) / 1024;
@@ -288,10 +454,23 @@ static void router_e(const Router& p, hipStream_t s) {
   else router_nv<T, 64>(p, s);
 }
 
+template <typename T>
+static void router_tiled(const Router& p, hipStream_t s) {
+  dim3 g((p.n_tokens + RT_TOK - 1) / RT_TOK), b(256);
+  if (p.n_experts <= 16) hipLaunchKernelGGL((router_tiled_kernel<T, 1>), g, b, 0, s, p);
+  else if (p.n_experts <= 32) hipLaunchKernelGGL((router_tiled_kernel<T, 2>), g, b, 0, s, p);
+  else hipLaunchKernelGGL((router_tiled_kernel<T, 4>), g, b, 0, s, p);
+}
+
 hipError_t launch_router(int dtype, const Router& p, hipStream_t s) {
   if (p.n_tokens == 0) return hipSuccess;
   if (p.hidden > ROUTER_MAX_H || p.hidden % 8 || p.n_experts > ROUTER_MAX_E || p.top_k > 8)
     return hipErrorInvalidValue;
+  if (p.n_tokens >= ROUTER_TILED_MIN_TOKENS && p.hidden % 64 == 0) {
+    if (dtype == 0) router_tiled<float>(p, s);
+    else router_tiled<bf16>(p, s);
+    return hipGetLastError();
+  }
   if (dtype == 0) router_e<float>(p, s);
   else router_e<bf16>(p, s);
   return hipGetLastError();

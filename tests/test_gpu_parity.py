@@ -238,9 +238,19 @@ def test_kv_pages_append_bit_exact():
     np.testing.assert_array_equal(step_pools[1].cpu().float().numpy(), vr)
 
 
-@pytest.mark.parametrize("kind", ["tiny_f32", "bf16"])
+@pytest.mark.parametrize("kind", ["tiny_f32", "bf16", "tiny_f32_t1100", "bf16_t1030"])
 def test_moe_forward_and_forced_selection(kind):
-    wl = W.tiny_f32(seed=1051, batch=24) if kind == "tiny_f32" else _bf16_small(seed=1052)
+    """Per-token router below 1024 tokens, the 16-tokens-per-workgroup router
+    from 1024 on (1100 and 1030 tokens: a ragged last workgroup)."""
+    if kind == "tiny_f32":
+        wl = W.tiny_f32(seed=1051, batch=24)
+    elif kind == "tiny_f32_t1100":
+        wl = W.tiny_f32(seed=1053, batch=1100)
+    elif kind == "bf16":
+        wl = _bf16_small(seed=1052)
+    else:
+        shape = replace(W.GPT_OSS_20B, hidden=512, n_q_heads=8, n_kv_heads=2, ffn_dim=512)  # 32 experts, top 4
+        wl = W.custom(shape, np.random.default_rng(1054).integers(0, 64, size=1030), np.ones(1030), 1054)
     s = wl.shape
     dw = mcpu.DeviceWeights(s, wl.weights)
     T = wl.n_tokens
