@@ -103,6 +103,16 @@ __device__ __forceinline__ float swiglu(float gate, float up, float alpha, float
   return gate / (1.0f + expf(-alpha * gate)) * (up + beta);
 }
 
+// 8 consecutive elements from fp32 (16 or 32 bytes; p 16-byte aligned)
+__device__ __forceinline__ void store8(float* p, const float v[8]) {
+  reinterpret_cast<float4*>(p)[0] = make_float4(v[0], v[1], v[2], v[3]);
+  reinterpret_cast<float4*>(p)[1] = make_float4(v[4], v[5], v[6], v[7]);
+}
+__device__ __forceinline__ void store8(bf16* p, const float v[8]) {
+  *reinterpret_cast<uint4*>(p) =
+      make_uint4(pack_bf16(v[0], v[1]), pack_bf16(v[2], v[3]), pack_bf16(v[4], v[5]), pack_bf16(v[6], v[7]));
+}
+
 // cr[m * ld + n]: the finished fp32 tile for token rows m0 .. m0 + mrows - 1 and
 // the nblk 16-row weight blocks starting at blk0.
 template <typename T, int EPI>
@@ -111,29 +121,54 @@ __device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mro
   const int tid = threadIdx.x, nt = blockDim.x;
   const float* bias = P.bias + (int64_t)grp * P.bias_group_stride;
   if constexpr (EPI == EPI_QKV) {
+    // One item = (token row m, 16-row block b): dims j0 .. j0 + 7 and
+    // d/2 + j0 .. d/2 + j0 + 7 of one head, so the token's position and page
+    // are looked up once per 8 rotary pairs and q and k leave in 8-element
+    // stores (a K page keeps 8 consecutive dims of a slot together).
     const int D = P.head_dim, tph = D / 16, half = D / 2;
-    for (int idx = tid; idx < mrows * nblk * 8; idx += nt) {
-      const int i = idx & 7, b = (idx >> 3) % nblk, m = (idx >> 3) / nblk, t = m0 + m;
+    for (int idx = tid; idx < mrows * nblk; idx += nt) {
+      const int b = idx % nblk, m = idx / nblk, t = m0 + m;
       const int blk = blk0 + b, head = blk / tph, ti = blk - head * tph;
-      const int j = 8 * ti + i;  // dim within the head, < D/2
-      const int f_lo = head * D + j, f_hi = f_lo + half;
-      float lo = cr[m * ld + 16 * b + i] + bias[f_lo];
-      float hi = cr[m * ld + 16 * b + 8 + i] + bias[f_hi];
+      const int j0 = 8 * ti;  // dim within the head, < D/2
+      const int f_lo = head * D + j0, f_hi = f_lo + half;
+      float lo[8], hi[8];
+      {
+        // the tile rows need not be 16-byte aligned (odd strides avoid bank
+        // conflicts in some kernels): 4-byte reads; bias rows are aligned
+        const float* c = cr + m * ld + 16 * b;
+        const float4* bl = reinterpret_cast<const float4*>(bias + f_lo);
+        const float4* bh = reinterpret_cast<const float4*>(bias + f_hi);
+        const float4 b0 = bl[0], b1 = bl[1], b2 = bh[0], b3 = bh[1];
+        const float bb[16] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w,
+                              b2.x, b2.y, b2.z, b2.w, b3.x, b3.y, b3.z, b3.w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          lo[i] = c[i] + bb[i];
+          hi[i] = c[8 + i] + bb[8 + i];
+        }
+      }
       const int pos = P.tok_pos[t];
-      if (head < P.hq + P.hkv) {  // q or k: rotate the pair (j, j + d/2)
+      if (head < P.hq + P.hkv) {  // q or k: rotate the pairs (j, j + d/2)
         if (pos < 0 || pos >= P.rope_max_pos) {
           set_error(P.err, 2);
           continue;
         }
-        const float c = P.rope_cos[(int64_t)pos * half + j], s = P.rope_sin[(int64_t)pos * half + j];
-        const float a = lo, bb = hi;
-        lo = a * c - bb * s;
-        hi = a * s + bb * c;
+        const float4* cp = reinterpret_cast<const float4*>(P.rope_cos + (int64_t)pos * half + j0);
+        const float4* sp = reinterpret_cast<const float4*>(P.rope_sin + (int64_t)pos * half + j0);
+        const float4 ca = cp[0], cb = cp[1], sa = sp[0], sb = sp[1];
+        const float cs[8] = {ca.x, ca.y, ca.z, ca.w, cb.x, cb.y, cb.z, cb.w};
+        const float sn[8] = {sa.x, sa.y, sa.z, sa.w, sb.x, sb.y, sb.z, sb.w};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float a = lo[i], bb = hi[i];
+          lo[i] = a * cs[i] - bb * sn[i];
+          hi[i] = a * sn[i] + bb * cs[i];
+        }
       }
       if (head < P.hq) {
         T* q = reinterpret_cast<T*>(P.q_out) + ((int64_t)t * P.hq + head) * D;
-        Elem<T>::store(q, j, lo);
-        Elem<T>::store(q, j + half, hi);
+        store8(q + j0, lo);
+        store8(q + j0 + half, hi);
         continue;
       }
       const int lp = pos >> 4;
@@ -146,12 +181,15 @@ __device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mro
       const int slot = pos & 15;
       if (head < P.hq + P.hkv) {
         T* kp = reinterpret_cast<T*>(P.k_pool) + ((int64_t)page * P.hkv + (head - P.hq)) * PAGE * D;
-        Elem<T>::store(kp, k_off(slot, j), lo);
-        Elem<T>::store(kp, k_off(slot, j + half), hi);
+        store8(kp + k_off(slot, j0), lo);
+        store8(kp + k_off(slot, j0 + half), hi);
       } else {
         T* vp = reinterpret_cast<T*>(P.v_pool) + ((int64_t)page * P.hkv + (head - P.hq - P.hkv)) * PAGE * D;
-        Elem<T>::store(vp, v_off(slot, j), lo);
-        Elem<T>::store(vp, v_off(slot, j + half), hi);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          Elem<T>::store(vp, v_off(slot, j0 + i), lo[i]);
+          Elem<T>::store(vp, v_off(slot, j0 + half + i), hi[i]);
+        }
       }
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
