@@ -387,7 +387,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
   constexpr int NCH = 4 * PE / CH;                      // chunks per step (K and V of two pages)
   constexpr int PT = NCH / 256;                         // chunks per thread
   static_assert(NCH % 256 == 0, "a step's pages must split evenly over the workgroup");
-  __shared__ __align__(16) T kv[2][4][PE];              // [buffer][K page a, K page b, V page a, V page b]
+  __shared__ __align__(16) T kv[2][4][PE];              // [buffer][K page a, K page b, V pages a and b interleaved]
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   const int g = blockIdx.x % P.hkv;
   const int blk = P.n_blocks - 1 - (int)(blockIdx.x / P.hkv);  // latest (heaviest) blocks first
@@ -459,11 +459,16 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
       st.v[u] = *reinterpret_cast<const u32x4*>(pool + id * page_elems + (int64_t)g * PE + off);
     }
   };
+  // K pages keep the page format; the V pages of a step are interleaved in
+  // blocks of 256 elements (the 64 lanes' 4-value fragments of one 16-dim
+  // tile): [tile n][page a, page b], so the two halves of a PV operand are
+  // 512 bytes apart and load as one register quadruple
   auto stage = [&](const Regs& st, int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < PT; ++u) {
       const int i = tid + 256 * u, piece = i / (PE / CH), off = (i % (PE / CH)) * CH;
-      *reinterpret_cast<u32x4*>(&kv[buf][piece][off]) = st.v[u];
+      T* dst = piece < 2 ? &kv[buf][piece][off] : &kv[buf][2][((off >> 8) * 2 + piece - 2) * 256 + (off & 255)];
+      *reinterpret_cast<u32x4*>(dst) = st.v[u];
     }
   };
 
@@ -560,12 +565,9 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
         thr[j] = (m_new + RESCALE) * inv_scale;
       }
     }
-    Frag4<T> va[D / 16], vb[D / 16];
+    PVFrag<T> vf[D / 16];
 #pragma unroll
-    for (int n = 0; n < D / 16; ++n) {
-      va[n].load(&kv[buf][2][(64 * n + lane) * 4]);
-      vb[n].load(&kv[buf][3][(64 * n + lane) * 4]);
-    }
+    for (int n = 0; n < D / 16; ++n) vf[n].load(&kv[buf][2][2 * n * 256 + lane * 4], &kv[buf][2][(2 * n + 1) * 256 + lane * 4]);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float msub = m_sub[j];
@@ -577,7 +579,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(AttnPrefill P) {
       }
       accl[j] = mma32_pv(one, one, pa, pb, accl[j]);
 #pragma unroll
-      for (int n = 0; n < D / 16; ++n) acc[n][j] = mma32_pv(va[n], vb[n], pa, pb, acc[n][j]);
+      for (int n = 0; n < D / 16; ++n) acc[n][j] = mma32_pv(vf[n], pa, pb, acc[n][j]);
     }
   };
 

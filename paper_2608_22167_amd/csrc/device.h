@@ -222,6 +222,35 @@ __device__ __forceinline__ f32x4 mma32_pv(const Frag4<float>& Va, const Frag4<fl
   acc = mma16_p(Va, pa, acc, nullptr);
   return mma16_p(Vb, pb, acc, nullptr);
 }
+// V operand of a two-page PV product: the lane's 4 values of page a, then
+// the same slots of page b, loaded straight into one register quadruple.
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+template <typename T> struct PVFrag;
+template <> struct PVFrag<bf16> {
+  u32x4_t v;
+  __device__ __forceinline__ void load(const bf16* a, const bf16* b) {
+    const u32x2_t x = *reinterpret_cast<const u32x2_t*>(a), y = *reinterpret_cast<const u32x2_t*>(b);
+    v = __builtin_shufflevector(x, y, 0, 1, 2, 3);
+  }
+};
+template <> struct PVFrag<float> {
+  Frag4<float> a, b;
+  __device__ __forceinline__ void load(const float* pa, const float* pb) {
+    a.load(pa);
+    b.load(pb);
+  }
+};
+__device__ __forceinline__ f32x4 mma32_pv(const PVFrag<bf16>& V, const float pa[4], const float pb[4], f32x4 acc) {
+  const uint4 bv = make_uint4(pack_bf16(pa[0], pa[1]), pack_bf16(pa[2], pa[3]), pack_bf16(pb[0], pb[1]),
+                              pack_bf16(pb[2], pb[3]));
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, V.v), __builtin_bit_cast(bf16x8_t, bv),
+                                                  acc, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma32_pv(const PVFrag<float>& V, const float pa[4], const float pb[4], f32x4 acc) {
+  acc = mma16_p(V.a, pa, acc, nullptr);
+  return mma16_p(V.b, pb, acc, nullptr);
+}
 __device__ __forceinline__ void ones(Frag4<bf16>& f) { f.v = make_uint2(0x3F803F80u, 0x3F803F80u); }
 __device__ __forceinline__ void ones(Frag4<float>& f) { f.v = make_float4(1.f, 1.f, 1.f, 1.f); }
 
