@@ -218,11 +218,14 @@ __global__ __launch_bounds__(PTH) void gemm_pipe_kernel(Gemm P) {
     for (int p = 0; p < 4; ++p) store(r1, p, st1);
   }
   __syncthreads();
-  u32x4 a[PNF], b0, b1;
+  // head fragments of a slice (its weight fragments and first two token-row
+  // fragments) in two sets by slice parity: slice i reads set i % 2 and
+  // fills set (i + 1) % 2, so the unrolled loop needs no register copies
+  u32x4 ah[2][PNF], bh[2][2];
 #pragma unroll
-  for (int nb = 0; nb < PNF; ++nb) a[nb] = ld16(st0 + woff + nb * 16 * PLD);
-  b0 = ld16(st0 + xoff);
-  b1 = ld16(st0 + xoff + 16 * PLD);
+  for (int nb = 0; nb < PNF; ++nb) ah[0][nb] = ld16(st0 + woff + nb * 16 * PLD);
+  bh[0][0] = ld16(st0 + xoff);
+  bh[0][1] = ld16(st0 + xoff + 16 * PLD);
 
   // Slice i (stage S = i % 3, register set R = i % 2): eight steps of four
   // products (token-row fragment s against the four weight-row fragments)
@@ -234,16 +237,16 @@ __global__ __launch_bounds__(PTH) void gemm_pipe_kernel(Gemm P) {
     bf16* cur = stage_of(S);
     bf16* nxt = stage_of((S + 1) % 3);
     bf16* wr = stage_of((S + 2) % 3);
+    constexpr int H = R;  // slice parity (the register set alternates with it)
+    u32x4* a = ah[H];
     u32x4 b[PMF];
-    b[0] = b0;
-    b[1] = b1;
-    u32x4 an[PNF], bn0, bn1;
+    b[0] = bh[H][0];
+    b[1] = bh[H][1];
 #pragma unroll
     for (int s = 0; s < PMF; ++s) {
       if (s + 2 < PMF) b[s + 2] = ld16(cur + xoff + (s + 2) * 16 * PLD);
-      else if (s + 2 == PMF) bn0 = ld16(nxt + xoff);
-      else bn1 = ld16(nxt + xoff + 16 * PLD);
-      if (s >= 4) an[s - 4] = ld16(nxt + woff + (s - 4) * 16 * PLD);
+      else bh[H ^ 1][s + 2 - PMF] = ld16(nxt + xoff + (s + 2 - PMF) * 16 * PLD);
+      if (s >= 4) ah[H ^ 1][s - 4] = ld16(nxt + woff + (s - 4) * 16 * PLD);
       if (s < 4) {
         store(rs[R], s, wr);
         fetch(rs[R], s, i + 2 + NR);
@@ -261,10 +264,6 @@ __global__ __launch_bounds__(PTH) void gemm_pipe_kernel(Gemm P) {
     PIPE_STEP(1, 1) PIPE_STEP(1, 1) PIPE_STEP(1, 1) PIPE_STEP(1, 1)
     PIPE_STEP(2, 0) PIPE_STEP(2, 0) PIPE_STEP(2, 0) PIPE_STEP(2, 0)
 #undef PIPE_STEP
-#pragma unroll
-    for (int nb = 0; nb < PNF; ++nb) a[nb] = an[nb];
-    b0 = bn0;
-    b1 = bn1;
     __syncthreads();
   };
   using I0 = std::integral_constant<int, 0>;
@@ -313,6 +312,194 @@ __global__ __launch_bounds__(PTH) void gemm_pipe_kernel(Gemm P) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 weights: the same tile and wavefront split, with every slice loaded
+// straight from global memory into LDS by 16-byte direct loads (a
+// wavefront's load fills 1 KB of LDS, lane l at byte 16 l), so staging costs
+// neither registers nor LDS write instructions. Five stages (all of the
+// LDS): while slice i is multiplied, the head of slice i + 1 is read, slices
+// i + 2 and i + 3 land and slice i + 4 is requested; before each barrier a
+// wavefront waits for its own loads of slice i + 2 (the barrier then
+// publishes them to all wavefronts). Rows
+// are 64 bytes with no padding; chunk q of row r sits in 16-byte slot
+// q ^ ((r >> 1) & 3) of its row, which keeps the fragment reads free of bank
+// conflicts, and each lane loads the global chunk its slot holds.
+// ---------------------------------------------------------------------------
+constexpr int DROW = PK * 2;              // bytes per staged row
+constexpr int DSTAGE = (PM + PN) * DROW;  // bytes per stage (32 KB)
+constexpr int DEP = 16;                   // epilogue rows per pass
+constexpr int DNS = 5;                    // stages
+static_assert(DEP * PCLD * 4 <= DSTAGE, "an epilogue pass fits one stage");
+__device__ __forceinline__ int dswz(int r) { return (r >> 1) & 3; }
+constexpr int BUF_DWORD3 = 0x00020000;  // raw buffer descriptor word 3 (gfx9 family)
+typedef __attribute__((address_space(3))) void* lds_void_t;
+
+template <int EPI>
+__global__ __launch_bounds__(PTH) void gemm_dma_kernel(Gemm P) {
+  __shared__ __align__(1024) uint8_t d0[DSTAGE];
+  __shared__ __align__(1024) uint8_t d1[DSTAGE];
+  __shared__ __align__(1024) uint8_t d2[DSTAGE];
+  __shared__ __align__(1024) uint8_t d3[DSTAGE];
+  __shared__ __align__(1024) uint8_t d4[DSTAGE];
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+
+  // the m-tile prefix lives in stage 4 until the first barrier after it is
+  // read (stage 4 first receives slice 4, requested after that barrier)
+  static_assert((TILE_MAXG + 1) * 4 <= DSTAGE, "the m-tile prefix fits a stage");
+  int grp, mt, tn;
+  if (!tile_of_block<PM, PN, PGM>(P, reinterpret_cast<int*>(d4), grp, mt, tn)) return;
+  const int gr0 = P.group_off ? P.group_off[grp] : 0;
+  const int gr1 = P.group_off ? P.group_off[grp + 1] : P.n_rows;
+  const int m0 = uniform(gr0 + mt * PM);
+  const int mrows = min(PM, gr1 - m0);
+  const int n0 = uniform(tn * PN), nrows = min(PN, P.n - n0);
+
+  // wavefront w loads rows 32 w + 16 j + [0, 16) of both operands (j = 0, 1);
+  // lane l lands in row + l / 4, slot l % 4, the home of chunk (l % 4) ^ swz.
+  // Rows past the tile's end repeat its last row (their results are dropped).
+  // Buffer loads: a uniform base (the tile's first row, or x itself when rows
+  // are gathered; the group's weights), a 32-bit per-lane row offset and the
+  // slice offset in a scalar register.
+  const int lr = lane >> 2, chunk = (lane & 3) ^ dswz(lr);
+  const uint8_t* xb = reinterpret_cast<const uint8_t*>(P.x) + (P.row_src ? 0 : (int64_t)m0 * P.k * 2);
+  const uint8_t* wb = reinterpret_cast<const uint8_t*>(P.w) + (int64_t)grp * P.w_group_stride * 2;
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(xb), 0, 0x7FFFFFFF, BUF_DWORD3);
+  const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wb), 0, 0x7FFFFFFF, BUF_DWORD3);
+  uint32_t xvo[2], wvo[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int rr = 32 * wave + 16 * j + lr;
+    const int rm = min(rr, mrows - 1);
+    xvo[j] = P.row_src ? (uint32_t)P.row_src[m0 + rm] * (uint32_t)(P.k * 2) + chunk * 16
+                       : (uint32_t)rm * (uint32_t)(P.k * 2) + chunk * 16;
+    const int rc = min(rr, nrows - 1);
+    const int blk = (n0 + rc) >> 4, nl = rc & 15;
+    const int wrow = EPI == EPI_QKV ? block_row<EPI_QKV>(P, blk, nl) : blk * 16 + nl;
+    wvo[j] = (uint32_t)wrow * (uint32_t)(P.k * 2) + chunk * 16;
+  }
+  const int ldst = 32 * wave * DROW;  // this wavefront's rows within an operand
+  const int nk = P.k / PK;
+
+  const int wm = wave & 1, wn = wave >> 1;
+  const int fr = lane & 15, slot = ((lane >> 4) ^ dswz(fr)) * 16;
+  const int xoff = (wm * (PM / 2) + fr) * DROW + slot;
+  const int woff = (PM + wn * PWN + fr) * DROW + slot;
+  f32x4 acc[PNF][PMF];
+#pragma unroll
+  for (int nb = 0; nb < PNF; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < PMF; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto stage_of = [&](int s) __attribute__((always_inline)) {
+    return s == 0 ? d0 : s == 1 ? d1 : s == 2 ? d2 : s == 3 ? d3 : d4;
+  };
+  // load p of a slice (0, 1: token rows, 2, 3: weight rows); slices past the
+  // end re-read the last one (never multiplied)
+  auto dma = [&](uint8_t* stg, int p, int ks) __attribute__((always_inline)) {
+    const int soff = uniform(min(ks, nk - 1) * (PK * 2));
+    uint8_t* dst = stg + (p < 2 ? 0 : PM * DROW) + ldst + 16 * (p & 1) * DROW;
+    if (p < 2) __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void_t)(dst), 16, xvo[p], soff, 0, 0);
+    else __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void_t)(dst), 16, wvo[p - 2], soff, 0, 0);
+  };
+  // each wavefront's own loads of all but the two latest slices done (4
+  // loads per slice), LDS reads done, then the barrier that publishes them
+  auto publish = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(8 | (7 << 4) | (0 << 8));  // vmcnt(8) expcnt(7) lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+  };
+
+  // prologue: slices 0 .. 3 requested, 0 and 1 published, head of slice 0 read
+#pragma unroll
+  for (int s = 0; s < DNS - 1; ++s)
+#pragma unroll
+    for (int p = 0; p < 4; ++p) dma(stage_of(s), p, s);
+  publish();
+  u32x4 ah[2][PNF], bh[2][2];
+#pragma unroll
+  for (int nb = 0; nb < PNF; ++nb) ah[0][nb] = ld16(d0 + woff + nb * 16 * DROW);
+  bh[0][0] = ld16(d0 + xoff);
+  bh[0][1] = ld16(d0 + xoff + 16 * DROW);
+
+  // slice i uses stage i % 5 and head set i % 2: the loop is unrolled ten times
+  auto slice = [&](auto S_, auto H_, int i) __attribute__((always_inline)) {
+    constexpr int S = decltype(S_)::value, H = decltype(H_)::value;
+    uint8_t* cur = stage_of(S);
+    uint8_t* nxt = stage_of((S + 1) % DNS);
+    uint8_t* req = stage_of((S + DNS - 1) % DNS);
+    u32x4* a = ah[H];
+    u32x4 b[PMF];
+    b[0] = bh[H][0];
+    b[1] = bh[H][1];
+#pragma unroll
+    for (int s = 0; s < PMF; ++s) {
+      if (s + 2 < PMF) b[s + 2] = ld16(cur + xoff + (s + 2) * 16 * DROW);
+      else bh[H ^ 1][s + 2 - PMF] = ld16(nxt + xoff + (s + 2 - PMF) * 16 * DROW);
+      if (s >= 4) ah[H ^ 1][s - 4] = ld16(nxt + woff + (s - 4) * 16 * DROW);
+      if (s < 4) dma(req, s, i + DNS - 1);
+#pragma unroll
+      for (int nb = 0; nb < PNF; ++nb) acc[nb][s] = mfma(a[nb], b[s], acc[nb][s]);
+    }
+#define DMA_STEP(NR, NM)                               \
+  __builtin_amdgcn_sched_group_barrier(0x100, NR, 0);  \
+  __builtin_amdgcn_sched_group_barrier(0x020, NM, 0);  \
+  __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    DMA_STEP(1, 1) DMA_STEP(1, 1) DMA_STEP(1, 1) DMA_STEP(1, 1)
+    DMA_STEP(2, 0) DMA_STEP(2, 0) DMA_STEP(2, 0) DMA_STEP(2, 0)
+#undef DMA_STEP
+    publish();
+  };
+  using C0 = std::integral_constant<int, 0>;
+  using C1 = std::integral_constant<int, 1>;
+  using C2 = std::integral_constant<int, 2>;
+  using C3 = std::integral_constant<int, 3>;
+  using C4 = std::integral_constant<int, 4>;
+  int i = 0;
+  for (; i + 10 <= nk; i += 10) {
+    slice(C0{}, C0{}, i);
+    slice(C1{}, C1{}, i + 1);
+    slice(C2{}, C0{}, i + 2);
+    slice(C3{}, C1{}, i + 3);
+    slice(C4{}, C0{}, i + 4);
+    slice(C0{}, C1{}, i + 5);
+    slice(C1{}, C0{}, i + 6);
+    slice(C2{}, C1{}, i + 7);
+    slice(C3{}, C0{}, i + 8);
+    slice(C4{}, C1{}, i + 9);
+  }
+  if (i < nk) slice(C0{}, C0{}, i);
+  if (i + 1 < nk) slice(C1{}, C1{}, i + 1);
+  if (i + 2 < nk) slice(C2{}, C0{}, i + 2);
+  if (i + 3 < nk) slice(C3{}, C1{}, i + 3);
+  if (i + 4 < nk) slice(C4{}, C0{}, i + 4);
+  if (i + 5 < nk) slice(C0{}, C1{}, i + 5);
+  if (i + 6 < nk) slice(C1{}, C0{}, i + 6);
+  if (i + 7 < nk) slice(C2{}, C1{}, i + 7);
+  if (i + 8 < nk) slice(C3{}, C0{}, i + 8);
+  __syncthreads();  // every load landed before stage 0 holds the fp32 tile
+
+  // acc[nb][mb][r] = C[m = wm*128 + 16 mb + fr][n = wn*64 + 16 nb + 4 (lane/16) + r]
+  float* cr = reinterpret_cast<float*>(d0);
+  for (int e0 = 0; e0 < PM; e0 += DEP) {
+    if (e0 >= mrows) break;  // uniform
+    if (wm == e0 / (PM / 2)) {
+#pragma unroll
+      for (int mb = 0; mb < PMF; ++mb) {
+        if (wm * (PM / 2) + mb * 16 == e0) {
+#pragma unroll
+          for (int nb = 0; nb < PNF; ++nb) {
+            const int n = wn * PWN + nb * 16 + 4 * (lane >> 4);
+            *reinterpret_cast<float4*>(cr + fr * PCLD + n) =
+                make_float4(acc[nb][mb][0], acc[nb][mb][1], acc[nb][mb][2], acc[nb][mb][3]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    epilogue<bf16, EPI>(P, cr, PCLD, m0 + e0, min(DEP, mrows - e0), n0 >> 4, nrows >> 4, grp);
+    __syncthreads();
+  }
+}
+
 }  // namespace
 
 bool pipe_gemm_applies(int dtype, const Gemm& g) {
@@ -327,9 +514,14 @@ hipError_t launch_gemm_pipe(int expert_fmt, const Gemm& g, hipStream_t s) {
   if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
   if (expert_fmt != 0 && !g.w_scales) return hipErrorInvalidValue;
   dim3 gd((unsigned)grid), bd(PTH);
+  // direct loads address rows with 32-bit offsets: from the tile's first row,
+  // or from x itself when rows are gathered, and within one group's weights
+  const int64_t xr = g.row_src ? (g.x_rows > 0 ? g.x_rows : g.n_rows) : PM;
+  const bool dma = xr * g.k * 2 < (1LL << 31) && (int64_t)g.n * g.k * 2 < (1LL << 31);
 #define PIPE_LAUNCH(E)                                                                          \
   do {                                                                                          \
     if (expert_fmt != 0) hipLaunchKernelGGL((gemm_pipe_kernel<E, 1>), gd, bd, 0, s, g);        \
+    else if (dma) hipLaunchKernelGGL((gemm_dma_kernel<E>), gd, bd, 0, s, g);                    \
     else hipLaunchKernelGGL((gemm_pipe_kernel<E, 0>), gd, bd, 0, s, g);                         \
   } while (0)
   switch (g.epi) {

@@ -125,6 +125,7 @@ struct Gemm {
   int rope_max_pos;
   int32_t* err;
   int max_rows_per_group;   // upper bound used to pick the m-tiling
+  int x_rows;               // rows of x when row_src gathers from it (0: n_rows)
 };
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s);
 // LDS-tiled path (gemm_tiled.hip): bf16, k a multiple of 64, at least

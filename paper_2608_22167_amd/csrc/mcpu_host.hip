@@ -269,7 +269,7 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   g1.x = m.hn; g1.row_src = m.src_tok; g1.group_off = m.group_off; g1.n_rows = T * K; g1.n_groups = E;
   g1.epi = EPI_SWIGLU; g1.bias = w->b_gu; g1.bias_group_stride = 2 * I; g1.out = m.act;
   g1.swiglu_alpha = c->swiglu_alpha; g1.swiglu_limit = c->swiglu_limit; g1.swiglu_beta = c->swiglu_beta;
-  g1.err = err; g1.max_rows_per_group = max_rows;
+  g1.err = err; g1.max_rows_per_group = max_rows; g1.x_rows = T;
   {
     Timed tm(MCPU_KERNEL_EXPERT_GU, st);
     HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g1, st));
