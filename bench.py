@@ -103,23 +103,32 @@ def roofline_of(work_bytes, work_flops, seconds, dtype):
             "frac": round(a / HBM_PEAK_GBS, 4)}
 
 
-def traffic_from_profile(kernel, kernel_src, workload_name):
+def source_hash(kernel):
+    """sha256[:16] over the sources the kernel is built from, in a fixed order."""
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES.get(kernel, ATTN_SOURCES):
+        h.update(open(os.path.join(ROOT, "paper_2608_22167_amd", "csrc", name), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(kernel, workload_name):
     """HBM bytes per launch from a committed rocprofv3 counter summary, if it
-    was taken on the current source of the kernel; else None."""
+    was taken on the current sources of the kernel; else None."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{workload_name}_counters.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    src_hash = hashlib.sha256(open(kernel_src, "rb").read()).hexdigest()[:16]
-    m = re.search(r"source sha256\[:16\]:\s*([0-9a-f]{16})", text)
+    m = re.search(r"sources sha256\[:16\]:\s*([0-9a-f]{16})", text)
     t = re.search(r"hbm bytes per launch:\s*([0-9.eE+]+)", text)
-    if not m or not t or m.group(1) != src_hash:
+    if not m or not t or m.group(1) != source_hash(kernel):
         return None
     return float(t.group(1))
 
 
-KERNEL_SOURCES = {"attn_split": "attention.hip", "attn_prefill": "attention.hip", "qkv": "gemm_tiled.hip",
-                  "oproj": "gemm_tiled.hip", "expert_gu": "gemm_tiled.hip", "expert_down": "gemm_tiled.hip"}
+ATTN_SOURCES = ("attention.hip", "device.h", "kernels.h")
+GEMM_SOURCES = ("gemm.hip", "gemm_tiled.hip", "gemm_pipe.hip", "gemm_epilogue.h", "device.h", "kernels.h")
+KERNEL_SOURCES = {"attn_split": ATTN_SOURCES, "attn_prefill": ATTN_SOURCES, "qkv": GEMM_SOURCES,
+                  "oproj": GEMM_SOURCES, "expert_gu": GEMM_SOURCES, "expert_down": GEMM_SOURCES}
 
 
 def cpu_cores():
@@ -326,8 +335,7 @@ def main():
     dom_us = float(per.mean()) * 1e3
     roofline = {"kernel": dominant + (" (full-attention layers)" if cols != list(range(bench.launches)) else "")}
     roofline.update(roofline_of(launch_bytes, launch_flops, dom_us * 1e-6, bench.shape.dtype))
-    src = os.path.join(ROOT, "paper_2608_22167_amd", "csrc", KERNEL_SOURCES.get(dominant, "attention.hip"))
-    roofline.update({"traffic": traffic_from_profile(dominant, src, args.workload), "avg_us": round(dom_us, 2),
+    roofline.update({"traffic": traffic_from_profile(dominant, args.workload), "avg_us": round(dom_us, 2),
                      "algorithmic_bytes": round(launch_bytes), "algorithmic_flops": round(launch_flops)})
     kernels_util = {k: roofline_of(b, f, breakdown[k] * 1e-6, bench.shape.dtype)
                     for k, (b, f) in work.items() if breakdown.get(k)}
