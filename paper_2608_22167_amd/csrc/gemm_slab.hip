@@ -1,0 +1,338 @@
+// Weight-streaming slabs for grouped GEMMs with up to about a hundred token
+// rows per weight matrix (gfx950, bf16 activations, bf16 or MXFP4 weights):
+// the expert projections of decode batches of up to a few thousand tokens.
+//
+// There each weight byte meets only a few dozen token rows, so the bound is
+// HBM, and the kernel's job is to keep enough weight bytes in flight. A
+// workgroup of four wavefronts owns one work item: up to 64 token rows of one
+// group against NS weight rows. Each wavefront streams its NS / 4 weight rows
+// straight from global memory into registers, already in matrix-core operand
+// order, through a ring of RC reduction chunks (128 indices each), so weights
+// never pass through LDS; the group's token rows, shared by the four
+// wavefronts (and by all the group's slabs, so they come from L2), are staged
+// per chunk through double-buffered LDS with a ring of register sets.
+//
+// MXFP4 weights are loaded 16 code bytes (32 weights) per lane: lane group g
+// of a 16-row fragment holds indices 32 g .. 32 g + 31 of the chunk, and
+// product s of the chunk takes indices 32 g + 8 s .. + 7 from every group,
+// the token-row fragments reading the same indices. A chunk's 32-weight blocks
+// then coincide with the lane groups, one E8M0 scale per lane, decoded in
+// registers with the packed e2m1 -> bf16 conversion (exact, as in the LDS
+// kernels). bf16 weights use the plain fragment order.
+//
+// Token rows sit in LDS as [half chunk][64 rows][128 B] with 16-byte chunk c
+// of row r in slot c ^ (r & 7): the fragment reads of 16 rows and the 8-lane
+// staging writes of one row both cover all bank groups. Reductions that end
+// in half a chunk (k % 128 == 64) skip the missing half: bf16 products are
+// not issued, MXFP4 weights of the missing half are zero.
+#include <type_traits>
+
+#include "device.h"
+#include "gemm_epilogue.h"
+#include "kernels.h"
+
+namespace mcpu {
+namespace {
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+constexpr int BUF_D3 = 0x00020000;  // raw buffer descriptor word 3 (gfx9 family)
+
+constexpr int SM = 64;              // token rows per item
+constexpr int SKC = 128;            // reduction indices per chunk
+constexpr int SXHALF = SM * 128;    // bytes of a staged half chunk (64 rows x 64 indices)
+constexpr int SXSTAGE = 2 * SXHALF; // bytes per chunk stage
+
+__device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b), c,
+                                                  0, 0, 0);
+}
+
+// Weight side of one wavefront: NF 16-row fragments.
+template <int NF, int WF>
+struct SlabW;
+
+// bf16: per chunk and fragment four 16-byte loads (products 0..3 of the chunk)
+template <int NF>
+struct SlabW<NF, 0> {
+  struct Regs {
+    u32x4 f[NF][4];
+  };
+  __amdgpu_buffer_rsrc_t rs;
+  uint32_t vo[NF];
+  __device__ __forceinline__ void init(const Gemm& P, int grp, const int* wrow, int g) {
+    const uint8_t* base = reinterpret_cast<const uint8_t*>(P.w) + (int64_t)grp * P.w_group_stride * 2;
+    rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), 0, 0x7FFFFFFF, BUF_D3);
+#pragma unroll
+    for (int nb = 0; nb < NF; ++nb) vo[nb] = (uint32_t)wrow[nb] * (uint32_t)(P.k * 2) + 16 * g;
+  }
+  __device__ __forceinline__ void fetch(Regs& r, int kc, int nsteps) const {
+#pragma unroll
+    for (int nb = 0; nb < NF; ++nb)
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        r.f[nb][t] = __builtin_amdgcn_raw_buffer_load_b128(rs, vo[nb], uniform((kc * SKC + 32 * min(t, nsteps - 1)) * 2), 0);
+  }
+  struct Dec {};
+  __device__ __forceinline__ void prepare(const Regs&, Dec&, uint32_t&, uint32_t) const {}
+  // fragment of product t
+  __device__ __forceinline__ u32x4 frag(const Regs& r, const Dec&, int nb, int t) const { return r.f[nb][t]; }
+};
+
+// MXFP4: per chunk and fragment one 16-byte code load and one scale byte
+template <int NF>
+struct SlabW<NF, 1> {
+  struct Regs {
+    u32x4 c[NF];
+    uint32_t s[NF];
+  };
+  __amdgpu_buffer_rsrc_t rc, rsc;
+  uint32_t vo[NF], so[NF];
+  int g;
+  __device__ __forceinline__ void init(const Gemm& P, int grp, const int* wrow, int g_) {
+    g = g_;
+    const uint8_t* cb = reinterpret_cast<const uint8_t*>(P.w) + (int64_t)grp * P.w_group_stride;
+    const uint8_t* sb = P.w_scales + (int64_t)grp * (P.w_group_stride / 16);
+    rc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(cb), 0, 0x7FFFFFFF, BUF_D3);
+    rsc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(sb), 0, 0x7FFFFFFF, BUF_D3);
+#pragma unroll
+    for (int nb = 0; nb < NF; ++nb) {
+      vo[nb] = (uint32_t)wrow[nb] * (uint32_t)(P.k / 2) + 16 * g;
+      so[nb] = (uint32_t)wrow[nb] * (uint32_t)(P.k / 32) + g;
+    }
+  }
+  __device__ __forceinline__ void fetch(Regs& r, int kc, int nsteps) const {
+    // in a half chunk, lane groups 2 and 3 read the first half again (their
+    // weights are zeroed when decoded)
+    const int off = nsteps == 4 ? 0 : -2 * (g >> 1);
+#pragma unroll
+    for (int nb = 0; nb < NF; ++nb) {
+      r.c[nb] = __builtin_amdgcn_raw_buffer_load_b128(rc, vo[nb] + 16 * off, uniform(kc * (SKC / 2)), 0);
+      r.s[nb] = __builtin_amdgcn_raw_buffer_load_b8(rsc, so[nb] + off, uniform(kc * (SKC / 32)), 0);
+    }
+  }
+  // per chunk and fragment: the scale as a float and a mask that zeroes the
+  // codes of a rejected scale or of a missing half chunk (keep)
+  struct Dec {
+    float scale[NF];
+    uint32_t mask[NF];
+  };
+  __device__ __forceinline__ void prepare(const Regs& r, Dec& d, uint32_t& bad, uint32_t keep) const {
+#pragma unroll
+    for (int nb = 0; nb < NF; ++nb) {
+      const uint32_t sc = r.s[nb];
+      const bool ok = sc >= 2u && sc <= 252u;
+      bad |= ok ? 0u : 1u;
+      d.scale[nb] = __uint_as_float(ok ? sc << 23 : 127u << 23);
+      d.mask[nb] = ok ? keep : 0u;
+    }
+  }
+  __device__ __forceinline__ u32x4 frag(const Regs& r, const Dec& d, int nb, int s) const {
+    const uint32_t w = r.c[nb][s] & d.mask[nb];
+    const float scale = d.scale[nb];
+    return u32x4{__builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, scale, 0)),
+                 __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, scale, 1)),
+                 __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, scale, 2)),
+                 __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, scale, 3))};
+  }
+};
+
+template <int NS, int WF, int RC, int EPI>
+__global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
+  constexpr int NF = NS / 64;  // weight fragments per wavefront
+  constexpr int CLD = NS + 4;  // fp32 tile row stride
+  constexpr int SMEM = 2 * SXSTAGE > SM * CLD * 4 ? 2 * SXSTAGE : SM * CLD * 4;
+  __shared__ __align__(16) unsigned char smem[SMEM];
+  __shared__ int mt_start[TILE_MAXG + 1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
+  const int fr = lane & 15, g = lane >> 4;
+
+  int grp, mt, tn;
+  if (!tile_of_block<SM, NS, 1>(P, mt_start, grp, mt, tn)) return;
+  const int gr0 = P.group_off ? P.group_off[grp] : 0;
+  const int gr1 = P.group_off ? P.group_off[grp + 1] : P.n_rows;
+  const int m0 = uniform(gr0 + mt * SM);
+  const int mrows = min(SM, gr1 - m0);
+  const int n0 = uniform(tn * NS), nrows = min(NS, P.n - n0);
+  const int mbs = uniform((mrows + 15) >> 4);  // token-row fragments holding rows
+  const int nk = (P.k + SKC - 1) / SKC;
+  const int tail_steps = (P.k % SKC) ? (P.k % SKC) / 32 : 4;
+
+  // weight rows of this wavefront: n0 + NS/4 * wave + 16 nb + fr (clamped; dropped)
+  SlabW<NF, WF> wl;
+  {
+    int wrow[NF];
+#pragma unroll
+    for (int nb = 0; nb < NF; ++nb) {
+      const int rr = min((NS / 4) * wave + 16 * nb + fr, nrows - 1);
+      const int blk = (n0 + rr) >> 4, nl = rr & 15;
+      wrow[nb] = EPI == EPI_QKV ? block_row<EPI_QKV>(P, blk, nl) : blk * 16 + nl;
+    }
+    wl.init(P, grp, wrow, g);
+  }
+
+  // token-row staging: thread t stages row t / 4 (of the 64), 16-byte chunks
+  // 2 (t % 4) and 2 (t % 4) + 1 of both half chunks; rows past the end repeat
+  // the last row (dropped)
+  const int xr = tid >> 2, xc = 2 * (tid & 3);
+  uint32_t xvo;
+  {
+    const int row = m0 + min(xr, mrows - 1);
+    const int src = P.row_src ? P.row_src[row] : row;
+    xvo = (uint32_t)src * (uint32_t)(P.k * 2) + 16 * xc;
+  }
+  const uint8_t* xbase = reinterpret_cast<const uint8_t*>(P.x);
+  const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(xbase), 0, 0x7FFFFFFF, BUF_D3);
+  struct XRegs {
+    u32x4 v[2][2];  // [half][chunk pair]
+  };
+  auto xfetch = [&](XRegs& r, int kc) __attribute__((always_inline)) {
+    kc = min(kc, nk - 1);
+    // a half chunk past k re-reads the first half (never multiplied)
+    const int h1 = (kc == nk - 1 && tail_steps < 4) ? 0 : 128;
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        r.v[h][q] = __builtin_amdgcn_raw_buffer_load_b128(xrs, xvo + 16 * q + (h ? h1 : 0), uniform(kc * SKC * 2), 0);
+  };
+  auto xstore = [&](const XRegs& r, int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        *reinterpret_cast<u32x4*>(smem + buf * SXSTAGE + h * SXHALF + xr * 128 + 16 * ((xc + q) ^ (xr & 7))) =
+            r.v[h][q];
+  };
+  // token-row fragment mb of product t (bf16 order) or s (MXFP4 order)
+  auto xfrag = [&](int buf, int mb, int t) __attribute__((always_inline)) {
+    int h, c8;
+    if (WF == 0) {
+      h = t >> 1;
+      c8 = 4 * (t & 1) + g;
+    } else {
+      h = g >> 1;
+      c8 = 4 * (g & 1) + t;
+    }
+    return *reinterpret_cast<const u32x4*>(smem + buf * SXSTAGE + h * SXHALF + (16 * mb + fr) * 128 +
+                                           16 * (c8 ^ (fr & 7)));
+  };
+
+  f32x4 acc[NF][4];
+#pragma unroll
+  for (int nb = 0; nb < NF; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint32_t bad_scale = 0;
+
+  // Chunk kc: weights from register set kc % RC (requested RC chunks ahead),
+  // token rows from LDS buffer kc & 1; afterwards chunk kc + 1's token rows
+  // are staged and chunk kc + 2's requested. Unrolled over RC (even) so the
+  // set indices are constants; only the products are conditional. The loop
+  // is instantiated per count of token-row fragments holding rows (MBS).
+  static_assert(RC % 2 == 0, "the unrolled ring must cover both LDS buffers");
+  typename SlabW<NF, WF>::Regs wr[RC];
+  XRegs xs[2];
+#pragma unroll
+  for (int u = 0; u < RC; ++u) {
+    wl.fetch(wr[u], min(u, nk - 1), (u == nk - 1) ? tail_steps : 4);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  xfetch(xs[0], 0);
+  xfetch(xs[1], 1);
+  xstore(xs[0], 0);
+  xfetch(xs[0], 2);
+  __syncthreads();
+  // MXFP4 in a half chunk: lane groups 2 and 3 hold no indices
+  const uint32_t keep_tail = (WF == 1 && tail_steps < 4 && g >= 2) ? 0u : ~0u;
+  auto run = [&](auto MBS_) __attribute__((always_inline)) {
+    constexpr int MBS = decltype(MBS_)::value;
+    for (int kc0 = 0; kc0 < nk; kc0 += RC) {
+#pragma unroll
+      for (int u = 0; u < RC; ++u) {
+        const int kc = kc0 + u;
+        const int buf = u & 1;
+        if (kc < nk) {
+          const bool tail = kc == nk - 1;
+          const int nsteps = tail ? tail_steps : 4;
+          typename SlabW<NF, WF>::Dec dec;
+          wl.prepare(wr[u], dec, bad_scale, tail ? keep_tail : ~0u);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            if (WF == 0 && t >= nsteps) break;  // bf16: missing half chunk
+            u32x4 xf[MBS];
+#pragma unroll
+            for (int mb = 0; mb < MBS; ++mb) xf[mb] = xfrag(buf, mb, t);
+#pragma unroll
+            for (int nb = 0; nb < NF; ++nb) {
+              const u32x4 wf = wl.frag(wr[u], dec, nb, t);
+#pragma unroll
+              for (int mb = 0; mb < MBS; ++mb) acc[nb][mb] = mfma_bf16(wf, xf[mb], acc[nb][mb]);
+            }
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        const int kn = kc + RC;
+        wl.fetch(wr[u], min(kn, nk - 1), (kn >= nk - 1) ? tail_steps : 4);
+        xstore(xs[(u + 1) & 1], buf ^ 1);
+        xfetch(xs[(u + 1) & 1], kc + 3);
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+      }
+    }
+  };
+  switch (mbs) {
+    case 1: run(std::integral_constant<int, 1>{}); break;
+    case 2: run(std::integral_constant<int, 2>{}); break;
+    case 3: run(std::integral_constant<int, 3>{}); break;
+    default: run(std::integral_constant<int, 4>{}); break;
+  }
+  if (bad_scale) set_error(P.err, 16);
+
+  // acc[nb][mb][r] = C[m = 16 mb + fr][n = NS/4 * wave + 16 nb + 4 g + r]
+  float* cr = reinterpret_cast<float*>(smem);
+#pragma unroll
+  for (int nb = 0; nb < NF; ++nb)
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      const int n = (NS / 4) * wave + 16 * nb + 4 * g;
+      *reinterpret_cast<float4*>(cr + (16 * mb + fr) * CLD + n) =
+          make_float4(acc[nb][mb][0], acc[nb][mb][1], acc[nb][mb][2], acc[nb][mb][3]);
+    }
+  __syncthreads();
+  epilogue<bf16, EPI>(P, cr, CLD, m0, mrows, n0 >> 4, nrows >> 4, grp);
+}
+
+template <int NS, int WF, int RC>
+hipError_t slab_launch(const Gemm& g, hipStream_t s) {
+  const int64_t grid = tile_grid(g, SM, NS);
+  if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
+  dim3 gd((unsigned)grid), bd(256);
+  switch (g.epi) {
+    case EPI_QKV: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_QKV>), gd, bd, 0, s, g); break;
+    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_RESIDUAL>), gd, bd, 0, s, g); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_SWIGLU>), gd, bd, 0, s, g); break;
+    default: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_BIAS>), gd, bd, 0, s, g); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool slab_gemm_applies(int dtype, int expert_fmt, const Gemm& g) {
+  if (dtype != 1 || g.k <= 0 || g.k % 64 || g.n % 16 || g.n_groups > TILE_MAXG || !g.group_off) return false;
+  // 32-bit buffer offsets: token rows from x itself, weights within one group
+  const int64_t xr = g.x_rows > 0 ? g.x_rows : g.n_rows;
+  if (xr * g.k * 2 >= (1LL << 31) || (int64_t)g.n * g.k * 2 >= (1LL << 31)) return false;
+  if (expert_fmt != 0) return (int64_t)g.n_rows <= (int64_t)SLAB_MAX_ROWS_FP4 * g.n_groups;
+  return !tiled_gemm_applies(dtype, g);
+}
+
+hipError_t launch_gemm_slab(int expert_fmt, const Gemm& g, hipStream_t s) {
+  if (expert_fmt != 0) {
+    if (!g.w_scales) return hipErrorInvalidValue;
+    return slab_launch<128, 1, 2>(g, s);
+  }
+  return slab_launch<128, 0, 2>(g, s);
+}
+
+}  // namespace mcpu

@@ -139,6 +139,13 @@ hipError_t launch_gemm_tiled(int expert_fmt, const Gemm& g, hipStream_t s);
 // launch has at least two tiles per compute unit (bf16 activations, k % 32 == 0).
 bool pipe_gemm_applies(int dtype, const Gemm& g);
 hipError_t launch_gemm_pipe(int expert_fmt, const Gemm& g, hipStream_t s);
+// Weight slabs (gemm_slab.hip): grouped GEMMs with bf16 activations whose
+// groups are too short for tiles (bf16 weights, under TILED_MIN_ROWS rows per
+// group) or whose MXFP4 weights dominate the traffic (up to SLAB_MAX_ROWS_FP4
+// rows per group on average); k a multiple of 64.
+constexpr int SLAB_MAX_ROWS_FP4 = 96;
+bool slab_gemm_applies(int dtype, int expert_fmt, const Gemm& g);
+hipError_t launch_gemm_slab(int expert_fmt, const Gemm& g, hipStream_t s);
 
 // ---- norms, router, permutation, combine --------------------------------
 

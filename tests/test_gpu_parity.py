@@ -347,15 +347,10 @@ def _moe_shape(hidden, ffn, fmt):
                    ffn_dim=ffn, expert_fmt=fmt)
 
 
-@pytest.mark.parametrize("fmt", ["dense", "mxfp4"])
-@pytest.mark.parametrize("hidden,ffn,T", [(512, 512, 1000), (1024, 1024, 3600)])
-def test_moe_forward_many_rows(fmt, hidden, ffn, T):
-    """Expert GEMMs with hundreds of rows per expert (64- and 128-row tiles,
-    ragged last tiles in every group)."""
-    s = _moe_shape(hidden, ffn, fmt)
-    wl = W.custom(s, [4], [1], 1071 + hidden)
+def _moe_forward_check(s, T, seed, h_seed):
+    wl = W.custom(s, [4], [1], seed)
     dw = mcpu.DeviceWeights(s, wl.weights)
-    h = W.synth_normal(9, 4, (T, s.hidden))
+    h = W.synth_normal(9, h_seed, (T, s.hidden))
     out = torch.empty((T, s.hidden), device="cuda")
     idx = torch.empty((T, s.top_k), dtype=torch.int32, device="cuda")
     wt = torch.empty((T, s.top_k), device="cuda")
@@ -371,6 +366,22 @@ def test_moe_forward_many_rows(fmt, hidden, ffn, T):
         f[tie] = idx.cpu().numpy()[tie]
         ref = O.moe(s, weights, h, force_idx=f)
     PT.check("moe out", _np(out), ref["out"], "bf16")
+
+
+@pytest.mark.parametrize("fmt", ["dense", "mxfp4"])
+@pytest.mark.parametrize("hidden,ffn,T", [(512, 512, 1000), (1024, 1024, 3600)])
+def test_moe_forward_many_rows(fmt, hidden, ffn, T):
+    """Expert GEMMs with hundreds of rows per expert (64- and 128-row tiles,
+    ragged last tiles in every group)."""
+    _moe_forward_check(_moe_shape(hidden, ffn, fmt), T, 1071 + hidden, 4)
+
+
+@pytest.mark.parametrize("fmt,T", [("dense", 40), ("mxfp4", 200), ("mxfp4", 350)])
+def test_moe_forward_slab_rows(fmt, T):
+    """Expert GEMMs on weight slabs: about 10 (bf16 weights) or 50 and 90
+    (MXFP4) rows per expert, so groups span one or two 64-row items with
+    ragged ends; 576 = 4.5 reduction chunks, so the last chunk is a half."""
+    _moe_forward_check(_moe_shape(576, 576, fmt), T, 1075, 6)
 
 
 def test_dense_projections_ragged_rows_sampled():
