@@ -69,6 +69,7 @@ __device__ int block_exclusive_scan(int local, int* sums, int& total) {
 __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnPlan P) {
   __shared__ int sums[160];
   const int tid = threadIdx.x, nt = blockDim.x;
+  for (int i = tid; i < P.n_zero; i += nt) P.zero[i] = 0;
   // tokens: positions and split counts (no splits for prefill sequences)
   const int per = (P.n_tokens + nt - 1) / nt;
   const int t0 = min(P.n_tokens, tid * per), t1 = min(P.n_tokens, t0 + per);

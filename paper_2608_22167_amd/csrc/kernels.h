@@ -21,6 +21,8 @@ struct AttnPlan {
   int32_t* split_start;     // [n_tokens + 1] out
   int32_t* blk_start;       // [batch + 1] out: first prefill block of each sequence
   int32_t* err;
+  int32_t* zero;            // [n_zero] words cleared for the layer's later kernels
+  int n_zero;
 };
 
 // Chunked prefill: the new tokens of a sequence attend causally to its pages
@@ -126,6 +128,13 @@ struct Gemm {
   int32_t* err;
   int max_rows_per_group;   // upper bound used to pick the m-tiling
   int x_rows;               // rows of x when row_src gathers from it (0: n_rows)
+  // reduction split over workgroups (one matrix, few rows): fp32 partial
+  // tiles, slab_split_part_floats(n, k, n_rows) of them, and SPLIT_MAX_TILES
+  // per-tile arrival counters that are zero on entry and left zero; nullptr
+  // disables the split
+  float* part;
+  int32_t* part_cnt;
+  int k_splits;             // set by the launcher
 };
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s);
 // LDS-tiled path (gemm_tiled.hip): bf16, k a multiple of 64, at least
@@ -145,6 +154,12 @@ hipError_t launch_gemm_pipe(int expert_fmt, const Gemm& g, hipStream_t s);
 // rows per group on average); k a multiple of 64.
 constexpr int SLAB_MAX_ROWS_FP4 = 96;
 bool slab_gemm_applies(int dtype, int expert_fmt, const Gemm& g);
+// One bf16 matrix against at most SPLIT_MAX_ROWS token rows: the slabs also
+// split the reduction so that every compute unit streams weights; the last
+// workgroup of a tile to finish sums the partial tiles in split order.
+constexpr int SPLIT_MAX_ROWS = 64;
+constexpr int SPLIT_MAX_TILES = 1024;
+size_t slab_split_part_floats(int n, int k, int n_rows);  // 0: no split for this shape
 hipError_t launch_gemm_slab(int expert_fmt, const Gemm& g, hipStream_t s);
 
 // ---- norms, router, permutation, combine --------------------------------

@@ -488,6 +488,19 @@ int moe_forward(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, int32_t 
   return run_moe(cfg, w, n_tokens, h, out, topk_idx, topk_w, force_idx, m, err_word(workspace), stream);
 }
 
+// fp32 partial tiles of the dense projections when they split the reduction
+// over workgroups (bf16 layers, a few rows): the most any row count up to
+// max_rows needs, so the carve does not depend on the call's row count
+size_t layer_split_floats(const mcpu_layer_cfg* c, int max_rows) {
+  if (c->dtype != MCPU_BF16) return 0;
+  const int H = c->hidden, D = c->head_dim;
+  size_t m = 0;
+  for (int r = 1; r <= std::min(max_rows, SPLIT_MAX_ROWS); ++r)
+    m = std::max({m, slab_split_part_floats((c->n_q_heads + 2 * c->n_kv_heads) * D, H, r),
+                  slab_split_part_floats(H, c->n_q_heads * D, r)});
+  return m;
+}
+
 size_t decode_layer_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_batch, int32_t max_tokens) {
   if (check_cfg(cfg)) return 0;
   int T = std::max(max_tokens, max_batch);
@@ -499,6 +512,8 @@ size_t decode_layer_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_batch,
   cv.take_bytes((size_t)T * cfg->n_q_heads * cfg->head_dim * db);     // o
   cv.take<float>((size_t)T * cfg->hidden);                            // h1
   carve_moe(cv, cfg, T);
+  cv.take<float>(layer_split_floats(cfg, T));                         // split partial tiles
+  cv.take<int32_t>(SPLIT_MAX_TILES);                                  // their arrival counters
   return (cv.off + 255) & ~size_t(255);
 }
 
@@ -534,11 +549,19 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
   void* o = cv.take_bytes((size_t)Tc * Hq * D * db);
   float* h1 = cv.take<float>((size_t)Tc * H);
   MoeBufs mb = carve_moe(cv, cfg, Tc);
+  const size_t split_floats = layer_split_floats(cfg, Tc);
+  float* part = cv.take<float>(split_floats);
+  int32_t* part_cnt = cv.take<int32_t>(SPLIT_MAX_TILES);
   int32_t* err = err_word(workspace);
 
   {
     Timed tm(MCPU_KERNEL_ATTN_PLAN, stream);
-    HIP_TRY(launch_attn_plan(make_plan(cfg, batch, seq_lens, cu_q, ph, ab, err), stream));
+    AttnPlan pl = make_plan(cfg, batch, seq_lens, cu_q, ph, ab, err);
+    if (split_floats) {  // the split GEMMs' counters start at zero
+      pl.zero = part_cnt;
+      pl.n_zero = SPLIT_MAX_TILES;
+    }
+    HIP_TRY(launch_attn_plan(pl, stream));
   }
 
   RmsNorm rn{};
@@ -554,6 +577,7 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
   gq.k_pool = pool->k; gq.v_pool = pool->v; gq.page_table = page_table; gq.max_pages = max_pages;
   gq.n_pages = pool->n_pages; gq.tok_seq = ab.tok_seq; gq.tok_pos = ab.tok_pos; gq.rope_cos = w->rope_cos;
   gq.rope_sin = w->rope_sin; gq.rope_max_pos = w->rope_max_pos; gq.err = err; gq.max_rows_per_group = T;
+  if (split_floats) { gq.part = part; gq.part_cnt = part_cnt; }
   {
     Timed tm(MCPU_KERNEL_QKV, stream);
     HIP_TRY(launch_gemm(cfg->dtype, MCPU_EXPERT_DENSE, gq, stream));
@@ -566,6 +590,7 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
   Gemm go{};
   go.w = w->w_o; go.n = H; go.k = Hq * D; go.x = o; go.n_rows = T; go.n_groups = 1; go.epi = EPI_RESIDUAL;
   go.bias = w->b_o; go.residual = x_in; go.out = h1; go.err = err; go.max_rows_per_group = T;
+  if (split_floats) { go.part = part; go.part_cnt = part_cnt; }
   {
     Timed tm(MCPU_KERNEL_OPROJ, stream);
     HIP_TRY(launch_gemm(cfg->dtype, MCPU_EXPERT_DENSE, go, stream));

@@ -398,6 +398,26 @@ def test_dense_projections_ragged_rows_sampled():
     compare_layer(sub, g, None, ref)
 
 
+def test_split_projections_repeatable_sampled():
+    """50 decode tokens: the dense projections split their reduction over
+    workgroups, one ragged 64-row tile and a reduction ending in half a chunk
+    (2880 = 22.5 x 128); a second run is bit-identical (partial tiles are
+    summed in split order whatever order they arrive in), and sampled
+    sequences match the oracle."""
+    rng = np.random.default_rng(1083)
+    ctx = rng.integers(1, 400, size=50)
+    wl = W.custom(W.GPT_OSS_20B, ctx, np.ones(50), 1083)
+    gpu, step = run_layer(wl)
+    again, _ = run_layer(wl)
+    for k in gpu:
+        np.testing.assert_array_equal(gpu[k], again[k])
+    seqs = sorted({0, 31, 48, 49} | {int(b) for b in rng.choice(50, 4, replace=False)})
+    sub, rows = W.restrict(wl, seqs)
+    g = {k: v[rows] for k, v in gpu.items()}
+    ref, _ = reference(sub, g)
+    compare_layer(sub, g, None, ref)
+
+
 @pytest.mark.parametrize("fmt", ["dense", "mxfp4"])
 def test_moe_forward_large_groups_sampled(fmt):
     """16384 tokens routed over the experts (thousands of rows each): the
