@@ -106,7 +106,12 @@ typedef struct mcpu_layer_cfg {
  *    MXFP4 experts: w_gu/w_d hold E2M1 codes, [E, rows, cols/2] bytes, low
  *    nibble = even column; s_gu/s_d hold E8M0 block scales [E, rows, cols/32].
  *  sinks [Hq]            one attention-sink logit per query head
- *  rope_cos, rope_sin [rope_max_pos, d/2]  rotation of the pair (j, j + d/2) */
+ *  rope_cos, rope_sin [rope_max_pos, d/2]  rotation of the pair (j, j + d/2)
+ *  w_gu_packed, w_d_packed  optional (NULL): bf16 dense experts w_gu and w_d
+ *    in the streaming order written by mcpu_pack_weights. The grouped GEMMs
+ *    of short expert groups (decode batches of a few hundred tokens) then
+ *    read each 16-row by 128-column block as 4 KiB in a row; w_gu and w_d
+ *    stay required for the other tilings. */
 typedef struct mcpu_layer_weights {
   const float* g1;
   const void* w_qkv;
@@ -126,7 +131,25 @@ typedef struct mcpu_layer_weights {
   const float* rope_cos;
   const float* rope_sin;
   int32_t rope_max_pos;
+  const void* w_gu_packed;
+  const void* w_d_packed;
 } mcpu_layer_weights;
+
+/* Weights in streaming order (bf16 only). src is [n_groups, rows, cols]
+ * row-major with cols contiguous; rows a multiple of 16, cols of 64. dst
+ * (mcpu_packed_weights_bytes bytes, caller-owned, not aliasing src) receives,
+ * per group, row block rb (16 rows) and column chunk c (128 columns), a
+ * 4096-byte block at ((group * rows/16 + rb) * ceil(cols/128) + c) * 4096:
+ * sixteen-byte piece t * 64 + lane (t = 0..3, lane = r + 16 j with r, j =
+ * 0..15, 0..3) holds src[group][16 rb + r][128 c + 32 t + 8 j .. + 7], zero
+ * past cols. That is the operand order of the 16 x 16 x 32 matrix-core
+ * products, so each product's weight fragment is one contiguous KiB.
+ * Asynchronous on stream; returns 0 on success or mcpu_status (EINVAL for
+ * bad sizes or NULL pointers, EUNSUPPORTED for a non-bf16 dtype) and then
+ * launches nothing. */
+size_t mcpu_packed_weights_bytes(int32_t n_groups, int32_t rows, int32_t cols);
+int mcpu_pack_weights(int32_t dtype, const void* src, void* dst, int32_t n_groups, int32_t rows, int32_t cols,
+                      hipStream_t stream);
 
 /* Opaque page pool: host-side free list over a caller-owned pair of device
  * pools (K and V, each n_pages * Hkv * 16 * d elements of the layer dtype). */

@@ -53,7 +53,9 @@ __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
 template <int NF, int WF>
 struct SlabW;
 
-// bf16: per chunk and fragment four 16-byte loads (products 0..3 of the chunk)
+// bf16: per chunk and fragment four 16-byte loads (products 0..3 of the
+// chunk), from row-major weights (each load: 16 rows x 64 bytes) or from the
+// streaming-order copy (each load: one contiguous KiB, whole cache lines)
 template <int NF>
 struct SlabW<NF, 0> {
   struct Regs {
@@ -61,18 +63,32 @@ struct SlabW<NF, 0> {
   };
   __amdgpu_buffer_rsrc_t rs;
   uint32_t vo[NF];
+  int kstep, tstep;  // bytes between chunks and between products of a row
   __device__ __forceinline__ void init(const Gemm& P, int grp, const int* wrow, int g) {
-    const uint8_t* base = reinterpret_cast<const uint8_t*>(P.w) + (int64_t)grp * P.w_group_stride * 2;
-    rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), 0, 0x7FFFFFFF, BUF_D3);
+    const uint8_t* base;
+    if (P.w_packed) {
+      const int nkc = (P.k + SKC - 1) / SKC;
+      base = reinterpret_cast<const uint8_t*>(P.w_packed) + (int64_t)grp * (P.n / 16) * nkc * 4096;
 #pragma unroll
-    for (int nb = 0; nb < NF; ++nb) vo[nb] = (uint32_t)wrow[nb] * (uint32_t)(P.k * 2) + 16 * g;
+      for (int nb = 0; nb < NF; ++nb)
+        vo[nb] = (uint32_t)(wrow[nb] >> 4) * (uint32_t)(nkc * 4096) + 16 * (wrow[nb] & 15) + 256 * g;
+      kstep = 4096;
+      tstep = 1024;
+    } else {
+      base = reinterpret_cast<const uint8_t*>(P.w) + (int64_t)grp * P.w_group_stride * 2;
+#pragma unroll
+      for (int nb = 0; nb < NF; ++nb) vo[nb] = (uint32_t)wrow[nb] * (uint32_t)(P.k * 2) + 16 * g;
+      kstep = SKC * 2;
+      tstep = 64;
+    }
+    rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), 0, 0x7FFFFFFF, BUF_D3);
   }
   __device__ __forceinline__ void fetch(Regs& r, int kc, int nsteps) const {
 #pragma unroll
     for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
       for (int t = 0; t < 4; ++t)
-        r.f[nb][t] = __builtin_amdgcn_raw_buffer_load_b128(rs, vo[nb], uniform((kc * SKC + 32 * min(t, nsteps - 1)) * 2), 0);
+        r.f[nb][t] = __builtin_amdgcn_raw_buffer_load_b128(rs, vo[nb], uniform(kc * kstep + tstep * min(t, nsteps - 1)), 0);
   }
   struct Dec {};
   __device__ __forceinline__ void prepare(const Regs&, Dec&, uint32_t&, uint32_t) const {}
@@ -417,8 +433,29 @@ bool slab_gemm_applies(int dtype, int expert_fmt, const Gemm& g) {
   // 32-bit buffer offsets: token rows from x itself, weights within one group
   const int64_t xr = g.x_rows > 0 ? g.x_rows : g.n_rows;
   if (xr * g.k * 2 >= (1LL << 31) || (int64_t)g.n * g.k * 2 >= (1LL << 31)) return false;
+  if (g.w_packed && (expert_fmt != 0 || (int64_t)g.n * ((g.k + SKC - 1) / SKC) * 256 >= (1LL << 31))) return false;
   if (expert_fmt != 0) return (int64_t)g.n_rows <= (int64_t)SLAB_MAX_ROWS_FP4 * g.n_groups;
   return !tiled_gemm_applies(dtype, g);
+}
+
+// One thread per 16-byte piece of the streaming-order copy: piece i of block
+// (group, row block, chunk) = i / 256 holds row 16 rb + lane % 16, columns
+// 128 c + 32 t + 8 (lane / 16) .. + 7, with t = i / 64 % 4 and lane = i % 64.
+__global__ __launch_bounds__(256) void pack_weights_kernel(const bf16* __restrict__ src, uint8_t* __restrict__ dst,
+                                                            int rows, int cols, int64_t pieces) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= pieces) return;
+  const int nkc = (cols + SKC - 1) / SKC, rbs = rows / 16;
+  const int lane = (int)(i & 63), t = (int)((i >> 6) & 3);
+  const int64_t blk = i >> 8;
+  const int c = (int)(blk % nkc);
+  const int64_t grb = blk / nkc;
+  const int rb = (int)(grb % rbs);
+  const int64_t grp = grb / rbs;
+  const int col = SKC * c + 32 * t + 8 * (lane >> 4);  // a multiple of 8; cols a multiple of 64
+  uint4 v = make_uint4(0u, 0u, 0u, 0u);
+  if (col < cols) v = *reinterpret_cast<const uint4*>(src + (grp * rows + 16 * rb + (lane & 15)) * cols + col);
+  *reinterpret_cast<uint4*>(dst + i * 16) = v;
 }
 
 hipError_t launch_gemm_slab(int expert_fmt, const Gemm& g, hipStream_t s) {
@@ -434,6 +471,16 @@ hipError_t launch_gemm_slab(int expert_fmt, const Gemm& g, hipStream_t s) {
     return slab_launch<128, 1, 2, false>(g, s, tile_grid(g, SM, 128));
   }
   return slab_launch<128, 0, 2, false>(g, s, tile_grid(g, SM, 128));
+}
+
+hipError_t launch_pack_weights(const void* src, void* dst, int groups, int rows, int cols, hipStream_t s) {
+  const int64_t pieces = (int64_t)groups * (rows / 16) * ((cols + SKC - 1) / SKC) * 256;
+  if (pieces <= 0) return hipSuccess;
+  const int64_t blocks = (pieces + 255) / 256;
+  if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(pack_weights_kernel, dim3((unsigned)blocks), dim3(256), 0, s, reinterpret_cast<const bf16*>(src),
+                     reinterpret_cast<uint8_t*>(dst), rows, cols, pieces);
+  return hipGetLastError();
 }
 
 }  // namespace mcpu

@@ -99,6 +99,7 @@ struct Gemm {
   // Y[row][n] = sum_k X[src(row)][k] * W[group][n][k], rows of a group are
   // group_off[g] .. group_off[g+1] (or 0 .. n_rows for one group).
   const void* w;
+  const void* w_packed;     // bf16 weights in streaming order (mcpu_pack_weights) or nullptr
   const uint8_t* w_scales;  // MXFP4 block scales or nullptr
   int64_t w_group_stride;   // elements (or bytes for MXFP4 codes) per group
   int n, k;
@@ -160,6 +161,8 @@ bool slab_gemm_applies(int dtype, int expert_fmt, const Gemm& g);
 constexpr int SPLIT_MAX_ROWS = 64;
 constexpr int SPLIT_MAX_TILES = 1024;
 size_t slab_split_part_floats(int n, int k, int n_rows);  // 0: no split for this shape
+// bf16 [groups][rows][cols] -> streaming order (the layout mcpu_pack_weights documents)
+hipError_t launch_pack_weights(const void* src, void* dst, int groups, int rows, int cols, hipStream_t s);
 hipError_t launch_gemm_slab(int expert_fmt, const Gemm& g, hipStream_t s);
 
 // ---- norms, router, permutation, combine --------------------------------

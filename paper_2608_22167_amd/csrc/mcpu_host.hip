@@ -232,6 +232,12 @@ int check_weights(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, bool att
     return fail(MCPU_EINVAL, "MXFP4 experts need the scale arrays s_gu and s_d");
   if (attn && (!w->g1 || !w->w_qkv || !w->b_qkv || !w->w_o || !w->b_o || !w->rope_cos || !w->rope_sin))
     return fail(MCPU_EINVAL, "an attention weight pointer is NULL");
+  if ((w->w_gu_packed || w->w_d_packed) && (c->expert_fmt != MCPU_EXPERT_DENSE || c->dtype != MCPU_BF16))
+    return fail(MCPU_EINVAL, "packed expert weights need bf16 dense experts");
+  if (w->w_gu_packed && (2 * c->ffn_dim % 16 || c->hidden % 64))
+    return fail(MCPU_EINVAL, "packed w_gu needs 2 * ffn_dim %% 16 == 0 and hidden %% 64 == 0");
+  if (w->w_d_packed && (c->hidden % 16 || c->ffn_dim % 64))
+    return fail(MCPU_EINVAL, "packed w_d needs hidden %% 16 == 0 and ffn_dim %% 64 == 0");
   return MCPU_OK;
 }
 
@@ -269,7 +275,7 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   g1.x = m.hn; g1.row_src = m.src_tok; g1.group_off = m.group_off; g1.n_rows = T * K; g1.n_groups = E;
   g1.epi = EPI_SWIGLU; g1.bias = w->b_gu; g1.bias_group_stride = 2 * I; g1.out = m.act;
   g1.swiglu_alpha = c->swiglu_alpha; g1.swiglu_limit = c->swiglu_limit; g1.swiglu_beta = c->swiglu_beta;
-  g1.err = err; g1.max_rows_per_group = max_rows; g1.x_rows = T;
+  g1.err = err; g1.max_rows_per_group = max_rows; g1.x_rows = T; g1.w_packed = w->w_gu_packed;
   {
     Timed tm(MCPU_KERNEL_EXPERT_GU, st);
     HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g1, st));
@@ -279,7 +285,7 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   g2.w = w->w_d; g2.w_scales = w->s_d; g2.w_group_stride = (int64_t)H * I / fdiv; g2.n = H; g2.k = I;
   g2.x = m.act; g2.group_off = m.group_off; g2.n_rows = T * K; g2.n_groups = E;
   g2.epi = EPI_BIAS; g2.bias = w->b_d; g2.bias_group_stride = H; g2.out = m.y;
-  g2.err = err; g2.max_rows_per_group = max_rows;
+  g2.err = err; g2.max_rows_per_group = max_rows; g2.w_packed = w->w_d_packed;
   {
     Timed tm(MCPU_KERNEL_EXPERT_DOWN, st);
     HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g2, st));
@@ -463,6 +469,25 @@ int paged_attention(const mcpu_layer_cfg* cfg, const float* sinks, mcpu_kv_pool*
   AttnBufs ab = carve_attention(cv, cfg, std::max(ph.n_tokens, batch));
   return run_attention(cfg, sinks, pool, batch, page_table, max_pages, seq_lens, cu_q, ph, q, o, ab,
                        err_word(workspace), stream, false);
+}
+
+size_t mcpu_packed_weights_bytes(int32_t n_groups, int32_t rows, int32_t cols) {
+  if (n_groups <= 0 || rows <= 0 || cols <= 0 || rows % 16 || cols % 64) return 0;
+  return (size_t)n_groups * (rows / 16) * ((cols + 127) / 128) * 4096;
+}
+
+int mcpu_pack_weights(int32_t dtype, const void* src, void* dst, int32_t n_groups, int32_t rows, int32_t cols,
+                      hipStream_t stream) {
+  if (dtype != MCPU_BF16) return fail(MCPU_EUNSUPPORTED, "streaming-order weights are bf16 only (dtype %d)", dtype);
+  const size_t bytes = mcpu_packed_weights_bytes(n_groups, rows, cols);
+  if (bytes == 0) return fail(MCPU_EINVAL, "groups %d, rows %d (multiple of 16), cols %d (multiple of 64)", n_groups, rows, cols);
+  if (!src || !dst) return fail(MCPU_EINVAL, "NULL pointer");
+  if ((uintptr_t)src % 16 || (uintptr_t)dst % 16) return fail(MCPU_EINVAL, "src and dst must be 16-byte aligned");
+  const uintptr_t s0 = (uintptr_t)src, s1 = s0 + (size_t)n_groups * rows * cols * 2;
+  const uintptr_t d0 = (uintptr_t)dst, d1 = d0 + bytes;
+  if (s0 < d1 && d0 < s1) return fail(MCPU_EINVAL, "src and dst overlap");
+  HIP_TRY(launch_pack_weights(src, dst, n_groups, rows, cols, stream));
+  return MCPU_OK;
 }
 
 size_t moe_forward_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_tokens) {

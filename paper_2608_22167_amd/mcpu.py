@@ -26,7 +26,7 @@ EXPORTED = ("mcpu_last_error", "kv_pool_create", "kv_pool_destroy", "kv_pool_fre
             "kv_pages_alloc", "kv_pages_free", "kv_pages_append", "paged_attention_workspace_size",
             "paged_attention", "moe_forward_workspace_size", "moe_forward",
             "decode_layer_workspace_size", "decode_layer", "mcpu_check_device_errors",
-            "mcpu_timing_start", "mcpu_timing_read")
+            "mcpu_timing_start", "mcpu_timing_read", "mcpu_packed_weights_bytes", "mcpu_pack_weights")
 
 KERNELS = ("attn_plan", "rmsnorm", "qkv", "attn_split", "attn_combine", "oproj", "router", "permute",
            "expert_gu", "expert_down", "moe_combine", "kv_append", "attn_prefill")
@@ -48,7 +48,8 @@ class LayerCfg(ctypes.Structure):
 class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "g1", "w_qkv", "b_qkv", "w_o", "b_o", "g2", "w_r", "b_r", "w_gu", "b_gu", "w_d", "b_d",
-        "s_gu", "s_d", "sinks", "rope_cos", "rope_sin")] + [("rope_max_pos", ctypes.c_int32)]
+        "s_gu", "s_d", "sinks", "rope_cos", "rope_sin")] + [("rope_max_pos", ctypes.c_int32)] + [
+        (n, ctypes.c_void_p) for n in ("w_gu_packed", "w_d_packed")]
 
 
 class Taps(ctypes.Structure):
@@ -86,6 +87,9 @@ def lib():
         L.decode_layer.argtypes = [vp, vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    vp, sz, vp]
         L.mcpu_check_device_errors.argtypes = [vp, vp, i32p]
+        L.mcpu_packed_weights_bytes.argtypes = [i32, i32, i32]
+        L.mcpu_packed_weights_bytes.restype = sz
+        L.mcpu_pack_weights.argtypes = [i32, vp, vp, i32, i32, i32, vp]
         L.mcpu_timing_start.argtypes = [i32, i32]
         L.mcpu_timing_read.argtypes = [i32, vp, i32, i32p]
         _LIB = L
@@ -135,14 +139,30 @@ def make_cfg(shape) -> LayerCfg:
                     swiglu_limit=shape.swiglu_limit, swiglu_beta=shape.swiglu_beta)
 
 
-class DeviceWeights:
-    """Layer parameters copied to the GPU, with the mcpu_layer_weights struct."""
+def packed_weights(w: torch.Tensor, stream=None) -> torch.Tensor:
+    """Streaming-order copy of bf16 weights [groups, rows, cols] (mcpu_pack_weights)."""
+    assert w.dtype == torch.bfloat16 and w.dim() == 3 and w.is_cuda and w.is_contiguous()
+    g, rows, cols = (int(d) for d in w.shape)
+    n = lib().mcpu_packed_weights_bytes(g, rows, cols)
+    if n == 0:
+        raise McpuError(MCPU_EINVAL, f"weights {tuple(w.shape)} cannot be packed (rows % 16, cols % 64)")
+    out = torch.empty(n, dtype=torch.uint8, device=w.device)
+    _check(lib().mcpu_pack_weights(MCPU_BF16, _ptr(w), _ptr(out), g, rows, cols, _stream(stream)))
+    return out
 
-    def __init__(self, shape, W, device="cuda"):
+
+class DeviceWeights:
+    """Layer parameters copied to the GPU, with the mcpu_layer_weights struct.
+    With pack=True, bf16 dense experts also get their streaming-order copies."""
+
+    def __init__(self, shape, W, device="cuda", pack=True):
         self.t = {k: v.to(device).contiguous() for k, v in W.items()}
         t = self.t
-        p = lambda k: _ptr(t[k]) if k in t else None
         mx = shape.expert_fmt == "mxfp4"
+        if pack and not mx and shape.dtype == "bf16" and shape.hidden % 64 == 0 and shape.ffn_dim % 64 == 0:
+            t["w_gu_packed"] = packed_weights(t["w_gu"])
+            t["w_d_packed"] = packed_weights(t["w_d"])
+        p = lambda k: _ptr(t[k]) if k in t else None
         self.struct = LayerWeights(
             g1=p("g1"), w_qkv=p("w_qkv"), b_qkv=p("b_qkv"), w_o=p("w_o"), b_o=p("b_o"), g2=p("g2"),
             w_r=p("w_r"), b_r=p("b_r"),
@@ -150,7 +170,8 @@ class DeviceWeights:
             w_d=p("w_d_codes") if mx else p("w_d"), b_d=p("b_d"),
             s_gu=p("w_gu_scales") if mx else None, s_d=p("w_d_scales") if mx else None,
             sinks=p("sinks"), rope_cos=p("rope_cos"), rope_sin=p("rope_sin"),
-            rope_max_pos=int(t["rope_cos"].shape[0]) if "rope_cos" in t else 0)
+            rope_max_pos=int(t["rope_cos"].shape[0]) if "rope_cos" in t else 0,
+            w_gu_packed=p("w_gu_packed"), w_d_packed=p("w_d_packed"))
 
 
 # ---------------------------------------------------------------------------

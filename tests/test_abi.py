@@ -79,3 +79,20 @@ def test_workspace_sizes_grow_with_batch():
     assert 0 < a < b
     assert mcpu.moe_forward_workspace_size(s, 64) < a
     assert mcpu.paged_attention_workspace_size(s, 64, 64) < a
+
+
+def test_packed_weights_size_and_argument_checks():
+    """mcpu_packed_weights_bytes: 4 KiB per 16-row x 128-column block, the last
+    column chunk padded; mcpu_pack_weights rejects bad arguments on the host
+    (dummy addresses, never dereferenced: every case returns before a launch)."""
+    L = mcpu.lib()
+    assert L.mcpu_packed_weights_bytes(32, 5760, 2880) == 32 * 360 * 23 * 4096
+    assert L.mcpu_packed_weights_bytes(2, 16, 64) == 2 * 4096
+    for bad in [(0, 16, 64), (1, 8, 64), (1, 16, 96), (1, 16, 0), (-1, 16, 64)]:
+        assert L.mcpu_packed_weights_bytes(*bad) == 0, bad
+    a, b = 1 << 20, 1 << 30
+    assert L.mcpu_pack_weights(mcpu.MCPU_F32, a, b, 1, 16, 64, None) == mcpu.MCPU_EUNSUPPORTED
+    assert L.mcpu_pack_weights(mcpu.MCPU_BF16, a, b, 1, 16, 96, None) == mcpu.MCPU_EINVAL
+    assert L.mcpu_pack_weights(mcpu.MCPU_BF16, None, b, 1, 16, 64, None) == mcpu.MCPU_EINVAL
+    assert L.mcpu_pack_weights(mcpu.MCPU_BF16, a + 8, b, 1, 16, 64, None) == mcpu.MCPU_EINVAL  # misaligned
+    assert L.mcpu_pack_weights(mcpu.MCPU_BF16, a, a + 1024, 1, 16, 64, None) == mcpu.MCPU_EINVAL  # overlap

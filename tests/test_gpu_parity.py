@@ -398,6 +398,53 @@ def test_dense_projections_ragged_rows_sampled():
     compare_layer(sub, g, None, ref)
 
 
+def test_pack_weights_layout_bit_exact():
+    """mcpu_pack_weights writes the documented streaming order, computed here on
+    the host piece by piece, with zeros past the last column (192 columns = 1.5
+    chunks of 128)."""
+    rng = np.random.default_rng(1077)
+    g, rows, cols = 3, 48, 192
+    w = torch.from_numpy(rng.standard_normal((g, rows, cols)).astype(np.float32)).to(torch.bfloat16)
+    packed = mcpu.packed_weights(w.cuda())
+    torch.cuda.synchronize()
+    got = packed.cpu().numpy().view(np.uint16).reshape(-1, 8)
+    src = w.view(torch.int16).numpy().view(np.uint16)
+    want = np.zeros_like(got)
+    i = 0
+    for e in range(g):
+        for rb in range(rows // 16):
+            for c in range(-(-cols // 128)):
+                for t in range(4):
+                    for lane in range(64):
+                        col = 128 * c + 32 * t + 8 * (lane // 16)
+                        if col < cols:
+                            want[i] = src[e, 16 * rb + lane % 16, col:col + 8]
+                        i += 1
+    assert i == got.shape[0]
+    np.testing.assert_array_equal(got, want)
+
+
+def test_moe_forward_packed_weights_bitwise_equal_row_major():
+    """Short expert groups read the streaming-order copy when it is given; the
+    products see the same operands in the same order, so the outputs are
+    bit-identical to those from the row-major weights."""
+    s = _moe_shape(576, 576, "dense")
+    T = 40
+    wl = W.custom(s, [4], [1], 1075)
+    h = W.synth_normal(9, 6, (T, s.hidden)).cuda()
+    outs = []
+    for pack in (False, True):
+        dw = mcpu.DeviceWeights(s, wl.weights, pack=pack)
+        assert ("w_gu_packed" in dw.t) == pack
+        out = torch.empty((T, s.hidden), device="cuda")
+        ws = mcpu.workspace(mcpu.moe_forward_workspace_size(s, T))
+        mcpu.moe_forward(s, dw, h, out, None, None, None, ws)
+        torch.cuda.synchronize()
+        assert mcpu.mcpu_check_device_errors(ws) == 0
+        outs.append(out.cpu())
+    assert torch.equal(outs[0], outs[1])
+
+
 def test_split_projections_repeatable_sampled():
     """50 decode tokens: the dense projections split their reduction over
     workgroups, one ragged 64-row tile and a reduction ending in half a chunk
