@@ -124,6 +124,31 @@ template <> struct Raw8<bf16> {
   }
 };
 
+// Step of the router's reduce-scatter: N partial sums per lane, partner at
+// lane distance O. The upper lane of each pair keeps the upper half of the
+// sums (adding its partner's copy), the lower lane the lower half; with one
+// sum left, partners just add. Templated so every index is a constant (a
+// runtime half-width would put the array in scratch memory).
+template <int N, int O, int E>
+__device__ __forceinline__ void reduce_scatter(float (&acc)[E], int lane) {
+  if constexpr (O >= 1) {
+    if constexpr (N > 1) {
+      constexpr int half = N / 2;
+      const bool upper = (lane & O) != 0;
+#pragma unroll
+      for (int j = 0; j < half; ++j) {
+        const float send = upper ? acc[j] : acc[j + half];
+        const float keep = upper ? acc[j + half] : acc[j];
+        acc[j] = keep + __shfl_xor(send, O, 64);
+      }
+      reduce_scatter<half, O / 2, E>(acc, lane);
+    } else {
+      acc[0] += __shfl_xor(acc[0], O, 64);
+      reduce_scatter<1, O / 2, E>(acc, lane);
+    }
+  }
+}
+
 // One workgroup per token. Thread i owns the 8-wide reduction chunks i, i+256,
 // ... and accumulates all E logits over them; partial logits are then summed
 // across lanes (wavefront butterflies) and across the 4 wavefronts (LDS).
@@ -186,29 +211,8 @@ __global__ __launch_bounds__(256) void router_kernel(Router P) {
   }
   // reduce-scatter across the 64 lanes: each halving step trades half of the
   // partial sums with the partner lane, so lane l ends with expert l / (64 / E)
-  {
-    int n = E;
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) {
-      if (n > 1) {
-        const bool upper = (lane & o) != 0;
-        const int half = n / 2;
-#pragma unroll
-        for (int j = 0; j < E / 2; ++j) {
-          if (j < half) {
-            const float send = upper ? acc[j] : acc[j + half];
-            const float keep = upper ? acc[j + half] : acc[j];
-            acc[j] = keep + __shfl_xor(send, o, 64);
-          }
-        }
-        n = half;
-      } else {
-        acc[0] += __shfl_xor(acc[0], o, 64);
-      }
-    }
-    const int e = lane / (64 / E);
-    if (lane % (64 / E) == 0) part[wave][e] = acc[0];
-  }
+  reduce_scatter<E, 32>(acc, lane);
+  if (lane % (64 / E) == 0) part[wave][lane / (64 / E)] = acc[0];
   __syncthreads();
   if (threadIdx.x < P.n_experts) {
     const int e = threadIdx.x;
@@ -218,10 +222,13 @@ __global__ __launch_bounds__(256) void router_kernel(Router P) {
   __syncthreads();
 
   if (wave == 0) {
+    // lane s < K keeps the s-th selection (registers only: the selection
+    // count is a runtime value, so an array indexed by it would live in
+    // scratch memory)
     const int NE = P.n_experts, K = P.top_k;
     float v = lane < NE ? logits[lane] : -INFINITY;
-    int sel_e[8];
-    float sel_v[8];
+    int my_e = 0;
+    float my_v = -INFINITY;
     for (int s = 0; s < K; ++s) {
       int e;
       if (P.force_idx) {
@@ -246,26 +253,20 @@ __global__ __launch_bounds__(256) void router_kernel(Router P) {
         e = bi;
         if (lane == e) v = -INFINITY;
       }
-      sel_e[s] = e;
-      sel_v[s] = logits[e];
+      if (lane == s) {
+        my_e = e;
+        my_v = logits[e];
+      }
     }
-    float mx = sel_v[0];
-    for (int s = 1; s < K; ++s) mx = fmaxf(mx, sel_v[s]);
-    float den = 0.f, wv[8];
-    for (int s = 0; s < K; ++s) {
-      wv[s] = expf(sel_v[s] - mx);
-      den += wv[s];
-    }
+    // softmax over the selections, maximum and sum taken in selection order
+    float mx = __shfl(my_v, 0, 64);
+    for (int s = 1; s < K; ++s) mx = fmaxf(mx, __shfl(my_v, s, 64));
+    const float ex = expf(my_v - mx);
+    float den = 0.f;
+    for (int s = 0; s < K; ++s) den += __shfl(ex, s, 64);
     if (lane < K) {
-      float mine = 0.f;
-      int me = 0;
-      for (int s = 0; s < K; ++s)
-        if (s == lane) {
-          mine = wv[s] / den;
-          me = sel_e[s];
-        }
-      P.idx_out[(int64_t)t * K + lane] = me;
-      P.w_out[(int64_t)t * K + lane] = mine;
+      P.idx_out[(int64_t)t * K + lane] = my_e;
+      P.w_out[(int64_t)t * K + lane] = ex / den;
     }
   }
 }

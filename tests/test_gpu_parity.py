@@ -378,9 +378,10 @@ def test_moe_forward_many_rows(fmt, hidden, ffn, T):
 
 @pytest.mark.parametrize("fmt,T", [("dense", 40), ("mxfp4", 200), ("mxfp4", 350)])
 def test_moe_forward_slab_rows(fmt, T):
-    """Expert GEMMs on weight slabs: about 10 (bf16 weights) or 50 and 90
-    (MXFP4) rows per expert, so groups span one or two 64-row items with
-    ragged ends; 576 = 4.5 reduction chunks, so the last chunk is a half."""
+    """Expert GEMMs on weight slabs: about 10 (bf16 weights, from the
+    streaming-order copy) or 50 and 90 (MXFP4) rows per expert, so groups span
+    one or two 64-row items with ragged ends; 576 = 4.5 reduction chunks, so
+    the last chunk is a half."""
     _moe_forward_check(_moe_shape(576, 576, fmt), T, 1075, 6)
 
 
