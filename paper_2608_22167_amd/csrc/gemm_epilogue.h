@@ -115,9 +115,37 @@ __device__ __forceinline__ void store8(bf16* p, const float v[8]) {
 
 // cr[m * ld + n]: the finished fp32 tile for token rows m0 .. m0 + mrows - 1 and
 // the nblk 16-row weight blocks starting at blk0.
+// A thread's bias values in the SwiGLU and bias/residual epilogues: the same
+// columns in every pass over a tile's rows, so a kernel that writes a tile in
+// several passes loads them once (epilogue_bias) and hands them to each pass.
+struct EpiBias {
+  float4 v;
+};
+template <int EPI>
+__device__ __forceinline__ EpiBias epilogue_bias(const Gemm& P, int blk0, int nblk, int grp) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const float* bias = P.bias + (int64_t)grp * P.bias_group_stride;
+  EpiBias e{make_float4(0.f, 0.f, 0.f, 0.f)};
+  if constexpr (EPI == EPI_SWIGLU) {
+    const int cols = nblk * 8;
+    if (cols <= nt && tid < (nt / cols) * cols) {
+      const int c = tid % cols, col = (blk0 + (c >> 3)) * 16 + 2 * (c & 7);
+      e.v.x = bias[col];
+      e.v.y = bias[col + 1];
+    }
+  } else if constexpr (EPI == EPI_RESIDUAL || EPI == EPI_BIAS) {
+    const int nq = nblk * 4;
+    if (nq <= nt && tid < (nt / nq) * nq) {
+      const int n = blk0 * 16 + 4 * (tid % nq);
+      e.v = make_float4(bias[n], bias[n + 1], bias[n + 2], bias[n + 3]);
+    }
+  }
+  return e;
+}
+
 template <typename T, int EPI>
 __device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mrows, int blk0, int nblk,
-                         int grp) {
+                         int grp, const EpiBias* pre = nullptr) {
   const int tid = threadIdx.x, nt = blockDim.x;
   const float* bias = P.bias + (int64_t)grp * P.bias_group_stride;
   if constexpr (EPI == EPI_QKV) {
@@ -193,30 +221,75 @@ __device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mro
       }
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
+    // A thread keeps one output column (its two bias values read once) and
+    // walks the rows, so no global load waits behind an earlier iteration's
+    // store (a loop that re-read the bias per element did, one L2 round trip
+    // per element). A wavefront's consecutive columns leave as one store per row.
     T* out = reinterpret_cast<T*>(P.out);
-    const int half_n = P.n / 2;
-    for (int idx = tid; idx < mrows * nblk * 8; idx += nt) {
-      const int j = idx & 7, b = (idx >> 3) % nblk, m = (idx >> 3) / nblk;
-      const int col = (blk0 + b) * 16 + 2 * j;
-      const float gate = cr[m * ld + 16 * b + 2 * j] + bias[col];
-      const float up = cr[m * ld + 16 * b + 2 * j + 1] + bias[col + 1];
-      Elem<T>::store(out, (int64_t)(m0 + m) * half_n + (blk0 + b) * 8 + j,
-                     swiglu(gate, up, P.swiglu_alpha, P.swiglu_limit, P.swiglu_beta));
+    const int half_n = P.n / 2, cols = nblk * 8;
+    if (cols <= nt) {
+      const int lanes = nt / cols;
+      if (tid < lanes * cols) {
+        const int c = tid % cols, b = c >> 3, j = c & 7;
+        const int col = (blk0 + b) * 16 + 2 * j;
+        const float bg = pre ? pre->v.x : bias[col], bu = pre ? pre->v.y : bias[col + 1];
+        const float* cp = cr + 16 * b + 2 * j;
+        T* op = out + (int64_t)m0 * half_n + (blk0 + b) * 8 + j;
+        for (int m = tid / cols; m < mrows; m += lanes)
+          Elem<T>::store(op, (int64_t)m * half_n,
+                         swiglu(cp[m * ld] + bg, cp[m * ld + 1] + bu, P.swiglu_alpha, P.swiglu_limit, P.swiglu_beta));
+      }
+    } else {
+      for (int idx = tid; idx < mrows * cols; idx += nt) {
+        const int j = idx & 7, b = (idx >> 3) % nblk, m = (idx >> 3) / nblk;
+        const int col = (blk0 + b) * 16 + 2 * j;
+        const float gate = cr[m * ld + 16 * b + 2 * j] + bias[col];
+        const float up = cr[m * ld + 16 * b + 2 * j + 1] + bias[col + 1];
+        Elem<T>::store(out, (int64_t)(m0 + m) * half_n + (blk0 + b) * 8 + j,
+                       swiglu(gate, up, P.swiglu_alpha, P.swiglu_limit, P.swiglu_beta));
+      }
     }
   } else {  // EPI_RESIDUAL, EPI_BIAS: fp32 rows, 4 consecutive features per thread
+    // As above: fixed features per thread (bias read once); residual rows of
+    // four passes are loaded before their stores.
     float* out = reinterpret_cast<float*>(P.out);
     const int nq = nblk * 4;
-    for (int idx = tid; idx < mrows * nq; idx += nt) {
-      const int q = idx % nq, m = idx / nq;
-      const int n = blk0 * 16 + 4 * q;
-      const int64_t o = (int64_t)(m0 + m) * P.n + n;
-      float4 v = make_float4(cr[m * ld + 4 * q] + bias[n], cr[m * ld + 4 * q + 1] + bias[n + 1],
-                             cr[m * ld + 4 * q + 2] + bias[n + 2], cr[m * ld + 4 * q + 3] + bias[n + 3]);
+    auto row = [&](int m, int q, const float4& bv, const float4* r) __attribute__((always_inline)) {
+      const int64_t o = (int64_t)(m0 + m) * P.n + blk0 * 16 + 4 * q;
+      float4 v = make_float4(cr[m * ld + 4 * q] + bv.x, cr[m * ld + 4 * q + 1] + bv.y,
+                             cr[m * ld + 4 * q + 2] + bv.z, cr[m * ld + 4 * q + 3] + bv.w);
       if constexpr (EPI == EPI_RESIDUAL) {
-        const float4 r = *reinterpret_cast<const float4*>(P.residual + o);
-        v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
+        v.x += r->x; v.y += r->y; v.z += r->z; v.w += r->w;
       }
       *reinterpret_cast<float4*>(out + o) = v;
+    };
+    if (nq <= nt) {
+      const int lanes = nt / nq;
+      if (tid < lanes * nq) {
+        const int q = tid % nq, n = blk0 * 16 + 4 * q;
+        const float4 bv = pre ? pre->v : make_float4(bias[n], bias[n + 1], bias[n + 2], bias[n + 3]);
+        for (int m = tid / nq; m < mrows; m += 4 * lanes) {
+          float4 r[4];
+          if constexpr (EPI == EPI_RESIDUAL) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+              if (m + u * lanes < mrows)
+                r[u] = *reinterpret_cast<const float4*>(P.residual + (int64_t)(m0 + m + u * lanes) * P.n + n);
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (m + u * lanes < mrows) row(m + u * lanes, q, bv, &r[u]);
+        }
+      }
+    } else {
+      for (int idx = tid; idx < mrows * nq; idx += nt) {
+        const int q = idx % nq, m = idx / nq, n = blk0 * 16 + 4 * q;
+        const float4 bv = make_float4(bias[n], bias[n + 1], bias[n + 2], bias[n + 3]);
+        float4 r;
+        if constexpr (EPI == EPI_RESIDUAL)
+          r = *reinterpret_cast<const float4*>(P.residual + (int64_t)(m0 + m) * P.n + n);
+        row(m, q, bv, &r);
+      }
     }
   }
 }

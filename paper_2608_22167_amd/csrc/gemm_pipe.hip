@@ -289,6 +289,7 @@ __global__ __launch_bounds__(PTH) void gemm_pipe_kernel(Gemm P) {
   // acc[nb][mb][r] = C[m = wm*128 + 16 mb + fr][n = wn*64 + 16 nb + 4 (lane/16) + r];
   // the fp32 tile goes through LDS (stage 0, free after the last barrier)
   float* cr = reinterpret_cast<float*>(st0);
+  const EpiBias eb = epilogue_bias<EPI>(P, n0 >> 4, nrows >> 4, grp);
 #pragma unroll
   for (int e0 = 0; e0 < PM; e0 += PEP) {
     if (e0 >= mrows) break;  // uniform
@@ -307,7 +308,7 @@ __global__ __launch_bounds__(PTH) void gemm_pipe_kernel(Gemm P) {
       }
     }
     __syncthreads();
-    epilogue<bf16, EPI>(P, cr, PCLD, m0 + e0, min(PEP, mrows - e0), n0 >> 4, nrows >> 4, grp);
+    epilogue<bf16, EPI>(P, cr, PCLD, m0 + e0, min(PEP, mrows - e0), n0 >> 4, nrows >> 4, grp, &eb);
     __syncthreads();
   }
 }
@@ -479,6 +480,7 @@ __global__ __launch_bounds__(PTH) void gemm_dma_kernel(Gemm P) {
 
   // acc[nb][mb][r] = C[m = wm*128 + 16 mb + fr][n = wn*64 + 16 nb + 4 (lane/16) + r]
   float* cr = reinterpret_cast<float*>(d0);
+  const EpiBias eb = epilogue_bias<EPI>(P, n0 >> 4, nrows >> 4, grp);
   for (int e0 = 0; e0 < PM; e0 += DEP) {
     if (e0 >= mrows) break;  // uniform
     if (wm == e0 / (PM / 2)) {
@@ -495,7 +497,7 @@ __global__ __launch_bounds__(PTH) void gemm_dma_kernel(Gemm P) {
       }
     }
     __syncthreads();
-    epilogue<bf16, EPI>(P, cr, PCLD, m0 + e0, min(DEP, mrows - e0), n0 >> 4, nrows >> 4, grp);
+    epilogue<bf16, EPI>(P, cr, PCLD, m0 + e0, min(DEP, mrows - e0), n0 >> 4, nrows >> 4, grp, &eb);
     __syncthreads();
   }
 }

@@ -256,6 +256,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_tiled_kernel(Gemm P) {
   // acc[nb][mb][r] = C[m = wm*BM/2 + 16 mb + fr][n = wn*BN/2 + 16 nb + 4 (lane/16) + r];
   // the fp32 tile goes through LDS EP rows at a time
   float* cr = reinterpret_cast<float*>(smem_raw);
+  const EpiBias eb = epilogue_bias<EPI>(P, n0 >> 4, nrows >> 4, grp);
 #pragma unroll
   for (int e0 = 0; e0 < BM; e0 += S::EP) {
     if (e0 >= mrows) break;  // uniform
@@ -269,7 +270,7 @@ __global__ __launch_bounds__(NW * 64) void gemm_tiled_kernel(Gemm P) {
               make_float4(acc[nb][mb][0], acc[nb][mb][1], acc[nb][mb][2], acc[nb][mb][3]);
       }
     __syncthreads();
-    epilogue<bf16, EPI>(P, cr, S::c_ld, m0 + e0, min(S::EP, mrows - e0), n0 >> 4, nrows >> 4, grp);
+    epilogue<bf16, EPI>(P, cr, S::c_ld, m0 + e0, min(S::EP, mrows - e0), n0 >> 4, nrows >> 4, grp, &eb);
     __syncthreads();
   }
 }
