@@ -39,6 +39,7 @@ int fail(int code, const char* fmt, ...) {
 constexpr int PAGE_SIZE = 16;
 constexpr int SPLIT_EXTRA = 4096;   // splits beyond one per token that the workspace holds
 constexpr int PPS_MIN = 16;         // minimum pages per attention split
+constexpr int PPS_MAX = 256;        // maximum, unless the workspace's split count needs more
 constexpr int TARGET_WAVES = 3072;  // (split, KV head) wavefronts the planner aims for (measured: ~100 pages per split)
 constexpr int PREFILL_MIN_Q = 16;   // sequences adding this many tokens or more use the prefill kernel
 
@@ -161,6 +162,9 @@ int plan_attention(const mcpu_layer_cfg* c, int batch, int max_pages, const int3
   out->n_blocks = (int)blocks;
   long long target = std::max<long long>(1, (long long)TARGET_WAVES / c->n_kv_heads);
   long long pps = std::max<long long>(PPS_MIN, (total_pages + target - 1) / target);
+  // long contexts: more, shorter splits, so a token's splits are not much longer
+  // than other tokens' single ones (the waves that finish last set the time)
+  pps = std::min<long long>(pps, PPS_MAX);
   pps = std::max<long long>(pps, (total_pages + SPLIT_EXTRA - 1) / SPLIT_EXTRA);
   long long splits = 0;
   for (int np : pages) splits += (np + pps - 1) / pps;
