@@ -141,6 +141,18 @@ def test_bf16_sliding_window_layer():
     compare_layer(wl, gpu, step)
 
 
+@pytest.mark.parametrize("batch", [1, 17])
+def test_bf16_layer_small_batches(batch):
+    """One decode token (every expert GEMM group holds at most one row, the
+    split projections one row of their 64-row tile) and 17 (one row past a
+    16-row fragment)."""
+    rng = np.random.default_rng(1024 + batch)
+    ctx = [int(c) for c in rng.integers(1, 900, size=batch)]
+    wl = _bf16_small(seed=1024 + batch, ctx=ctx)
+    gpu, step = run_layer(wl)
+    compare_layer(wl, gpu, step)
+
+
 def test_bf16_sink_stress_layer():
     # Sinks of std 3 make some heads put nearly all weight on one key. With a
     # one-key context that head's output is the new token's bf16-stored value,
