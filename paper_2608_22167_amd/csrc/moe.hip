@@ -149,6 +149,57 @@ __device__ __forceinline__ void reduce_scatter(float (&acc)[E], int lane) {
   }
 }
 
+// Top-k experts of token t and their softmax weights (wavefront 0 of the
+// workgroup; logits in LDS): lane s < k keeps the s-th selection in registers
+// (the selection count is a runtime value, so an array indexed by it would
+// live in scratch memory); ties go to the lower expert id; forced selections
+// replace the arg-max when given.
+__device__ __forceinline__ void router_topk(const Router& P, const float* logits, int t, int lane) {
+  const int NE = P.n_experts, K = P.top_k;
+  float v = lane < NE ? logits[lane] : -INFINITY;
+  int my_e = 0;
+  float my_v = -INFINITY;
+  for (int s = 0; s < K; ++s) {
+    int e;
+    if (P.force_idx) {
+      e = P.force_idx[(int64_t)t * K + s];
+      if (e < 0 || e >= NE) {
+        if (lane == 0) set_error(P.err, 4);
+        e = 0;
+      }
+    } else {
+      // arg-max over lanes, ties to the lower expert id
+      float bv = v;
+      int bi = lane;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) {
+        const float ov = __shfl_xor(bv, o, 64);
+        const int oi = __shfl_xor(bi, o, 64);
+        if (ov > bv || (ov == bv && oi < bi)) {
+          bv = ov;
+          bi = oi;
+        }
+      }
+      e = bi;
+      if (lane == e) v = -INFINITY;
+    }
+    if (lane == s) {
+      my_e = e;
+      my_v = logits[e];
+    }
+  }
+  // softmax over the selections, maximum and sum taken in selection order
+  float mx = __shfl(my_v, 0, 64);
+  for (int s = 1; s < K; ++s) mx = fmaxf(mx, __shfl(my_v, s, 64));
+  const float ex = expf(my_v - mx);
+  float den = 0.f;
+  for (int s = 0; s < K; ++s) den += __shfl(ex, s, 64);
+  if (lane < K) {
+    P.idx_out[(int64_t)t * K + lane] = my_e;
+    P.w_out[(int64_t)t * K + lane] = ex / den;
+  }
+}
+
 // One workgroup per token. Thread i owns the 8-wide reduction chunks i, i+256,
 // ... and accumulates all E logits over them; partial logits are then summed
 // across lanes (wavefront butterflies) and across the 4 wavefronts (LDS).
@@ -221,54 +272,104 @@ __global__ __launch_bounds__(256) void router_kernel(Router P) {
   }
   __syncthreads();
 
-  if (wave == 0) {
-    // lane s < K keeps the s-th selection (registers only: the selection
-    // count is a runtime value, so an array indexed by it would live in
-    // scratch memory)
-    const int NE = P.n_experts, K = P.top_k;
-    float v = lane < NE ? logits[lane] : -INFINITY;
-    int my_e = 0;
-    float my_v = -INFINITY;
-    for (int s = 0; s < K; ++s) {
-      int e;
-      if (P.force_idx) {
-        e = P.force_idx[(int64_t)t * K + s];
-        if (e < 0 || e >= NE) {
-          if (lane == 0) set_error(P.err, 4);
-          e = 0;
-        }
-      } else {
-        // arg-max over lanes, ties to the lower expert id
-        float bv = v;
-        int bi = lane;
+  if (wave == 0) router_topk(P, logits, t, lane);
+}
+
+// Router for one token per workgroup of 1024 threads: 1024 / E threads per
+// expert, thread l of expert e taking the 8-wide reduction chunks l, l + TPE,
+// ... of its router row. All of a thread's router-weight loads are issued at
+// the start, together with the residual row's, so the whole kernel waits for
+// memory once; the normalised row then goes through LDS, each expert's
+// partial sums meet in a butterfly over its threads (across two wavefronts
+// through LDS when E = 8), and wavefront 0 takes the top k as above.
+constexpr int RW_THREADS = 1024;
+
+template <typename T, int E, int NV, int CPT>
+__global__ __launch_bounds__(RW_THREADS) void router_wide_kernel(Router P) {
+  constexpr int TPE = RW_THREADS / E;  // threads per expert
+  constexpr int TW = TPE < 64 ? TPE : 64;
+  __shared__ float hn[ROUTER_MAX_H];
+  __shared__ float logits[E];
+  __shared__ float half_sum[E];
+  __shared__ float scratch[RW_THREADS / 64];
+  const int t = blockIdx.x, H = P.hidden, tid = threadIdx.x, lane = lane_id(), wave = tid >> 6;
+  const int e = tid / TPE, l = tid % TPE;
+  const int nchunk = H / 8;
+
+  // router-weight chunks of this thread (rows past n_experts and chunks past
+  // the row read valid addresses and are not used)
+  const T* wr = reinterpret_cast<const T*>(P.w_r) + (int64_t)(e < P.n_experts ? e : 0) * H;
+  Raw8<T> raw[CPT];
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-          const float ov = __shfl_xor(bv, o, 64);
-          const int oi = __shfl_xor(bi, o, 64);
-          if (ov > bv || (ov == bv && oi < bi)) {
-            bv = ov;
-            bi = oi;
-          }
-        }
-        e = bi;
-        if (lane == e) v = -INFINITY;
-      }
-      if (lane == s) {
-        my_e = e;
-        my_v = logits[e];
-      }
-    }
-    // softmax over the selections, maximum and sum taken in selection order
-    float mx = __shfl(my_v, 0, 64);
-    for (int s = 1; s < K; ++s) mx = fmaxf(mx, __shfl(my_v, s, 64));
-    const float ex = expf(my_v - mx);
-    float den = 0.f;
-    for (int s = 0; s < K; ++s) den += __shfl(ex, s, 64);
-    if (lane < K) {
-      P.idx_out[(int64_t)t * K + lane] = my_e;
-      P.w_out[(int64_t)t * K + lane] = ex / den;
+  for (int i = 0; i < CPT; ++i) {
+    const int c = l + TPE * i;
+    raw[i].load(wr + 8 * (c < nchunk ? c : 0));
+  }
+  // residual row and gain: float4 j of thread t is features 4 (t + 1024 j) ..
+  float4 hv[NV], gv[NV];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = (tid + RW_THREADS * j) * 4;
+    const int ii = i < H ? i : 0;
+    hv[j] = *reinterpret_cast<const float4*>(P.h + (int64_t)t * H + ii);
+    gv[j] = *reinterpret_cast<const float4*>(P.g2 + ii);
+  }
+#pragma unroll
+  for (int j = 0; j < NV; ++j)
+    if ((tid + RW_THREADS * j) * 4 < H)
+      ss += hv[j].x * hv[j].x + hv[j].y * hv[j].y + hv[j].z * hv[j].z + hv[j].w * hv[j].w;
+  // sum of squares over the workgroup
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) ss += __shfl_xor(ss, o, 64);
+  if (lane == 0) scratch[wave] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int w = 0; w < RW_THREADS / 64; ++w) tot += scratch[w];
+  const float inv = 1.0f / sqrtf(tot / (float)H + P.eps);
+  T* hq = reinterpret_cast<T*>(P.hn_out) + (int64_t)t * H;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = (tid + RW_THREADS * j) * 4;
+    if (i < H) {
+      const float4 v = make_float4(hv[j].x * inv * gv[j].x, hv[j].y * inv * gv[j].y, hv[j].z * inv * gv[j].z,
+                                   hv[j].w * inv * gv[j].w);
+      *reinterpret_cast<float4*>(hn + i) = v;
+      store4(hq + i, v);
     }
   }
+  __syncthreads();
+
+  float acc = 0.f;
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = l + TPE * i;
+    if (c < nchunk) {
+      float w[8];
+      raw[i].widen(w);
+      const float4 x0 = *reinterpret_cast<const float4*>(hn + 8 * c);
+      const float4 x1 = *reinterpret_cast<const float4*>(hn + 8 * c + 4);
+      acc += x0.x * w[0] + x0.y * w[1] + x0.z * w[2] + x0.w * w[3] + x1.x * w[4] + x1.y * w[5] + x1.z * w[6] +
+             x1.w * w[7];
+    }
+  }
+  // over the expert's threads: a butterfly within the wavefront, then (TPE =
+  // 128) the two wavefronts' halves through LDS
+#pragma unroll
+  for (int o = TW / 2; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
+  if constexpr (TPE > 64) {
+    if (l == 64) half_sum[e] = acc;
+    __syncthreads();
+    if (l == 0) acc += half_sum[e];
+  }
+  if (l == 0 && e < P.n_experts) {
+    const float v = acc + P.b_r[e];
+    logits[e] = v;
+    if (P.logits_out) P.logits_out[(int64_t)t * P.n_experts + e] = v;
+  }
+  __syncthreads();
+  if (wave == 0) router_topk(P, logits, t, lane);
 }
 
 // Router for many tokens: a workgroup owns 16 tokens, so the router weights
@@ -447,12 +548,48 @@ static void router_nv(const Router& p, hipStream_t s) {
   else hipLaunchKernelGGL((router_kernel<T, E, 8>), g, b, 0, s, p);
 }
 
+// The wide router when each thread's share of its expert row is at most 16
+// chunks (8 for fp32 weights) with 1024 / E threads per expert, else one
+// workgroup of 256 threads per token.
+template <typename T, int E>
+static void router_pick(const Router& p, hipStream_t s) {
+  constexpr int TPE = RW_THREADS / E;
+  const int cpt = (p.hidden / 8 + TPE - 1) / TPE;
+  const int nv = (p.hidden + 4 * RW_THREADS - 1) / (4 * RW_THREADS);
+  dim3 g(p.n_tokens), b(RW_THREADS);
+#define RW(NV, CPT) hipLaunchKernelGGL((router_wide_kernel<T, E, NV, CPT>), g, b, 0, s, p)
+  if constexpr (sizeof(T) == 4) {  // fp32 weights: 8 registers a chunk, at most 8 chunks
+    if (nv == 1 && cpt <= 4) RW(1, 4);
+    else if (nv == 1 && cpt <= 8) RW(1, 8);
+    else router_nv<T, E>(p, s);
+  } else {
+    if (nv == 1 && cpt <= 4) RW(1, 4);
+    else if (nv == 1 && cpt <= 8) RW(1, 8);
+    else if (nv == 1 && cpt <= 12) RW(1, 12);
+    else if (nv == 1 && cpt <= 16) RW(1, 16);
+    else if (nv == 2 && cpt <= 16) RW(2, 16);
+    else router_nv<T, E>(p, s);
+  }
+#undef RW
+}
+
+// Up to one wide workgroup per compute unit; more tokens than that run
+// faster on the 256-thread workgroups (several resident per compute unit).
+constexpr int ROUTER_WIDE_MAX_TOKENS = 256;
+
 template <typename T>
 static void router_e(const Router& p, hipStream_t s) {
-  if (p.n_experts <= 8) router_nv<T, 8>(p, s);
-  else if (p.n_experts <= 16) router_nv<T, 16>(p, s);
-  else if (p.n_experts <= 32) router_nv<T, 32>(p, s);
-  else router_nv<T, 64>(p, s);
+  if (p.n_tokens > ROUTER_WIDE_MAX_TOKENS) {
+    if (p.n_experts <= 8) router_nv<T, 8>(p, s);
+    else if (p.n_experts <= 16) router_nv<T, 16>(p, s);
+    else if (p.n_experts <= 32) router_nv<T, 32>(p, s);
+    else router_nv<T, 64>(p, s);
+    return;
+  }
+  if (p.n_experts <= 8) router_pick<T, 8>(p, s);
+  else if (p.n_experts <= 16) router_pick<T, 16>(p, s);
+  else if (p.n_experts <= 32) router_pick<T, 32>(p, s);
+  else router_pick<T, 64>(p, s);
 }
 
 template <typename T>

@@ -252,8 +252,11 @@ def test_kv_pages_append_bit_exact():
 
 @pytest.mark.parametrize("kind", ["tiny_f32", "bf16", "tiny_f32_t1100", "bf16_t1030"])
 def test_moe_forward_and_forced_selection(kind):
-    """Per-token router below 1024 tokens, the 16-tokens-per-workgroup router
-    from 1024 on (1100 and 1030 tokens: a ragged last workgroup)."""
+    """Routers: one token per 1024-thread workgroup up to 256 tokens (24 and 10
+    tokens here; 8 experts put an expert's threads in two wavefronts), one per
+    256-thread workgroup below 1024 (the 350- and 1000-token cases elsewhere),
+    16 tokens per workgroup from 1024 on (1100 and 1030 tokens: a ragged last
+    workgroup)."""
     if kind == "tiny_f32":
         wl = W.tiny_f32(seed=1051, batch=24)
     elif kind == "tiny_f32_t1100":
