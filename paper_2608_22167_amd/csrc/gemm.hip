@@ -1,4 +1,5 @@
-// Weight-streaming grouped GEMM for the decode step on gfx950.
+// Weight-streaming grouped GEMM on gfx950: the general fallback (fp32 layers,
+// shapes the weight-slab and tiled kernels do not take).
 //
 // At decode every projection of the layer is skinny: a few to a few hundred
 // token rows against a weight matrix that is read exactly once, so the kernels
@@ -225,12 +226,12 @@ hipError_t gemm_launch_cfg(const Gemm& g, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Tiling choice. Grouped (expert) GEMMs have thousands of slabs, so each
-// wavefront streams whole rows (WK = 1). Dense projections have few slabs, so
-// the reduction is split across wavefronts to keep enough loads in flight.
-// (Measured on MI355X over the gpt-oss-20b decode shapes: 64-row batches
-// favour 2 wavefronts x 2 blocks per slab with a 2-deep ring; 256-row batches
-// favour 8 token blocks per pass so hot experts re-stream their rows less.)
+// Tiling choice (this kernel serves the shapes the weight-slab and tiled
+// kernels do not take: fp32 layers, 65-127-row dense projections, reductions
+// that are not a multiple of 64). Grouped (expert) GEMMs have many slabs, so
+// each wavefront streams whole rows (WK = 1); dense projections have few, so
+// four wavefronts split the reduction to keep loads in flight. Deeper rings
+// measured no faster for the 16-64-row dense shapes.
 template <typename T>
 static hipError_t gemm_dispatch(const Gemm& g, hipStream_t s) {
   const int mb = (g.max_rows_per_group + 15) / 16;
