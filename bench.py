@@ -126,9 +126,21 @@ def traffic_from_profile(kernel, workload_name):
 
 
 ATTN_SOURCES = ("attention.hip", "device.h", "kernels.h")
-GEMM_SOURCES = ("gemm.hip", "gemm_tiled.hip", "gemm_pipe.hip", "gemm_epilogue.h", "device.h", "kernels.h")
+GEMM_SOURCES = ("gemm.hip", "gemm_tiled.hip", "gemm_pipe.hip", "gemm_slab.hip", "gemm_epilogue.h", "device.h", "kernels.h")
 KERNEL_SOURCES = {"attn_split": ATTN_SOURCES, "attn_prefill": ATTN_SOURCES, "qkv": GEMM_SOURCES,
                   "oproj": GEMM_SOURCES, "expert_gu": GEMM_SOURCES, "expert_down": GEMM_SOURCES}
+
+
+def timed_passes(fn, min_seconds=10.0, max_passes=50):
+    """Runs fn until at least min_seconds have passed (at least once, at most
+    max_passes times): (passes, seconds)."""
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        fn()
+        passes += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds or passes >= max_passes:
+            return passes, dt
 
 
 def cpu_cores():
@@ -188,13 +200,11 @@ class LayerBench:
         seqs = np.sort(seqs)
         sub, _ = W.restrict(wl, seqs)
         weights = O.Weights(sub.shape, sub.weights)
-        t0 = time.perf_counter()
-        O.decode_layer(sub, weights)
-        dt = time.perf_counter() - t0
-        return {"value": round(sub.n_tokens / dt, 3), "unit": "tokens/s (all tokens of the sample)",
+        passes, dt = timed_passes(lambda: O.decode_layer(sub, weights))
+        return {"value": round(passes * sub.n_tokens / dt, 3), "unit": "tokens/s (all tokens of the sample)",
                 "cores": cpu_cores(), "kind": "oracle",
                 "sample": f"{len(seqs)} of {wl.batch} sequences (seeded), {sub.n_tokens} tokens, one layer step, "
-                          f"{dt:.2f} s wall"}
+                          f"{passes} passes in {dt:.2f} s wall"}
 
 
 class StackBench:

@@ -50,9 +50,10 @@ __device__ __forceinline__ void band_order(int L, int mt_g, int n_tn, int& mt, i
 // Items are cut into eight contiguous ranges, one per XCD (workgroups are
 // dealt to the XCDs round robin), so that a band's reuse stays in one L2.
 // Returns false for a workgroup past the last item. Contains a barrier: every
-// thread of the workgroup calls it.
+// thread of the workgroup calls it. row_start (LDS, TILE_MAXG + 1 ints), if
+// given, receives each group's first row and, last, the end of the last group.
 template <int BM, int BN, int GM>
-__device__ bool tile_of_block(const Gemm& P, int* mt_start, int& grp, int& mt, int& tn) {
+__device__ bool tile_of_block(const Gemm& P, int* mt_start, int& grp, int& mt, int& tn, int* row_start = nullptr) {
   const int lane = threadIdx.x & 63, wave = uniform((int)threadIdx.x >> 6);
   const int G = P.n_groups;
   if (wave == 0) {  // one wavefront, 64 groups per pass
@@ -64,6 +65,10 @@ __device__ bool tile_of_block(const Gemm& P, int* mt_start, int& grp, int& mt, i
         const int r0 = P.group_off ? P.group_off[g] : 0;
         const int r1 = P.group_off ? P.group_off[g + 1] : P.n_rows;
         cnt = (max(r1 - r0, 0) + BM - 1) / BM;
+        if (row_start) {  // the group's rows, r0 .. r1 - 1
+          row_start[g] = r0;
+          if (g == G - 1) row_start[G] = r1;
+        }
       }
       const int incl = wave_incl_scan(cnt);
       if (g < G) mt_start[g] = carry + incl - cnt;

@@ -161,6 +161,7 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
   constexpr int SMEM = 2 * SXSTAGE > SM * CLD * 4 ? 2 * SXSTAGE : SM * CLD * 4;
   __shared__ __align__(16) unsigned char smem[SMEM];
   __shared__ int mt_start[TILE_MAXG + 1];
+  __shared__ int row_start[TILE_MAXG + 1];
   __shared__ int last_split;
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
   const int fr = lane & 15, g = lane >> 4;
@@ -173,15 +174,10 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
     ks = uniform((int)blockIdx.x % P.k_splits);
     mt = tile / ntn;
     tn = tile % ntn;
-  } else if (!tile_of_block<SM, NS, 1>(P, mt_start, grp, mt, tn)) {
+  } else if (!tile_of_block<SM, NS, 1>(P, mt_start, grp, mt, tn, row_start)) {
     return;
   }
-  const int gr0 = P.group_off ? P.group_off[grp] : 0;
-  const int gr1 = P.group_off ? P.group_off[grp + 1] : P.n_rows;
-  const int m0 = uniform(gr0 + mt * SM);
-  const int mrows = min(SM, gr1 - m0);
   const int n0 = uniform(tn * NS), nrows = min(NS, P.n - n0);
-  const int mbs = uniform((mrows + 15) >> 4);  // token-row fragments holding rows
   const int nk = (P.k + SKC - 1) / SKC;
   const int tail_steps = (P.k % SKC) ? (P.k % SKC) / 32 : 4;
   // this workgroup's chunks: kb .. kb + nkl - 1
@@ -200,17 +196,34 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
     }
     wl.init(P, grp, wrow, g);
   }
+  // The group's rows come from LDS; the source row of this thread's staged
+  // token row is requested first and waited for only after the first RC
+  // chunks of weights have been requested (loads complete in order), so that
+  // its latency overlaps the start of the weight stream.
+  const int gr0 = P.group_off ? row_start[grp] : 0;
+  const int gr1 = P.group_off ? row_start[grp + 1] : P.n_rows;
+  const int m0 = uniform(gr0 + mt * SM);
+  const int mrows = min(SM, gr1 - m0);
+  const int mbs = uniform((mrows + 15) >> 4);  // token-row fragments holding rows
+  const int xr = tid >> 2, xc = 2 * (tid & 3);
+  const int xrow = m0 + min(xr, mrows - 1);
+  const int src = P.row_src ? P.row_src[xrow] : xrow;
+  typename SlabW<NF, WF>::Regs wr[RC];
+  // weights of this workgroup's chunk i (clamped to its last)
+  auto wfetch = [&](typename SlabW<NF, WF>::Regs& r, int i) __attribute__((always_inline)) {
+    const int kc = kb + min(i, nkl - 1);
+    wl.fetch(r, kc, kc == nk - 1 ? tail_steps : 4);
+  };
+#pragma unroll
+  for (int u = 0; u < RC; ++u) {
+    wfetch(wr[u], u);
+    __builtin_amdgcn_sched_barrier(0);
+  }
 
   // token-row staging: thread t stages row t / 4 (of the 64), 16-byte chunks
   // 2 (t % 4) and 2 (t % 4) + 1 of both half chunks; rows past the end repeat
   // the last row (dropped)
-  const int xr = tid >> 2, xc = 2 * (tid & 3);
-  uint32_t xvo;
-  {
-    const int row = m0 + min(xr, mrows - 1);
-    const int src = P.row_src ? P.row_src[row] : row;
-    xvo = (uint32_t)src * (uint32_t)(P.k * 2) + 16 * xc;
-  }
+  const uint32_t xvo = (uint32_t)src * (uint32_t)(P.k * 2) + 16 * xc;
   const uint8_t* xbase = reinterpret_cast<const uint8_t*>(P.x);
   const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(xbase), 0, 0x7FFFFFFF, BUF_D3);
   struct XRegs {
@@ -257,26 +270,16 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
 
   // Chunk kc: weights from register set kc % RC (requested RC chunks ahead),
   // token rows from LDS buffer kc & 1; afterwards chunk kc + 1's token rows
-  // are staged and chunk kc + 2's requested. Unrolled over RC (even) so the
-  // set indices are constants; only the products are conditional. The loop
-  // is instantiated per count of token-row fragments holding rows (MBS).
+  // are staged from registers and chunk kc + 2's requested, ahead of the
+  // weights of chunk kc + RC, so that waiting for them leaves the weights in
+  // flight. Unrolled over RC (even) so the set indices are constants; only
+  // the products are conditional. The loop is instantiated per count of
+  // token-row fragments holding rows (MBS).
   static_assert(RC % 2 == 0, "the unrolled ring must cover both LDS buffers");
-  typename SlabW<NF, WF>::Regs wr[RC];
-  XRegs xs[2];
-  // weights of this workgroup's chunk i (clamped to its last)
-  auto wfetch = [&](typename SlabW<NF, WF>::Regs& r, int i) __attribute__((always_inline)) {
-    const int kc = kb + min(i, nkl - 1);
-    wl.fetch(r, kc, kc == nk - 1 ? tail_steps : 4);
-  };
-#pragma unroll
-  for (int u = 0; u < RC; ++u) {
-    wfetch(wr[u], u);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  xfetch(xs[0], 0);
-  xfetch(xs[1], 1);
-  xstore(xs[0], 0);
-  xfetch(xs[0], 2);
+  XRegs xs;
+  xfetch(xs, 0);
+  xstore(xs, 0);
+  xfetch(xs, 1);
   __syncthreads();
   // MXFP4 in a half chunk: lane groups 2 and 3 hold no indices
   const uint32_t keep_tail = (WF == 1 && tail_steps < 4 && g >= 2) ? 0u : ~0u;
@@ -307,9 +310,9 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
           }
         }
         __builtin_amdgcn_sched_barrier(0);
+        xstore(xs, buf ^ 1);
+        xfetch(xs, kc + 2);
         wfetch(wr[u], kc + RC);
-        xstore(xs[(u + 1) & 1], buf ^ 1);
-        xfetch(xs[(u + 1) & 1], kc + 3);
         __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
       }
