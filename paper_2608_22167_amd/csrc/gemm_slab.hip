@@ -400,13 +400,17 @@ hipError_t slab_launch(const Gemm& g, hipStream_t s, int64_t grid) {
   return hipGetLastError();
 }
 
-// Split plan of one matrix: 64-wide slabs, the reduction in four parts (at
-// least two chunks each). Measured on MI355X for 16-64 rows against the
-// gpt-oss-20b projections (weights from HBM): 2880 x 4096 in 14 us against
-// 26 us unsplit; 5120 x 2880 in 22 us against 26. Finer splits or 128-wide
-// slabs were slower (more partial traffic, shorter pipelines).
+// Split plan of one matrix: 64-wide slabs, the reduction in up to four parts
+// (at least two chunks each), as many as bring the launch near SPLIT_WG
+// workgroups. Measured on MI355X for 16-64 rows against the gpt-oss-20b
+// projections (weights from HBM): 2880 x 4096 (45 slabs) in 14 us with four
+// parts against 17 with two and 22 unsplit; 5120 x 2880 (80 slabs) in 18.5 us
+// with two against 20.7 with four and 23 unsplit. Finer splits, 128-wide
+// slabs or a split of 256-512-row tiles were slower (more partial traffic,
+// shorter pipelines).
 constexpr int NSPLIT = 64;
 constexpr int SPLIT_K = 4;
+constexpr int SPLIT_WG = 192;
 struct SplitPlan {
   int tiles = 0, k_splits = 0;
 };
@@ -418,7 +422,8 @@ SplitPlan split_plan(int n, int k, int n_rows) {
   if (tiles > SPLIT_MAX_TILES) return p;
   const int nk = (k + SKC - 1) / SKC;
   p.tiles = tiles;
-  p.k_splits = std::max(1, std::min({SPLIT_K, nk / 2, SPLIT_MAX_K}));
+  const int want = (SPLIT_WG + tiles / 2) / tiles;  // SPLIT_WG / tiles, rounded
+  p.k_splits = std::max(1, std::min({want, SPLIT_K, nk / 2, SPLIT_MAX_K}));
   return p;
 }
 
