@@ -4,8 +4,9 @@
 //
 // There each weight byte meets only a few dozen token rows, so the bound is
 // HBM, and the kernel's job is to keep enough weight bytes in flight. A
-// workgroup of four wavefronts owns one work item: up to 64 token rows of one
-// group against NS weight rows. Each wavefront streams its NS / 4 weight rows
+// workgroup of four wavefronts owns one work item: up to SMT token rows of one
+// group (64; 128 for MXFP4 groups of over 32 rows on average, so that a group
+// just past 64 rows decodes its weights once) against NS weight rows. Each wavefront streams its NS / 4 weight rows
 // straight from global memory into registers, already in matrix-core operand
 // order, through a ring of RC reduction chunks (128 indices each), so weights
 // never pass through LDS; the group's token rows, shared by the four
@@ -38,10 +39,8 @@ namespace {
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int BUF_D3 = 0x00020000;  // raw buffer descriptor word 3 (gfx9 family)
 
-constexpr int SM = 64;              // token rows per item
+constexpr int SM = 64;              // token rows per item (split projections; experts: 64 or 128)
 constexpr int SKC = 128;            // reduction indices per chunk
-constexpr int SXHALF = SM * 128;    // bytes of a staged half chunk (64 rows x 64 indices)
-constexpr int SXSTAGE = 2 * SXHALF; // bytes per chunk stage
 constexpr int SPLIT_MAX_K = 16;     // most reduction splits of one tile
 
 __device__ __forceinline__ f32x4 mfma_bf16(u32x4 a, u32x4 b, f32x4 c) {
@@ -154,11 +153,17 @@ struct SlabW<NF, 1> {
   }
 };
 
-template <int NS, int WF, int RC, int EPI, bool SPLIT>
+template <int NS, int WF, int RC, int EPI, bool SPLIT, int SMT>
 __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
-  constexpr int NF = NS / 64;  // weight fragments per wavefront
-  constexpr int CLD = NS + 4;  // fp32 tile row stride
-  constexpr int SMEM = 2 * SXSTAGE > SM * CLD * 4 ? 2 * SXSTAGE : SM * CLD * 4;
+  static_assert(SMT == 64 || SMT == 128, "items of 64 or 128 token rows");
+  static_assert(!SPLIT || SMT == SM, "split tiles have 64 token rows");
+  constexpr int NF = NS / 64;        // weight fragments per wavefront
+  constexpr int MB = SMT / 16;       // token-row fragments per item
+  constexpr int XR = SMT / 64;       // token rows each thread stages
+  constexpr int CLD = NS + 4;        // fp32 tile row stride
+  constexpr int SXHALF = SMT * 128;  // bytes of a staged half chunk (SMT rows x 64 indices)
+  constexpr int SXSTAGE = 2 * SXHALF;
+  constexpr int SMEM = 2 * SXSTAGE > SMT * CLD * 4 ? 2 * SXSTAGE : SMT * CLD * 4;
   __shared__ __align__(16) unsigned char smem[SMEM];
   __shared__ int mt_start[TILE_MAXG + 1];
   __shared__ int row_start[TILE_MAXG + 1];
@@ -174,7 +179,7 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
     ks = uniform((int)blockIdx.x % P.k_splits);
     mt = tile / ntn;
     tn = tile % ntn;
-  } else if (!tile_of_block<SM, NS, 1>(P, mt_start, grp, mt, tn, row_start)) {
+  } else if (!tile_of_block<SMT, NS, 1>(P, mt_start, grp, mt, tn, row_start)) {
     return;
   }
   const int n0 = uniform(tn * NS), nrows = min(NS, P.n - n0);
@@ -202,12 +207,16 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
   // its latency overlaps the start of the weight stream.
   const int gr0 = P.group_off ? row_start[grp] : 0;
   const int gr1 = P.group_off ? row_start[grp + 1] : P.n_rows;
-  const int m0 = uniform(gr0 + mt * SM);
-  const int mrows = min(SM, gr1 - m0);
+  const int m0 = uniform(gr0 + mt * SMT);
+  const int mrows = min(SMT, gr1 - m0);
   const int mbs = uniform((mrows + 15) >> 4);  // token-row fragments holding rows
   const int xr = tid >> 2, xc = 2 * (tid & 3);
-  const int xrow = m0 + min(xr, mrows - 1);
-  const int src = P.row_src ? P.row_src[xrow] : xrow;
+  int src[XR];
+#pragma unroll
+  for (int j = 0; j < XR; ++j) {
+    const int xrow = m0 + min(xr + 64 * j, mrows - 1);
+    src[j] = P.row_src ? P.row_src[xrow] : xrow;
+  }
   typename SlabW<NF, WF>::Regs wr[RC];
   // weights of this workgroup's chunk i (clamped to its last)
   auto wfetch = [&](typename SlabW<NF, WF>::Regs& r, int i) __attribute__((always_inline)) {
@@ -220,32 +229,39 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
     __builtin_amdgcn_sched_barrier(0);
   }
 
-  // token-row staging: thread t stages row t / 4 (of the 64), 16-byte chunks
-  // 2 (t % 4) and 2 (t % 4) + 1 of both half chunks; rows past the end repeat
-  // the last row (dropped)
-  const uint32_t xvo = (uint32_t)src * (uint32_t)(P.k * 2) + 16 * xc;
+  // token-row staging: thread t stages rows t / 4 + 64 j (j < SMT / 64),
+  // 16-byte chunks 2 (t % 4) and 2 (t % 4) + 1 of both half chunks; rows past
+  // the end repeat the last row (dropped)
+  uint32_t xvo[XR];
+#pragma unroll
+  for (int j = 0; j < XR; ++j) xvo[j] = (uint32_t)src[j] * (uint32_t)(P.k * 2) + 16 * xc;
   const uint8_t* xbase = reinterpret_cast<const uint8_t*>(P.x);
   const __amdgpu_buffer_rsrc_t xrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(xbase), 0, 0x7FFFFFFF, BUF_D3);
   struct XRegs {
-    u32x4 v[2][2];  // [half][chunk pair]
+    u32x4 v[XR][2][2];  // [row][half][chunk pair]
   };
   auto xfetch = [&](XRegs& r, int i) __attribute__((always_inline)) {
     const int kc = kb + min(i, nkl - 1);
     // a half chunk past k re-reads the first half (never multiplied)
     const int h1 = (kc == nk - 1 && tail_steps < 4) ? 0 : 128;
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int j = 0; j < XR; ++j)
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
-        r.v[h][q] = __builtin_amdgcn_raw_buffer_load_b128(xrs, xvo + 16 * q + (h ? h1 : 0), uniform(kc * SKC * 2), 0);
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          r.v[j][h][q] =
+              __builtin_amdgcn_raw_buffer_load_b128(xrs, xvo[j] + 16 * q + (h ? h1 : 0), uniform(kc * SKC * 2), 0);
   };
   auto xstore = [&](const XRegs& r, int buf) __attribute__((always_inline)) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int j = 0; j < XR; ++j)
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
-        *reinterpret_cast<u32x4*>(smem + buf * SXSTAGE + h * SXHALF + xr * 128 + 16 * ((xc + q) ^ (xr & 7))) =
-            r.v[h][q];
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          *reinterpret_cast<u32x4*>(smem + buf * SXSTAGE + h * SXHALF + (xr + 64 * j) * 128 +
+                                    16 * ((xc + q) ^ (xr & 7))) = r.v[j][h][q];
   };
   // token-row fragment mb of product t (bf16 order) or s (MXFP4 order)
   auto xfrag = [&](int buf, int mb, int t) __attribute__((always_inline)) {
@@ -261,11 +277,11 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
                                            16 * (c8 ^ (fr & 7)));
   };
 
-  f32x4 acc[NF][4];
+  f32x4 acc[NF][MB];
 #pragma unroll
   for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int mb = 0; mb < MB; ++mb) acc[nb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
   uint32_t bad_scale = 0;
 
   // Chunk kc: weights from register set kc % RC (requested RC chunks ahead),
@@ -322,7 +338,17 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
     case 1: run(std::integral_constant<int, 1>{}); break;
     case 2: run(std::integral_constant<int, 2>{}); break;
     case 3: run(std::integral_constant<int, 3>{}); break;
-    default: run(std::integral_constant<int, 4>{}); break;
+    case 4: run(std::integral_constant<int, 4>{}); break;
+    default:
+      if constexpr (MB > 4) {
+        switch (mbs) {
+          case 5: run(std::integral_constant<int, 5>{}); break;
+          case 6: run(std::integral_constant<int, 6>{}); break;
+          case 7: run(std::integral_constant<int, 7>{}); break;
+          default: run(std::integral_constant<int, MB>{}); break;
+        }
+      }
+      break;
   }
   if (bad_scale) set_error(P.err, 16);
 
@@ -334,14 +360,14 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
       // Partials are stored and loaded at device scope (SC1: coherent across
       // the XCDs' L2 caches without a cache-wide write-back or invalidate);
       // the stores are complete (vmcnt 0) before the arrival is counted.
-      constexpr int PT = NF * 4 * 256 * 16;  // bytes per partial tile
+      constexpr int PT = NF * MB * 256 * 16;  // bytes per partial tile
       constexpr int SC1 = 16;
       const __amdgpu_buffer_rsrc_t prs = __builtin_amdgcn_make_buffer_rsrc(
           reinterpret_cast<uint8_t*>(P.part) + (int64_t)tile * P.k_splits * PT, 0, 0x7FFFFFFF, BUF_D3);
 #pragma unroll
       for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
+        for (int mb = 0; mb < MB; ++mb)
           if (mb < mbs)
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[nb][mb]), prs,
                                                    ((nb * 4 + mb) * 256 + tid) * 16, ks * PT, SC1);
@@ -356,7 +382,7 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
 #pragma unroll
       for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
-        for (int mb = 0; mb < 4; ++mb)
+        for (int mb = 0; mb < MB; ++mb)
           if (mb < mbs) {
             const uint32_t vo = ((nb * 4 + mb) * 256 + tid) * 16;
             u32x4 v[SPLIT_MAX_K];
@@ -378,7 +404,7 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
 #pragma unroll
   for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
+    for (int mb = 0; mb < MB; ++mb) {
       const int n = (NS / 4) * wave + 16 * nb + 4 * g;
       *reinterpret_cast<float4*>(cr + (16 * mb + fr) * CLD + n) =
           make_float4(acc[nb][mb][0], acc[nb][mb][1], acc[nb][mb][2], acc[nb][mb][3]);
@@ -387,15 +413,15 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
   epilogue<bf16, EPI>(P, cr, CLD, m0, mrows, n0 >> 4, nrows >> 4, grp);
 }
 
-template <int NS, int WF, int RC, bool SPLIT>
+template <int NS, int WF, int RC, bool SPLIT, int SMT = SM>
 hipError_t slab_launch(const Gemm& g, hipStream_t s, int64_t grid) {
   if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
   dim3 gd((unsigned)grid), bd(256);
   switch (g.epi) {
-    case EPI_QKV: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_QKV, SPLIT>), gd, bd, 0, s, g); break;
-    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_RESIDUAL, SPLIT>), gd, bd, 0, s, g); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_SWIGLU, SPLIT>), gd, bd, 0, s, g); break;
-    default: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_BIAS, SPLIT>), gd, bd, 0, s, g); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_QKV, SPLIT, SMT>), gd, bd, 0, s, g); break;
+    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_RESIDUAL, SPLIT, SMT>), gd, bd, 0, s, g); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_SWIGLU, SPLIT, SMT>), gd, bd, 0, s, g); break;
+    default: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_BIAS, SPLIT, SMT>), gd, bd, 0, s, g); break;
   }
   return hipGetLastError();
 }
@@ -476,6 +502,10 @@ hipError_t launch_gemm_slab(int expert_fmt, const Gemm& g, hipStream_t s) {
   }
   if (expert_fmt != 0) {
     if (!g.w_scales) return hipErrorInvalidValue;
+    // groups of over 32 rows on average: 128-row items, so that a group just
+    // past 64 rows is one item (its weights decoded once) instead of two
+    if ((int64_t)g.n_rows > 32LL * g.n_groups)
+      return slab_launch<128, 1, 2, false, 128>(g, s, tile_grid(g, 128, 128));
     return slab_launch<128, 1, 2, false>(g, s, tile_grid(g, SM, 128));
   }
   return slab_launch<128, 0, 2, false>(g, s, tile_grid(g, SM, 128));

@@ -394,10 +394,30 @@ def test_moe_forward_many_rows(fmt, hidden, ffn, T):
 @pytest.mark.parametrize("fmt,T", [("dense", 40), ("mxfp4", 200), ("mxfp4", 350)])
 def test_moe_forward_slab_rows(fmt, T):
     """Expert GEMMs on weight slabs: about 10 (bf16 weights, from the
-    streaming-order copy) or 50 and 90 (MXFP4) rows per expert, so groups span
-    one or two 64-row items with ragged ends; 576 = 4.5 reduction chunks, so
-    the last chunk is a half."""
+    streaming-order copy; 64-row items) or 50 and 90 (MXFP4; 128-row items)
+    rows per expert, so every group is one item with a ragged end; 576 = 4.5
+    reduction chunks, so the last chunk is a half."""
     _moe_forward_check(_moe_shape(576, 576, fmt), T, 1075, 6)
+
+
+def test_moe_forward_mxfp4_slab_hot_expert():
+    """MXFP4 slabs with one expert far above the average: every one of 300
+    tokens picks expert 0 (300 rows: two full 128-row items and a ragged
+    third) and one of experts 1-7 (about 43 rows each, one item), 75 rows per
+    expert on average."""
+    s = _moe_shape(576, 576, "mxfp4")
+    T = 300
+    wl = W.custom(s, [4], [1], 1095)
+    dw = mcpu.DeviceWeights(s, wl.weights)
+    h = W.synth_normal(9, 10, (T, s.hidden))
+    force = np.stack([np.zeros(T, dtype=np.int32), 1 + np.arange(T, dtype=np.int32) % 7], axis=1)
+    out = torch.empty((T, s.hidden), device="cuda")
+    ws = mcpu.workspace(mcpu.moe_forward_workspace_size(s, T))
+    mcpu.moe_forward(s, dw, h.cuda(), out, None, None, torch.from_numpy(force).cuda(), ws)
+    torch.cuda.synchronize()
+    assert mcpu.mcpu_check_device_errors(ws) == 0
+    ref = O.moe(s, O.Weights(s, wl.weights), h, force_idx=force)
+    PT.check("moe out", _np(out), ref["out"], "bf16")
 
 
 def test_dense_projections_ragged_rows_sampled():
