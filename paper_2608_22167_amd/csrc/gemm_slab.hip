@@ -6,12 +6,13 @@
 // HBM, and the kernel's job is to keep enough weight bytes in flight. A
 // workgroup of four wavefronts owns one work item: up to SMT token rows of one
 // group (64; 128 for MXFP4 groups of over 32 rows on average, so that a group
-// just past 64 rows decodes its weights once) against NS weight rows. Each wavefront streams its NS / 4 weight rows
-// straight from global memory into registers, already in matrix-core operand
-// order, through a ring of RC reduction chunks (128 indices each), so weights
-// never pass through LDS; the group's token rows, shared by the four
-// wavefronts (and by all the group's slabs, so they come from L2), are staged
-// per chunk through double-buffered LDS with a ring of register sets.
+// just past 64 rows decodes its weights once) against NS weight rows. Each
+// wavefront streams its NS / 4 weight rows straight from global memory into
+// registers, already in matrix-core operand order, through a ring of RC
+// reduction chunks (128 indices each), so weights never pass through LDS; the
+// group's token rows, shared by the four wavefronts (and by all the group's
+// slabs, so they come from L2), are staged per chunk through double-buffered
+// LDS from one register set.
 //
 // MXFP4 weights are loaded 16 code bytes (32 weights) per lane: lane group g
 // of a 16-row fragment holds indices 32 g .. 32 g + 31 of the chunk, and
@@ -21,7 +22,7 @@
 // registers with the packed e2m1 -> bf16 conversion (exact, as in the LDS
 // kernels). bf16 weights use the plain fragment order.
 //
-// Token rows sit in LDS as [half chunk][64 rows][128 B] with 16-byte chunk c
+// Token rows sit in LDS as [half chunk][SMT rows][128 B] with 16-byte chunk c
 // of row r in slot c ^ (r & 7): the fragment reads of 16 rows and the 8-lane
 // staging writes of one row both cover all bank groups. Reductions that end
 // in half a chunk (k % 128 == 64) skip the missing half: bf16 products are
