@@ -3,21 +3,25 @@
 Each sampled sequence is independent of the others given its own cache pages,
 so the reference restricts the step to the sample: it regenerates on the host
 exactly the pages those sequences read (the generator is counter based) and
-chains the per-layer reference from the step's input through every layer,
-each layer's output feeding the next. Each layer is evaluated twice: once to
-learn the routing (which does not depend on the expert weights), then, after
-drawing and dequantising only the experts that routing uses, with that
-selection forced.
+evaluates the per-layer reference on them. Each layer is evaluated twice:
+once to learn the routing (which does not depend on the expert weights),
+then, after drawing and dequantising only the experts that routing uses,
+with the selection forced.
 
-Routing is an argmax, so wherever two experts' logits are closer than the
-two computations can be apart, either choice is correct. Given the GPU run's
-selections, and optionally its logits, a row whose GPU set differs from the
-reference's is accepted when every swapped pair of experts lies within the
-row's gap of each other under the reference's logits; the gap is 1e-3, or
-twice the row's largest logit difference between the two runs when that is
-larger (each side may be off by that much). An accepted row continues with
-the GPU's set, one of the correct results; any other difference is a
-mismatch.
+Two ways of chaining the layers:
+ - teacher-forced (`reference_layer`): every layer starts from the residual
+   rows the GPU run fed into that layer, so each layer is held to the
+   single-layer bar on its own;
+ - free-running (`reference_stack`): each layer starts from the reference's
+   own output of the layer before. Errors then accumulate with depth, so this
+   chain only bounds the drift; wherever the GPU picked another expert set,
+   the chain adopts it (and counts the row) so that both runs keep computing
+   the same function.
+
+Routing is an argmax, so wherever two experts' logits are closer than the two
+computations can be apart, either choice is correct. `swap_ok` states that
+rule for a differing selection: each expert the GPU took instead of one of the
+reference's must lie within the tie gap of it under the reference's logits.
 """
 from __future__ import annotations
 
@@ -29,12 +33,18 @@ from oracle import oracle as O
 TIE_GAP = 1e-3  # the single-layer bar: the k-th and (k+1)-th fp32 logits within 1e-3
 
 
-def _swap_ok(ref_logits, ref_sel, gpu_sel, gap):
-    """True where each expert the GPU took instead of one of the reference's is
-    within gap of it under the reference's logits."""
+def swap_ok(ref_logits, ref_sel, gpu_sel, gap=TIE_GAP):
+    """Per row: True where the two selections are the same set, or where every
+    expert in the GPU's set but not the reference's has a reference logit no
+    more than `gap` below every expert it displaced (a scalar or per-row gap)."""
+    ref_logits = np.asarray(ref_logits, np.float64)
+    gap = np.broadcast_to(np.asarray(gap, np.float64), (len(ref_sel),))
     ok = np.ones(len(ref_sel), bool)
     for r in range(len(ref_sel)):
         a, b = set(int(e) for e in ref_sel[r]), set(int(e) for e in gpu_sel[r])
+        if len(b) != len(gpu_sel[r]):
+            ok[r] = False  # an expert repeated within one row is never a top-k selection
+            continue
         for e_ref in a - b:
             for e_gpu in b - a:
                 if ref_logits[r, e_ref] - ref_logits[r, e_gpu] > gap[r]:
@@ -42,66 +52,97 @@ def _swap_ok(ref_logits, ref_sel, gpu_sel, gap):
     return ok
 
 
-def reference_stack(spec, seqs, n_layers=None, gpu_idx=None, gpu_logits=None):
-    """seqs: sampled sequence ids; gpu_idx: [L][B][k] selections of the GPU run;
-    gpu_logits: [L][B][E] its router logits. Returns (final residual [n, H]
-    float64, per-layer dicts with the layer's output `out`, selection `idx`,
-    accepted differing rows `adopted`, the rows' logit gaps `gap`, the largest
-    logit difference `logit_err` and `mismatch`, the rows whose GPU selection
-    is not a correct one)."""
-    from paper_2608_22167_amd import workload as W
-    seqs = np.asarray(sorted(int(s) for s in seqs))
-    L = spec.n_layers if n_layers is None else n_layers
-    x = W.stack_x_in(spec)[torch.from_numpy(seqs)].double().numpy()
-    info = []
-    s0 = spec.shape(0)
-    E, I, H = s0.n_experts, s0.ffn_dim, s0.hidden
-    # dense fp32 expert arrays reused by every layer: the routing pass never
-    # reads them, the second pass reads only the experts re-drawn for the layer
-    w_gu = np.zeros((E, 2 * I, H), np.float32)
-    w_d = np.zeros((E, H, I), np.float32)
-    for layer in range(L):
+class _Experts:
+    """Dense fp32 expert arrays reused by every layer; only the experts a
+    layer's sample routes to are drawn and dequantised for it."""
+
+    def __init__(self, spec):
+        s0 = spec.shape(0)
+        E, I, H = s0.n_experts, s0.ffn_dim, s0.hidden
+        self.w_gu = np.zeros((E, 2 * I, H), np.float32)
+        self.w_d = np.zeros((E, H, I), np.float32)
+
+    def draw(self, spec, layer, experts):
+        from paper_2608_22167_amd import workload as W
         s = spec.shape(layer)
-        pt = spec.page_table(layer)[seqs]
-        used = np.unique(pt[pt >= 0])
-        remap = -np.ones(spec.n_pages(layer), np.int64)
-        remap[used] = np.arange(len(used))
-        Wd = W.stack_weights_host(spec, layer, experts=[])
-        Wd["w_gu"], Wd["w_d"] = w_gu, w_d
-        sub = W.Workload(name="stack_sample", shape=s, seed=spec.seed, seq_lens=spec.seq_lens[seqs],
-                         q_lens=np.ones(len(seqs), np.int32),
-                         page_table=np.where(pt >= 0, remap[np.maximum(pt, 0)], -1).astype(np.int32),
-                         n_pages=len(used), weights=Wd)
-        sub.k_pool = W.stack_pages_host(spec, layer, "k", used)
-        sub.v_pool = W.stack_pages_host(spec, layer, "v", used)
-        sub.x_in = torch.from_numpy(x)
-        weights = O.Weights(s, Wd)
-        # routing pass (expert weights are still zero)
-        ra = O.decode_layer(sub, weights)
-        sel = ra["idx"].copy()
-        n = len(seqs)
-        mismatch, adopted = np.zeros(n, bool), np.zeros(n, bool)
-        gap, logit_err = np.full(n, TIE_GAP), np.zeros(n)
-        if gpu_idx is not None:
-            g = np.asarray(gpu_idx[layer])[seqs]
-            if gpu_logits is not None:
-                logit_err = np.abs(np.asarray(gpu_logits[layer], np.float64)[seqs] - ra["logits"]).max(1)
-                gap = np.maximum(gap, 2.0 * logit_err)
-            differ = (np.sort(g, 1) != np.sort(sel, 1)).any(1)
-            ok = _swap_ok(ra["logits"], sel, g, gap)
-            adopted = differ & ok
-            mismatch = differ & ~ok
-            sel[adopted] = g[adopted]
-        # draw and dequantise only the experts the sample uses
-        for e in np.unique(sel):
+        I, H = s.ffn_dim, s.hidden
+        for e in np.unique(experts):
             e = int(e)
-            for key, arr, rows, cols in (("w_gu", w_gu, 2 * I, H), ("w_d", w_d, H, I)):
+            for key, arr, rows, cols in (("w_gu", self.w_gu, 2 * I, H), ("w_d", self.w_d, H, I)):
                 codes = W.synth_bytes(spec.seed, spec.tid(layer, key + "_codes"), (rows, cols // 2),
                                       offset=e * rows * (cols // 2))
                 raw = W.synth_bytes(spec.seed, spec.tid(layer, key + "_scales"), (rows, cols // 32),
                                     offset=e * rows * (cols // 32))
                 O.mxfp4_dequant(codes, 117 + raw % 3, rows, cols, out=arr[e])
-        rb = O.decode_layer(sub, weights, force_idx=sel)
+
+
+def _layer_sample(spec, layer, seqs, x, experts):
+    """The step of one layer restricted to sequences seqs, with input rows x."""
+    from paper_2608_22167_amd import workload as W
+    s = spec.shape(layer)
+    pt = spec.page_table(layer)[seqs]
+    used = np.unique(pt[pt >= 0])
+    remap = -np.ones(spec.n_pages(layer), np.int64)
+    remap[used] = np.arange(len(used))
+    Wd = W.stack_weights_host(spec, layer, experts=[])
+    Wd["w_gu"], Wd["w_d"] = experts.w_gu, experts.w_d
+    sub = W.Workload(name="stack_sample", shape=s, seed=spec.seed, seq_lens=spec.seq_lens[seqs],
+                     q_lens=np.ones(len(seqs), np.int32),
+                     page_table=np.where(pt >= 0, remap[np.maximum(pt, 0)], -1).astype(np.int32),
+                     n_pages=len(used), weights=Wd)
+    sub.k_pool = W.stack_pages_host(spec, layer, "k", used)
+    sub.v_pool = W.stack_pages_host(spec, layer, "v", used)
+    sub.x_in = torch.from_numpy(np.ascontiguousarray(x, np.float64))
+    return sub, O.Weights(s, Wd)
+
+
+def reference_layer(spec, layer, seqs, x, choose=None, experts=None):
+    """Layer `layer` on sequences seqs (sorted ids) from input rows x [n, H].
+    choose(routing) -> selection [n, k] picks the expert sets to evaluate
+    given the routing pass's dict (logits, idx); by default the reference's
+    own. Returns (routing pass, final pass) dicts of oracle.decode_layer."""
+    seqs = np.asarray(seqs)
+    if experts is None:
+        experts = _Experts(spec)
+    sub, weights = _layer_sample(spec, layer, seqs, x, experts)
+    ra = O.decode_layer(sub, weights)  # routing pass: logits and sets do not read the expert weights
+    sel = ra["idx"].copy() if choose is None else np.asarray(choose(ra), np.int32)
+    experts.draw(spec, layer, sel)
+    rb = O.decode_layer(sub, weights, force_idx=sel)
+    return ra, rb
+
+
+def reference_stack(spec, seqs, n_layers=None, gpu_idx=None):
+    """Free-running chain through the first n_layers layers for seqs. gpu_idx
+    ([L][B][k], optional): where the GPU's set for a sampled row differs from
+    the reference's, the chain continues with the GPU's set. Returns (final
+    residual [n, H] float64, per-layer dicts: `out`, `idx` (the set used),
+    `adopted` (rows that took the GPU's set), `gap` (each row's reference
+    logit gap between the displaced and the adopted experts, 0 where equal))."""
+    seqs = np.asarray(sorted(int(s) for s in seqs))
+    L = spec.n_layers if n_layers is None else n_layers
+    from paper_2608_22167_amd import workload as W
+    x = W.stack_x_in(spec)[torch.from_numpy(seqs)].double().numpy()
+    experts = _Experts(spec)
+    info = []
+    for layer in range(L):
+        rec = {}
+
+        def choose(ra, layer=layer, rec=rec):
+            sel = ra["idx"].copy()
+            adopted = np.zeros(len(seqs), bool)
+            gap = np.zeros(len(seqs))
+            if gpu_idx is not None:
+                g = np.asarray(gpu_idx[layer])[seqs]
+                adopted = (np.sort(g, 1) != np.sort(sel, 1)).any(1)
+                for r in np.nonzero(adopted)[0]:
+                    a, b = set(sel[r].tolist()), set(g[r].tolist())
+                    gap[r] = max(ra["logits"][r, e] - ra["logits"][r, f] for e in a - b for f in b - a)
+                sel[adopted] = g[adopted]
+            rec.update(idx=sel, adopted=adopted, gap=gap)
+            return sel
+
+        _, rb = reference_layer(spec, layer, seqs, x, choose, experts)
         x = rb["out"]
-        info.append(dict(out=x, idx=sel, adopted=adopted, gap=gap, logit_err=logit_err, mismatch=mismatch))
+        info.append(dict(out=x, **rec))
     return x, info

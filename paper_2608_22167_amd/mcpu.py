@@ -369,13 +369,18 @@ class DeviceStack:
         ws = max(decode_layer_workspace_size(spec.shape(i), B, B) for i in range(min(2, self.n_layers)))
         self.ws = workspace(ws, device)
 
-    def run(self, stream=None, logits: Optional[torch.Tensor] = None) -> torch.Tensor:
+    def run(self, stream=None, logits: Optional[torch.Tensor] = None, rows: Optional[torch.Tensor] = None,
+            inputs: Optional[torch.Tensor] = None) -> torch.Tensor:
         """One step through every layer; returns the final residual stream.
-        logits, if given ([n_layers, B, E] fp32), receives each layer's router logits."""
+        logits, if given ([n_layers, B, E] fp32), receives each layer's router
+        logits; inputs, if given ([n_layers, len(rows), H] fp32), receives the
+        residual-stream rows `rows` (device int64) that enter each layer."""
         x = self.x_in
         for i in range(self.n_layers):
             y = self.buf[i % 2]
             pt = self.pt_sw if self.spec.is_sw(i) else self.pt_full
+            if inputs is not None:
+                torch.index_select(x, 0, rows, out=inputs[i])
             taps = None if logits is None else Taps(logits=logits[i].data_ptr())
             decode_layer(self.spec.shape(i), self.weights[i], self.pools[i], pt, self.seq_lens, None,
                          self.host_seq_lens, None, x, y, self.topk_idx[i], None, taps, self.ws, stream)

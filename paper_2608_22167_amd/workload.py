@@ -477,12 +477,14 @@ class StackSpec:
         return per_key * (n_full * full + (self.n_layers - n_full) * sw)
 
 
-def stack24(seed=1005, batch=512, median=8192, cap=65536, n_layers=24, slack=1.05) -> StackSpec:
-    """24-layer gpt-oss-20b-shaped stack, bf16 attention and router, MXFP4 experts."""
+def stack24(seed=1005, batch=512, median=8192, cap=65536, n_layers=24, slack=1.05,
+            base: LayerShape = None) -> StackSpec:
+    """24-layer gpt-oss-20b-shaped stack, bf16 attention and router, MXFP4
+    experts (base: another bf16 layer shape for small test stacks)."""
     rng = np.random.default_rng(seed + 1)
     ctx = lognormal_lengths(rng, batch, median, 1.0, cap)
     q = np.ones(batch, dtype=np.int32)
-    full = replace(GPT_OSS_20B, expert_fmt="mxfp4")
+    full = replace(GPT_OSS_20B if base is None else base, expert_fmt="mxfp4", window=0)
     sw = replace(full, window=128)
     pt_f, np_f = _pages(ctx, q, 0, np.random.default_rng(seed + 2), slack)
     pt_s, np_s = _pages(ctx, q, 128, np.random.default_rng(seed + 3), slack)

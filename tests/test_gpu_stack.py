@@ -3,11 +3,10 @@ MXFP4 experts) on the GPU against the CPU reference, and the device twin of
 the seeded input generator against the host generator.
 
 The stack is generated in HBM by the device generator; the reference
-regenerates on the host only what its sampled sequences read and chains its
-own layers from the step's input. A stack is compared at L times the
-single-layer tolerance: each layer adds its own rounding error, and the
-residual connection passes the errors of earlier layers on with a gain close
-to one.
+regenerates on the host only what its sampled sequences read. Each layer is
+compared at the single-layer bar from the residual rows the GPU fed into it
+(teacher-forced); the reference's own free-running chain is reported as the
+drift over depth.
 """
 import numpy as np
 import pytest
@@ -69,19 +68,24 @@ def _sample(spec, extra, seed):
 def _run(spec, n_layers, seqs):
     st = mcpu.DeviceStack(spec, n_layers=n_layers)
     rows = torch.tensor(seqs, device="cuda")
+    H = spec.shape_full.hidden
     logits = torch.empty((n_layers, spec.batch, spec.shape_full.n_experts), dtype=torch.float32, device="cuda")
-    out = st.run(logits=logits)
+    inputs = torch.empty((n_layers, len(seqs), H), dtype=torch.float32, device="cuda")
+    outputs = torch.empty((n_layers, len(seqs), H), dtype=torch.float32, device="cuda")
+    out = st.run(logits=logits, rows=rows, inputs=inputs)
     torch.cuda.synchronize()
     assert st.device_errors() == 0
-    got = out.index_select(0, rows).double().cpu().numpy()
-    idx = st.topk_idx.cpu().numpy()
-    lg = logits.cpu().numpy()
+    # layer i's output is layer i+1's input; the last layer's is the step's output
+    outputs[:-1] = inputs[1:]
+    outputs[-1] = out.index_select(0, rows)
+    got = dict(inputs=inputs.double().cpu().numpy(), outputs=outputs.double().cpu().numpy(),
+               idx=st.topk_idx.cpu().numpy(), logits=logits.cpu().numpy())
     again = st.run()
     torch.cuda.synchronize()
     assert torch.equal(out, again), "stack step is not repeatable"
     del st, out, again
     torch.cuda.empty_cache()
-    return got, idx, lg
+    return got
 
 
 def _gpu_topk_consistent(idx, logits, rows):
@@ -94,16 +98,47 @@ def _gpu_topk_consistent(idx, logits, rows):
 
 
 def _compare(spec, n_layers, seqs):
-    got, idx, lg = _run(spec, n_layers, seqs)
-    _gpu_topk_consistent(idx, lg, seqs)
-    ref, info = OS.reference_stack(spec, seqs, n_layers=n_layers, gpu_idx=idx, gpu_logits=lg)
-    for layer, d in enumerate(info):
-        assert not d["mismatch"].any(), \
-            f"layer {layer}: router sets differ at sampled rows {np.nonzero(d['mismatch'])[0]} " \
-            f"(logit differences {d['logit_err']})"
-        # the logits themselves stay within the depth-scaled bar
-        assert d["logit_err"].max() <= 2e-2 * (layer + 1), (layer, d["logit_err"])
-    return PT.check(f"stack{n_layers}", got, ref, "bf16", scale=n_layers)
+    """Teacher-forced: every layer, started from the rows the GPU fed into it,
+    meets the single-layer bar (max-abs 2e-2, rel-L2 1e-2 on the layer's
+    output; expert sets exact unless every swapped expert is within the 1e-3
+    logit gap under the reference's logits, in which case the reference is
+    evaluated with the GPU's set). The free-running reference chain is then
+    reported as the drift over depth and bounded by depth x the bar."""
+    got = _run(spec, n_layers, seqs)
+    _gpu_topk_consistent(got["idx"], got["logits"], seqs)
+    seqs = np.asarray(seqs)
+    experts = OS._Experts(spec)
+    errs = []
+    for layer in range(n_layers):
+        g_idx = got["idx"][layer][seqs]
+        state = {}
+
+        def choose(ra, g_idx=g_idx, state=state):
+            sel = ra["idx"].copy()
+            differ = (np.sort(g_idx, 1) != np.sort(sel, 1)).any(1)
+            ok = OS.swap_ok(ra["logits"], sel, g_idx, OS.TIE_GAP)
+            assert ok.all(), f"layer {layer}: router sets differ beyond the tie gap at sampled rows " \
+                             f"{seqs[~ok]}: GPU {g_idx[~ok]} vs reference {sel[~ok]}"
+            sel[differ] = g_idx[differ]
+            state["swapped"] = int(differ.sum())
+            return sel
+
+        ra, rb = OS.reference_layer(spec, layer, seqs, got["inputs"][layer], choose, experts)
+        lerr = np.abs(got["logits"][layer][seqs].astype(np.float64) - ra["logits"]).max()
+        mx, rl = PT.check(f"stack layer {layer}", got["outputs"][layer], rb["out"], "bf16")
+        # the layer's own increment (both sides start from the same rows): rel-L2 against its norm
+        x0 = got["inputs"][layer]
+        PT.check(f"stack layer {layer} increment", got["outputs"][layer] - x0, rb["out"] - x0, "bf16")
+        errs.append((layer, mx, rl, lerr, state["swapped"]))
+        print(f"  layer {layer:2d}: max-abs {mx:.2e} rel-L2 {rl:.2e} logit err {lerr:.2e} "
+              f"near-tie swaps {state['swapped']}", flush=True)
+    # drift of the free-running chain (reported; bounded by depth x the bar)
+    ref, info = OS.reference_stack(spec, seqs, n_layers=n_layers, gpu_idx=got["idx"])
+    adopted = sum(int(d["adopted"].sum()) for d in info)
+    mx = np.abs(got["outputs"][-1] - ref).max()
+    print(f"  free-running chain after {n_layers} layers: max-abs {mx:.2e}, rel-L2 "
+          f"{PT.rel_l2(got['outputs'][-1], ref):.2e}, GPU sets adopted {adopted}")
+    PT.check(f"stack{n_layers} drift", got["outputs"][-1], ref, "bf16", scale=n_layers)
 
 
 def test_stack_depth4_small_batch():
