@@ -17,7 +17,10 @@
  * queries, the new keys and values written to the paged cache, the attention
  * output, the normalised rows the experts read and the SwiGLU activations.
  * Everything between two such points (the products' sums, the softmax, the
- * residual stream, the router logits) stays in float64.
+ * residual stream, the router logits) stays in float64. A second mode
+ * (kv_only) rounds the cache entries only and keeps every activation in
+ * float64; it measures how much of the GPU's distance from the reference
+ * comes from the activations it stores.
  *
  * Only the tests, the smoke check and the benchmark's CPU-baseline leg use
  * this file. It shares no code, header or table with the GPU library.
@@ -44,6 +47,7 @@ typedef struct {
   int32_t page_size; /* must be 16 */
   int32_t window;    /* 0: full attention; else keys p-window+1 .. p */
   int32_t kv_bf16;   /* 1: the layer (cache and stored activations) is bfloat16 */
+  int32_t kv_only;   /* 1: round only the cache entries; keep every activation unrounded */
   double rms_eps, swiglu_alpha, swiglu_limit, swiglu_beta;
 } orc_cfg;
 
@@ -77,8 +81,10 @@ void orc_round_bf16_array(int64_t n, const double* in, double* out) {
 
 /* a value as the layer stores it: bfloat16 or binary32 */
 static double stored(const orc_cfg* c, double v) { return c->kv_bf16 ? orc_round_bf16(v) : (double)(float)v; }
+/* an activation the layer stores (not a cache entry): rounded unless kv_only */
+static double stored_act(const orc_cfg* c, double v) { return c->kv_only ? v : stored(c, v); }
 static void stored_array(const orc_cfg* c, int64_t n, double* v) {
-  for (int64_t i = 0; i < n; ++i) v[i] = stored(c, v[i]);
+  for (int64_t i = 0; i < n; ++i) v[i] = stored_act(c, v[i]);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -295,7 +301,7 @@ static void expert_ffn(const orc_cfg* c, const orc_weights* w, int e, const doub
   int H = c->hidden, I = c->ffn_dim;
   linear(1, H, 2 * I, hn, w->w_gu + (int64_t)e * 2 * I * H, w->b_gu + (int64_t)e * 2 * I, gu);
   for (int j = 0; j < I; ++j)
-    act[j] = stored(c, orc_swiglu(gu[2 * j], gu[2 * j + 1], c->swiglu_alpha, c->swiglu_limit, c->swiglu_beta));
+    act[j] = stored_act(c, orc_swiglu(gu[2 * j], gu[2 * j + 1], c->swiglu_alpha, c->swiglu_limit, c->swiglu_beta));
   linear(1, I, H, act, w->w_d + (int64_t)e * H * I, w->b_d + (int64_t)e * H, y);
 }
 
@@ -356,12 +362,17 @@ int orc_moe(const orc_cfg* c, const orc_weights* w, int T, const double* h, doub
 /*   h1 = x + o . W_o^T + b_o;  out = MoE(h1).                                */
 /* ------------------------------------------------------------------------ */
 
-int orc_decode_layer(const orc_cfg* c, const orc_weights* w, int B, const int32_t* page_table,
-                     int max_pages, int n_pages, const int32_t* seq_lens, const int32_t* cu_q,
-                     float* k_pool, float* v_pool, const double* x_in, double* x_out,
-                     double* q_out, double* o_out, double* h1_out, int32_t* idx_out,
-                     double* w_out, double* logits_out, double* moe_out,
-                     const int32_t* force_idx) {
+/* n_eval / eval_rows (optional): every new token is projected and appended,  */
+/* but attention, the output projection and the MoE are evaluated only for   */
+/* the listed rows (ascending), whose results fill the outputs in that order */
+/* (x_in and force_idx are still indexed by row). A token's result depends   */
+/* only on its own row and the cache, so this changes no value.              */
+static int decode_layer_rows(const orc_cfg* c, const orc_weights* w, int B, const int32_t* page_table,
+                             int max_pages, int n_pages, const int32_t* seq_lens, const int32_t* cu_q,
+                             float* k_pool, float* v_pool, const double* x_in, int n_eval,
+                             const int32_t* eval_rows, double* x_out, double* q_out, double* o_out,
+                             double* h1_out, int32_t* idx_out, double* w_out, double* logits_out,
+                             double* moe_out, const int32_t* force_idx) {
   int H = c->hidden, d = c->head_dim, Hq = c->n_q_heads, Hkv = c->n_kv_heads;
   int QKV = (Hq + 2 * Hkv) * d, A = Hq * d;
   if (c->page_size != ORC_PAGE || Hq % Hkv) return ORC_EINVAL;
@@ -372,15 +383,25 @@ int orc_decode_layer(const orc_cfg* c, const orc_weights* w, int B, const int32_
     int r0 = cu_q ? cu_q[b] : b, r1 = cu_q ? cu_q[b + 1] : b + 1;
     for (int r = r0; r < r1; ++r) { tok_seq[r] = b; tok_pos[r] = seq_lens[b] + (r - r0); }
   }
+  int NE = eval_rows ? n_eval : T;
+  int32_t* rows = (int32_t*)malloc(sizeof(int32_t) * (size_t)(NE > 0 ? NE : 1));
+  for (int e = 0; e < NE; ++e) rows[e] = eval_rows ? eval_rows[e] : e;
   double* xn = (double*)malloc(sizeof(double) * (size_t)T * H);
   double* qkv = (double*)malloc(sizeof(double) * (size_t)T * QKV);
   double* q = (double*)malloc(sizeof(double) * (size_t)T * A);
   double* kn = (double*)malloc(sizeof(double) * (size_t)T * Hkv * d);
   double* vn = (double*)malloc(sizeof(double) * (size_t)T * Hkv * d);
-  double* o = (double*)malloc(sizeof(double) * (size_t)T * A);
-  double* h1 = (double*)malloc(sizeof(double) * (size_t)T * H);
+  int32_t* e_seq = (int32_t*)malloc(sizeof(int32_t) * (size_t)(NE > 0 ? NE : 1));
+  int32_t* e_pos = (int32_t*)malloc(sizeof(int32_t) * (size_t)(NE > 0 ? NE : 1));
+  double* eq = (double*)malloc(sizeof(double) * (size_t)(NE > 0 ? NE : 1) * A);
+  double* ex = (double*)malloc(sizeof(double) * (size_t)(NE > 0 ? NE : 1) * H);
+  int32_t* ef = force_idx ? (int32_t*)malloc(sizeof(int32_t) * (size_t)(NE > 0 ? NE : 1) * c->top_k) : NULL;
+  double* o = (double*)malloc(sizeof(double) * (size_t)(NE > 0 ? NE : 1) * A);
+  double* h1 = (double*)malloc(sizeof(double) * (size_t)(NE > 0 ? NE : 1) * H);
   int rc = ORC_OK;
 
+  for (int e = 0; e < NE; ++e)
+    if (rows[e] < 0 || rows[e] >= T || (e > 0 && rows[e] <= rows[e - 1])) { rc = ORC_EINVAL; goto done; }
   orc_rmsnorm(T, H, x_in, w->g1, c->rms_eps, xn);
   stored_array(c, (int64_t)T * H, xn);
 #pragma omp parallel for schedule(static)
@@ -403,22 +424,51 @@ int orc_decode_layer(const orc_cfg* c, const orc_weights* w, int B, const int32_
   }
   rc = orc_kv_append(c, T, tok_seq, tok_pos, kn, vn, k_pool, v_pool, page_table, max_pages, n_pages);
   if (rc) goto done;
-  rc = orc_attention(c, T, tok_seq, tok_pos, q, k_pool, v_pool, page_table, max_pages, n_pages,
-                     w->sinks, o);
-  if (rc) goto done;
-  stored_array(c, (int64_t)T * A, o);
-#pragma omp parallel for schedule(static)
-  for (int t = 0; t < T; ++t) {
-    linear(1, A, H, o + (int64_t)t * A, w->w_o, w->b_o, h1 + (int64_t)t * H);
-    for (int n = 0; n < H; ++n) h1[(int64_t)t * H + n] += x_in[(int64_t)t * H + n];
+  for (int e = 0; e < NE; ++e) {
+    e_seq[e] = tok_seq[rows[e]];
+    e_pos[e] = tok_pos[rows[e]];
+    memcpy(eq + (int64_t)e * A, q + (int64_t)rows[e] * A, sizeof(double) * (size_t)A);
+    memcpy(ex + (int64_t)e * H, x_in + (int64_t)rows[e] * H, sizeof(double) * (size_t)H);
+    if (ef) memcpy(ef + (int64_t)e * c->top_k, force_idx + (int64_t)rows[e] * c->top_k, sizeof(int32_t) * (size_t)c->top_k);
   }
-  rc = orc_moe(c, w, T, h1, x_out, idx_out, w_out, logits_out, moe_out, force_idx);
-  if (q_out) memcpy(q_out, q, sizeof(double) * (size_t)T * A);
-  if (o_out) memcpy(o_out, o, sizeof(double) * (size_t)T * A);
-  if (h1_out) memcpy(h1_out, h1, sizeof(double) * (size_t)T * H);
+  rc = orc_attention(c, NE, e_seq, e_pos, eq, k_pool, v_pool, page_table, max_pages, n_pages, w->sinks, o);
+  if (rc) goto done;
+  stored_array(c, (int64_t)NE * A, o);
+#pragma omp parallel for schedule(static)
+  for (int e = 0; e < NE; ++e) {
+    linear(1, A, H, o + (int64_t)e * A, w->w_o, w->b_o, h1 + (int64_t)e * H);
+    for (int n = 0; n < H; ++n) h1[(int64_t)e * H + n] += ex[(int64_t)e * H + n];
+  }
+  rc = orc_moe(c, w, NE, h1, x_out, idx_out, w_out, logits_out, moe_out, ef);
+  if (q_out) memcpy(q_out, eq, sizeof(double) * (size_t)NE * A);
+  if (o_out) memcpy(o_out, o, sizeof(double) * (size_t)NE * A);
+  if (h1_out) memcpy(h1_out, h1, sizeof(double) * (size_t)NE * H);
 done:
-  free(tok_seq); free(tok_pos); free(xn); free(qkv); free(q); free(kn); free(vn); free(o); free(h1);
+  free(tok_seq); free(tok_pos); free(rows); free(xn); free(qkv); free(q); free(kn); free(vn);
+  free(e_seq); free(e_pos); free(eq); free(ex); free(ef); free(o); free(h1);
   return rc;
+}
+
+int orc_decode_layer(const orc_cfg* c, const orc_weights* w, int B, const int32_t* page_table,
+                     int max_pages, int n_pages, const int32_t* seq_lens, const int32_t* cu_q,
+                     float* k_pool, float* v_pool, const double* x_in, double* x_out,
+                     double* q_out, double* o_out, double* h1_out, int32_t* idx_out,
+                     double* w_out, double* logits_out, double* moe_out,
+                     const int32_t* force_idx) {
+  return decode_layer_rows(c, w, B, page_table, max_pages, n_pages, seq_lens, cu_q, k_pool, v_pool, x_in, 0,
+                           NULL, x_out, q_out, o_out, h1_out, idx_out, w_out, logits_out, moe_out, force_idx);
+}
+
+int orc_decode_layer_rows(const orc_cfg* c, const orc_weights* w, int B, const int32_t* page_table,
+                          int max_pages, int n_pages, const int32_t* seq_lens, const int32_t* cu_q,
+                          float* k_pool, float* v_pool, const double* x_in, int n_eval,
+                          const int32_t* eval_rows, double* x_out, double* q_out, double* o_out,
+                          double* h1_out, int32_t* idx_out, double* w_out, double* logits_out,
+                          double* moe_out, const int32_t* force_idx) {
+  if (!eval_rows) return ORC_EINVAL;
+  return decode_layer_rows(c, w, B, page_table, max_pages, n_pages, seq_lens, cu_q, k_pool, v_pool, x_in,
+                           n_eval, eval_rows, x_out, q_out, o_out, h1_out, idx_out, w_out, logits_out,
+                           moe_out, force_idx);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -453,4 +503,100 @@ int orc_mxfp4_dequant(int64_t rows, int cols, const uint8_t* codes, const uint8_
       }
     }
   return bad ? ORC_EINVAL : ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Generation ends: the vocabulary head and next-token sampling.             */
+/* The rollouts sample at a fixed temperature (0.7 in the paper's training   */
+/* details) and the GRPO update rescores whole trajectories under the policy */
+/* (Sec. 3.2, Sec. 4).                                                        */
+/* ------------------------------------------------------------------------ */
+
+/* Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): a round maps counter  */
+/* (c0, c1, c2, c3) under key (k0, k1) to                                    */
+/*   (hi(B*c2) ^ c1 ^ k0, lo(B*c2), hi(A*c0) ^ c3 ^ k1, lo(A*c0))            */
+/* with A = 0xD2511F53, B = 0xCD9E8D57 (hi/lo: upper and lower 32 bits of the */
+/* 64-bit product); ten rounds, the key advanced by (0x9E3779B9, 0xBB67AE85)  */
+/* before every round after the first.                                       */
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+  uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3], k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; ++round) {
+    if (round > 0) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+    uint64_t pa = (uint64_t)0xD2511F53u * c0, pb = (uint64_t)0xCD9E8D57u * c2;
+    uint32_t n0 = (uint32_t)(pb >> 32) ^ c1 ^ k0, n1 = (uint32_t)pb;
+    uint32_t n2 = (uint32_t)(pa >> 32) ^ c3 ^ k1, n3 = (uint32_t)pa;
+    c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+  }
+  out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+#define ORC_SAMPLE_TAG 0x4C4D5330u
+
+/* The uniform draw of vocabulary entry v for (seed, sequence, position):    */
+/* word v % 4 of Philox at counter (v / 4, pos, seq, tag), key (seed low,     */
+/* seed high); u = (w / 2^9 rounded down + 1/2) / 2^23, strictly in (0, 1).   */
+double orc_sample_uniform(uint64_t seed, int seq, int pos, int v) {
+  uint32_t ctr[4] = {(uint32_t)v / 4u, (uint32_t)pos, (uint32_t)seq, ORC_SAMPLE_TAG};
+  uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)}, w[4];
+  orc_philox4x32_10(ctr, key, w);
+  return ((double)(w[v % 4] >> 9) + 0.5) / 8388608.0;
+}
+
+/* Gumbel noise of a uniform: g = -log(-log u). */
+double orc_gumbel(double u) { return -log(-log(u)); }
+
+/* Vocabulary head for T rows of the residual stream x [T][H]:               */
+/*   xn = RMSNorm(x; g_final), stored (bf16); l_v = xn . W_lm[v] (float64);   */
+/*   s = l / temperature (temperature > 0), else s = l;                       */
+/*   lse = log sum_v e^{s_v};                                                 */
+/*   token = argmax_v (s_v + g_v) with g_v the Gumbel noise of the row's      */
+/*   (seed, seq, pos) draws (temperature > 0), or argmax_v l_v (greedy);      */
+/*   the maximum is taken over values rounded to fp32 (the precision the GPU  */
+/*   decides in), the lower id on equal values;                               */
+/*   logprob = s_token - lse; target_logprob = s_target - lse.                */
+/* logits_out (optional) receives l [T][V]; pert_out (optional) the float64   */
+/* perturbed scores s + g [T][V] before rounding.                              */
+int orc_lm_head(int T, int H, int V, const double* x, const float* g_final, double eps, const float* w_lm,
+                double temperature, uint64_t seed, const int32_t* seq_ids, const int32_t* positions,
+                const int32_t* targets, int32_t* tokens, double* logprob, double* lse_out,
+                double* target_logprob, double* logits_out, double* pert_out) {
+  int greedy = !(temperature > 0.0);
+  if (!greedy && (!seq_ids || !positions)) return ORC_EINVAL;
+#pragma omp parallel for schedule(dynamic)
+  for (int t = 0; t < T; ++t) {
+    double* xn = (double*)malloc(sizeof(double) * (size_t)H);
+    double* s = (double*)malloc(sizeof(double) * (size_t)V);
+    orc_rmsnorm(1, H, x + (int64_t)t * H, g_final, eps, xn);
+    for (int h = 0; h < H; ++h) xn[h] = orc_round_bf16(xn[h]);
+    double mx = -INFINITY;
+    for (int v = 0; v < V; ++v) {
+      double l = 0.0;
+      const float* w = w_lm + (int64_t)v * H;
+      for (int h = 0; h < H; ++h) l += xn[h] * (double)w[h];
+      if (logits_out) logits_out[(int64_t)t * V + v] = l;
+      s[v] = greedy ? l : l / temperature;
+      if (s[v] > mx) mx = s[v];
+    }
+    double sum = 0.0;
+    for (int v = 0; v < V; ++v) sum += exp(s[v] - mx);
+    double lse = mx + log(sum);
+    int best = -1;
+    float bv = 0.0f;
+    for (int v = 0; v < V; ++v) {
+      double p = s[v];
+      if (!greedy) p += orc_gumbel(orc_sample_uniform(seed, seq_ids[t], positions[t], v));
+      if (pert_out) pert_out[(int64_t)t * V + v] = p;
+      float pf = (float)p;
+      if (best < 0 || pf > bv) { best = v; bv = pf; }
+    }
+    if (tokens) tokens[t] = best;
+    if (logprob) logprob[t] = s[best] - lse;
+    if (lse_out) lse_out[t] = lse;
+    if (target_logprob && targets) {
+      int tg = targets[t];
+      target_logprob[t] = (tg >= 0 && tg < V) ? s[tg] - lse : -INFINITY;
+    }
+    free(xn); free(s);
+  }
+  return ORC_OK;
 }

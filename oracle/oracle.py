@@ -21,7 +21,7 @@ c_i32p = ctypes.POINTER(ctypes.c_int32)
 class OrcCfg(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "hidden", "n_q_heads", "n_kv_heads", "head_dim", "n_experts", "top_k", "ffn_dim",
-        "page_size", "window", "kv_bf16")] + [
+        "page_size", "window", "kv_bf16", "kv_only")] + [
         (n, ctypes.c_double) for n in ("rms_eps", "swiglu_alpha", "swiglu_limit", "swiglu_beta")]
 
 
@@ -55,9 +55,18 @@ def lib():
         L.orc_moe.argtypes = [vp, vp, i32, vp, vp, vp, vp, vp, vp, vp]
         L.orc_decode_layer.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp, vp, vp, vp, vp,
                                        vp, vp, vp, vp, vp, vp, vp, vp]
+        L.orc_decode_layer_rows.argtypes = [vp, vp, i32, vp, i32, i32, vp, vp, vp, vp, vp, i32, vp,
+                                            vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.orc_e2m1.restype = f64
         L.orc_e2m1.argtypes = [i32]
         L.orc_mxfp4_dequant.argtypes = [i64, i32, vp, vp, vp]
+        L.orc_philox4x32_10.argtypes = [vp, vp, vp]
+        L.orc_sample_uniform.restype = f64
+        L.orc_sample_uniform.argtypes = [ctypes.c_uint64, i32, i32, i32]
+        L.orc_gumbel.restype = f64
+        L.orc_gumbel.argtypes = [f64]
+        L.orc_lm_head.argtypes = [i32, i32, i32, vp, vp, f64, vp, f64, ctypes.c_uint64, vp, vp, vp, vp, vp, vp,
+                                  vp, vp, vp]
         L.orc_pool_to_logical.argtypes = [vp, i32, vp, vp, vp, vp]
         L.orc_pool_from_logical.argtypes = [vp, i32, vp, vp, vp, vp]
     return _LIB
@@ -86,11 +95,12 @@ def _p(a: Optional[np.ndarray]):
     return None if a is None else a.ctypes.data
 
 
-def make_cfg(shape) -> OrcCfg:
+def make_cfg(shape, kv_only=False) -> OrcCfg:
     return OrcCfg(hidden=shape.hidden, n_q_heads=shape.n_q_heads, n_kv_heads=shape.n_kv_heads,
                   head_dim=shape.head_dim, n_experts=shape.n_experts, top_k=shape.top_k,
                   ffn_dim=shape.ffn_dim, page_size=shape.page_size, window=shape.window,
-                  kv_bf16=1 if shape.dtype == "bf16" else 0, rms_eps=shape.rms_eps,
+                  kv_bf16=1 if shape.dtype == "bf16" else 0, kv_only=1 if kv_only else 0,
+                  rms_eps=shape.rms_eps,
                   swiglu_alpha=shape.swiglu_alpha, swiglu_limit=shape.swiglu_limit,
                   swiglu_beta=shape.swiglu_beta)
 
@@ -241,12 +251,14 @@ def moe(shape, weights: Weights, h, force_idx=None) -> Dict[str, np.ndarray]:
 
 
 def decode_layer(wl, weights: Optional[Weights] = None, force_idx=None, k_pool=None,
-                 v_pool=None) -> Dict[str, np.ndarray]:
+                 v_pool=None, rows=None, kv_only=False) -> Dict[str, np.ndarray]:
     """One decoder-layer step of workload wl. Returns every intermediate the
     tests compare: q (after rotation), o, h1, moe, out, idx, w, logits and the
-    pools after the append."""
+    pools after the append. rows (optional, ascending token rows): every new
+    token is appended, but only these rows are evaluated and returned (in
+    that order). kv_only: round only the cache entries (see mcpu_oracle.c)."""
     s = wl.shape
-    cfg = make_cfg(s)
+    cfg = make_cfg(s, kv_only)
     if weights is None:
         weights = Weights(s, wl.weights)
     kp = _np(wl.k_pool if k_pool is None else k_pool, np.float32).copy()
@@ -256,16 +268,72 @@ def decode_layer(wl, weights: Optional[Weights] = None, force_idx=None, k_pool=N
     cu = None if wl.is_decode else _np(wl.cu_q, np.int32)
     x = _np(wl.x_in, np.float64)
     T, H = x.shape
+    sel = None if rows is None else _np(rows, np.int32)
+    if sel is not None:
+        T = len(sel)
     r = dict(out=np.empty((T, H)), q=np.empty((T, s.n_q_heads, s.head_dim)),
              o=np.empty((T, s.n_q_heads * s.head_dim)), h1=np.empty((T, H)),
              idx=np.empty((T, s.top_k), dtype=np.int32), w=np.empty((T, s.top_k)),
              logits=np.empty((T, s.n_experts)), moe=np.empty((T, H)))
     fi = None if force_idx is None else _np(force_idx, np.int32)
-    rc = lib().orc_decode_layer(ctypes.byref(cfg), ctypes.byref(weights.struct), wl.batch, _p(pt),
-                                pt.shape[1], kp.shape[0], _p(sl), _p(cu), _p(kp), _p(vpl), _p(x),
-                                _p(r["out"]), _p(r["q"]), _p(r["o"]), _p(r["h1"]), _p(r["idx"]),
-                                _p(r["w"]), _p(r["logits"]), _p(r["moe"]), _p(fi))
+    outs = (_p(r["out"]), _p(r["q"]), _p(r["o"]), _p(r["h1"]), _p(r["idx"]), _p(r["w"]), _p(r["logits"]),
+            _p(r["moe"]), _p(fi))
+    if sel is None:
+        rc = lib().orc_decode_layer(ctypes.byref(cfg), ctypes.byref(weights.struct), wl.batch, _p(pt),
+                                    pt.shape[1], kp.shape[0], _p(sl), _p(cu), _p(kp), _p(vpl), _p(x), *outs)
+    else:
+        rc = lib().orc_decode_layer_rows(ctypes.byref(cfg), ctypes.byref(weights.struct), wl.batch, _p(pt),
+                                         pt.shape[1], kp.shape[0], _p(sl), _p(cu), _p(kp), _p(vpl), _p(x),
+                                         len(sel), _p(sel), *outs)
     if rc:
         raise ValueError("decode_layer: invalid input (missing page or position beyond RoPE table)")
     r["k_pool"], r["v_pool"] = kp, vpl
+    return r
+
+
+# ---------------------------------------------------------------------------
+# generation ends: vocabulary head and sampling
+# ---------------------------------------------------------------------------
+
+
+def philox4x32_10(ctr, key) -> np.ndarray:
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.empty(4, dtype=np.uint32)
+    lib().orc_philox4x32_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def sample_uniform(seed: int, seq: int, pos: int, v: int) -> float:
+    return lib().orc_sample_uniform(seed, seq, pos, v)
+
+
+def gumbel(u: float) -> float:
+    return lib().orc_gumbel(u)
+
+
+def lm_head(x, g_final, w_lm, eps, temperature, seed=0, seq_ids=None, positions=None, targets=None,
+            want_logits=False) -> Dict[str, np.ndarray]:
+    """Vocabulary head and next-token choice for rows x [T, H] (see
+    orc_lm_head). Returns tokens, logprob, lse, target_logprob (if targets),
+    and logits / pert [T, V] if want_logits."""
+    xx = _np(x, np.float64)
+    T, H = xx.shape
+    g = _np(g_final, np.float32)
+    w = _np(w_lm, np.float32)
+    V = w.shape[0]
+    si = None if seq_ids is None else _np(seq_ids, np.int32)
+    ps = None if positions is None else _np(positions, np.int32)
+    tg = None if targets is None else _np(targets, np.int32)
+    r = dict(tokens=np.empty(T, np.int32), logprob=np.empty(T), lse=np.empty(T))
+    if tg is not None:
+        r["target_logprob"] = np.empty(T)
+    if want_logits:
+        r["logits"] = np.empty((T, V))
+        r["pert"] = np.empty((T, V))
+    rc = lib().orc_lm_head(T, H, V, _p(xx), _p(g), eps, _p(w), float(temperature), int(seed), _p(si), _p(ps),
+                           _p(tg), _p(r["tokens"]), _p(r["logprob"]), _p(r["lse"]), _p(r.get("target_logprob")),
+                           _p(r.get("logits")), _p(r.get("pert")))
+    if rc:
+        raise ValueError("lm_head: sampling needs seq_ids and positions")
     return r

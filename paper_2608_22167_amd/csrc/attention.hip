@@ -369,13 +369,12 @@ struct PrefillShape {
   static constexpr int QB = 4 * TPW;    // tokens per workgroup
 };
 
+// Only the groupings with a kernel instance (prefill_impl) report a block
+// size; for the others the planner sends every chunk to split-K attention.
 int prefill_block_tokens(int group) {
   switch (group) {
-    case 1: return PrefillShape<1>::QB;
-    case 2: return PrefillShape<2>::QB;
     case 4: return PrefillShape<4>::QB;
     case 8: return PrefillShape<8>::QB;
-    case 16: return PrefillShape<16>::QB;
     default: return 0;
   }
 }

@@ -98,12 +98,13 @@ def stored(x, dtype):
     return bf16(x) if dtype == "bf16" else x.astype(np.float32).astype(np.float64)
 
 
-def moe_token(hn, W, shape, force=None):
+def moe_token(hn, W, shape, force=None, kv_only=False):
     """The router reads hn itself; the experts read its stored copy and store
-    their SwiGLU activations."""
+    their SwiGLU activations (kv_only: neither is rounded)."""
     f = lambda k: np.asarray(W[k], dtype=np.float64)
+    act = (lambda x, dt: np.asarray(x, np.float64)) if kv_only else stored
     logits = f("w_r") @ hn + f("b_r")
-    hs = stored(hn, shape.dtype)
+    hs = act(hn, shape.dtype)
     lf = logits.astype(np.float32)
     order = np.argsort(-lf, kind="stable")
     sel = order[: shape.top_k] if force is None else np.asarray(force)
@@ -112,8 +113,8 @@ def moe_token(hn, W, shape, force=None):
     acc = np.zeros(shape.hidden)
     for e, we in zip(sel, w):
         gu = f("w_gu")[e] @ hs + f("b_gu")[e]
-        a = stored(swiglu(gu[0::2], gu[1::2], shape.swiglu_alpha, shape.swiglu_limit, shape.swiglu_beta),
-                   shape.dtype)
+        a = act(swiglu(gu[0::2], gu[1::2], shape.swiglu_alpha, shape.swiglu_limit, shape.swiglu_beta),
+                shape.dtype)
         acc += we * (f("w_d")[e] @ a + f("b_d")[e])
     return acc, sel, w, logits
 
@@ -125,16 +126,18 @@ def weights_np(W):
     return out
 
 
-def decode_layer(wl):
-    """Whole step, dense. Returns dict(out, o, h1, idx, w, q)."""
+def decode_layer(wl, kv_only=False):
+    """Whole step, dense. Returns dict(out, o, h1, idx, w, q). kv_only: only
+    the cache entries are rounded to the layer dtype, no activation."""
     s = wl.shape
+    act = (lambda x, dt: np.asarray(x, np.float64)) if kv_only else stored
     W = weights_np(wl.weights)
     x = wl.x_in.double().numpy()
     T = x.shape[0]
     kl, vl = pool_to_logical(wl.k_pool.float().numpy().astype(np.float64),
                              wl.v_pool.float().numpy().astype(np.float64))
     d, Hq, Hkv = s.head_dim, s.n_q_heads, s.n_kv_heads
-    xn = stored(rmsnorm(x, W["g1"], s.rms_eps), s.dtype)
+    xn = act(rmsnorm(x, W["g1"], s.rms_eps), s.dtype)
     qkv = xn @ W["w_qkv"].T + W["b_qkv"]
     A = Hq * d
     cu = wl.cu_q
@@ -155,22 +158,22 @@ def decode_layer(wl):
         for i, r in enumerate(range(r0, r1)):
             p = L0 + i
             row = qkv[r]
-            q = stored(rope(row[:A].reshape(Hq, d), p, W["rope_cos"], W["rope_sin"]), s.dtype)
+            q = act(rope(row[:A].reshape(Hq, d), p, W["rope_cos"], W["rope_sin"]), s.dtype)
             k = stored(rope(row[A:A + Hkv * d].reshape(Hkv, d), p, W["rope_cos"], W["rope_sin"]), s.dtype)
             v = stored(row[A + Hkv * d:].reshape(Hkv, d), s.dtype)
             Kd[p], Vd[p] = k, v
             q_all[r] = q
         for i, r in enumerate(range(r0, r1)):
             p = L0 + i
-            o_all[r] = stored(attention_dense(q_all[r], Kd, Vd, p, s.window, W["sinks"],
-                                              1.0 / np.sqrt(d)).reshape(-1), s.dtype)
+            o_all[r] = act(attention_dense(q_all[r], Kd, Vd, p, s.window, W["sinks"],
+                                           1.0 / np.sqrt(d)).reshape(-1), s.dtype)
     h1 = x + o_all @ W["w_o"].T + W["b_o"]
     hn = rmsnorm(h1, W["g2"], s.rms_eps)
     out = np.zeros_like(h1)
     idx = np.zeros((T, s.top_k), dtype=np.int64)
     ws = np.zeros((T, s.top_k))
     for t in range(T):
-        acc, sel, w, _ = moe_token(hn[t], W, s)
+        acc, sel, w, _ = moe_token(hn[t], W, s, kv_only=kv_only)
         out[t] = h1[t] + acc
         idx[t], ws[t] = sel, w
     return dict(out=out, o=o_all, h1=h1, idx=idx, w=ws, q=q_all)

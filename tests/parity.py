@@ -49,3 +49,21 @@ def check_router(gpu_idx, ref_idx, ref_logits, k):
     bad = (~tie) & (g != r).any(1)
     assert not bad.any(), f"router sets differ at tokens {np.nonzero(bad)[0][:10]}"
     return tie
+
+
+def bf16_ulp(x):
+    """Spacing of bfloat16 numbers at |x| (normal range; 2^-133 below it)."""
+    a = np.abs(np.asarray(x, np.float64))
+    e = np.floor(np.log2(np.maximum(a, 2.0 ** -126)))
+    return np.exp2(e - 7)
+
+
+def weights_by_expert(gpu_idx, gpu_w, ref_idx, ref_w):
+    """Top-k weights of both sides in ascending expert order per token (the
+    sets must already agree), for element-wise comparison."""
+    gi, ri = np.asarray(gpu_idx), np.asarray(ref_idx)
+    go, ro = np.argsort(gi, 1, kind="stable"), np.argsort(ri, 1, kind="stable")
+    gs, rs = np.take_along_axis(gi, go, 1), np.take_along_axis(ri, ro, 1)
+    assert (gs == rs).all(), "expert sets differ"
+    return (np.take_along_axis(np.asarray(gpu_w, np.float64), go, 1),
+            np.take_along_axis(np.asarray(ref_w, np.float64), ro, 1))

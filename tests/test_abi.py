@@ -68,7 +68,8 @@ def test_page_allocator_all_or_nothing_and_double_free():
     assert L.kv_pages_free(h, 2, ids.ctypes.data) == 0
     assert L.kv_pages_alloc(h, 3, out.ctypes.data) == 0
     np.testing.assert_array_equal(out[:3], [1, 3, 4])         # lowest free ids first
-    assert "not allocated" in L.mcpu_last_error().decode() or True
+    assert L.kv_pages_free(h, 1, np.array([9], np.int32).ctypes.data) == mcpu.MCPU_EINVAL
+    assert "not allocated" in L.mcpu_last_error().decode()
     L.kv_pool_destroy(h)
 
 
@@ -96,3 +97,98 @@ def test_packed_weights_size_and_argument_checks():
     assert L.mcpu_pack_weights(mcpu.MCPU_BF16, None, b, 1, 16, 64, None) == mcpu.MCPU_EINVAL
     assert L.mcpu_pack_weights(mcpu.MCPU_BF16, a + 8, b, 1, 16, 64, None) == mcpu.MCPU_EINVAL  # misaligned
     assert L.mcpu_pack_weights(mcpu.MCPU_BF16, a, a + 1024, 1, 16, 64, None) == mcpu.MCPU_EINVAL  # overlap
+
+
+# dummy device addresses: never dereferenced, every call below returns on the host
+_DUMMY = 1 << 32
+
+
+def _dummy_weights(mxfp4=False, drop=None):
+    names = [n for n, _ in mcpu.LayerWeights._fields_ if n != "rope_max_pos"]
+    kw = {n: _DUMMY + 4096 * i for i, n in enumerate(names)}
+    kw["w_gu_packed"] = kw["w_d_packed"] = None
+    if not mxfp4:
+        kw["s_gu"] = kw["s_d"] = None
+    if drop:
+        kw[drop] = None
+    return mcpu.LayerWeights(rope_max_pos=4096, **kw)
+
+
+def _decode_call(shape, w, ws_bytes, x_in=_DUMMY + (1 << 24), page_table=_DUMMY + (2 << 24), pool=None):
+    L = mcpu.lib()
+    cfg = mcpu.make_cfg(shape)
+    if pool is None:
+        rc, pool = _fake_pool(shape, 64)
+        assert rc == 0
+    hs = np.array([5, 17, 40], np.int32)
+    rc = L.decode_layer(ctypes.byref(cfg), ctypes.byref(w), pool, 3, page_table, 8, _DUMMY + (3 << 24), None,
+                        hs.ctypes.data, None, x_in, _DUMMY + (4 << 24), None, None, None,
+                        _DUMMY + (5 << 24), ws_bytes, None)
+    return rc
+
+
+def test_decode_layer_rejects_null_pointers_and_small_workspace():
+    """Host-detected errors return before any launch (mcpu.h): NULL weight and
+    buffer pointers give MCPU_EINVAL, a workspace below
+    decode_layer_workspace_size gives MCPU_ENOMEM, each with a message."""
+    L = mcpu.lib()
+    s = W.TINY
+    need = mcpu.decode_layer_workspace_size(s, 3, 3)
+    for name in ("g1", "w_qkv", "w_o", "rope_cos", "g2", "w_r", "w_gu", "b_d"):
+        assert _decode_call(s, _dummy_weights(drop=name), need) == mcpu.MCPU_EINVAL, name
+        assert "NULL" in L.mcpu_last_error().decode()
+    assert _decode_call(s, _dummy_weights(), need, x_in=None) == mcpu.MCPU_EINVAL
+    assert _decode_call(s, _dummy_weights(), need, page_table=None) == mcpu.MCPU_EINVAL
+    # MXFP4 experts without their scale arrays
+    mx = replace(W.GPT_OSS_20B, expert_fmt="mxfp4")
+    w = _dummy_weights(mxfp4=True, drop="s_gu")
+    assert _decode_call(mx, w, mcpu.decode_layer_workspace_size(mx, 3, 3)) == mcpu.MCPU_EINVAL
+    assert "scale" in L.mcpu_last_error().decode()
+    # workspace one byte short
+    assert _decode_call(s, _dummy_weights(), need - 1) == mcpu.MCPU_ENOMEM
+    assert "workspace" in L.mcpu_last_error().decode()
+    # the pool of another layer shape
+    rc, other = _fake_pool(replace(W.TINY, head_dim=64), 64)
+    assert rc == 0
+    assert _decode_call(s, _dummy_weights(), need, pool=other) == mcpu.MCPU_EINVAL
+
+
+def test_moe_forward_rejects_null_pointers_and_small_workspace():
+    L = mcpu.lib()
+    s = W.TINY
+    cfg = mcpu.make_cfg(s)
+    need = mcpu.moe_forward_workspace_size(s, 10)
+
+    def call(w, h=_DUMMY + (1 << 24), out=_DUMMY + (2 << 24), ws=_DUMMY + (3 << 24), nbytes=need, n=10):
+        return L.moe_forward(ctypes.byref(cfg), ctypes.byref(w), n, h, out, None, None, None, ws, nbytes, None)
+
+    for name in ("g2", "w_r", "b_r", "w_gu", "b_gu", "w_d", "b_d"):
+        assert call(_dummy_weights(drop=name)) == mcpu.MCPU_EINVAL, name
+    assert call(_dummy_weights(), h=None) == mcpu.MCPU_EINVAL
+    assert call(_dummy_weights(), out=None) == mcpu.MCPU_EINVAL
+    assert call(_dummy_weights(), ws=None) == mcpu.MCPU_EINVAL
+    assert call(_dummy_weights(), nbytes=need - 256) == mcpu.MCPU_ENOMEM
+    assert call(_dummy_weights(), n=-1) == mcpu.MCPU_EINVAL
+    assert call(_dummy_weights(), h=None, n=0) == mcpu.MCPU_OK   # nothing to do, nothing launched
+
+
+def test_paged_attention_rejects_mismatched_cu_q_and_small_workspace():
+    L = mcpu.lib()
+    s = W.TINY
+    cfg = mcpu.make_cfg(s)
+    rc, pool = _fake_pool(s, 64)
+    assert rc == 0
+    hs = np.array([5, 17], np.int32)
+    hc = np.array([0, 1, 2], np.int32)
+    need = mcpu.paged_attention_workspace_size(s, 2, 2)
+    d = _DUMMY
+    # cu_q given without its host copy
+    assert L.paged_attention(ctypes.byref(cfg), None, pool, 2, d, 8, d, d, hs.ctypes.data, None, d, d, d, need,
+                             None) == mcpu.MCPU_EINVAL
+    assert L.paged_attention(ctypes.byref(cfg), None, pool, 2, d, 8, d, d, hs.ctypes.data, hc.ctypes.data, d, d,
+                             d, need - 1, None) == mcpu.MCPU_ENOMEM
+    # a position beyond the page table's width
+    far = np.array([5, 8 * 16], np.int32)
+    assert L.paged_attention(ctypes.byref(cfg), None, pool, 2, d, 8, d, None, far.ctypes.data, None, d, d, d,
+                             need, None) == mcpu.MCPU_EINVAL
+    assert "beyond page table" in L.mcpu_last_error().decode()

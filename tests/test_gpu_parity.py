@@ -69,15 +69,23 @@ def compare_layer(wl, gpu, step=None, ref=None):
     PT.check("moe", gpu["out"] - gpu["h1"], ref["out"] - ref["h1"], dt)
     PT.check("out", gpu["out"], ref["out"], dt)
     np.testing.assert_allclose(gpu["w"].sum(1), 1.0, rtol=1e-5)
+    PT.check("topk_w", *PT.weights_by_expert(gpu["idx"], gpu["w"], ref["idx"], ref["w"]), dt)
     if step is not None:
         check_appended(wl, step, ref)
     return ref
 
 
 def check_appended(wl, step, ref):
-    """New keys/values in the device pools against the reference's, at the
-    layer tolerance (the GPU feeds the projection bf16-rounded activations,
-    so its k/v differ from the fp64 reference by more than one storage ulp)."""
+    """New keys/values in the device pools against the reference's. Both sides
+    round the normalised row to bf16 and project it; they differ in the
+    projection's summation order (fp32 vs float64) before rounding to the
+    cache dtype, which moves an entry by at most one bf16 ulp. Where the two
+    RMSNorms (fp32 vs float64) straddle a bf16 rounding boundary of one
+    element of the normalised row, every k and v of that token also moves by
+    |w| x ulp(xn) (about 1e-4, at most about 1.5e-3). So every entry is
+    within max(1 bf16 ulp, 2e-3) of the reference's (one ulp from magnitude
+    0.5 up); the share of entries beyond one ulp is printed. An fp32 cache is
+    held to the fp32 bar."""
     s = wl.shape
     kp = step.k_pool.cpu().float().numpy()
     vp = step.v_pool.cpu().float().numpy()
@@ -92,8 +100,18 @@ def check_appended(wl, step, ref):
             slot = pos % 16
             got_k.append(kl[0, :, slot]); want_k.append(krl[0, :, slot])
             got_v.append(vl[0, :, slot]); want_v.append(vrl[0, :, slot])
-    PT.check("appended k", np.stack(got_k), np.stack(want_k), s.dtype)
-    PT.check("appended v", np.stack(got_v), np.stack(want_v), s.dtype)
+    for name, got, want in (("k", got_k, want_k), ("v", got_v, want_v)):
+        got, want = np.stack(got), np.stack(want)
+        if s.dtype == "bf16":
+            ulp = PT.bf16_ulp(np.maximum(np.abs(got), np.abs(want)))
+            err = np.abs(got - want)
+            bad = err > np.maximum(ulp, 2e-3)
+            assert not bad.any(), f"appended {name}: {int(bad.sum())} entries beyond max(1 ulp, 2e-3), " \
+                                  f"worst {err.max():.3e}"
+            print(f"  appended {name}: {float((err > ulp).mean()):.2e} of entries beyond one bf16 ulp "
+                  f"(max {float((err / ulp).max()):.2f} ulps)")
+        else:
+            PT.check(f"appended {name}", got, want, s.dtype)
 
 
 # ---------------------------------------------------------------------------------- tiny fp32
@@ -212,6 +230,44 @@ def test_attention_page_permutation_bitwise():
     np.testing.assert_array_equal(a, b)
 
 
+def test_attention_split_count_invariance_fp32():
+    """The same query over the same pages, in batches whose total length makes
+    the planner cut its 188 pages into 12, 6 and 2 splits (16, 37 and 184
+    pages per split): the fp32 results agree within 1e-6 relative, and with
+    the reference at the fp32 bar. Filler queries share one run of pages, so
+    the batch is long without a large pool."""
+    s = replace(W.TINY, window=0)
+    ctx = 3000                                   # 188 pages
+    n_pages = 200
+    rng = np.random.default_rng(1035)
+    shp = (n_pages, s.n_kv_heads, 16, s.head_dim)
+    k_pool = torch.from_numpy(rng.standard_normal(shp).astype(np.float32))
+    v_pool = torch.from_numpy(rng.standard_normal(shp).astype(np.float32))
+    row = rng.permutation(n_pages)[:188].astype(np.int32)
+    q0 = torch.from_numpy(rng.standard_normal((1, s.n_q_heads, s.head_dim)).astype(np.float32))
+    sinks = torch.from_numpy(rng.uniform(-2, 6, s.n_q_heads).astype(np.float32))
+    pool = mcpu.KVPool(s, k_pool.cuda(), v_pool.cuda())
+    outs = []
+    for n_fill in (0, 300, 1500):
+        B = 1 + n_fill
+        pt = np.tile(row, (B, 1))
+        sl = np.full(B, ctx - 1, np.int32)       # each query at position ctx - 1 sees ctx keys
+        q = torch.cat([q0, torch.from_numpy(rng.standard_normal((n_fill, s.n_q_heads, s.head_dim))
+                                            .astype(np.float32))]) if n_fill else q0
+        o = torch.empty((B, s.attn_dim), device="cuda")
+        ws = mcpu.workspace(mcpu.paged_attention_workspace_size(s, B, B))
+        mcpu.paged_attention(s, sinks.cuda(), pool, torch.from_numpy(pt).cuda(), torch.from_numpy(sl).cuda(),
+                             None, sl, None, q.cuda(), o, ws)
+        torch.cuda.synchronize()
+        assert mcpu.mcpu_check_device_errors(ws) == 0
+        outs.append(_np(o[:1]))
+    for o in outs[1:]:
+        assert PT.rel_l2(o, outs[0]) <= 1e-6, PT.rel_l2(o, outs[0])
+    ref = O.attention(s, [0], [ctx - 1], q0, k_pool, v_pool, row[None, :], sinks).reshape(1, -1)
+    for o in outs:
+        PT.check("o(split count)", o, ref, "f32")
+
+
 def test_attention_missing_page_sets_device_error():
     wl = _bf16_small(seed=1033)
     wl.page_table[9, 3] = -1
@@ -283,6 +339,9 @@ def test_moe_forward_and_forced_selection(kind):
         f[tie] = idx.cpu().numpy()[tie]
         ref = O.moe(s, O.Weights(s, wl.weights), h, force_idx=f)
     PT.check("moe out", _np(out), ref["out"], s.dtype)
+    # the same rows in, so the weights differ only by the logits' summation order
+    gw, rw = PT.weights_by_expert(idx.cpu().numpy(), _np(wt), ref["idx"], ref["w"])
+    np.testing.assert_allclose(gw, rw, atol=1e-5, rtol=0)
     # forced selection, including a repeated expert within one token
     force = np.random.default_rng(1).integers(0, s.n_experts, size=(T, s.top_k)).astype(np.int32)
     force[0, :] = force[0, 0]
@@ -297,29 +356,31 @@ def test_moe_forward_and_forced_selection(kind):
 # ---------------------------------------------------------------------------------- full size, sampled
 
 
-def _sampled(wl, n=6):
-    order = np.argsort(wl.seq_lens)
-    pick = {int(order[0]), int(order[-1])}
-    rng = np.random.default_rng(wl.seed)
-    for b in rng.permutation(wl.batch):
-        if len(pick) >= n:
-            break
-        pick.add(int(b))
-    return sorted(pick)
-
-
 @pytest.mark.parametrize("which", ["full_b64", "sliding_b256"])
-def test_full_size_sampled(which):
+def test_full_size_every_sequence(which):
+    """The 64-sequence full-attention and the 256-sequence sliding-window
+    layers the benchmark times, every token against the reference (appended
+    K/V included). Then, as a report and not a gate, the same GPU output
+    against the reference that rounds only the cache entries (every
+    activation kept in float64): how far the result depends on rounding the
+    activations the layer stores."""
     wl = W.full_b64() if which == "full_b64" else W.sliding_b256()
     gpu, step = run_layer(wl)
-    seqs = _sampled(wl)
-    sub, rows = W.restrict(wl, seqs)
-    g = {k: v[rows] for k, v in gpu.items()}
-    ref, _ = reference(sub, g)
-    compare_layer(sub, g, None, ref)
-    # every token: finite output and weights summing to one
-    assert np.isfinite(gpu["out"]).all()
-    np.testing.assert_allclose(gpu["w"].sum(1), 1.0, rtol=1e-5)
+    ref, tie = reference(wl, gpu)
+    compare_layer(wl, gpu, step, ref)
+    kv = O.decode_layer(wl, kv_only=True)
+    k = wl.shape.top_k
+    gap_ok = ~PT.near_tie_tokens(kv["logits"], k)
+    flips = (np.sort(gpu["idx"], 1) != np.sort(kv["idx"], 1)).any(1)
+    both = ~flips
+    print(f"\n  {which}: vs the storage-rounding reference: out max-abs "
+          f"{np.abs(gpu['out'] - ref['out']).max():.3e}, rel-L2 {PT.rel_l2(gpu['out'], ref['out']):.3e}, "
+          f"near ties {int(tie.sum())}"
+          f"\n  {which}: vs the cache-only-rounding reference: out max-abs "
+          f"{np.abs(gpu['out'] - kv['out']).max():.3e}, rel-L2 {PT.rel_l2(gpu['out'], kv['out']):.3e} "
+          f"(same sets: max-abs {np.abs(gpu['out'] - kv['out'])[both].max(initial=0):.3e}), "
+          f"router set flips {int(flips.sum())} of {wl.n_tokens}, "
+          f"{int((flips & gap_ok).sum())} of them at a reference gap above 1e-3")
 
 
 # ---------------------------------------------------------------------------------- MXFP4 experts

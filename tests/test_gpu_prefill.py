@@ -38,6 +38,16 @@ def test_prefill_tiny_f32_layer():
     compare_layer(wl, gpu, step)
 
 
+@pytest.mark.parametrize("hq,hkv", [(16, 1), (4, 2)])
+def test_prefill_head_groupings_without_prefill_kernel(hq, hkv):
+    """16 and 2 query heads per KV head have no prefill-kernel instance: their
+    chunks go to split-K attention, with the same results."""
+    shape = replace(W.TINY, n_q_heads=hq, n_kv_heads=hkv)
+    wl = W.custom(shape, [0, 10, 100, 3], [20, 70, 1, 33], 1105 + hq, sink_std=1.0)
+    gpu, step = run_layer(wl)
+    compare_layer(wl, gpu, step)
+
+
 @pytest.mark.parametrize("window", [0, 128])
 def test_prefill_bf16_layer(window):
     shape = replace(W.GPT_OSS_20B, window=window)
@@ -46,10 +56,10 @@ def test_prefill_bf16_layer(window):
     compare_layer(wl, gpu, step)
 
 
-def _attention(wl, sinks, pool_k, pool_v, page_table):
+def _attention(wl, sinks, pool_k, pool_v, page_table, q_scale=1.0):
     s = wl.shape
     T = wl.n_tokens
-    q = W.synth_normal(wl.seed, 901, (T, s.n_q_heads, s.head_dim), dtype=s.torch_dtype)
+    q = W.synth_normal(wl.seed, 901, (T, s.n_q_heads, s.head_dim), std=q_scale, dtype=s.torch_dtype)
     pool = mcpu.KVPool(s, pool_k.cuda(), pool_v.cuda())
     o = torch.empty((T, s.n_q_heads * s.head_dim), dtype=s.torch_dtype, device="cuda")
     ws = mcpu.workspace(mcpu.paged_attention_workspace_size(s, wl.batch, T))
@@ -84,6 +94,24 @@ def test_prefill_attention_sink_stress_and_page_permutation(window):
     assert torch.equal(o.view(torch.int16), o2.view(torch.int16))
 
 
+@pytest.mark.parametrize("window", [0, 128])
+def test_prefill_attention_large_scores_and_extreme_sinks(window):
+    """Queries scaled x 50 (scores up to about 200, so the lazy rescale of the
+    running maximum is taken on most steps) with sinks of +30 and -30: the
+    max-subtracted softmax stays finite and matches the reference."""
+    shape = replace(W.GPT_OSS_20B, window=window)
+    wl = W.custom(shape, [0, 900, 47, 16], [96, 130, 40, 1], 1113 + window, weights=False)
+    sinks = torch.from_numpy(np.tile([30.0, -30.0, 0.5, 4.0], shape.n_q_heads // 4).astype(np.float32))
+    q, o = _attention(wl, sinks, wl.k_pool, wl.v_pool, wl.page_table, q_scale=50.0)
+    tok_seq = np.repeat(np.arange(wl.batch), wl.q_lens)
+    tok_pos = np.concatenate([wl.seq_lens[b] + np.arange(wl.q_lens[b]) for b in range(wl.batch)])
+    ref = O.attention(shape, tok_seq, tok_pos, q, wl.k_pool, wl.v_pool, wl.page_table, sinks)
+    got = o.float().numpy().reshape(ref.shape)
+    assert np.isfinite(got).all()
+    PT.check("prefill attention (q x 50, sinks +-30)", got, ref, shape.dtype)
+    assert np.abs(got[:, 1::4]).max() > 0.1   # the -30 sink heads: peaked, not averaged away
+
+
 def _run_layer_rows(wl, rows):
     """decode_layer on the whole step; only the given token rows come back."""
     step = mcpu.DeviceStep(wl)
@@ -116,4 +144,30 @@ def test_mixed_step_full_size_sampled():
     g, finite, wsum_ok = _run_layer_rows(wl, rows)
     assert finite and wsum_ok
     ref, _ = reference(sub, g)
+    compare_layer(sub, g, None, ref)
+
+
+def test_mixed_step_full_size_longest_chunk_sampled():
+    """The full-size mixed step on the prefill sequence with the longest
+    context among those adding at least 2048 tokens: every chunk token is
+    appended by the reference, and a seeded subset of its rows (first, last
+    and eight others) goes through attention, the output projection and the
+    MoE, so the chunk's ring of pages is compared at full depth."""
+    wl = W.mixed_prefill()
+    pre = np.nonzero(wl.q_lens >= 2048)[0]
+    b = int(pre[np.argmax(wl.seq_lens[pre])])
+    sub, rows = W.restrict(wl, [b])
+    n = int(wl.q_lens[b])
+    rng = np.random.default_rng(1114)
+    local = np.unique(np.concatenate([[0, n - 1], rng.choice(n, 8, replace=False)])).astype(np.int32)
+    g, finite, wsum_ok = _run_layer_rows(wl, np.asarray(rows)[local])
+    assert finite and wsum_ok
+    print(f"  sequence {b}: {int(wl.seq_lens[b])} cached + {n} new tokens, rows {local.tolist()}")
+    ref = O.decode_layer(sub, rows=local)
+    tie = PT.check_router(g["idx"], ref["idx"], ref["logits"], sub.shape.top_k)
+    if tie.any():
+        force = np.zeros((sub.n_tokens, sub.shape.top_k), np.int32)
+        force[local] = ref["idx"]
+        force[local[tie]] = g["idx"][tie]
+        ref = O.decode_layer(sub, rows=local, force_idx=force)
     compare_layer(sub, g, None, ref)

@@ -406,6 +406,41 @@ def test_decode_layer_matches_dense_bruteforce(kind):
     np.testing.assert_allclose(r["out"], ref["out"], rtol=1e-10, atol=1e-11)
 
 
+@pytest.mark.parametrize("kind", ["bf16_small", "bf16_window"])
+def test_decode_layer_cache_only_rounding_matches_dense_bruteforce(kind):
+    """The reporting mode that rounds only the cache entries (no stored
+    activations) against the dense brute force with the same rule; it must
+    differ from the default mode (the rounding points are real)."""
+    from dataclasses import replace
+    shape = replace(W.GPT_OSS_20B, hidden=192, n_q_heads=8, n_kv_heads=2, head_dim=64,
+                    n_experts=8, top_k=3, ffn_dim=96, window=128 if kind == "bf16_window" else 0)
+    wl = W.custom(shape, [3, 16, 130, 257], [1, 3, 1, 2], 33, sink_std=1.0)
+    r = O.decode_layer(wl, kv_only=True)
+    ref = BF.decode_layer(wl, kv_only=True)
+    np.testing.assert_allclose(r["q"], ref["q"], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(r["o"], ref["o"], rtol=1e-10, atol=1e-12)
+    np.testing.assert_array_equal(r["idx"], ref["idx"])
+    np.testing.assert_allclose(r["out"], ref["out"], rtol=1e-10, atol=1e-11)
+    assert np.abs(r["out"] - O.decode_layer(wl)["out"]).max() > 1e-6
+
+
+def test_decode_layer_row_subset_equals_full_step():
+    """Evaluating a subset of rows (every token still appended) returns exactly
+    the full step's values at those rows, including a forced selection."""
+    from dataclasses import replace
+    shape = replace(W.TINY, window=0)
+    wl = W.custom(shape, [33, 0, 60, 7], [5, 20, 1, 3], 44)
+    full = O.decode_layer(wl)
+    rows = np.array([0, 4, 6, 24, 27])
+    sub = O.decode_layer(wl, rows=rows)
+    for k in ("out", "q", "o", "h1", "idx", "w", "logits", "moe"):
+        np.testing.assert_array_equal(sub[k], full[k][rows], err_msg=k)
+    np.testing.assert_array_equal(sub["k_pool"], full["k_pool"])
+    force = np.tile(np.arange(shape.top_k, dtype=np.int32), (wl.n_tokens, 1))
+    fsub = O.decode_layer(wl, rows=rows, force_idx=force)
+    np.testing.assert_array_equal(fsub["out"], O.decode_layer(wl, force_idx=force)["out"][rows])
+
+
 def test_decode_layer_chunk_equals_sequential_decode():
     from dataclasses import replace
     shape = replace(W.TINY, window=0)
