@@ -147,6 +147,23 @@ def cpu_cores():
     return int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
 
 
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo), for the CPU baseline."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+# Writing this many bytes between timed steps evicts the previous step's data
+# from the L2 caches and the 256 MB memory-side cache (MALL), so every step
+# reads its weights and cache pages from HBM.
+FLUSH_BYTES = 1 << 30
+
+
 class LayerBench:
     """One decoder layer over a batch (decode_layer once per step)."""
 
@@ -202,7 +219,7 @@ class LayerBench:
         weights = O.Weights(sub.shape, sub.weights)
         passes, dt = timed_passes(lambda: O.decode_layer(sub, weights))
         return {"value": round(passes * sub.n_tokens / dt, 3), "unit": "tokens/s (all tokens of the sample)",
-                "cores": cpu_cores(), "kind": "oracle",
+                "cores": cpu_cores(), "cpu": cpu_model(), "kind": "oracle",
                 "sample": f"{len(seqs)} of {wl.batch} sequences (seeded), {sub.n_tokens} tokens, one layer step, "
                           f"{passes} passes in {dt:.2f} s wall"}
 
@@ -255,7 +272,8 @@ class StackBench:
         t0 = time.perf_counter()
         OS.reference_stack(spec, seqs)
         dt = time.perf_counter() - t0
-        return {"value": round(len(seqs) / dt, 4), "unit": "tokens/s", "cores": cpu_cores(), "kind": "oracle",
+        return {"value": round(len(seqs) / dt, 4), "unit": "tokens/s", "cores": cpu_cores(), "cpu": cpu_model(),
+                "kind": "oracle",
                 "sample": f"{len(seqs)} of {spec.batch} sequences (seeded, contexts "
                           f"{', '.join(str(int(spec.seq_lens[i])) for i in seqs)}) through all {spec.n_layers} "
                           f"layers, pages and used experts regenerated on the host, {dt:.2f} s wall"}
@@ -266,7 +284,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default 50; 5 for a stack or mixed step)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 10; 2 for a stack or mixed step)")
-    ap.add_argument("--workload", default="full_b64")
+    ap.add_argument("--workload", default="sliding_b256")
+    ap.add_argument("--no-flush", action="store_true", help="do not evict the caches between timed steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="after the benchmark, run 5 device-to-device copies of MIB MiB, the "
@@ -296,12 +315,19 @@ def main():
     if bench.errors():
         raise SystemExit("device error during warm-up")
 
+    flush = None if args.no_flush else torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
+
+    def evict(i):
+        if flush is not None:
+            flush.fill_(i & 0xFF)
+
     # per-kernel breakdown (microseconds per step, all launches), untimed pass
     nb = min(K, 20)
     cap = 4 * nb * bench.launches
     for k in mcpu.KERNELS:
         mcpu.mcpu_timing_start(k, cap)
-    for _ in range(nb):
+    for i in range(nb):
+        evict(i)
         bench.run()
     torch.cuda.synchronize()
     breakdown = {}
@@ -321,22 +347,27 @@ def main():
     # timed region: HIP events around the dominant kernel's launches
     n_launch = K * bench.launches
     mcpu.mcpu_timing_start(dominant, n_launch)
+    # each step between its own event pair; the cache eviction runs between
+    # steps, outside the events
     stream = torch.cuda.current_stream()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(K):
+    for i, (a, b) in enumerate(evs):
+        evict(i)
+        a.record(stream)
         bench.run()
-    ev1.record(stream)
+        b.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_step = ev0.elapsed_time(ev1) / K
+    step_ms = np.array([a.elapsed_time(b) for a, b in evs], np.float64)
+    ms_step = float(step_ms.mean())
     dom_ms = np.asarray(mcpu.mcpu_timing_read(dominant, n_launch), np.float64)
     mcpu.mcpu_timing_start(dominant, 0)
     if bench.errors():
         raise SystemExit("device error during timing")
-    log(f"timed {K} steps: {ms_step * 1e3:.1f} us/step (wall {wall / K * 1e6:.1f} us/step)")
+    log(f"timed {K} steps: {ms_step * 1e3:.1f} us/step mean, median {np.median(step_ms) * 1e3:.1f} "
+        f"(wall {wall / K * 1e6:.1f} us/step with cache eviction)")
 
     cols = bench.dominant_launches(dominant)
     per = dom_ms.reshape(K, -1)[:, cols]
@@ -369,7 +400,9 @@ def main():
     decode_tokens = t_dec if t_pre else bench.tokens
     out = {
         "metric": METRIC, "value": round(decode_tokens / (ms_step * 1e-3), 1), "unit": "tokens/s",
-        "n_gpus": 1, "steps": K, "warmup": warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True,
+        "n_gpus": 1, "steps": K, "warmup": warmup, "ms_per_step": round(ms_step, 4),
+        "ms_per_step_p10_p50_p90": [round(float(np.percentile(step_ms, p)), 4) for p in (10, 50, 90)],
+        "caches_evicted_between_steps": flush is not None, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": bench.shape.dtype, "data": "synthetic",
         "config": bench.config(),
         "roofline": roofline,
