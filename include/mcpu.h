@@ -72,8 +72,9 @@ enum {
   MCPU_DEVERR_ROPE = 2,  /* a position was >= rope_max_pos; that token's q/k were not written */
   MCPU_DEVERR_EXPERT = 4, /* a top-k expert id outside [0, n_experts) was passed in */
   MCPU_DEVERR_PLAN = 8,   /* device seq_lens / cu_q disagree with the host copies */
-  MCPU_DEVERR_MXFP4 = 16  /* an MXFP4 block scale outside [2, 252]: scaled values would not be
+  MCPU_DEVERR_MXFP4 = 16, /* an MXFP4 block scale outside [2, 252]: scaled values would not be
                              normal bfloat16; that block contributed zero */
+  MCPU_DEVERR_TOKEN = 32  /* a token id outside [0, vocab) (embed_tokens); its row was zeroed */
 };
 
 /* Layer configuration (host struct, by value semantics).
@@ -246,6 +247,59 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
                  float* topk_w, const mcpu_taps* taps, void* workspace, size_t ws_bytes,
                  hipStream_t stream);
 
+/* ---- Generation around the layer stack --------------------------------- */
+/* The Run stage generates each trajectory's next tokens at the rollout
+ * temperature (0.7 in the paper's training details) and, for the GRPO update,
+ * scores whole trajectories under the policy (Sec. 3.2 on the rollout
+ * pipeline; Sec. 4 and its training-details appendix). These calls supply the
+ * two ends of the stack for that: token embedding in front of it, the final
+ * RMSNorm, the vocabulary projection and sampling behind it. */
+
+/* Vocabulary head (host struct; device pointers owned by the caller).
+ *  hidden H (multiple of 64), vocab V (multiple of 16), V * H * 2 < 2^31.
+ *  g_final [H] fp32 RMSNorm gain; w_lm [V, H] bf16 row-major (the unembedding,
+ *  no bias); w_lm_packed: optional (NULL) streaming-order copy of w_lm
+ *  (mcpu_pack_weights with n_groups 1), read by few-row batches. */
+typedef struct mcpu_lm_head {
+  int32_t hidden, vocab;
+  float rms_eps;
+  const float* g_final;
+  const void* w_lm;
+  const void* w_lm_packed;
+} mcpu_lm_head;
+
+/* Next-token sampling and log-probabilities for n_tokens rows.
+ *  x [T, H] fp32 residual rows (the stack's output for each row's last token).
+ *  xn = RMSNorm(x; g_final) stored as bf16; logits l = xn . w_lm^T (fp32
+ *  accumulation); s = l / temperature.
+ *  temperature > 0: the sampled token is argmax_v (s_v + g_v) (the Gumbel-max
+ *    form of drawing from softmax(s)), g_v = -log(-log u_v), u_v = ((w >> 9) +
+ *    1/2) / 2^23 with w word v % 4 of Philox4x32-10 (key = seed low, high
+ *    32 bits) at counter (v / 4, positions[t], seq_ids[t], 0x4C4D5330); so a
+ *    row's draw depends only on (seed, sequence id, position), never on the
+ *    batch it is in. Equal perturbed scores go to the lower id.
+ *  temperature <= 0: greedy, argmax_v l_v (lower id on ties); s = l.
+ *  Outputs (device, [T], each nullable): tokens_out the chosen id,
+ *  logprob_out its log-probability s_tok - logsumexp(s), lse_out logsumexp(s),
+ *  target_logprob_out s_target - logsumexp(s) for targets[t] (device [T],
+ *  nullable; ids in [0, V), else the value is -inf).
+ *  seq_ids / positions: device int32 [T], required when sampling.
+ *  workspace >= lm_head_workspace_size(H, V, T) bytes (first 256 bytes: the
+ *  error word, as for decode_layer). Host-detected errors launch nothing. */
+size_t lm_head_workspace_size(int32_t hidden, int32_t vocab, int32_t max_tokens);
+int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, float temperature, uint64_t seed,
+                   const int32_t* seq_ids, const int32_t* positions, const int32_t* targets, int32_t* tokens_out,
+                   float* logprob_out, float* target_logprob_out, float* lse_out, void* workspace,
+                   size_t ws_bytes, hipStream_t stream);
+
+/* Token embedding: x_out[t] = table[tokens[t]] widened to fp32.
+ *  table [vocab, hidden] bf16 (16-byte aligned), tokens device int32 [T],
+ *  x_out [T, hidden] fp32 (16-byte aligned), hidden a multiple of 8. An id
+ *  outside [0, vocab) writes a zero row and sets MCPU_DEVERR_TOKEN in the
+ *  workspace's error word (workspace >= 256 bytes). */
+int embed_tokens(const void* table, int32_t vocab, int32_t hidden, int32_t n_tokens, const int32_t* tokens,
+                 float* x_out, void* workspace, size_t ws_bytes, hipStream_t stream);
+
 /* Kernel timing, a profiling aid. mcpu_timing_start(kernel, n) arms the
  * library to record a HIP event pair on the launching stream around each of
  * the next n launches of that kernel (n = 0 disarms it); mcpu_timing_read
@@ -266,7 +320,8 @@ enum {
   MCPU_KERNEL_MOE_COMBINE = 10,
   MCPU_KERNEL_KV_APPEND = 11,
   MCPU_KERNEL_ATTN_PREFILL = 12, /* chunked-prefill attention */
-  MCPU_KERNEL_COUNT = 13
+  MCPU_KERNEL_LM_HEAD = 13,      /* vocabulary projection + sampling summaries */
+  MCPU_KERNEL_COUNT = 14
 };
 int mcpu_timing_start(int kernel, int n);
 int mcpu_timing_read(int kernel, float* ms, int n, int* n_recorded);

@@ -255,6 +255,35 @@ __device__ __forceinline__ void ones(Frag4<bf16>& f) { f.v = make_uint2(0x3F803F
 __device__ __forceinline__ void ones(Frag4<float>& f) { f.v = make_float4(1.f, 1.f, 1.f, 1.f); }
 
 // ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as
+// easy as 1, 2, 3", SC 2011): ten rounds of two 32 x 32 -> 64-bit products
+// with the multipliers 0xD2511F53 and 0xCD9E8D57, the key bumped by the Weyl
+// constants 0x9E3779B9 and 0xBB67AE85 between rounds.
+struct U32x4 {
+  uint32_t x, y, z, w;
+};
+__device__ __forceinline__ U32x4 philox4x32_10(U32x4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) {
+      k0 += 0x9E3779B9u;
+      k1 += 0xBB67AE85u;
+    }
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+    c = U32x4{hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0};
+  }
+  return c;
+}
+
+// Gumbel noise from a 32-bit draw: u = (top 23 bits + 1/2) / 2^23, strictly
+// inside (0, 1) and exact in binary32, then g = -log(-log u); -log u is taken
+// as -log1p(u - 1) (u - 1 is exact), so it keeps full precision as u -> 1.
+__device__ __forceinline__ float gumbel_of(uint32_t w) {
+  const float u = ((float)(w >> 9) + 0.5f) * 0x1p-23f;
+  return -logf(-log1pf(u - 1.0f));
+}
+
 // page format (see include/mcpu.h)
 // ---------------------------------------------------------------------------
 

@@ -6,6 +6,7 @@
 //   EPI_RESIDUAL + bias + residual (fp32), e.g. h1 = x + o W_o^T + b_o
 //   EPI_SWIGLU   + bias, gate/up pairs (rows 2j, 2j+1) -> clamped SwiGLU
 //   EPI_BIAS     + bias (fp32)
+//   EPI_LOGITS   vocabulary logits -> per-row, per-64-column sampling summaries
 #pragma once
 #include "device.h"
 #include "kernels.h"
@@ -252,6 +253,59 @@ __device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mro
         const float up = cr[m * ld + 16 * b + 2 * j + 1] + bias[col + 1];
         Elem<T>::store(out, (int64_t)(m0 + m) * half_n + (blk0 + b) * 8 + j,
                        swiglu(gate, up, P.swiglu_alpha, P.swiglu_limit, P.swiglu_beta));
+      }
+    }
+  } else if constexpr (EPI == EPI_LOGITS) {
+    // Sixteen lanes per (row, 64-column slot), four consecutive columns each
+    // (one Philox draw gives their four noise words): the slot's maximum of s,
+    // its sum of exp(s - max), the largest s + g with its column (lowest
+    // column on equal values) and the target's s, reduced across the sixteen
+    // lanes and stored as one LogitSlot.
+    LogitSlot* out = reinterpret_cast<LogitSlot*>(P.out);
+    const int n_slots = (P.n + LOGIT_SLOT - 1) / LOGIT_SLOT;
+    const int nslot = (nblk * 16 + LOGIT_SLOT - 1) / LOGIT_SLOT, c_end = (blk0 + nblk) * 16;
+    const int sub = tid & 15;
+    const float NEG = -__builtin_inff();
+    for (int it = tid >> 4; it < mrows * nslot; it += nt >> 4) {
+      const int m = it / nslot, j = it - m * nslot, row = m0 + m;
+      const int c0 = blk0 * 16 + j * LOGIT_SLOT + 4 * sub;
+      const float* cp = cr + m * ld + j * LOGIT_SLOT + 4 * sub;
+      float sv[4], g[4] = {0.f, 0.f, 0.f, 0.f};
+      if (!P.greedy && c0 < c_end) {
+        const U32x4 r = philox4x32_10(U32x4{(uint32_t)(c0 >> 2), (uint32_t)P.row_pos[row], (uint32_t)P.row_seq[row],
+                                            LOGIT_RNG_TAG},
+                                      (uint32_t)P.seed, (uint32_t)(P.seed >> 32));
+        g[0] = gumbel_of(r.x); g[1] = gumbel_of(r.y); g[2] = gumbel_of(r.z); g[3] = gumbel_of(r.w);
+      }
+      const int tgt = P.target ? P.target[row] : -1;
+      float mx = NEG, pert = NEG, sb = NEG, st = NEG;
+      int bi = 0x7FFFFFFF;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = c0 + i < c_end;
+        sv[i] = ok ? cp[i] * P.inv_temp : NEG;
+        mx = fmaxf(mx, sv[i]);
+        const float pv = sv[i] + g[i];
+        if (ok && pv > pert) { pert = pv; sb = sv[i]; bi = c0 + i; }
+        if (ok && c0 + i == tgt) st = sv[i];
+      }
+#pragma unroll
+      for (int o = 8; o; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 16));
+      float sum = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sum += c0 + i < c_end ? expf(sv[i] - mx) : 0.f;
+#pragma unroll
+      for (int o = 8; o; o >>= 1) {
+        sum += __shfl_xor(sum, o, 16);
+        const float p2 = __shfl_xor(pert, o, 16), s2 = __shfl_xor(sb, o, 16);
+        const int i2 = __shfl_xor(bi, o, 16);
+        if (p2 > pert || (p2 == pert && i2 < bi)) { pert = p2; sb = s2; bi = i2; }
+        st = fmaxf(st, __shfl_xor(st, o, 16));
+      }
+      if (sub == 0) {
+        LogitSlot r;
+        r.m = mx; r.l = sum; r.pert = pert; r.s_best = sb; r.idx = bi; r.s_tgt = st; r.pad[0] = r.pad[1] = 0.f;
+        out[(int64_t)row * n_slots + (c0 / LOGIT_SLOT)] = r;
       }
     }
   } else {  // EPI_RESIDUAL, EPI_BIAS: fp32 rows, 4 consecutive features per thread

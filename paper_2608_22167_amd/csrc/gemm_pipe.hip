@@ -530,6 +530,11 @@ hipError_t launch_gemm_pipe(int expert_fmt, const Gemm& g, hipStream_t s) {
     case EPI_QKV: PIPE_LAUNCH(EPI_QKV); break;
     case EPI_RESIDUAL: PIPE_LAUNCH(EPI_RESIDUAL); break;
     case EPI_SWIGLU: PIPE_LAUNCH(EPI_SWIGLU); break;
+    case EPI_LOGITS:  // vocabulary logits: bf16 weights only
+      if (expert_fmt != 0) return hipErrorNotSupported;
+      if (dma) hipLaunchKernelGGL((gemm_dma_kernel<EPI_LOGITS>), gd, bd, 0, s, g);
+      else hipLaunchKernelGGL((gemm_pipe_kernel<EPI_LOGITS, 0>), gd, bd, 0, s, g);
+      break;
     default: PIPE_LAUNCH(EPI_BIAS); break;
   }
 #undef PIPE_LAUNCH

@@ -422,6 +422,13 @@ hipError_t slab_launch(const Gemm& g, hipStream_t s, int64_t grid) {
     case EPI_QKV: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_QKV, SPLIT, SMT>), gd, bd, 0, s, g); break;
     case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_RESIDUAL, SPLIT, SMT>), gd, bd, 0, s, g); break;
     case EPI_SWIGLU: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_SWIGLU, SPLIT, SMT>), gd, bd, 0, s, g); break;
+    case EPI_LOGITS:  // vocabulary logits: bf16 weights, one reduction pass
+      if constexpr (WF == 0 && !SPLIT) {
+        hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_LOGITS, SPLIT, SMT>), gd, bd, 0, s, g);
+        break;
+      } else {
+        return hipErrorNotSupported;
+      }
     default: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_BIAS, SPLIT, SMT>), gd, bd, 0, s, g); break;
   }
   return hipGetLastError();

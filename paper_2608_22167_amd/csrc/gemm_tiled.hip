@@ -284,6 +284,13 @@ static hipError_t tiled_launch(const Gemm& g, hipStream_t s) {
     case EPI_QKV: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, NW, EPI_QKV, WF>), gd, bd, 0, s, g); break;
     case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, NW, EPI_RESIDUAL, WF>), gd, bd, 0, s, g); break;
     case EPI_SWIGLU: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, NW, EPI_SWIGLU, WF>), gd, bd, 0, s, g); break;
+    case EPI_LOGITS:  // vocabulary logits: bf16 weights
+      if constexpr (WF == 0) {
+        hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, NW, EPI_LOGITS, WF>), gd, bd, 0, s, g);
+        break;
+      } else {
+        return hipErrorNotSupported;
+      }
     default: hipLaunchKernelGGL((gemm_tiled_kernel<BM, BN, BK, R, NW, EPI_BIAS, WF>), gd, bd, 0, s, g); break;
   }
   return hipGetLastError();

@@ -93,7 +93,22 @@ hipError_t launch_kv_append(int dtype, int head_dim, const KvAppend& p, hipStrea
 
 // ---- weight-streaming GEMMs with fused epilogues -------------------------
 
-enum EpiKind { EPI_QKV = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_BIAS = 3 };
+enum EpiKind { EPI_QKV = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_BIAS = 3, EPI_LOGITS = 4 };
+
+// EPI_LOGITS: the output columns are vocabulary logits l (no bias). Nothing
+// [rows, n] is written; per row and 64-column slot the epilogue leaves one
+// LogitSlot record summarising s = l * inv_temp over the slot, from which
+// lm_sample_reduce forms the row's sample and log-probabilities.
+constexpr int LOGIT_SLOT = 64;
+struct LogitSlot {
+  float m;       // max of s over the slot
+  float l;       // sum of exp(s - m) over the slot
+  float pert;    // max of s + g (Gumbel noise g; g = 0 when greedy)
+  float s_best;  // s at that column
+  int32_t idx;   // that column (the lowest one on equal values)
+  float s_tgt;   // s at the row's target column if it lies in the slot, else -inf
+  float pad[2];
+};
 
 struct Gemm {
   // Y[row][n] = sum_k X[src(row)][k] * W[group][n][k], rows of a group are
@@ -136,7 +151,18 @@ struct Gemm {
   float* part;
   int32_t* part_cnt;
   int k_splits;             // set by the launcher
+  // EPI_LOGITS: LogitSlot records [rows][ceil(n / LOGIT_SLOT)] in `out`;
+  // s = l * inv_temp (greedy: inv_temp = 1 and no noise); the noise of row r,
+  // column v comes from Philox4x32-10 keyed by seed at counter
+  // (v / 4, row_pos[r], row_seq[r], LOGIT_RNG_TAG), word v % 4
+  float inv_temp;
+  int greedy;
+  uint64_t seed;
+  const int32_t* row_seq;
+  const int32_t* row_pos;
+  const int32_t* target;    // [rows] column whose s is recorded, or nullptr
 };
+constexpr uint32_t LOGIT_RNG_TAG = 0x4C4D5330u;  // counter word 3 of the sampling draws
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s);
 // LDS-tiled path (gemm_tiled.hip): bf16, k a multiple of 64, at least
 // TILED_MIN_TOTAL_ROWS rows in all and groups averaging TILED_MIN_ROWS rows;

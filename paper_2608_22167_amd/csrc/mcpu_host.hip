@@ -13,6 +13,7 @@
 
 #include "../../include/mcpu.h"
 #include "kernels.h"
+#include "kernels_lm.h"
 
 using namespace mcpu;
 
@@ -634,6 +635,76 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
     if (taps->o) HIP_TRY(hipMemcpyAsync(taps->o, o, (size_t)T * Hq * D * db, hipMemcpyDeviceToDevice, stream));
     if (taps->h1) HIP_TRY(hipMemcpyAsync(taps->h1, h1, (size_t)T * H * 4, hipMemcpyDeviceToDevice, stream));
   }
+  return MCPU_OK;
+}
+
+size_t lm_head_workspace_size(int32_t hidden, int32_t vocab, int32_t max_tokens) {
+  if (hidden <= 0 || vocab <= 0 || max_tokens < 0) return 0;
+  Carve cv(nullptr);
+  cv.take<int32_t>(2);                                                            // row range
+  cv.take_bytes((size_t)std::max(max_tokens, 1) * hidden * 2);                     // normalised rows
+  cv.take<LogitSlot>((size_t)std::max(max_tokens, 1) * ((vocab + LOGIT_SLOT - 1) / LOGIT_SLOT));
+  return (cv.off + 255) & ~size_t(255);
+}
+
+int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, float temperature, uint64_t seed,
+                   const int32_t* seq_ids, const int32_t* positions, const int32_t* targets, int32_t* tokens_out,
+                   float* logprob_out, float* target_logprob_out, float* lse_out, void* workspace,
+                   size_t ws_bytes, hipStream_t stream) {
+  if (!lm) return fail(MCPU_EINVAL, "lm is NULL");
+  const int H = lm->hidden, V = lm->vocab;
+  if (H <= 0 || H % 64 || H > 8192) return fail(MCPU_EINVAL, "hidden %d must be a multiple of 64 in (0, 8192]", H);
+  if (V <= 0 || V % 16) return fail(MCPU_EINVAL, "vocab %d must be a positive multiple of 16", V);
+  if ((int64_t)V * H * 2 >= (1LL << 31)) return fail(MCPU_EUNSUPPORTED, "vocab x hidden too large for one matrix");
+  if (!(lm->rms_eps >= 0.f)) return fail(MCPU_EINVAL, "rms_eps");
+  if (n_tokens < 0) return fail(MCPU_EINVAL, "n_tokens %d", n_tokens);
+  if (n_tokens == 0) return MCPU_OK;
+  if (!lm->g_final || !lm->w_lm || !x || !workspace) return fail(MCPU_EINVAL, "NULL pointer");
+  const bool greedy = !(temperature > 0.f);
+  if (!greedy && (!seq_ids || !positions)) return fail(MCPU_EINVAL, "sampling needs seq_ids and positions");
+  if (!greedy && !(temperature < 1e30f)) return fail(MCPU_EINVAL, "temperature %g", (double)temperature);
+  if (targets && !target_logprob_out) return fail(MCPU_EINVAL, "targets given without target_logprob_out");
+  const size_t need = lm_head_workspace_size(H, V, n_tokens);
+  if (ws_bytes < need) return fail(MCPU_ENOMEM, "workspace %zu bytes < %zu needed", ws_bytes, need);
+  Carve cv(workspace);
+  int32_t* goff = cv.take<int32_t>(2);
+  void* xn = cv.take_bytes((size_t)n_tokens * H * 2);
+  const int n_slots = (V + LOGIT_SLOT - 1) / LOGIT_SLOT;
+  LogitSlot* slots = cv.take<LogitSlot>((size_t)n_tokens * n_slots);
+
+  FinalNorm fn{};
+  fn.x = x; fn.g = lm->g_final; fn.n_tokens = n_tokens; fn.hidden = H; fn.eps = lm->rms_eps; fn.out = xn;
+  fn.group_off = goff;
+  HIP_TRY(launch_final_norm(fn, stream));
+
+  Gemm g{};
+  g.w = lm->w_lm; g.w_packed = lm->w_lm_packed; g.n = V; g.k = H; g.x = xn; g.group_off = goff;
+  g.n_rows = n_tokens; g.n_groups = 1; g.epi = EPI_LOGITS; g.out = slots; g.err = err_word(workspace);
+  g.max_rows_per_group = n_tokens; g.x_rows = n_tokens;
+  g.inv_temp = greedy ? 1.f : 1.f / temperature; g.greedy = greedy ? 1 : 0; g.seed = seed;
+  g.row_seq = seq_ids; g.row_pos = positions; g.target = targets;
+  {
+    Timed tm(MCPU_KERNEL_LM_HEAD, stream);
+    HIP_TRY(launch_gemm(MCPU_BF16, MCPU_EXPERT_DENSE, g, stream));
+  }
+  LmReduce r{};
+  r.slots = slots; r.n_rows = n_tokens; r.n_slots = n_slots; r.tokens = tokens_out; r.logprob = logprob_out;
+  r.lse = lse_out; r.target_logprob = targets ? target_logprob_out : nullptr;
+  HIP_TRY(launch_lm_reduce(r, stream));
+  return MCPU_OK;
+}
+
+int embed_tokens(const void* table, int32_t vocab, int32_t hidden, int32_t n_tokens, const int32_t* tokens,
+                 float* x_out, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (vocab <= 0 || hidden <= 0 || hidden % 8 || n_tokens < 0) return fail(MCPU_EINVAL, "bad sizes");
+  if (n_tokens == 0) return MCPU_OK;
+  if (!table || !tokens || !x_out || !workspace) return fail(MCPU_EINVAL, "NULL pointer");
+  if ((uintptr_t)table % 16 || (uintptr_t)x_out % 16) return fail(MCPU_EINVAL, "table and x_out must be 16-byte aligned");
+  if (ws_bytes < 256) return fail(MCPU_ENOMEM, "workspace smaller than 256 bytes");
+  EmbedArgs a{};
+  a.table = table; a.tokens = tokens; a.vocab = vocab; a.hidden = hidden; a.n_tokens = n_tokens; a.x = x_out;
+  a.err = err_word(workspace);
+  HIP_TRY(launch_embed(a, stream));
   return MCPU_OK;
 }
 

@@ -26,10 +26,12 @@ EXPORTED = ("mcpu_last_error", "kv_pool_create", "kv_pool_destroy", "kv_pool_fre
             "kv_pages_alloc", "kv_pages_free", "kv_pages_append", "paged_attention_workspace_size",
             "paged_attention", "moe_forward_workspace_size", "moe_forward",
             "decode_layer_workspace_size", "decode_layer", "mcpu_check_device_errors",
-            "mcpu_timing_start", "mcpu_timing_read", "mcpu_packed_weights_bytes", "mcpu_pack_weights")
+            "mcpu_timing_start", "mcpu_timing_read", "mcpu_packed_weights_bytes", "mcpu_pack_weights",
+            "lm_head_workspace_size", "lm_head_sample", "embed_tokens")
 
 KERNELS = ("attn_plan", "rmsnorm", "qkv", "attn_split", "attn_combine", "oproj", "router", "permute",
-           "expert_gu", "expert_down", "moe_combine", "kv_append", "attn_prefill")
+           "expert_gu", "expert_down", "moe_combine", "kv_append", "attn_prefill", "lm_head")
+DEVERR_TOKEN = 32
 
 
 class McpuError(RuntimeError):
@@ -50,6 +52,11 @@ class LayerWeights(ctypes.Structure):
         "g1", "w_qkv", "b_qkv", "w_o", "b_o", "g2", "w_r", "b_r", "w_gu", "b_gu", "w_d", "b_d",
         "s_gu", "s_d", "sinks", "rope_cos", "rope_sin")] + [("rope_max_pos", ctypes.c_int32)] + [
         (n, ctypes.c_void_p) for n in ("w_gu_packed", "w_d_packed")]
+
+
+class LmHead(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("g_final", ctypes.c_void_p), ("w_lm", ctypes.c_void_p), ("w_lm_packed", ctypes.c_void_p)]
 
 
 class Taps(ctypes.Structure):
@@ -90,6 +97,11 @@ def lib():
         L.mcpu_packed_weights_bytes.argtypes = [i32, i32, i32]
         L.mcpu_packed_weights_bytes.restype = sz
         L.mcpu_pack_weights.argtypes = [i32, vp, vp, i32, i32, i32, vp]
+        L.lm_head_workspace_size.argtypes = [i32, i32, i32]
+        L.lm_head_workspace_size.restype = sz
+        L.lm_head_sample.argtypes = [vp, i32, vp, ctypes.c_float, ctypes.c_uint64, vp, vp, vp, vp, vp, vp, vp,
+                                     vp, sz, vp]
+        L.embed_tokens.argtypes = [vp, i32, i32, i32, vp, vp, vp, sz, vp]
         L.mcpu_timing_start.argtypes = [i32, i32]
         L.mcpu_timing_read.argtypes = [i32, vp, i32, i32p]
         _LIB = L
@@ -299,6 +311,46 @@ def mcpu_timing_read(kernel: str, n: int) -> np.ndarray:
     rec = ctypes.c_int32(0)
     _check(lib().mcpu_timing_read(KERNELS.index(kernel), _ptr(ms), n, ctypes.byref(rec)))
     return ms[:rec.value].astype(np.float64)
+
+
+# ---------------------------------------------------------------------------
+# generation ends: embedding, vocabulary head, sampling
+# ---------------------------------------------------------------------------
+
+
+class DeviceLmHead:
+    """Final RMSNorm gain and unembedding [V, H] bf16 on the GPU, with the
+    mcpu_lm_head struct; pack=True adds the streaming-order copy that
+    few-row batches read."""
+
+    def __init__(self, g_final, w_lm, rms_eps=1e-5, device="cuda", pack=True):
+        self.g = g_final.to(device=device, dtype=torch.float32).contiguous()
+        self.w = w_lm.to(device=device, dtype=torch.bfloat16).contiguous()
+        V, H = (int(d) for d in self.w.shape)
+        self.hidden, self.vocab = H, V
+        self.packed = packed_weights(self.w.view(1, V, H)) if pack and H % 64 == 0 else None
+        self.struct = LmHead(hidden=H, vocab=V, rms_eps=rms_eps, g_final=_ptr(self.g), w_lm=_ptr(self.w),
+                             w_lm_packed=_ptr(self.packed))
+
+
+def lm_head_workspace_size(hidden, vocab, max_tokens) -> int:
+    return lib().lm_head_workspace_size(hidden, vocab, max_tokens)
+
+
+def lm_head_sample(head: DeviceLmHead, x, temperature, seed=0, seq_ids=None, positions=None, targets=None,
+                   tokens=None, logprob=None, target_logprob=None, lse=None, workspace=None, stream=None):
+    """lm_head_sample on rows x [T, H] fp32; outputs are device tensors (nullable)."""
+    T = int(x.shape[0])
+    _check(lib().lm_head_sample(ctypes.byref(head.struct), T, _ptr(x), float(temperature), int(seed),
+                                _ptr(seq_ids), _ptr(positions), _ptr(targets), _ptr(tokens), _ptr(logprob),
+                                _ptr(target_logprob), _ptr(lse), _ptr(workspace),
+                                workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def embed_tokens(table, tokens, x_out, workspace, stream=None):
+    V, H = (int(d) for d in table.shape)
+    _check(lib().embed_tokens(_ptr(table), V, H, int(tokens.shape[0]), _ptr(tokens), _ptr(x_out), _ptr(workspace),
+                              workspace.numel() * workspace.element_size(), _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

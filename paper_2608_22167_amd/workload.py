@@ -192,6 +192,34 @@ TID = dict(g1=1, w_qkv=2, b_qkv=3, w_o=4, b_o=5, g2=6, w_r=7, b_r=8, w_gu=9, b_g
            w_gu_codes=30, w_gu_scales=31, w_d_codes=32, w_d_scales=33)
 
 # --------------------------------------------------------------------------
+# the generation ends: token embedding, final RMSNorm gain, unembedding
+# (gpt-oss vocabulary of 201088 ids); the embedding rows are N(0, 1) like the
+# residual stream the layer workloads start from
+# --------------------------------------------------------------------------
+
+GPT_OSS_VOCAB = 201088
+LM_TID = dict(g_final=90, w_lm=91, embed=92)
+
+
+def lm_weights_host(seed: int, hidden: int, vocab: int, embed: bool = True) -> Dict[str, torch.Tensor]:
+    W = dict(g_final=synth_normal(seed, LM_TID["g_final"], (hidden,), std=0.02, mean=1.0),
+             w_lm=synth_normal(seed, LM_TID["w_lm"], (vocab, hidden), std=0.02, dtype=torch.bfloat16))
+    if embed:
+        W["embed"] = synth_normal(seed, LM_TID["embed"], (vocab, hidden), dtype=torch.bfloat16)
+    return W
+
+
+def lm_weights_device(seed: int, hidden: int, vocab: int, device="cuda") -> Dict[str, torch.Tensor]:
+    """The same tensors generated in HBM (the host regenerates any rows it needs)."""
+    W = dict(g_final=synth_normal(seed, LM_TID["g_final"], (hidden,), std=0.02, mean=1.0).to(device))
+    W["w_lm"] = fill_normal_device(torch.empty((vocab, hidden), dtype=torch.bfloat16, device=device), seed,
+                                   LM_TID["w_lm"], std=0.02)
+    W["embed"] = fill_normal_device(torch.empty((vocab, hidden), dtype=torch.bfloat16, device=device), seed,
+                                    LM_TID["embed"])
+    return W
+
+
+# --------------------------------------------------------------------------
 # workload
 # --------------------------------------------------------------------------
 
