@@ -247,6 +247,24 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
                  float* topk_w, const mcpu_taps* taps, void* workspace, size_t ws_bytes,
                  hipStream_t stream);
 
+/* decode_layer for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * step, arguments and results as decode_layer, but its workspace is a static
+ * device array inside the library (128 MiB per GPU, held until the process
+ * ends) instead of a caller buffer. It calls
+ * no allocating routine. A step whose decode_layer_workspace_size exceeds
+ * that returns MCPU_ENOMEM and launches nothing (gpt-oss-20b shapes: up to
+ * about 480 decode tokens). Every call on a GPU shares that GPU's array:
+ * calls that overlap on one GPU (two streams, two threads) race and must be
+ * serialised by the caller. device_errors (device int32, nullable) receives
+ * the step's device error bits (MCPU_DEVERR_*), which are then cleared, so
+ * each call reports only its own. */
+int decode_layer_noalloc(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv_pool* pool,
+                         int32_t batch, const int32_t* page_table, int32_t max_pages, const int32_t* seq_lens,
+                         const int32_t* cu_q, const int32_t* host_seq_lens, const int32_t* host_cu_q,
+                         const float* x_in, float* x_out, int32_t* topk_idx, float* topk_w, const mcpu_taps* taps,
+                         int32_t* device_errors, hipStream_t stream);
+
 /* ---- Generation around the layer stack --------------------------------- */
 /* The Run stage generates each trajectory's next tokens at the rollout
  * temperature (0.7 in the paper's training details) and, for the GRPO update,

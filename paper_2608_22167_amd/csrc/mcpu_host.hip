@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <set>
 #include <string>
 #include <vector>
@@ -705,6 +706,72 @@ int embed_tokens(const void* table, int32_t vocab, int32_t hidden, int32_t n_tok
   a.table = table; a.tokens = tokens; a.vocab = vocab; a.hidden = hidden; a.n_tokens = n_tokens; a.x = x_out;
   a.err = err_word(workspace);
   HIP_TRY(launch_embed(a, stream));
+  return MCPU_OK;
+}
+
+}  // extern "C"
+
+// ---- decode_layer without allocation ------------------------------------
+// The workspace of decode_layer_noalloc is this file-scope device array. In
+// host code its name is only a stand-in: the device address of each GPU's
+// copy comes from hipGetSymbolAddress, looked up once per device and kept.
+namespace {
+constexpr size_t SCRATCH_BYTES = size_t(128) << 20;
+static __device__ __align__(256) unsigned char scratch[SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+int scratch_for_current_device(void** out) {
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(MCPU_EUNSUPPORTED, "device %d beyond the scratch table", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr) return fail(MCPU_EHIP, "hipGetSymbolAddress returned no address for the scratch array");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return MCPU_OK;
+}
+
+// Moves the call's device error word to the caller's output (or drops it)
+// and clears it, so every call starts from zero without a memset.
+__global__ void take_errors_kernel(int32_t* word, int32_t* out) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    if (out) *out = *word;
+    *word = 0;
+  }
+}
+}  // namespace
+
+extern "C" {
+
+int decode_layer_noalloc(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv_pool* pool,
+                         int32_t batch, const int32_t* page_table, int32_t max_pages, const int32_t* seq_lens,
+                         const int32_t* cu_q, const int32_t* host_seq_lens, const int32_t* host_cu_q,
+                         const float* x_in, float* x_out, int32_t* topk_idx, float* topk_w, const mcpu_taps* taps,
+                         int32_t* device_errors, hipStream_t stream) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (batch <= 0) return fail(MCPU_EINVAL, "batch %d", batch);
+  if (!host_seq_lens) return fail(MCPU_EINVAL, "host_seq_lens is NULL");
+  if (host_cu_q && host_cu_q[batch] < 0) return fail(MCPU_EINVAL, "host_cu_q[batch] < 0");
+  const int T = host_cu_q ? host_cu_q[batch] : batch;
+  const size_t need = decode_layer_workspace_size(cfg, batch, T);
+  if (need == 0 || need > SCRATCH_BYTES)
+    return fail(MCPU_ENOMEM, "decode_layer_noalloc: this step needs %zu bytes of scratch; the static scratch "
+                "holds %zu (use decode_layer with a workspace)", need, SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((rc = scratch_for_current_device(&ws))) return rc;
+  if ((rc = decode_layer(cfg, w, pool, batch, page_table, max_pages, seq_lens, cu_q, host_seq_lens, host_cu_q, x_in,
+                         x_out, topk_idx, topk_w, taps, ws, SCRATCH_BYTES, stream)))
+    return rc;
+  hipLaunchKernelGGL(take_errors_kernel, dim3(1), dim3(64), 0, stream, err_word(ws), device_errors);
+  HIP_TRY(hipGetLastError());
   return MCPU_OK;
 }
 

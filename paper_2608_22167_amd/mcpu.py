@@ -27,7 +27,8 @@ EXPORTED = ("mcpu_last_error", "kv_pool_create", "kv_pool_destroy", "kv_pool_fre
             "paged_attention", "moe_forward_workspace_size", "moe_forward",
             "decode_layer_workspace_size", "decode_layer", "mcpu_check_device_errors",
             "mcpu_timing_start", "mcpu_timing_read", "mcpu_packed_weights_bytes", "mcpu_pack_weights",
-            "lm_head_workspace_size", "lm_head_sample", "embed_tokens")
+            "lm_head_workspace_size", "lm_head_sample", "embed_tokens", "decode_layer_noalloc")
+NOALLOC_SCRATCH_BYTES = 128 << 20  # the static scratch of decode_layer_noalloc, per GPU
 
 KERNELS = ("attn_plan", "rmsnorm", "qkv", "attn_split", "attn_combine", "oproj", "router", "permute",
            "expert_gu", "expert_down", "moe_combine", "kv_append", "attn_prefill", "lm_head")
@@ -93,6 +94,7 @@ def lib():
         L.decode_layer_workspace_size.restype = sz
         L.decode_layer.argtypes = [vp, vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                    vp, sz, vp]
+        L.decode_layer_noalloc.argtypes = [vp, vp, vp, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.mcpu_check_device_errors.argtypes = [vp, vp, i32p]
         L.mcpu_packed_weights_bytes.argtypes = [i32, i32, i32]
         L.mcpu_packed_weights_bytes.restype = sz
@@ -292,6 +294,19 @@ def decode_layer(shape, weights: DeviceWeights, pool: KVPool, page_table, seq_le
                               _ptr(topk_idx), _ptr(topk_w),
                               ctypes.byref(taps) if taps is not None else None,
                               _ptr(workspace), workspace.numel(), _stream(stream)))
+
+
+def decode_layer_noalloc(shape, weights: DeviceWeights, pool: KVPool, page_table, seq_lens, cu_q, host_seq_lens,
+                         host_cu_q, x_in, x_out, topk_idx=None, topk_w=None, taps: Optional[Taps] = None,
+                         device_errors=None, stream=None):
+    """decode_layer on the library's static scratch (no workspace argument)."""
+    cfg = make_cfg(shape)
+    hs, hc = _host_i32(host_seq_lens), _host_i32(host_cu_q)
+    _check(lib().decode_layer_noalloc(ctypes.byref(cfg), ctypes.byref(weights.struct), pool.handle,
+                                      int(seq_lens.shape[0]), _ptr(page_table), int(page_table.shape[1]),
+                                      _ptr(seq_lens), _ptr(cu_q), _ptr(hs), _ptr(hc), _ptr(x_in), _ptr(x_out),
+                                      _ptr(topk_idx), _ptr(topk_w), ctypes.byref(taps) if taps is not None else None,
+                                      _ptr(device_errors), _stream(stream)))
 
 
 def mcpu_check_device_errors(workspace, stream=None) -> int:
