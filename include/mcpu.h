@@ -287,7 +287,9 @@ typedef struct mcpu_lm_head {
 } mcpu_lm_head;
 
 /* Next-token sampling and log-probabilities for n_tokens rows.
- *  x [T, H] fp32 residual rows (the stack's output for each row's last token).
+ *  x [*, H] fp32 residual rows (the stack's output); row t of the head reads
+ *  x[x_rows[t]] (x_rows: device int32 [T], e.g. each sequence's last new
+ *  token; the caller keeps them in range), or x[t] when x_rows is NULL.
  *  xn = RMSNorm(x; g_final) stored as bf16; logits l = xn . w_lm^T (fp32
  *  accumulation); s = l / temperature.
  *  temperature > 0: the sampled token is argmax_v (s_v + g_v) (the Gumbel-max
@@ -301,11 +303,14 @@ typedef struct mcpu_lm_head {
  *  logprob_out its log-probability s_tok - logsumexp(s), lse_out logsumexp(s),
  *  target_logprob_out s_target - logsumexp(s) for targets[t] (device [T],
  *  nullable; ids in [0, V), else the value is -inf).
- *  seq_ids / positions: device int32 [T], required when sampling.
+ *  seq_ids / positions: device int32 [T], required when sampling (temperature
+ *  > 0 with tokens_out or logprob_out requested); without those outputs no
+ *  draws are made (scoring targets at a temperature).
  *  workspace >= lm_head_workspace_size(H, V, T) bytes (first 256 bytes: the
  *  error word, as for decode_layer). Host-detected errors launch nothing. */
 size_t lm_head_workspace_size(int32_t hidden, int32_t vocab, int32_t max_tokens);
-int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, float temperature, uint64_t seed,
+int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, const int32_t* x_rows,
+                   float temperature, uint64_t seed,
                    const int32_t* seq_ids, const int32_t* positions, const int32_t* targets, int32_t* tokens_out,
                    float* logprob_out, float* target_logprob_out, float* lse_out, void* workspace,
                    size_t ws_bytes, hipStream_t stream);

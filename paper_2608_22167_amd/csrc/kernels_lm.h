@@ -18,7 +18,8 @@ struct EmbedArgs {
 hipError_t launch_embed(const EmbedArgs& p, hipStream_t s);
 
 struct FinalNorm {
-  const float* x;  // [n_tokens][hidden] fp32 residual stream
+  const float* x;  // [*][hidden] fp32 residual stream
+  const int32_t* rows;  // [n_tokens] rows of x to normalise, or nullptr (row t)
   const float* g;  // [hidden]
   int n_tokens, hidden;
   float eps;

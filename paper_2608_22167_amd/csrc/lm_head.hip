@@ -40,7 +40,7 @@ __global__ __launch_bounds__(256) void final_norm_kernel(FinalNorm P) {
     P.group_off[0] = 0;
     P.group_off[1] = P.n_tokens;
   }
-  const float* x = P.x + (int64_t)t * P.hidden;
+  const float* x = P.x + (int64_t)(P.rows ? P.rows[t] : t) * P.hidden;
   float ss = 0.f;
   for (int c = 4 * tid; c < P.hidden; c += 4 * blockDim.x) {
     const float4 v = *reinterpret_cast<const float4*>(x + c);

@@ -648,7 +648,8 @@ size_t lm_head_workspace_size(int32_t hidden, int32_t vocab, int32_t max_tokens)
   return (cv.off + 255) & ~size_t(255);
 }
 
-int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, float temperature, uint64_t seed,
+int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, const int32_t* x_rows,
+                   float temperature, uint64_t seed,
                    const int32_t* seq_ids, const int32_t* positions, const int32_t* targets, int32_t* tokens_out,
                    float* logprob_out, float* target_logprob_out, float* lse_out, void* workspace,
                    size_t ws_bytes, hipStream_t stream) {
@@ -662,7 +663,9 @@ int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, flo
   if (n_tokens == 0) return MCPU_OK;
   if (!lm->g_final || !lm->w_lm || !x || !workspace) return fail(MCPU_EINVAL, "NULL pointer");
   const bool greedy = !(temperature > 0.f);
-  if (!greedy && (!seq_ids || !positions)) return fail(MCPU_EINVAL, "sampling needs seq_ids and positions");
+  // the draws are needed only when a sampled token (or its log-probability) is asked for
+  const bool draws = !greedy && (tokens_out || logprob_out);
+  if (draws && (!seq_ids || !positions)) return fail(MCPU_EINVAL, "sampling needs seq_ids and positions");
   if (!greedy && !(temperature < 1e30f)) return fail(MCPU_EINVAL, "temperature %g", (double)temperature);
   if (targets && !target_logprob_out) return fail(MCPU_EINVAL, "targets given without target_logprob_out");
   const size_t need = lm_head_workspace_size(H, V, n_tokens);
@@ -674,7 +677,7 @@ int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, flo
   LogitSlot* slots = cv.take<LogitSlot>((size_t)n_tokens * n_slots);
 
   FinalNorm fn{};
-  fn.x = x; fn.g = lm->g_final; fn.n_tokens = n_tokens; fn.hidden = H; fn.eps = lm->rms_eps; fn.out = xn;
+  fn.x = x; fn.rows = x_rows; fn.g = lm->g_final; fn.n_tokens = n_tokens; fn.hidden = H; fn.eps = lm->rms_eps; fn.out = xn;
   fn.group_off = goff;
   HIP_TRY(launch_final_norm(fn, stream));
 
@@ -682,7 +685,7 @@ int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, flo
   g.w = lm->w_lm; g.w_packed = lm->w_lm_packed; g.n = V; g.k = H; g.x = xn; g.group_off = goff;
   g.n_rows = n_tokens; g.n_groups = 1; g.epi = EPI_LOGITS; g.out = slots; g.err = err_word(workspace);
   g.max_rows_per_group = n_tokens; g.x_rows = n_tokens;
-  g.inv_temp = greedy ? 1.f : 1.f / temperature; g.greedy = greedy ? 1 : 0; g.seed = seed;
+  g.inv_temp = greedy ? 1.f : 1.f / temperature; g.greedy = draws ? 0 : 1; g.seed = seed;
   g.row_seq = seq_ids; g.row_pos = positions; g.target = targets;
   {
     Timed tm(MCPU_KERNEL_LM_HEAD, stream);

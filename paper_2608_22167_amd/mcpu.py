@@ -101,8 +101,8 @@ def lib():
         L.mcpu_pack_weights.argtypes = [i32, vp, vp, i32, i32, i32, vp]
         L.lm_head_workspace_size.argtypes = [i32, i32, i32]
         L.lm_head_workspace_size.restype = sz
-        L.lm_head_sample.argtypes = [vp, i32, vp, ctypes.c_float, ctypes.c_uint64, vp, vp, vp, vp, vp, vp, vp,
-                                     vp, sz, vp]
+        L.lm_head_sample.argtypes = [vp, i32, vp, vp, ctypes.c_float, ctypes.c_uint64, vp, vp, vp, vp, vp, vp,
+                                     vp, vp, sz, vp]
         L.embed_tokens.argtypes = [vp, i32, i32, i32, vp, vp, vp, sz, vp]
         L.mcpu_timing_start.argtypes = [i32, i32]
         L.mcpu_timing_read.argtypes = [i32, vp, i32, i32p]
@@ -353,10 +353,12 @@ def lm_head_workspace_size(hidden, vocab, max_tokens) -> int:
 
 
 def lm_head_sample(head: DeviceLmHead, x, temperature, seed=0, seq_ids=None, positions=None, targets=None,
-                   tokens=None, logprob=None, target_logprob=None, lse=None, workspace=None, stream=None):
-    """lm_head_sample on rows x [T, H] fp32; outputs are device tensors (nullable)."""
-    T = int(x.shape[0])
-    _check(lib().lm_head_sample(ctypes.byref(head.struct), T, _ptr(x), float(temperature), int(seed),
+                   tokens=None, logprob=None, target_logprob=None, lse=None, workspace=None, stream=None,
+                   x_rows=None):
+    """lm_head_sample on rows x [T, H] fp32 (or on rows x[x_rows]); outputs
+    are device tensors (nullable)."""
+    T = int(x.shape[0] if x_rows is None else x_rows.shape[0])
+    _check(lib().lm_head_sample(ctypes.byref(head.struct), T, _ptr(x), _ptr(x_rows), float(temperature), int(seed),
                                 _ptr(seq_ids), _ptr(positions), _ptr(targets), _ptr(tokens), _ptr(logprob),
                                 _ptr(target_logprob), _ptr(lse), _ptr(workspace),
                                 workspace.numel() * workspace.element_size(), _stream(stream)))

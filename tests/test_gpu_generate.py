@@ -155,3 +155,94 @@ def test_embed_tokens_bit_exact_and_bad_id():
     mcpu.embed_tokens(table, torch.from_numpy(ids).cuda(), x, ws)
     assert mcpu.mcpu_check_device_errors(ws) & mcpu.DEVERR_TOKEN
     assert float(x[5].abs().max()) == 0.0
+
+
+# ------------------------------------------------------------------------------ the generator
+
+
+def _generator_case():
+    from paper_2608_22167_amd.generate import GenSpec, Generator
+    base = W.replace(W.GPT_OSS_20B, hidden=256, n_q_heads=8, n_kv_heads=2, head_dim=64, n_experts=8, top_k=2,
+                     ffn_dim=256)
+    spec = GenSpec(n_layers=4, base=base, vocab=4096, window=128, pages_full=512, pages_sw=128, max_ctx=4096)
+    return spec, Generator(spec, max_tokens_per_step=512)
+
+
+def test_generator_turns_against_reference_trajectories():
+    """Continuous batching over multi-turn trajectories: five sequences join
+    at different steps, generate 6-token turns, wait, take tool observations
+    of 5-60 tokens, and leave after three turns. Every sampled token and its
+    log-probability is checked against the reference trajectory (its whole
+    history as one causal prefill, then the head with the same draws); window
+    pages stay bounded while sequences grow, and every page comes back."""
+    from oracle import generate as OG
+    spec, gen = _generator_case()
+    free0 = gen.free_pages()
+    rng = np.random.default_rng(7)
+    prompts = {sid: rng.integers(0, spec.vocab, n).tolist() for sid, n in zip(range(5), [3, 40, 17, 1, 100])}
+    join = {0: 0, 1: 0, 2: 3, 3: 5, 4: 9}
+    turns = {sid: 0 for sid in prompts}
+    made = {sid: 0 for sid in prompts}
+    samples = {sid: [] for sid in prompts}      # (position, token, logprob)
+    waiting, finished, histories = {}, set(), {}
+    max_sw = 0
+    step = 0
+    while len(finished) < len(prompts):
+        for sid, at in join.items():
+            if at == step:
+                gen.add(sid, prompts[sid])
+        for sid in list(waiting):
+            waiting[sid] -= 1
+            if waiting[sid] == 0:
+                del waiting[sid]
+                gen.resume(sid, rng.integers(0, spec.vocab, int(rng.integers(5, 60))).tolist())
+        out = gen.step()
+        for sid, (tok, lp) in out.items():
+            s = gen.seqs[sid]
+            samples[sid].append((s.length, tok, lp))
+            made[sid] += 1
+            if made[sid] % 6 == 0:           # the turn ends in a tool call
+                turns[sid] += 1
+                gen.hold(sid)
+                if turns[sid] == 3:
+                    histories[sid] = list(s.history) + [tok]
+                    gen.release(sid)
+                    finished.add(sid)
+                else:
+                    waiting[sid] = 2
+        max_sw = max([max_sw] + [len(s.pages_sw) for s in gen.seqs.values()])
+        step += 1
+        assert step < 400
+    assert gen.check_errors() == 0
+    assert gen.free_pages() == free0, "pages leaked"
+    assert max_sw <= 128 // 16 + 2, max_sw
+    ss = spec.stack_spec()
+    lw = [W.stack_weights_host(ss, i) for i in range(spec.n_layers)]
+    lm = W.lm_weights_host(spec.seed, ss.shape_full.hidden, spec.vocab)
+    near = 0
+    for sid, hist in histories.items():
+        rows = OG.trajectory_rows(ss, lw, lm["embed"], hist[:-1])
+        pos = np.array([p for p, _, _ in samples[sid]])
+        ref = O.lm_head(rows[pos - 1], lm["g_final"], lm["w_lm"], ss.shape_full.rms_eps, spec.temperature,
+                        seed=spec.seed, seq_ids=np.full(len(pos), sid, np.int32), positions=pos, want_logits=True)
+        got = dict(tokens=np.array([t for _, t, _ in samples[sid]]), logprob=np.array([l for _, _, l in samples[sid]]),
+                   lse=ref["lse"])
+        # the history holds the GPU's tokens: each one must be the reference's draw
+        np.testing.assert_array_equal(np.array(hist)[pos], got["tokens"])
+        near += _check(got, ref)
+    print(f"  {step} steps, {sum(len(v) for v in samples.values())} sampled tokens, {near} near ties, "
+          f"at most {max_sw} window pages per sequence")
+    # the log-probability pass over the finished trajectories
+    trajs = [histories[sid] for sid in sorted(histories)]
+    scores = gen.score(trajs)
+    assert gen.free_pages() == free0
+    for sid, tr, sc in zip(sorted(histories), trajs, scores):
+        rows = OG.trajectory_rows(ss, lw, lm["embed"], tr[:-1])
+        n = len(tr) - 1
+        ref = O.lm_head(rows, lm["g_final"], lm["w_lm"], ss.shape_full.rms_eps, spec.temperature,
+                        seq_ids=np.zeros(n, np.int32), positions=np.zeros(n, np.int32),
+                        targets=np.array(tr[1:], np.int32))
+        np.testing.assert_allclose(sc, ref["target_logprob"], atol=LP_TOL, rtol=0)
+        # a sampled token's log-probability is the same number from both passes
+        for p, tok, lp in samples[sid]:
+            assert abs(sc[p - 1] - lp) <= LP_TOL
