@@ -158,9 +158,11 @@ def cpu_model():
     return "unknown"
 
 
-# Writing this many bytes between timed steps evicts the previous step's data
+# Reading this many bytes between timed steps evicts the previous step's data
 # from the L2 caches and the 256 MB memory-side cache (MALL), so every step
-# reads its weights and cache pages from HBM.
+# reads its weights and cache pages from HBM. A read leaves clean lines
+# behind; a write would leave dirty ones whose write-back then competes with
+# the next step's first kernels.
 FLUSH_BYTES = 1 << 30
 
 
@@ -315,11 +317,11 @@ def main():
     if bench.errors():
         raise SystemExit("device error during warm-up")
 
-    flush = None if args.no_flush else torch.empty(FLUSH_BYTES, dtype=torch.uint8, device="cuda")
+    flush = None if args.no_flush else torch.ones(FLUSH_BYTES // 2, dtype=torch.float16, device="cuda")
 
     def evict(i):
         if flush is not None:
-            flush.fill_(i & 0xFF)
+            torch.sum(flush)
 
     # per-kernel breakdown (microseconds per step, all launches), untimed pass
     nb = min(K, 20)

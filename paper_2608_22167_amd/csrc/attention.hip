@@ -87,7 +87,19 @@ __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnPlan P) {
     P.tok_seq[t] = b;
     P.tok_pos[t] = pos;
     P.split_start[t] = run;
-    run += is_prefill(P, b) ? 0 : token_splits(pos, P.window, P.pps);
+    const int ns = is_prefill(P, b) ? 0 : token_splits(pos, P.window, P.pps);
+    // the token's ns splits share its np pages evenly (sizes differ by at most one)
+    const int lo = P.window > 0 ? max(0, pos - P.window + 1) : 0;
+    const int first = lo / PAGE, np = pos / PAGE - first + 1;
+    for (int k = 0; k < ns && run + k < P.host_total_splits; ++k) {
+      SplitDesc d;
+      d.t = t; d.b = b; d.p = pos; d.lo = lo;
+      d.pg0 = first + (int)((int64_t)k * np / ns);
+      d.pg1 = first + (int)((int64_t)(k + 1) * np / ns);
+      d.pad0 = d.pad1 = 0;
+      P.split_desc[run + k] = d;
+    }
+    run += ns;
   }
   if (tid == 0) {
     P.split_start[P.n_tokens] = total;
@@ -132,52 +144,112 @@ struct PageFrags {
   }
 };
 
+// Online-softmax state of one wavefront: the running maximum (log2 units), the
+// running sum and the value accumulator (lane (hl, grp) holds dims
+// 16 n + 4 grp .. + 3 of query head hl).
+template <int D>
+struct SoftmaxAcc {
+  float m = -INFINITY, l = 0.f;
+  f32x4 acc[D / 16];
+  __device__ __forceinline__ SoftmaxAcc() {
+#pragma unroll
+    for (int n = 0; n < D / 16; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  // One page: S^T = K q^T on the matrix cores, mask keys outside [lo, p] (and
+  // the whole page if `valid` is false), rescale, and O^T += V^T P^T.
+  template <typename T>
+  __device__ __forceinline__ void page(const PageFrags<T, D>& cur, const Frag<T> (&qf)[D / 32], bool valid,
+                                       int key0, int lo, int p, float scale_log2) {
+    f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < D / 32; ++c) sc = mma32(cur.k[c], qf[c], sc);
+    // sc[r] = score of key slot key0 + r for query head lane % 16
+    float x[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int pos = key0 + r;
+      x[r] = (valid && pos >= lo && pos <= p) ? sc[r] * scale_log2 : -INFINITY;
+    }
+    float mloc = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+    const float m_new = fmaxf(m, mloc);
+    // m_new is -inf only while every key so far was masked (missing pages)
+    const bool live = m_new != -INFINITY;
+    const float alpha = live ? __builtin_amdgcn_exp2f(m - m_new) : 1.0f;
+    float pr[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) pr[r] = live ? __builtin_amdgcn_exp2f(x[r] - m_new) : 0.f;
+    l *= alpha;
+#pragma unroll
+    for (int n = 0; n < D / 16; ++n) {
+      acc[n] *= alpha;
+      acc[n] = mma16_p(cur.v[n], pr, acc[n], n == 0 ? &l : nullptr);
+    }
+    m = m_new;
+  }
+  // the sum over the wavefront's four key-row groups
+  __device__ __forceinline__ float l_total() const {
+    float t = l + __shfl_xor(l, 16, 64);
+    return t + __shfl_xor(t, 32, 64);
+  }
+};
+
+// The token, position and page range of split s (shared by both kernels).
+struct SplitRange {
+  int t, b, p, lo, pg0, pg1;
+};
+// (the plan kernel wrote it as one 32-byte record: a single load, where a
+// search over split_start would chain several dependent ones)
+__device__ __forceinline__ SplitRange split_range(const AttnSplit& P, int s) {
+  const SplitDesc d = P.split_desc[s];
+  SplitRange r;
+  r.t = uniform(d.t);
+  r.b = uniform(d.b);
+  r.p = uniform(d.p);
+  r.lo = uniform(d.lo);
+  r.pg0 = uniform(d.pg0);
+  r.pg1 = uniform(d.pg1);
+  // a record the plan did not write (device arrays disagree with the host's
+  // plan) may be stale: every field is checked before it addresses memory
+  if (r.t < 0 || r.t >= P.n_tokens || r.b < 0 || r.b >= P.batch || r.p < 0 || r.p / PAGE >= P.max_pages ||
+      r.pg0 < 0 || r.pg0 >= r.pg1 || r.pg1 > P.max_pages) {
+    if (lane_id() == 0) set_error(P.err, 1);
+    r.t = 0;
+    r.b = 0;
+    r.pg0 = r.pg1 = 0;
+  }
+  return r;
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void load_q(Frag<T> (&qf)[D / 32], const AttnSplit& P, int t, int g) {
+  const int lane = lane_id(), G = P.hq / P.hkv, hl = lane & 15, grp = lane >> 4;
+  const T* qb = reinterpret_cast<const T*>(P.q) + ((int64_t)t * P.hq + g * G + hl) * D + 8 * grp;
+#pragma unroll
+  for (int c = 0; c < D / 32; ++c) {
+    if (hl < G) qf[c].load(qb + 32 * c); else qf[c].zero();
+  }
+}
+
 template <typename T, int D, int WAVES, int PF>
 __global__ __launch_bounds__(64 * WAVES) void attn_split_kernel(AttnSplit P) {
   const int lane = lane_id();
   const int item = blockIdx.x * WAVES + uniform(threadIdx.x >> 6);
   const int s = item / P.hkv, g = item - (item / P.hkv) * P.hkv;
   if (s >= P.n_splits) return;
-
-  // token owning split s: last t with split_start[t] <= s
-  int lo_t = 0, hi_t = P.n_tokens - 1;
-  while (lo_t < hi_t) {
-    int mid = (lo_t + hi_t + 1) >> 1;
-    if (P.split_start[mid] <= s) lo_t = mid; else hi_t = mid - 1;
-  }
-  const int t = uniform(lo_t);
-  const int b = uniform(P.tok_seq[t]), p = uniform(P.tok_pos[t]);
-  const int lo = P.window > 0 ? max(0, p - P.window + 1) : 0;
-  // the token's ns splits share its np pages evenly (sizes differ by at most one)
-  const int first = lo / PAGE, np = p / PAGE - first + 1;
-  const int ns = uniform(P.split_start[t + 1]) - uniform(P.split_start[t]);
-  const int k = s - uniform(P.split_start[t]);
-  int pg0 = ns > 0 ? first + (int)((int64_t)k * np / ns) : 0;
-  int pg1 = ns > 0 ? first + (int)((int64_t)(k + 1) * np / ns) : 0;
+  const SplitRange R = split_range(P, s);
+  const int pg0 = R.pg0, pg1 = R.pg1;
   const int G = P.hq / P.hkv;
   const int hl = lane & 15, grp = lane >> 4;
-  if (p < 0 || p / PAGE >= P.max_pages || pg0 < 0 || pg0 >= pg1) {
-    // positions outside the page table (device arrays disagree with the plan)
-    if (lane == 0) set_error(P.err, 1);
-    pg0 = pg1 = 0;
-  }
-
   Frag<T> qf[D / 32];
-  const T* qb = reinterpret_cast<const T*>(P.q) + ((int64_t)t * P.hq + g * G + hl) * D + 8 * grp;
-#pragma unroll
-  for (int c = 0; c < D / 32; ++c) {
-    if (hl < G) qf[c].load(qb + 32 * c); else qf[c].zero();
-  }
+  load_q<T, D>(qf, P, R.t, g);
 
   const T* kpool = reinterpret_cast<const T*>(P.k_pool);
   const T* vpool = reinterpret_cast<const T*>(P.v_pool);
-  const int32_t* ptab = P.page_table + (int64_t)b * P.max_pages;
+  const int32_t* ptab = P.page_table + (int64_t)R.b * P.max_pages;
   const int64_t head_off = (int64_t)g * PAGE * D, page_elems = (int64_t)P.hkv * PAGE * D;
-
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4 acc[D / 16];
-#pragma unroll
-  for (int n = 0; n < D / 16; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  SoftmaxAcc<D> st;
 
   // PF-deep ring of pages: while page i is consumed, pages i+1 .. i+PF-1 are
   // in flight and page i+PF is issued into its slot. Loads are branch-free: a
@@ -196,35 +268,7 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_kernel(AttnSplit P) {
     ring[slot].load(kpool + id * page_elems + head_off, vpool + id * page_elems + head_off, lane);
   };
   auto consume = [&](int slot, int i) {
-    const PageFrags<T, D>& cur = ring[slot];
-    f32x4 sc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int c = 0; c < D / 32; ++c) sc = mma32(cur.k[c], qf[c], sc);
-    // sc[r] = score of key slot 4 * grp + r for query head hl
-    const int key0 = (pg0 + i) * PAGE + 4 * grp;
-    float x[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int pos = key0 + r;
-      x[r] = (ok[slot] && pos >= lo && pos <= p) ? sc[r] * P.scale_log2 : -INFINITY;
-    }
-    float mloc = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_run, mloc);
-    // m_new is -inf only while every key so far was masked (missing pages)
-    const bool live = m_new != -INFINITY;
-    const float alpha = live ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.0f;
-    float pr[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) pr[r] = live ? __builtin_amdgcn_exp2f(x[r] - m_new) : 0.f;
-    l_run *= alpha;
-#pragma unroll
-    for (int n = 0; n < D / 16; ++n) {
-      acc[n] *= alpha;
-      acc[n] = mma16_p(cur.v[n], pr, acc[n], n == 0 ? &l_run : nullptr);
-    }
-    m_run = m_new;
+    st.page(ring[slot], qf, ok[slot], (pg0 + i) * PAGE + 4 * grp, R.lo, R.p, P.scale_log2);
   };
   if (npg > 0) {
 #pragma unroll
@@ -242,18 +286,82 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_kernel(AttnSplit P) {
       if (i + u < npg) consume(u, i + u);
   }
 
-  float l_tot = l_run + __shfl_xor(l_run, 16, 64);
-  l_tot += __shfl_xor(l_tot, 32, 64);
+  const float l_tot = st.l_total();
   if (hl < G) {
     const int64_t row = (int64_t)s * P.hq + g * G + hl;
     if (grp == 0) {
-      P.part_ml[row * 2 + 0] = m_run;
+      P.part_ml[row * 2 + 0] = st.m;
       P.part_ml[row * 2 + 1] = l_tot;
     }
     float* pa = P.part_acc + row * D + 4 * grp;
 #pragma unroll
     for (int n = 0; n < D / 16; ++n)
-      *reinterpret_cast<float4*>(pa + 16 * n) = make_float4(acc[n][0], acc[n][1], acc[n][2], acc[n][3]);
+      *reinterpret_cast<float4*>(pa + 16 * n) = make_float4(st.acc[n][0], st.acc[n][1], st.acc[n][2], st.acc[n][3]);
+  }
+}
+
+// Sliding-window layers: every decode token's window spans at most MAXP pages
+// and is one split. One wavefront per (token, KV head) reads the window's page
+// ids with one vector load (lane j: page j), issues every page's K and V loads
+// at once, and finishes the token itself: the sink joins the normaliser and o
+// is written in the layer dtype, so no partials and no combine pass are
+// needed. (The split-K kernel, whose pages follow a page-table load each and
+// keep two in flight, left short windows waiting on memory latency.)
+template <typename T, int D, int MAXP>
+__global__ __launch_bounds__(64) void attn_window_kernel(AttnSplit P) {
+  const int lane = lane_id();
+  const int s = blockIdx.x / P.hkv, g = blockIdx.x - (blockIdx.x / P.hkv) * P.hkv;
+  if (s >= P.n_splits) return;
+  const SplitRange R = split_range(P, s);
+  if (R.pg0 == R.pg1) return;  // an invalid record (error bit set): no token to finish
+  const int npg = min(R.pg1 - R.pg0, MAXP);
+  if (lane == 0 && R.pg1 - R.pg0 > MAXP) set_error(P.err, 8);  // the launch does not fit this plan
+  const int G = P.hq / P.hkv;
+  const int hl = lane & 15, grp = lane >> 4;
+  const int my_id = lane < npg ? P.page_table[(int64_t)R.b * P.max_pages + R.pg0 + lane] : 0;
+  Frag<T> qf[D / 32];
+  load_q<T, D>(qf, P, R.t, g);
+  const T* kpool = reinterpret_cast<const T*>(P.k_pool);
+  const T* vpool = reinterpret_cast<const T*>(P.v_pool);
+  const int64_t head_off = (int64_t)g * PAGE * D, page_elems = (int64_t)P.hkv * PAGE * D;
+  PageFrags<T, D> pages[MAXP];
+  bool ok[MAXP];
+#pragma unroll
+  for (int u = 0; u < MAXP; ++u) {
+    ok[u] = false;
+    if (u < npg) {  // wave-uniform
+      int id = __shfl(my_id, u, 64);
+      const bool good = id >= 0 && id < P.n_pages;
+      if (!good && lane == 0) set_error(P.err, 1);
+      ok[u] = good;
+      id = good ? id : 0;
+      pages[u].load(kpool + id * page_elems + head_off, vpool + id * page_elems + head_off, lane);
+    }
+  }
+  SoftmaxAcc<D> st;
+#pragma unroll
+  for (int u = 0; u < MAXP; ++u)
+    if (u < npg) st.page(pages[u], qf, ok[u], (R.pg0 + u) * PAGE + 4 * grp, R.lo, R.p, P.scale_log2);
+  const float l_tot = st.l_total();
+  if (hl < G) {
+    // o_h = 2^{m - M} acc / (2^{sink log2e - M} + 2^{m - M} l), M = max(sink log2e, m)
+    const int h = g * G + hl;
+    float M = P.sinks ? P.sinks[h] * LOG2E : -INFINITY;
+    float L = P.sinks ? 1.0f : 0.0f;
+    float f = 0.f;
+    if (st.m != -INFINITY) {
+      if (st.m > M) {
+        L *= __builtin_amdgcn_exp2f(M - st.m);
+        M = st.m;
+      }
+      f = __builtin_amdgcn_exp2f(st.m - M);
+      L += f * l_tot;
+    }
+    T* o = reinterpret_cast<T*>(P.o) + ((int64_t)R.t * P.hq + h) * D + 4 * grp;
+#pragma unroll
+    for (int n = 0; n < D / 16; ++n)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) Elem<T>::store(o, 16 * n + r, L > 0.f ? f * st.acc[n][r] / L : 0.f);
   }
 }
 
@@ -262,7 +370,11 @@ hipError_t split_impl(const AttnSplit& p, hipStream_t s) {
   int64_t items = (int64_t)p.n_splits * p.hkv;
   int blocks = (int)((items + WAVES - 1) / WAVES);
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_split_kernel<T, D, WAVES, PF>), dim3(blocks), dim3(64 * WAVES), 0, s, p);
+  if (p.o) {
+    hipLaunchKernelGGL((attn_window_kernel<T, D, WINDOW_MAX_PAGES>), dim3((unsigned)items), dim3(64), 0, s, p);
+  } else {
+    hipLaunchKernelGGL((attn_split_kernel<T, D, WAVES, PF>), dim3(blocks), dim3(64 * WAVES), 0, s, p);
+  }
   return hipGetLastError();
 }
 

@@ -8,6 +8,12 @@ namespace mcpu {
 
 // ---- attention -----------------------------------------------------------
 
+// One split of a token's visible pages: token t of sequence b at position p,
+// keys from lo, pages pg0 .. pg1 - 1 (logical page indices).
+struct SplitDesc {
+  int32_t t, b, p, lo, pg0, pg1, pad0, pad1;
+};
+
 struct AttnPlan {
   const int32_t* seq_lens;  // [batch]
   const int32_t* cu_q;      // [batch+1] or nullptr (one token per sequence)
@@ -19,6 +25,7 @@ struct AttnPlan {
   int32_t* tok_seq;         // [n_tokens] out
   int32_t* tok_pos;         // [n_tokens] out
   int32_t* split_start;     // [n_tokens + 1] out
+  SplitDesc* split_desc;    // [host_total_splits] out
   int32_t* blk_start;       // [batch + 1] out: first prefill block of each sequence
   int32_t* err;
   int32_t* zero;            // [n_zero] words cleared for the layer's later kernels
@@ -52,12 +59,21 @@ struct AttnSplit {
   const int32_t* tok_seq;
   const int32_t* tok_pos;
   const int32_t* split_start;
-  int n_tokens, n_splits, hq, hkv, window, pps;
+  const SplitDesc* split_desc;  // [n_splits], written by the plan kernel
+  int batch, n_tokens, n_splits, hq, hkv, window, pps;
   float scale_log2;  // log2(e) / sqrt(D)
   float* part_ml;    // [S][Hq][2] running max (log2 units) and sum
   float* part_acc;   // [S][Hq][D]
   int32_t* err;
+  // Set o (and sinks) to finish each token in the split pass (sliding-window
+  // layers whose window fits WINDOW_MAX_PAGES pages, one split per token):
+  // o [T][Hq * D] is written directly and no partials are stored.
+  const float* sinks;
+  void* o;
 };
+// pages a window of at most WINDOW_MAX_KEYS keys can touch
+constexpr int WINDOW_MAX_KEYS = 128;
+constexpr int WINDOW_MAX_PAGES = (WINDOW_MAX_KEYS + 14) / 16 + 1;
 
 struct AttnCombine {
   const float* part_ml;

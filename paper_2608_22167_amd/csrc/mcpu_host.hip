@@ -179,6 +179,7 @@ int plan_attention(const mcpu_layer_cfg* c, int batch, int max_pages, const int3
 
 struct AttnBufs {
   int32_t *tok_seq, *tok_pos, *split_start, *blk_start;
+  SplitDesc* split_desc;
   float *part_ml, *part_acc;
 };
 
@@ -189,6 +190,7 @@ AttnBufs carve_attention(Carve& cv, const mcpu_layer_cfg* c, int max_tokens) {
   b.tok_pos = cv.take<int32_t>(max_tokens);
   b.split_start = cv.take<int32_t>(max_tokens + 1);
   b.blk_start = cv.take<int32_t>(max_tokens + 1);  // max_tokens >= batch here
+  b.split_desc = cv.take<SplitDesc>(S);
   b.part_ml = cv.take<float>(S * c->n_q_heads * 2);
   b.part_acc = cv.take<float>(S * c->n_q_heads * c->head_dim);
   return b;
@@ -202,7 +204,7 @@ AttnPlan make_plan(const mcpu_layer_cfg* c, int batch, const int32_t* seq_lens, 
   pl.window = c->window; pl.pps = ph.pps; pl.host_total_splits = ph.n_splits;
   pl.prefill_min_q = ph.prefill_min_q; pl.prefill_qb = ph.prefill_qb; pl.host_total_blocks = ph.n_blocks;
   pl.tok_seq = ab.tok_seq; pl.tok_pos = ab.tok_pos; pl.split_start = ab.split_start;
-  pl.blk_start = ab.blk_start; pl.err = err;
+  pl.split_desc = ab.split_desc; pl.blk_start = ab.blk_start; pl.err = err;
   return pl;
 }
 
@@ -335,19 +337,22 @@ int run_attention(const mcpu_layer_cfg* c, const float* sinks, mcpu_kv_pool* poo
   AttnSplit sp{};
   sp.q = q; sp.k_pool = pool->k; sp.v_pool = pool->v; sp.page_table = page_table;
   sp.max_pages = max_pages; sp.n_pages = pool->n_pages;
-  sp.tok_seq = ab.tok_seq; sp.tok_pos = ab.tok_pos; sp.split_start = ab.split_start;
-  sp.n_tokens = ph.n_tokens; sp.n_splits = ph.n_splits; sp.hq = c->n_q_heads; sp.hkv = c->n_kv_heads;
+  sp.tok_seq = ab.tok_seq; sp.tok_pos = ab.tok_pos; sp.split_start = ab.split_start; sp.split_desc = ab.split_desc;
+  sp.batch = batch; sp.n_tokens = ph.n_tokens; sp.n_splits = ph.n_splits; sp.hq = c->n_q_heads; sp.hkv = c->n_kv_heads;
   sp.window = c->window; sp.pps = ph.pps;
   sp.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)c->head_dim));
   sp.part_ml = ab.part_ml; sp.part_acc = ab.part_acc; sp.err = err;
+  // short windows: one split per token, finished in the split pass itself
+  const bool one_pass = c->window > 0 && c->window <= WINDOW_MAX_KEYS && ph.pps >= WINDOW_MAX_PAGES;
+  if (one_pass) { sp.o = o; sp.sinks = sinks; }
   {
     Timed tm(MCPU_KERNEL_ATTN_SPLIT, st);
     HIP_TRY(launch_attn_split(c->dtype, c->head_dim, sp, st));
   }
-  AttnCombine cb{};
-  cb.part_ml = ab.part_ml; cb.part_acc = ab.part_acc; cb.split_start = ab.split_start; cb.sinks = sinks;
-  cb.n_tokens = ph.n_tokens; cb.n_splits = ph.n_splits; cb.hq = c->n_q_heads; cb.o = o;
-  {
+  if (!one_pass) {
+    AttnCombine cb{};
+    cb.part_ml = ab.part_ml; cb.part_acc = ab.part_acc; cb.split_start = ab.split_start; cb.sinks = sinks;
+    cb.n_tokens = ph.n_tokens; cb.n_splits = ph.n_splits; cb.hq = c->n_q_heads; cb.o = o;
     Timed tm(MCPU_KERNEL_ATTN_COMBINE, st);
     HIP_TRY(launch_attn_combine(c->dtype, c->head_dim, cb, st));
   }
