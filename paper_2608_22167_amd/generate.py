@@ -94,6 +94,7 @@ class Generator:
                                      for i in range(min(2, spec.n_layers))), device)
         self.lm_ws = mcpu.workspace(mcpu.lm_head_workspace_size(s0.hidden, spec.vocab, max_tokens_per_step), device)
         self.seqs: Dict[int, _Seq] = {}
+        self.held: Dict[int, List[int]] = {}   # a sequence's sampled token kept back while its turn waits
         self.steps = 0
 
     # ------------------------------------------------------------------ sequences
@@ -109,6 +110,7 @@ class Generator:
     def release(self, sid: int) -> None:
         """Free every page of sequence sid and forget it."""
         s = self.seqs.pop(sid)
+        self.held.pop(sid, None)
         if self.alloc_full is not None and s.pages_full:
             mcpu.kv_pages_free(self.alloc_full, np.array(s.pages_full, np.int32))
         if s.pages_sw:
@@ -223,13 +225,12 @@ class Generator:
         """Drop the sequence's pending sampled token (its turn ended); the
         token is still part of the trajectory: it is fed with the next input."""
         s = self.seqs[sid]
-        self._held = getattr(self, "_held", {})
-        self._held[sid] = s.pending[:]
+        self.held[sid] = s.pending[:]
         s.pending.clear()
 
     def resume(self, sid: int, observation: Sequence[int]) -> None:
         """Append a tool observation after the held token."""
-        held = getattr(self, "_held", {}).pop(sid, [])
+        held = self.held.pop(sid, [])
         self.add(sid, list(held) + list(observation))
 
     def check_errors(self) -> int:
