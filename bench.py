@@ -26,7 +26,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+# dense matrix-core peaks; products with MXFP8 activations run at the fp8 rate
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3, "mxfp8": 5000.0}
 METRIC = "decode tokens/s on 1 MI355X (gpt-oss-20b-shape layer); % of HBM / MFMA peak"
 PREFILL_MIN_Q = 16  # chunks of this many new tokens or more go to the prefill kernel
 
@@ -40,7 +41,8 @@ def log(msg):
 def make_workload(name):
     from paper_2608_22167_amd import workload as W
     makers = {"full_b64": W.full_b64, "sliding_b256": W.sliding_b256, "tiny_f32": W.tiny_f32,
-              "mixed_prefill": W.mixed_prefill, "stack24": W.stack24}
+              "mixed_prefill": W.mixed_prefill, "stack24": W.stack24,
+              "mixed_prefill_mxfp4": lambda: W.mixed_prefill(expert_fmt="mxfp4_native")}
     if name not in makers:
         raise SystemExit(f"unknown workload {name}; one of {sorted(makers)}")
     return makers[name]()
@@ -77,7 +79,7 @@ def layer_work(s, seq_lens, q_lens, idx):
             t_dec += int(q)
     rows = T * k
     touched = len(np.unique(idx))
-    wb = (lambda r, c: r * c // 2 + r * c // 32) if s.expert_fmt == "mxfp4" else (lambda r, c: r * c * eb)
+    wb = (lambda r, c: r * c // 2 + r * c // 32) if s.expert_fmt != "dense" else (lambda r, c: r * c * eb)
     work = {
         "attn_split": (dec_pairs * kvb + t_dec * A * eb, 4 * A * dec_pairs),
         "qkv": (s.qkv_dim * H * eb + T * H * eb + T * s.qkv_dim * eb, 2 * T * s.qkv_dim * H),
@@ -88,6 +90,13 @@ def layer_work(s, seq_lens, q_lens, idx):
     if t_pre:
         work["attn_prefill"] = (pre_keys * kvb + 2 * t_pre * A * eb, 4 * A * pre_pairs)
     return work, t_dec, t_pre
+
+
+def peak_key(kernel, shape):
+    """The matrix-core peak a kernel's products run against."""
+    if shape.expert_fmt == "mxfp4_native" and kernel in ("expert_gu", "expert_down"):
+        return "mxfp8"
+    return shape.dtype
 
 
 def roofline_of(work_bytes, work_flops, seconds, dtype):
@@ -297,7 +306,7 @@ def main():
         print(json.dumps({"error": "this benchmark runs on one GPU; the decode step is not sharded "
                                    "across GPUs in this build", "n_gpus": args.gpus}))
         raise SystemExit(2)
-    heavy = args.workload in STACK_WORKLOADS or args.workload == "mixed_prefill"
+    heavy = args.workload in STACK_WORKLOADS or args.workload.startswith("mixed_prefill")
     K = args.steps if args.steps is not None else (5 if heavy else 50)
     warmup = args.warmup if args.warmup is not None else (2 if heavy else 10)
 
@@ -377,10 +386,10 @@ def main():
     launch_flops = float(np.mean([per_launch[c][dominant][1] for c in cols]))
     dom_us = float(per.mean()) * 1e3
     roofline = {"kernel": dominant + (" (full-attention layers)" if cols != list(range(bench.launches)) else "")}
-    roofline.update(roofline_of(launch_bytes, launch_flops, dom_us * 1e-6, bench.shape.dtype))
+    roofline.update(roofline_of(launch_bytes, launch_flops, dom_us * 1e-6, peak_key(dominant, bench.shape)))
     roofline.update({"traffic": traffic_from_profile(dominant, args.workload), "avg_us": round(dom_us, 2),
                      "algorithmic_bytes": round(launch_bytes), "algorithmic_flops": round(launch_flops)})
-    kernels_util = {k: roofline_of(b, f, breakdown[k] * 1e-6, bench.shape.dtype)
+    kernels_util = {k: roofline_of(b, f, breakdown[k] * 1e-6, peak_key(k, bench.shape))
                     for k, (b, f) in work.items() if breakdown.get(k)}
     kernels_util = {k: f"{v['achieved']} {v['unit']} ({100 * v['frac']:.1f}% {v['bound']})"
                     for k, v in kernels_util.items()}

@@ -64,7 +64,11 @@ typedef enum {
 } mcpu_status;
 
 enum { MCPU_F32 = 0, MCPU_BF16 = 1 };               /* layer dtype */
-enum { MCPU_EXPERT_DENSE = 0, MCPU_EXPERT_MXFP4 = 1 }; /* expert weight format */
+/* expert weight format: dense (layer dtype); MXFP4 weights decoded to bf16
+ * for bf16 products; or MXFP4 weights on the scaled matrix cores against
+ * MXFP8 activations (the normalised rows and the SwiGLU activations are
+ * quantized per 32 elements, see moe_forward) */
+enum { MCPU_EXPERT_DENSE = 0, MCPU_EXPERT_MXFP4 = 1, MCPU_EXPERT_MXFP4_NATIVE = 2 };
 
 /* Device error bits (mcpu_check_device_errors). */
 enum {
@@ -215,7 +219,13 @@ int paged_attention(const mcpu_layer_cfg* cfg, const float* sinks, mcpu_kv_pool*
  *  topk_idx [n_tokens, k] int32 and topk_w [n_tokens, k] fp32 (device,
  *  nullable) receive the selection in descending logit order.
  *  force_idx (device, nullable, [n_tokens, k]): use these experts instead of
- *  the router's choice (weights still softmax of their logits). */
+ *  the router's choice (weights still softmax of their logits).
+ *  MCPU_EXPERT_MXFP4_NATIVE: the experts read hn (stored bf16) and the SwiGLU
+ *  activations (stored bf16) as MXFP8 (OCP MX v1.0): per row, blocks of 32
+ *  along the reduction share the E8M0 scale 2^(floor(log2 max|v|) - 8), and
+ *  each element is v / scale rounded to nearest-even FP8 E4M3, saturating at
+ *  448; products on the scaled matrix cores, fp32 accumulation (hidden and
+ *  ffn_dim multiples of 64). */
 size_t moe_forward_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_tokens);
 int moe_forward(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, int32_t n_tokens,
                 const float* h, float* out, int32_t* topk_idx, float* topk_w,
@@ -314,6 +324,14 @@ int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, con
                    const int32_t* seq_ids, const int32_t* positions, const int32_t* targets, int32_t* tokens_out,
                    float* logprob_out, float* target_logprob_out, float* lse_out, void* workspace,
                    size_t ws_bytes, hipStream_t stream);
+
+/* MXFP8 quantization of bf16 rows, the activation format of the native
+ * MXFP4 experts (see moe_forward): in [rows, cols] bf16 (16-byte aligned,
+ * cols a multiple of 32) -> codes [rows, cols] FP8 E4M3 (16-byte aligned) and
+ * scales [rows, cols / 32] E8M0; an all-zero block gets scale byte 0.
+ * Asynchronous on stream. */
+int mcpu_mxfp8_quantize(const void* in, int64_t rows, int32_t cols, uint8_t* codes, uint8_t* scales,
+                        hipStream_t stream);
 
 /* Token embedding: x_out[t] = table[tokens[t]] widened to fp32.
  *  table [vocab, hidden] bf16 (16-byte aligned), tokens device int32 [T],

@@ -48,6 +48,7 @@ typedef struct {
   int32_t window;    /* 0: full attention; else keys p-window+1 .. p */
   int32_t kv_bf16;   /* 1: the layer (cache and stored activations) is bfloat16 */
   int32_t kv_only;   /* 1: round only the cache entries; keep every activation unrounded */
+  int32_t act_mx;    /* 1: the expert products read MXFP8 (E4M3) activations, see orc_mxfp8_quant */
   double rms_eps, swiglu_alpha, swiglu_limit, swiglu_beta;
 } orc_cfg;
 
@@ -81,6 +82,8 @@ void orc_round_bf16_array(int64_t n, const double* in, double* out) {
 
 /* a value as the layer stores it: bfloat16 or binary32 */
 static double stored(const orc_cfg* c, double v) { return c->kv_bf16 ? orc_round_bf16(v) : (double)(float)v; }
+void orc_mxfp8_round_row(int64_t n, double* v);
+
 /* an activation the layer stores (not a cache entry): rounded unless kv_only */
 static double stored_act(const orc_cfg* c, double v) { return c->kv_only ? v : stored(c, v); }
 static void stored_array(const orc_cfg* c, int64_t n, double* v) {
@@ -302,6 +305,7 @@ static void expert_ffn(const orc_cfg* c, const orc_weights* w, int e, const doub
   linear(1, H, 2 * I, hn, w->w_gu + (int64_t)e * 2 * I * H, w->b_gu + (int64_t)e * 2 * I, gu);
   for (int j = 0; j < I; ++j)
     act[j] = stored_act(c, orc_swiglu(gu[2 * j], gu[2 * j + 1], c->swiglu_alpha, c->swiglu_limit, c->swiglu_beta));
+  if (c->act_mx) orc_mxfp8_round_row(I, act);  /* the second product reads the stored row in MXFP8 */
   linear(1, I, H, act, w->w_d + (int64_t)e * H * I, w->b_d + (int64_t)e * H, y);
 }
 
@@ -329,6 +333,7 @@ int orc_moe(const orc_cfg* c, const orc_weights* w, int T, const double* h, doub
     orc_rmsnorm(1, H, h + (int64_t)t * H, w->g2, c->rms_eps, hn);
     linear(1, H, E, hn, w->w_r, w->b_r, lg);
     stored_array(c, H, hn);  /* the router reads hn as computed; the experts its stored copy */
+    if (c->act_mx) orc_mxfp8_round_row(H, hn);  /* ... in MXFP8 when the experts take MXFP8 rows */
     if (force_idx) memcpy(sel, force_idx + (int64_t)t * k, sizeof(int32_t) * (size_t)k);
     else orc_topk(E, k, lg, sel);
     double mx = -INFINITY, den = 0.0;
@@ -599,4 +604,67 @@ int orc_lm_head(int T, int H, int V, const double* x, const float* g_final, doub
     free(xn); free(s);
   }
   return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* MXFP8 activations for the scaled matrix-core expert products (OCP        */
+/* Microscaling Formats v1.0): blocks of 32 consecutive elements of a row    */
+/* along the reduction axis share one E8M0 scale X = 2^e with                */
+/*   e = floor(log2(max |v|)) - 8   (8: the largest exponent of E4M3),       */
+/* and each element is v / X rounded to the nearest FP8 E4M3 value (ties to  */
+/* the even code), saturating at +-448. E4M3: sign, 4 exponent bits (bias 7), */
+/* 3 mantissa bits; exponent 0 holds the subnormals m / 8 * 2^-6; S.1111.111 */
+/* is NaN (never produced). An all-zero block gets scale byte 0 and zeros.   */
+/* The input is the stored bf16 row, so both sides quantize identical values. */
+/* ------------------------------------------------------------------------ */
+
+double orc_e4m3(int code) {
+  int sign = (code >> 7) & 1, ex = (code >> 3) & 15, man = code & 7;
+  if (ex == 15 && man == 7) return NAN;
+  double mag = ex == 0 ? ldexp((double)man / 8.0, -6) : ldexp(1.0 + man / 8.0, ex - 7);
+  return sign ? -mag : mag;
+}
+
+/* the nearest E4M3 code to x (ties to the even code), |x| saturating at 448 */
+int orc_e4m3_encode(double x) {
+  int sign = x < 0 ? 0x80 : 0;
+  double a = fabs(x);
+  int best = 0;
+  double bd = INFINITY;
+  for (int c = 0; c <= 0x7E; ++c) {  /* the 127 finite non-negative codes, ascending */
+    double d = fabs(orc_e4m3(c) - a);
+    if (d < bd || (d == bd && (c & 1) == 0)) { bd = d; best = c; }
+  }
+  if (best == 0) sign = 0;  /* no negative zero */
+  return sign | best;
+}
+
+int orc_mxfp8_quant(int64_t rows, int cols, const double* in, uint8_t* codes, uint8_t* scales) {
+  if (cols % 32) return ORC_EINVAL;
+  for (int64_t r = 0; r < rows; ++r)
+    for (int blk = 0; blk < cols / 32; ++blk) {
+      const double* v = in + r * cols + 32 * blk;
+      double amax = 0.0;
+      for (int j = 0; j < 32; ++j) if (fabs(v[j]) > amax) amax = fabs(v[j]);
+      int e = -127;
+      if (amax > 0.0) {
+        int ex;
+        frexp(amax, &ex);  /* amax = f * 2^ex, f in [0.5, 1): floor(log2 amax) = ex - 1 */
+        e = ex - 1 - 8;
+        if (e < -127) e = -127;
+        if (e > 127) e = 127;
+      }
+      scales[r * (cols / 32) + blk] = (uint8_t)(e + 127);
+      for (int j = 0; j < 32; ++j) codes[r * cols + 32 * blk + j] = (uint8_t)orc_e4m3_encode(ldexp(v[j], -e));
+    }
+  return ORC_OK;
+}
+
+/* a row replaced by its MXFP8 value (quantize, then decode exactly) */
+void orc_mxfp8_round_row(int64_t n, double* v) {
+  uint8_t codes[32], scale;
+  for (int64_t b = 0; b + 32 <= n; b += 32) {
+    orc_mxfp8_quant(1, 32, v + b, codes, &scale);
+    for (int j = 0; j < 32; ++j) v[b + j] = ldexp(orc_e4m3(codes[j]), (int)scale - 127);
+  }
 }

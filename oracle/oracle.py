@@ -21,7 +21,7 @@ c_i32p = ctypes.POINTER(ctypes.c_int32)
 class OrcCfg(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "hidden", "n_q_heads", "n_kv_heads", "head_dim", "n_experts", "top_k", "ffn_dim",
-        "page_size", "window", "kv_bf16", "kv_only")] + [
+        "page_size", "window", "kv_bf16", "kv_only", "act_mx")] + [
         (n, ctypes.c_double) for n in ("rms_eps", "swiglu_alpha", "swiglu_limit", "swiglu_beta")]
 
 
@@ -67,6 +67,10 @@ def lib():
         L.orc_gumbel.argtypes = [f64]
         L.orc_lm_head.argtypes = [i32, i32, i32, vp, vp, f64, vp, f64, ctypes.c_uint64, vp, vp, vp, vp, vp, vp,
                                   vp, vp, vp]
+        L.orc_e4m3.restype = f64
+        L.orc_e4m3.argtypes = [i32]
+        L.orc_e4m3_encode.argtypes = [f64]
+        L.orc_mxfp8_quant.argtypes = [i64, i32, vp, vp, vp]
         L.orc_pool_to_logical.argtypes = [vp, i32, vp, vp, vp, vp]
         L.orc_pool_from_logical.argtypes = [vp, i32, vp, vp, vp, vp]
     return _LIB
@@ -100,6 +104,7 @@ def make_cfg(shape, kv_only=False) -> OrcCfg:
                   head_dim=shape.head_dim, n_experts=shape.n_experts, top_k=shape.top_k,
                   ffn_dim=shape.ffn_dim, page_size=shape.page_size, window=shape.window,
                   kv_bf16=1 if shape.dtype == "bf16" else 0, kv_only=1 if kv_only else 0,
+                  act_mx=1 if getattr(shape, "expert_fmt", "") == "mxfp4_native" else 0,
                   rms_eps=shape.rms_eps,
                   swiglu_alpha=shape.swiglu_alpha, swiglu_limit=shape.swiglu_limit,
                   swiglu_beta=shape.swiglu_beta)
@@ -337,3 +342,22 @@ def lm_head(x, g_final, w_lm, eps, temperature, seed=0, seq_ids=None, positions=
     if rc:
         raise ValueError("lm_head: sampling needs seq_ids and positions")
     return r
+
+
+def e4m3(code: int) -> float:
+    return lib().orc_e4m3(code)
+
+
+def e4m3_encode(x: float) -> int:
+    return lib().orc_e4m3_encode(float(x))
+
+
+def mxfp8_quant(x):
+    """Rows x [R, C] (C a multiple of 32) -> (codes uint8 [R, C], scales uint8 [R, C/32])."""
+    xx = _np(x, np.float64)
+    R, C = xx.shape
+    codes = np.empty((R, C), np.uint8)
+    scales = np.empty((R, C // 32), np.uint8)
+    if lib().orc_mxfp8_quant(R, C, _p(xx), _p(codes), _p(scales)):
+        raise ValueError("mxfp8_quant: columns must be a multiple of 32")
+    return codes, scales

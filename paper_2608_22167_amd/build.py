@@ -15,14 +15,14 @@ HIP_FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I" + os.path.join(ROOT, "include"),
 ]
-SOURCES = ["attention.hip", "gemm.hip", "gemm_tiled.hip", "gemm_pipe.hip", "gemm_slab.hip", "moe.hip", "lm_head.hip",
-           "mcpu_host.hip"]
+SOURCES = ["attention.hip", "gemm.hip", "gemm_tiled.hip", "gemm_pipe.hip", "gemm_slab.hip", "gemm_mx.hip", "moe.hip",
+           "lm_head.hip", "mcpu_host.hip"]
 # per-source code generation: the tiled GEMM and the attention kernels keep
 # their matrix-core accumulators in ordinary VGPRs (the AGPR form shuffles them
 # between loop iterations and needs more registers in all)
 _VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 SOURCE_FLAGS = {"gemm_tiled.hip": _VGPR_FORM, "gemm_pipe.hip": _VGPR_FORM, "gemm_slab.hip": _VGPR_FORM,
-                "attention.hip": _VGPR_FORM}
+                "gemm_mx.hip": _VGPR_FORM, "attention.hip": _VGPR_FORM}
 
 
 def _run(cmd):

@@ -254,6 +254,7 @@ static hipError_t gemm_dispatch_mxfp4(const Gemm& g, hipStream_t s) {
 
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s) {
   if (g.n_groups == 0 || g.n == 0) return hipSuccess;
+  if (expert_fmt == 2) return dtype == 1 ? launch_gemm_mx(g, s) : hipErrorNotSupported;  // MXFP8 x MXFP4
   if (g.epi == EPI_LOGITS) {  // the slab, tiled and pipelined kernels carry the logits epilogue
     if (slab_gemm_applies(dtype, expert_fmt, g)) return launch_gemm_slab(expert_fmt, g, s);
     if (tiled_gemm_applies(dtype, g)) return launch_gemm_tiled(expert_fmt, g, s);

@@ -134,7 +134,8 @@ struct Gemm {
   const uint8_t* w_scales;  // MXFP4 block scales or nullptr
   int64_t w_group_stride;   // elements (or bytes for MXFP4 codes) per group
   int n, k;
-  const void* x;            // [*, k] layer dtype
+  const void* x;            // [*, k] layer dtype (MXFP8 experts: E4M3 codes)
+  const uint8_t* x_scales;  // MXFP8 activations: E8M0 scales [*, k / 32], else nullptr
   const int32_t* row_src;   // nullptr = identity
   const int32_t* group_off; // nullptr = one group of n_rows rows
   int n_rows, n_groups;
@@ -180,6 +181,19 @@ struct Gemm {
 };
 constexpr uint32_t LOGIT_RNG_TAG = 0x4C4D5330u;  // counter word 3 of the sampling draws
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s);
+// Scaled matrix-core products (gemm_mx.hip): MXFP8 activations (x, x_scales)
+// times MXFP4 weights (w, w_scales); k a multiple of 64, n of 16.
+bool mx_gemm_applies(const Gemm& g);
+hipError_t launch_gemm_mx(const Gemm& g, hipStream_t s);
+// bf16 rows -> MXFP8: codes [rows][cols] E4M3, scales [rows][cols / 32] E8M0
+struct MxQuant {
+  const void* in;  // [rows][cols] bf16
+  int64_t rows;
+  int cols;
+  uint8_t* codes;
+  uint8_t* scales;
+};
+hipError_t launch_mx_quant(const MxQuant& p, hipStream_t s);
 // LDS-tiled path (gemm_tiled.hip): bf16, k a multiple of 64, at least
 // TILED_MIN_TOTAL_ROWS rows in all and groups averaging TILED_MIN_ROWS rows;
 // n_rows must then hold the total row count.

@@ -65,10 +65,13 @@ int check_cfg(const mcpu_layer_cfg* c) {
   if (c->n_experts <= 0 || c->n_experts > 64) return fail(MCPU_EINVAL, "n_experts %d not in [1, 64]", c->n_experts);
   if (c->top_k <= 0 || c->top_k > std::min(8, c->n_experts)) return fail(MCPU_EINVAL, "top_k %d", c->top_k);
   if (c->window < 0) return fail(MCPU_EINVAL, "window %d", c->window);
-  if (c->expert_fmt != MCPU_EXPERT_DENSE && c->expert_fmt != MCPU_EXPERT_MXFP4)
+  if (c->expert_fmt != MCPU_EXPERT_DENSE && c->expert_fmt != MCPU_EXPERT_MXFP4 &&
+      c->expert_fmt != MCPU_EXPERT_MXFP4_NATIVE)
     return fail(MCPU_EINVAL, "expert_fmt %d", c->expert_fmt);
-  if (c->expert_fmt == MCPU_EXPERT_MXFP4 && c->dtype != MCPU_BF16)
+  if (c->expert_fmt != MCPU_EXPERT_DENSE && c->dtype != MCPU_BF16)
     return fail(MCPU_EUNSUPPORTED, "MXFP4 experts need a bf16 layer");
+  if (c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE && (c->hidden % 64 || c->ffn_dim % 64))
+    return fail(MCPU_EUNSUPPORTED, "native MXFP4 experts need hidden and ffn_dim multiples of 64");
   if (!(c->rms_eps >= 0.f)) return fail(MCPU_EINVAL, "rms_eps");
   return MCPU_OK;
 }
@@ -215,6 +218,8 @@ struct MoeBufs {
   int32_t *group_off, *pos_of, *src_tok, *chunk_cnt;
   void* act;
   float* y;
+  // native MXFP4 experts: MXFP8 copies of hn and act (codes, scales)
+  uint8_t *hq, *hs, *aq, *as;
 };
 
 MoeBufs carve_moe(Carve& cv, const mcpu_layer_cfg* c, int max_tokens) {
@@ -229,6 +234,13 @@ MoeBufs carve_moe(Carve& cv, const mcpu_layer_cfg* c, int max_tokens) {
   m.chunk_cnt = cv.take<int32_t>((T * K + PERM_CHUNK - 1) / PERM_CHUNK * c->n_experts);
   m.act = cv.take_bytes(T * K * c->ffn_dim * db);
   m.y = cv.take<float>(T * K * c->hidden);
+  m.hq = m.hs = m.aq = m.as = nullptr;
+  if (c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE) {
+    m.hq = cv.take<uint8_t>(T * c->hidden);
+    m.hs = cv.take<uint8_t>(T * c->hidden / 32);
+    m.aq = cv.take<uint8_t>(T * K * c->ffn_dim);
+    m.as = cv.take<uint8_t>(T * K * c->ffn_dim / 32);
+  }
   return m;
 }
 
@@ -236,7 +248,7 @@ int check_weights(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, bool att
   if (!w) return fail(MCPU_EINVAL, "weights is NULL");
   if (!w->g2 || !w->w_r || !w->b_r || !w->w_gu || !w->b_gu || !w->w_d || !w->b_d)
     return fail(MCPU_EINVAL, "a MoE weight pointer is NULL");
-  if (c->expert_fmt == MCPU_EXPERT_MXFP4 && (!w->s_gu || !w->s_d))
+  if (c->expert_fmt != MCPU_EXPERT_DENSE && (!w->s_gu || !w->s_d))
     return fail(MCPU_EINVAL, "MXFP4 experts need the scale arrays s_gu and s_d");
   if (attn && (!w->g1 || !w->w_qkv || !w->b_qkv || !w->w_o || !w->b_o || !w->rope_cos || !w->rope_sin))
     return fail(MCPU_EINVAL, "an attention weight pointer is NULL");
@@ -277,10 +289,16 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
 
   const int max_rows = force_idx ? T * K : T;  // a token picks each expert at most once
   // per-expert stride: elements for dense experts, bytes of E2M1 codes for MXFP4
-  const int64_t fdiv = c->expert_fmt == MCPU_EXPERT_MXFP4 ? 2 : 1;
+  const int64_t fdiv = c->expert_fmt != MCPU_EXPERT_DENSE ? 2 : 1;
+  const bool native = c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE;
+  if (native) {  // the first product reads the normalised rows in MXFP8
+    MxQuant q{};
+    q.in = m.hn; q.rows = T; q.cols = H; q.codes = m.hq; q.scales = m.hs;
+    HIP_TRY(launch_mx_quant(q, st));
+  }
   Gemm g1{};
   g1.w = w->w_gu; g1.w_scales = w->s_gu; g1.w_group_stride = (int64_t)2 * I * H / fdiv; g1.n = 2 * I; g1.k = H;
-  g1.x = m.hn; g1.row_src = m.src_tok; g1.group_off = m.group_off; g1.n_rows = T * K; g1.n_groups = E;
+  g1.x = native ? (const void*)m.hq : m.hn; g1.x_scales = native ? m.hs : nullptr; g1.row_src = m.src_tok; g1.group_off = m.group_off; g1.n_rows = T * K; g1.n_groups = E;
   g1.epi = EPI_SWIGLU; g1.bias = w->b_gu; g1.bias_group_stride = 2 * I; g1.out = m.act;
   g1.swiglu_alpha = c->swiglu_alpha; g1.swiglu_limit = c->swiglu_limit; g1.swiglu_beta = c->swiglu_beta;
   g1.err = err; g1.max_rows_per_group = max_rows; g1.x_rows = T; g1.w_packed = w->w_gu_packed;
@@ -289,9 +307,14 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
     HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g1, st));
   }
 
+  if (native) {  // ... and the second its SwiGLU activations in MXFP8
+    MxQuant q{};
+    q.in = m.act; q.rows = (int64_t)T * K; q.cols = I; q.codes = m.aq; q.scales = m.as;
+    HIP_TRY(launch_mx_quant(q, st));
+  }
   Gemm g2{};
   g2.w = w->w_d; g2.w_scales = w->s_d; g2.w_group_stride = (int64_t)H * I / fdiv; g2.n = H; g2.k = I;
-  g2.x = m.act; g2.group_off = m.group_off; g2.n_rows = T * K; g2.n_groups = E;
+  g2.x = native ? (const void*)m.aq : m.act; g2.x_scales = native ? m.as : nullptr; g2.group_off = m.group_off; g2.n_rows = T * K; g2.n_groups = E;
   g2.epi = EPI_BIAS; g2.bias = w->b_d; g2.bias_group_stride = H; g2.out = m.y;
   g2.err = err; g2.max_rows_per_group = max_rows; g2.w_packed = w->w_d_packed;
   {
@@ -700,6 +723,18 @@ int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, con
   r.slots = slots; r.n_rows = n_tokens; r.n_slots = n_slots; r.tokens = tokens_out; r.logprob = logprob_out;
   r.lse = lse_out; r.target_logprob = targets ? target_logprob_out : nullptr;
   HIP_TRY(launch_lm_reduce(r, stream));
+  return MCPU_OK;
+}
+
+int mcpu_mxfp8_quantize(const void* in, int64_t rows, int32_t cols, uint8_t* codes, uint8_t* scales,
+                        hipStream_t stream) {
+  if (rows < 0 || cols <= 0 || cols % 32) return fail(MCPU_EINVAL, "rows %lld, cols %d (a multiple of 32)", (long long)rows, cols);
+  if (rows == 0) return MCPU_OK;
+  if (!in || !codes || !scales) return fail(MCPU_EINVAL, "NULL pointer");
+  if ((uintptr_t)in % 16 || (uintptr_t)codes % 16) return fail(MCPU_EINVAL, "in and codes must be 16-byte aligned");
+  MxQuant q{};
+  q.in = in; q.rows = rows; q.cols = cols; q.codes = codes; q.scales = scales;
+  HIP_TRY(launch_mx_quant(q, stream));
   return MCPU_OK;
 }
 

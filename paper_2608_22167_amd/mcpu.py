@@ -19,7 +19,8 @@ LIB_PATH = os.path.join(_HERE, "libmcpu.so")
 
 MCPU_OK, MCPU_EINVAL, MCPU_ENOMEM, MCPU_EHIP, MCPU_EUNSUPPORTED, MCPU_EDEVICE = 0, -1, -2, -3, -4, -5
 MCPU_F32, MCPU_BF16 = 0, 1
-MCPU_EXPERT_DENSE, MCPU_EXPERT_MXFP4 = 0, 1
+MCPU_EXPERT_DENSE, MCPU_EXPERT_MXFP4, MCPU_EXPERT_MXFP4_NATIVE = 0, 1, 2
+_EXPERT_FMT = {"dense": MCPU_EXPERT_DENSE, "mxfp4": MCPU_EXPERT_MXFP4, "mxfp4_native": MCPU_EXPERT_MXFP4_NATIVE}
 DEVERR_PAGE, DEVERR_ROPE, DEVERR_EXPERT, DEVERR_PLAN, DEVERR_MXFP4 = 1, 2, 4, 8, 16
 
 EXPORTED = ("mcpu_last_error", "kv_pool_create", "kv_pool_destroy", "kv_pool_free_pages",
@@ -27,7 +28,8 @@ EXPORTED = ("mcpu_last_error", "kv_pool_create", "kv_pool_destroy", "kv_pool_fre
             "paged_attention", "moe_forward_workspace_size", "moe_forward",
             "decode_layer_workspace_size", "decode_layer", "mcpu_check_device_errors",
             "mcpu_timing_start", "mcpu_timing_read", "mcpu_packed_weights_bytes", "mcpu_pack_weights",
-            "lm_head_workspace_size", "lm_head_sample", "embed_tokens", "decode_layer_noalloc")
+            "lm_head_workspace_size", "lm_head_sample", "embed_tokens", "decode_layer_noalloc",
+            "mcpu_mxfp8_quantize")
 NOALLOC_SCRATCH_BYTES = 128 << 20  # the static scratch of decode_layer_noalloc, per GPU
 
 KERNELS = ("attn_plan", "rmsnorm", "qkv", "attn_split", "attn_combine", "oproj", "router", "permute",
@@ -104,6 +106,7 @@ def lib():
         L.lm_head_sample.argtypes = [vp, i32, vp, vp, ctypes.c_float, ctypes.c_uint64, vp, vp, vp, vp, vp, vp,
                                      vp, vp, sz, vp]
         L.embed_tokens.argtypes = [vp, i32, i32, i32, vp, vp, vp, sz, vp]
+        L.mcpu_mxfp8_quantize.argtypes = [vp, ctypes.c_int64, i32, vp, vp, vp]
         L.mcpu_timing_start.argtypes = [i32, i32]
         L.mcpu_timing_read.argtypes = [i32, vp, i32, i32p]
         _LIB = L
@@ -148,7 +151,7 @@ def make_cfg(shape) -> LayerCfg:
                     head_dim=shape.head_dim, n_experts=shape.n_experts, top_k=shape.top_k,
                     ffn_dim=shape.ffn_dim, page_size=shape.page_size, window=shape.window,
                     dtype=MCPU_F32 if shape.dtype == "f32" else MCPU_BF16,
-                    expert_fmt=MCPU_EXPERT_DENSE if shape.expert_fmt == "dense" else MCPU_EXPERT_MXFP4,
+                    expert_fmt=_EXPERT_FMT[shape.expert_fmt],
                     rms_eps=shape.rms_eps, swiglu_alpha=shape.swiglu_alpha,
                     swiglu_limit=shape.swiglu_limit, swiglu_beta=shape.swiglu_beta)
 
@@ -172,7 +175,7 @@ class DeviceWeights:
     def __init__(self, shape, W, device="cuda", pack=True):
         self.t = {k: v.to(device).contiguous() for k, v in W.items()}
         t = self.t
-        mx = shape.expert_fmt == "mxfp4"
+        mx = shape.expert_fmt != "dense"
         if pack and not mx and shape.dtype == "bf16" and shape.hidden % 64 == 0 and shape.ffn_dim % 64 == 0:
             t["w_gu_packed"] = packed_weights(t["w_gu"])
             t["w_d_packed"] = packed_weights(t["w_d"])
@@ -362,6 +365,16 @@ def lm_head_sample(head: DeviceLmHead, x, temperature, seed=0, seq_ids=None, pos
                                 _ptr(seq_ids), _ptr(positions), _ptr(targets), _ptr(tokens), _ptr(logprob),
                                 _ptr(target_logprob), _ptr(lse), _ptr(workspace),
                                 workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def mxfp8_quantize(x, stream=None):
+    """bf16 rows [R, C] on the GPU -> (codes uint8 [R, C], scales uint8 [R, C/32])."""
+    assert x.dtype == torch.bfloat16 and x.is_contiguous()
+    R, C = (int(d) for d in x.shape)
+    codes = torch.empty((R, C), dtype=torch.uint8, device=x.device)
+    scales = torch.empty((R, C // 32), dtype=torch.uint8, device=x.device)
+    _check(lib().mcpu_mxfp8_quantize(_ptr(x), R, C, _ptr(codes), _ptr(scales), _stream(stream)))
+    return codes, scales
 
 
 def embed_tokens(table, tokens, x_out, workspace, stream=None):

@@ -42,7 +42,7 @@ class LayerShape:
     ffn_dim: int
     window: int = 0            # 0 = full attention, else keys [p-window+1, p]
     dtype: str = "bf16"        # "f32" or "bf16": matrices, KV cache, GEMM operands
-    expert_fmt: str = "dense"  # "dense" (same dtype) or "mxfp4"
+    expert_fmt: str = "dense"  # "dense" (same dtype), "mxfp4", or "mxfp4_native" (MXFP8 activations)
     page_size: int = PAGE
     rms_eps: float = 1e-5
     swiglu_alpha: float = 1.702
@@ -50,7 +50,7 @@ class LayerShape:
     swiglu_beta: float = 1.0
 
     def __post_init__(self):
-        if self.dtype not in ("f32", "bf16") or self.expert_fmt not in ("dense", "mxfp4"):
+        if self.dtype not in ("f32", "bf16") or self.expert_fmt not in ("dense", "mxfp4", "mxfp4_native"):
             raise ValueError(f"dtype {self.dtype!r} / expert_fmt {self.expert_fmt!r}")
 
     @property
@@ -418,16 +418,18 @@ def sliding_b256(seed=1003, batch=256, median=4096, cap=32768, **kw) -> Workload
 
 
 def mixed_prefill(seed=1004, n_dec=192, n_pre=64, ctx_lo=1024, ctx_hi=24576,
-                  chunk_lo=256, chunk_hi=4096, **kw) -> Workload:
+                  chunk_lo=256, chunk_hi=4096, expert_fmt="dense", **kw) -> Workload:
     """Mixed step: n_dec decode sequences + n_pre sequences appending tool-observation
-    chunks of U{256..4096} tokens; contexts U{1024..24576}; full attention, bf16."""
+    chunks of U{256..4096} tokens; contexts U{1024..24576}; full attention, bf16
+    (experts bf16, or MXFP4 with expert_fmt)."""
     rng = np.random.default_rng(seed + 1)
     B = n_dec + n_pre
     ctx = rng.integers(ctx_lo, ctx_hi + 1, size=B)
     q = np.ones(B, dtype=np.int32)
     q[n_dec:] = rng.integers(chunk_lo, chunk_hi + 1, size=n_pre)
-    return make_workload("mixed_bf16_%ddec_%dpre" % (n_dec, n_pre),
-                         kw.pop("shape", GPT_OSS_20B), ctx, q, seed, **kw)
+    shape = replace(kw.pop("shape", GPT_OSS_20B), expert_fmt=expert_fmt)
+    tag = {"dense": "bf16", "mxfp4": "mxfp4", "mxfp4_native": "mxfp4x8"}[expert_fmt]
+    return make_workload("mixed_%s_%ddec_%dpre" % (tag, n_dec, n_pre), shape, ctx, q, seed, **kw)
 
 
 def restrict(wl: Workload, seqs):

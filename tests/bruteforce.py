@@ -100,11 +100,13 @@ def stored(x, dtype):
 
 def moe_token(hn, W, shape, force=None, kv_only=False):
     """The router reads hn itself; the experts read its stored copy and store
-    their SwiGLU activations (kv_only: neither is rounded)."""
+    their SwiGLU activations (kv_only: neither is rounded). Native MXFP4
+    experts read both stored rows as MXFP8."""
     f = lambda k: np.asarray(W[k], dtype=np.float64)
     act = (lambda x, dt: np.asarray(x, np.float64)) if kv_only else stored
+    mx = (lambda x: mxfp8_round(x)) if shape.expert_fmt == "mxfp4_native" else (lambda x: x)
     logits = f("w_r") @ hn + f("b_r")
-    hs = act(hn, shape.dtype)
+    hs = mx(act(hn, shape.dtype))
     lf = logits.astype(np.float32)
     order = np.argsort(-lf, kind="stable")
     sel = order[: shape.top_k] if force is None else np.asarray(force)
@@ -113,8 +115,8 @@ def moe_token(hn, W, shape, force=None, kv_only=False):
     acc = np.zeros(shape.hidden)
     for e, we in zip(sel, w):
         gu = f("w_gu")[e] @ hs + f("b_gu")[e]
-        a = act(swiglu(gu[0::2], gu[1::2], shape.swiglu_alpha, shape.swiglu_limit, shape.swiglu_beta),
-                shape.dtype)
+        a = mx(act(swiglu(gu[0::2], gu[1::2], shape.swiglu_alpha, shape.swiglu_limit, shape.swiglu_beta),
+                   shape.dtype))
         acc += we * (f("w_d")[e] @ a + f("b_d")[e])
     return acc, sel, w, logits
 
@@ -177,3 +179,27 @@ def decode_layer(wl, kv_only=False):
         out[t] = h1[t] + acc
         idx[t], ws[t] = sel, w
     return dict(out=out, o=o_all, h1=h1, idx=idx, w=ws, q=q_all)
+
+
+# MXFP8 (OCP MX v1.0) restated with numpy: the E4M3 grid spacing at |v| is
+# 2^(max(floor(log2 |v|), -6) - 3); round half to even on that grid (numpy's
+# rint), saturate at 448; scale 2^(floor(log2 amax) - 8) per 32 elements.
+def e4m3_round(y):
+    y = np.asarray(y, np.float64)
+    a = np.abs(y)
+    with np.errstate(divide="ignore"):
+        ex = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    step = np.exp2(np.maximum(ex, -6.0) - 3.0)
+    r = np.rint(a / step) * step
+    return np.sign(y) * np.minimum(r, 448.0)
+
+
+def mxfp8_round(x):
+    """Rows x [..., C] (C % 32 == 0) replaced by their MXFP8 values."""
+    x = np.asarray(x, np.float64)
+    b = x.reshape(-1, 32)
+    amax = np.abs(b).max(axis=1, keepdims=True)
+    with np.errstate(divide="ignore"):
+        e = np.where(amax > 0, np.floor(np.log2(np.where(amax > 0, amax, 1.0))) - 8.0, -127.0)
+    e = np.clip(e, -127.0, 127.0)
+    return (e4m3_round(b / np.exp2(e)) * np.exp2(e)).reshape(x.shape)
