@@ -225,7 +225,8 @@ int paged_attention(const mcpu_layer_cfg* cfg, const float* sinks, mcpu_kv_pool*
  *  along the reduction share the E8M0 scale 2^(floor(log2 max|v|) - 8), and
  *  each element is v / scale rounded to nearest-even FP8 E4M3, saturating at
  *  448; products on the scaled matrix cores, fp32 accumulation (hidden and
- *  ffn_dim multiples of 64). */
+ *  ffn_dim multiples of 64 and at most 3072, else MCPU_EUNSUPPORTED; s_gu and
+ *  s_d 16-byte aligned). */
 size_t moe_forward_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_tokens);
 int moe_forward(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, int32_t n_tokens,
                 const float* h, float* out, int32_t* topk_idx, float* topk_w,

@@ -16,10 +16,15 @@
 //
 // Tile 256 token rows x 256 weight rows, eight wavefronts (2 x 4), each
 // owning 128 x 64 = 4 x 2 products of 32 x 32; the reduction runs in stages
-// of 128 (two products deep) through two LDS buffers, one barrier per stage. LDS rows are 160 B (A, 128 B
-// of data) and 96 B (B, 64 B) apart, which keeps the 16-byte fragment reads
-// free of bank conflicts. The finished fp32 tile goes through LDS to the
-// fused epilogue (gemm_epilogue.h), 32 rows at a time.
+// of 128 (two products deep) through two LDS buffers, one barrier per stage.
+// LDS rows are 160 B (A, 128 B of data) and 96 B (B, 64 B) apart, which keeps
+// the 16-byte fragment reads free of bank conflicts. Scales: the activation
+// rows' four scale bytes of a stage are one dword (the operand layout groups
+// them so), staged with the codes; the tile's weight scales, a contiguous run
+// of 256 rows, are copied to LDS once and read from there for the whole
+// reduction, so no scale byte costs a separate memory request. The finished
+// fp32 tile goes through LDS to the fused epilogue (gemm_epilogue.h), 32 rows
+// at a time.
 #include <type_traits>
 
 #include "device.h"
@@ -37,9 +42,11 @@ constexpr int XM = 256, XN = 256, XK = 128;  // output tile, reduction per stage
 constexpr int XTH = 512;
 constexpr int XA_LD = 160, XB_LD = 96;       // staged row strides (bytes)
 constexpr int XA_BYTES = XM * XA_LD, XB_BYTES = XN * XB_LD;
-constexpr int XSTAGE = XA_BYTES + XB_BYTES + 4 * (XM + XN);
+constexpr int XSTAGE = XA_BYTES + XB_BYTES + 4 * XM;  // + the token rows' scale dwords
+constexpr int XBS_BYTES = XN * (MX_MAX_K / 32);       // the tile's weight scales
 constexpr int XEP = 32, XCLD = XN + 4;       // epilogue pass rows, fp32 row stride
 static_assert(XEP * XCLD * 4 <= XSTAGE, "an epilogue pass fits one stage");
+static_assert(2 * XSTAGE + XBS_BYTES + 4 * (TILE_MAXG + 1) <= 160 * 1024, "LDS");
 constexpr int XGM = 2;                       // m-tiles per band
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
@@ -47,7 +54,7 @@ __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4
 
 template <int EPI>
 __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
-  __shared__ __align__(16) uint8_t lds[2 * XSTAGE];
+  __shared__ __align__(16) uint8_t lds[2 * XSTAGE + XBS_BYTES];
   __shared__ int mt_start[TILE_MAXG + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
 
@@ -58,53 +65,54 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   const int m0 = uniform(gr0 + mt * XM);
   const int mrows = min(XM, gr1 - m0);
   const int n0 = uniform(tn * XN), nrows = min(XN, P.n - n0);
-  const int K = P.k;
+  const int K = P.k, kb32 = K / 32, lda = mx_code_stride(K);
+  const uint32_t xrows = (uint32_t)(P.x_rows > 0 ? P.x_rows : P.n_rows);
 
   // staging: A chunk c = tid + 512 j (j < 4) is row c / 8, 16-byte piece c % 8;
   // B chunk c = tid + 512 j (j < 2) is row c / 4, piece c % 4; threads 0-255
-  // stage the four A scale bytes of row tid, threads 256-511 those of B row
-  // tid - 256. Rows past the tile's end repeat its last row (results dropped).
-  // Token rows, one expert's weights and the scale rows are addressed by
-  // 32-bit offsets from uniform bases (the host checks that they fit).
+  // stage the scale dword of token row tid. Rows past the tile's end repeat
+  // its last row (results dropped). Token rows, one expert's weights and the
+  // scale rows are addressed by 32-bit offsets from uniform bases (the host
+  // checks that they fit).
   const uint8_t* xq = reinterpret_cast<const uint8_t*>(P.x);
   const uint8_t* wq = reinterpret_cast<const uint8_t*>(P.w) + grp * P.w_group_stride;
-  const uint8_t* ws = P.w_scales + grp * (P.w_group_stride / 16);
-  const int kb32 = K / 32;
-  // a thread's staging pieces: A piece tid & 7 (bytes 16 (tid & 7) of a
-  // 128-byte row slice) of rows tid / 8 + 64 j; B piece tid & 3 of rows
-  // tid / 4 + 128 j
+  const uint8_t* ws = P.w_scales + grp * (P.w_group_stride / 16) + (uint32_t)n0 * (uint32_t)kb32;
   const uint32_t a_piece = 16u * (tid & 7), b_piece = 16u * (tid & 3);
-  uint32_t a_off[4], b_off[2], s_off;
+  uint32_t a_off[4], b_off[2], s_row;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int r = (tid + XTH * j) >> 3;
     const int row = m0 + min(r, mrows - 1);
     const int src = P.row_src ? P.row_src[row] : row;
-    a_off[j] = (uint32_t)src * (uint32_t)K;
+    a_off[j] = (uint32_t)src * (uint32_t)lda;
   }
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int r = (tid + XTH * j) >> 2;
     b_off[j] = (uint32_t)(n0 + min(r, nrows - 1)) * (uint32_t)(K / 2);
   }
-  const bool s_is_a = tid < 256;  // threads 0-255: token-row scales, 256-511: weight-row scales
-  const uint8_t* s_base = s_is_a ? P.x_scales : ws;
   {
-    const int r = tid & 255;
-    if (s_is_a) {
-      const int row = m0 + min(r, mrows - 1);
-      s_off = (uint32_t)(P.row_src ? P.row_src[row] : row) * (uint32_t)kb32;
-    } else {
-      s_off = (uint32_t)(n0 + min(r, nrows - 1)) * (uint32_t)kb32;
-    }
+    const int row = m0 + min(tid & 255, mrows - 1);
+    s_row = (uint32_t)(P.row_src ? P.row_src[row] : row);
   }
+
+  // the tile's weight scales [256 rows][kb32] into LDS (rows past the end
+  // get scale 1; the run is a multiple of 16 bytes since n is of 16)
+  uint8_t* bsc = lds + 2 * XSTAGE;
+  {
+    const int span = nrows * kb32;
+    const u32x4 one = {0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu};
+    for (int c = 16 * tid; c < XN * kb32; c += 16 * XTH) st16(bsc + c, c < span ? ld16(ws + c) : one);
+  }
+
   struct Regs {
     u32x4 a[4], b[2];
     uint32_t s;
   };
   // Past the end of the reduction (a last stage of 64) the pieces are zero:
   // the load address is clamped into the row and the value replaced, so no
-  // load is conditional and none leaves the row.
+  // load is conditional and none leaves the row; scale bytes past the end
+  // become 1.
   auto fetch = [&](Regs& g, int st) __attribute__((always_inline)) {
     const int k0 = st * XK;
     const u32x4 z = {0u, 0u, 0u, 0u};
@@ -120,21 +128,22 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
       const u32x4 v = ld16(wq + (b_off[j] + kb_c));
       g.b[j] = kb < K / 2 ? v : z;
     }
-    uint32_t s = 0;
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int blk = k0 / 32 + b;
-      const uint32_t v = s_base[s_off + (uint32_t)min(blk, kb32 - 1)];
-      s |= (blk < kb32 ? v : 127u) << (8 * b);
+    if (tid < 256) {
+      uint32_t s = *reinterpret_cast<const uint32_t*>(P.x_scales + ((uint32_t)st * xrows + s_row) * 4u);
+      const int valid = kb32 - 4 * st;  // uniform
+      if (valid < 4) {
+        const uint32_t keep = (1u << (8 * valid)) - 1u;
+        s = (s & keep) | (0x7F7F7F7Fu & ~keep);
+      }
+      g.s = s;
     }
-    g.s = s;
   };
   auto store = [&](const Regs& g, uint8_t* stage) __attribute__((always_inline)) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) st16(stage + ((tid + XTH * j) >> 3) * XA_LD + a_piece, g.a[j]);
 #pragma unroll
     for (int j = 0; j < 2; ++j) st16(stage + XA_BYTES + ((tid + XTH * j) >> 2) * XB_LD + b_piece, g.b[j]);
-    *reinterpret_cast<uint32_t*>(stage + XA_BYTES + XB_BYTES + 4 * tid) = g.s;
+    if (tid < 256) *reinterpret_cast<uint32_t*>(stage + XA_BYTES + XB_BYTES + 4 * tid) = g.s;
   };
 
   // wavefront (wm, wn): token rows wm * 128 + [0, 128), weight rows wn * 64 + [0, 64)
@@ -148,22 +157,19 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
 #pragma unroll
       for (int j = 0; j < 16; ++j) acc[rt][ct][j] = 0.f;
 
-  // KS (1 or 2, a compile-time count) products deep per fragment pair
-  auto compute = [&](const uint8_t* stage, auto KS_) __attribute__((always_inline)) {
-    constexpr int KS = decltype(KS_)::value;
+  // the two product depths of stage st, one at a time (the next depth's
+  // fragments are not read ahead: their registers would spill the accumulators)
+  auto compute = [&](const uint8_t* stage, int st) __attribute__((always_inline)) {
     const uint8_t* sa = stage + XA_BYTES + XB_BYTES;
-    const uint8_t* sb = sa + 4 * XM;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      // one product depth at a time: the next depth's fragments are not read
-      // ahead (their registers would spill the accumulators)
-      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll 1
+    for (int ks = 0; ks < 2; ++ks) {
       union Op {
         v8i v;
         u32x4 h[2];
       };
       Op a[4], b[2];
       int sca[4], scb[2];
+      const int blk = min(4 * st + 2 * ks + fg, kb32 - 1);
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt) {
         const int row = wm * 128 + rt * 32 + fr;
@@ -177,7 +183,7 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
         const int row = wn * 64 + ct * 32 + fr;
         b[ct].h[0] = ld16(stage + XA_BYTES + row * XB_LD + 32 * ks + 16 * fg);
         b[ct].h[1] = u32x4{0u, 0u, 0u, 0u};
-        scb[ct] = sb[row * 4 + 2 * ks + fg];
+        scb[ct] = bsc[row * kb32 + blk];
       }
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt)
@@ -206,7 +212,7 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
     if (more) fetch(r, s + 1);
     // a last stage of 64 (k % 128 == 64) has its second half zero-filled: its
     // products add zero, and one code path keeps the accumulators in place
-    compute(cur, std::integral_constant<int, 2>{});
+    compute(cur, s);
     if (more) store(r, nxt);
     __syncthreads();
   }
@@ -287,7 +293,11 @@ __global__ __launch_bounds__(256) void mx_quant_kernel(MxQuant P) {
     e = (int)((__float_as_uint(amax) >> 23) & 0xFF) - 127 - 8;
     e = max(-127, min(127, e));
   }
-  P.scales[row * per_row + c0 / 32] = (uint8_t)(e + 127);
+  // the GEMM operand layout: code rows padded to whole 128-byte lines, the
+  // four scale bytes of a row's 128 columns in one dword
+  const int64_t sidx = P.gemm_layout ? ((int64_t)(c0 / 128) * P.rows + row) * 4 + (c0 / 32) % 4
+                                     : row * per_row + c0 / 32;
+  P.scales[sidx] = (uint8_t)(e + 127);
   const float inv = __uint_as_float((uint32_t)(127 - e) << 23);  // 2^-e, a normal power of two for e in [-127, 119]
   uint32_t out[8];
 #pragma unroll
@@ -297,7 +307,7 @@ __global__ __launch_bounds__(256) void mx_quant_kernel(MxQuant P) {
     for (int i = 0; i < 4; ++i) w |= e4m3_of(v[4 * q + i] * inv) << (8 * i);
     out[q] = w;
   }
-  uint8_t* dst = P.codes + row * P.cols + c0;
+  uint8_t* dst = P.codes + row * (P.gemm_layout ? mx_code_stride(P.cols) : P.cols) + c0;
   st16(dst, u32x4{out[0], out[1], out[2], out[3]});
   st16(dst + 16, u32x4{out[4], out[5], out[6], out[7]});
 }
@@ -305,10 +315,13 @@ __global__ __launch_bounds__(256) void mx_quant_kernel(MxQuant P) {
 }  // namespace
 
 bool mx_gemm_applies(const Gemm& g) {
-  // 32-bit offsets: token rows from x itself, one group's codes
+  // 32-bit offsets: token rows and their scales from x itself, one group's
+  // codes and scales
   const int64_t xr = g.x_rows > 0 ? g.x_rows : g.n_rows;
-  return g.k > 0 && g.k % 64 == 0 && g.n % 16 == 0 && g.n_groups <= TILE_MAXG && g.x_scales && g.w_scales &&
-         xr * g.k < (1LL << 32) && (int64_t)g.n * g.k / 2 < (1LL << 32);
+  return g.k > 0 && g.k % 64 == 0 && g.k <= MX_MAX_K && g.n % 16 == 0 && g.n_groups <= TILE_MAXG && g.x_scales &&
+         g.w_scales && (uintptr_t)g.w_scales % 16 == 0 && (uintptr_t)g.x % 16 == 0 &&
+         (uintptr_t)g.x_scales % 4 == 0 && xr * mx_code_stride(g.k) < (1LL << 32) &&
+         mx_scale_bytes(xr, g.k) < (1LL << 32) && (int64_t)g.n * g.k / 2 < (1LL << 32);
 }
 
 hipError_t launch_gemm_mx(const Gemm& g, hipStream_t s) {

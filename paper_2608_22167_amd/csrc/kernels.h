@@ -182,16 +182,25 @@ struct Gemm {
 constexpr uint32_t LOGIT_RNG_TAG = 0x4C4D5330u;  // counter word 3 of the sampling draws
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s);
 // Scaled matrix-core products (gemm_mx.hip): MXFP8 activations (x, x_scales)
-// times MXFP4 weights (w, w_scales); k a multiple of 64, n of 16.
+// times MXFP4 weights (w, w_scales); k a multiple of 64 and at most MX_MAX_K
+// (the tile's weight scales stay in LDS for the whole reduction), n a
+// multiple of 16, w_scales 16-byte aligned. The activations are in the GEMM
+// operand layout that mx_quant writes: codes [x_rows][mx_code_stride(k)]
+// (every row starts on a 128-byte line) and scales in dwords of four blocks,
+// [ceil(k / 128)][x_rows][4].
+constexpr int MX_MAX_K = 3072;
+__host__ __device__ constexpr int mx_code_stride(int k) { return (k + 127) / 128 * 128; }
+__host__ __device__ constexpr int64_t mx_scale_bytes(int64_t rows, int k) { return (int64_t)((k + 127) / 128) * rows * 4; }
 bool mx_gemm_applies(const Gemm& g);
 hipError_t launch_gemm_mx(const Gemm& g, hipStream_t s);
-// bf16 rows -> MXFP8: codes [rows][cols] E4M3, scales [rows][cols / 32] E8M0
+// bf16 rows -> MXFP8 (E4M3 codes, E8M0 scales per 32 columns)
 struct MxQuant {
   const void* in;  // [rows][cols] bf16
   int64_t rows;
   int cols;
   uint8_t* codes;
   uint8_t* scales;
+  int gemm_layout;  // 0: codes [rows][cols], scales [rows][cols / 32]; 1: the GEMM operand layout
 };
 hipError_t launch_mx_quant(const MxQuant& p, hipStream_t s);
 // LDS-tiled path (gemm_tiled.hip): bf16, k a multiple of 64, at least

@@ -70,8 +70,10 @@ int check_cfg(const mcpu_layer_cfg* c) {
     return fail(MCPU_EINVAL, "expert_fmt %d", c->expert_fmt);
   if (c->expert_fmt != MCPU_EXPERT_DENSE && c->dtype != MCPU_BF16)
     return fail(MCPU_EUNSUPPORTED, "MXFP4 experts need a bf16 layer");
-  if (c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE && (c->hidden % 64 || c->ffn_dim % 64))
-    return fail(MCPU_EUNSUPPORTED, "native MXFP4 experts need hidden and ffn_dim multiples of 64");
+  if (c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE &&
+      (c->hidden % 64 || c->ffn_dim % 64 || c->hidden > MX_MAX_K || c->ffn_dim > MX_MAX_K))
+    return fail(MCPU_EUNSUPPORTED, "native MXFP4 experts need hidden and ffn_dim multiples of 64, at most %d",
+                MX_MAX_K);
   if (!(c->rms_eps >= 0.f)) return fail(MCPU_EINVAL, "rms_eps");
   return MCPU_OK;
 }
@@ -236,10 +238,11 @@ MoeBufs carve_moe(Carve& cv, const mcpu_layer_cfg* c, int max_tokens) {
   m.y = cv.take<float>(T * K * c->hidden);
   m.hq = m.hs = m.aq = m.as = nullptr;
   if (c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE) {
-    m.hq = cv.take<uint8_t>(T * c->hidden);
-    m.hs = cv.take<uint8_t>(T * c->hidden / 32);
-    m.aq = cv.take<uint8_t>(T * K * c->ffn_dim);
-    m.as = cv.take<uint8_t>(T * K * c->ffn_dim / 32);
+    // in the GEMM operand layout (whole-line code rows, scale dwords)
+    m.hq = cv.take<uint8_t>(T * mx_code_stride(c->hidden));
+    m.hs = cv.take<uint8_t>(mx_scale_bytes(T, c->hidden));
+    m.aq = cv.take<uint8_t>(T * K * mx_code_stride(c->ffn_dim));
+    m.as = cv.take<uint8_t>(mx_scale_bytes(T * K, c->ffn_dim));
   }
   return m;
 }
@@ -293,7 +296,7 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   const bool native = c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE;
   if (native) {  // the first product reads the normalised rows in MXFP8
     MxQuant q{};
-    q.in = m.hn; q.rows = T; q.cols = H; q.codes = m.hq; q.scales = m.hs;
+    q.in = m.hn; q.rows = T; q.cols = H; q.codes = m.hq; q.scales = m.hs; q.gemm_layout = 1;
     HIP_TRY(launch_mx_quant(q, st));
   }
   Gemm g1{};
@@ -309,7 +312,7 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
 
   if (native) {  // ... and the second its SwiGLU activations in MXFP8
     MxQuant q{};
-    q.in = m.act; q.rows = (int64_t)T * K; q.cols = I; q.codes = m.aq; q.scales = m.as;
+    q.in = m.act; q.rows = (int64_t)T * K; q.cols = I; q.codes = m.aq; q.scales = m.as; q.gemm_layout = 1;
     HIP_TRY(launch_mx_quant(q, st));
   }
   Gemm g2{};
