@@ -14,17 +14,23 @@
 // So each lane's A bytes are two 16-byte halves of a staged 64-byte row
 // slice and its B bytes one 16-byte quarter of a 32-byte slice.
 //
-// Tile 256 token rows x 256 weight rows, eight wavefronts (2 x 4), each
-// owning 128 x 64 = 4 x 2 products of 32 x 32; the reduction runs in stages
-// of 128 (two products deep) through two LDS buffers, one barrier per stage.
-// LDS rows are 160 B (A, 128 B of data) and 96 B (B, 64 B) apart, which keeps
-// the 16-byte fragment reads free of bank conflicts. Scales: the activation
-// rows' four scale bytes of a stage are one dword (the operand layout groups
-// them so), staged with the codes; the tile's weight scales, a contiguous run
-// of 256 rows, are copied to LDS once and read from there for the whole
-// reduction, so no scale byte costs a separate memory request. The finished
-// fp32 tile goes through LDS to the fused epilogue (gemm_epilogue.h), 32 rows
-// at a time.
+// Tile 256 token rows x 256 weight rows, eight wavefronts (4 x 2), each
+// owning 64 x 128 = 2 x 4 products of 32 x 32. The reduction runs in slices
+// of 64 (one product deep) through a ring of five LDS stages that 16-byte
+// buffer loads fill straight from global memory (a wavefront's load fills
+// 1 KB of LDS, lane l at byte 16 l), so staging costs neither registers nor
+// LDS write instructions. While slice i is multiplied, the fragments of
+// slice i + 1 are read, and slice i + 4 is requested into the stage slice
+// i - 1 left; before each barrier a wavefront waits for its own loads of
+// slice i + 2, which the barrier then publishes.
+//   Stage layout: token rows 64 B (chunk q of row r in slot q ^ ((r >> 1) & 3)),
+// weight rows 32 B (chunk q in slot q ^ (((r >> 2) ^ (r >> 3)) & 1)), which
+// keeps the fragment reads free of bank conflicts, then the token rows' scale
+// dwords (32 rows per 256 B). Scales: the activation rows' four scale bytes of two slices are one
+// dword (the operand layout groups them so); the tile's weight scales, a
+// contiguous run of 256 rows, are copied to LDS once and read from there for
+// the whole reduction. The finished fp32 tile goes through LDS to the fused
+// epilogue (gemm_epilogue.h), 16 rows at a time.
 #include <type_traits>
 
 #include "device.h"
@@ -37,24 +43,32 @@ namespace {
 typedef int32_t v8i __attribute__((ext_vector_type(8)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-constexpr int XM = 256, XN = 256, XK = 128;  // output tile, reduction per stage
+constexpr int XM = 256, XN = 256, XK = 64;  // output tile, reduction per slice
 constexpr int XTH = 512;
-constexpr int XA_LD = 160, XB_LD = 96;       // staged row strides (bytes)
-constexpr int XA_BYTES = XM * XA_LD, XB_BYTES = XN * XB_LD;
-constexpr int XSTAGE = XA_BYTES + XB_BYTES + 4 * XM;  // + the token rows' scale dwords
-constexpr int XBS_BYTES = XN * (MX_MAX_K / 32);       // the tile's weight scales
-constexpr int XEP = 32, XCLD = XN + 4;       // epilogue pass rows, fp32 row stride
+constexpr int XS_A = XM * XK, XS_B = XN * XK / 2, XS_S = 8 * 256;
+constexpr int XSTAGE = XS_A + XS_B + XS_S;  // 26 KB
+constexpr int XBS_BYTES = XN * (MX_MAX_K / 32);  // the tile's weight scales
+constexpr int XEP = 16, XCLD = XN + 4;      // epilogue pass rows, fp32 row stride
 static_assert(XEP * XCLD * 4 <= XSTAGE, "an epilogue pass fits one stage");
-static_assert(2 * XSTAGE + XBS_BYTES + 4 * (TILE_MAXG + 1) <= 160 * 1024, "LDS");
-constexpr int XGM = 2;                       // m-tiles per band
+static_assert(5 * XSTAGE + XBS_BYTES + 4 * (TILE_MAXG + 1) <= 160 * 1024, "LDS");
+constexpr int XGM = 2;                      // m-tiles per band
+constexpr int XBUF_DWORD3 = 0x00020000;     // raw buffer descriptor word 3 (gfx9 family)
 
 __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<const u32x4*>(p); }
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
+__device__ __forceinline__ int swz_a(int r) { return (r >> 1) & 3; }
+__device__ __forceinline__ int swz_b(int r) { return ((r >> 2) ^ (r >> 3)) & 1; }
 
 template <int EPI>
 __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
-  __shared__ __align__(16) uint8_t lds[2 * XSTAGE + XBS_BYTES];
+  __shared__ __align__(1024) uint8_t d0[XSTAGE];
+  __shared__ __align__(1024) uint8_t d1[XSTAGE];
+  __shared__ __align__(1024) uint8_t d2[XSTAGE];
+  __shared__ __align__(1024) uint8_t d3[XSTAGE];
+  __shared__ __align__(1024) uint8_t d4[XSTAGE];
+  __shared__ __align__(16) uint8_t bsc[XBS_BYTES];
   __shared__ int mt_start[TILE_MAXG + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
 
@@ -65,174 +79,204 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   const int m0 = uniform(gr0 + mt * XM);
   const int mrows = min(XM, gr1 - m0);
   const int n0 = uniform(tn * XN), nrows = min(XN, P.n - n0);
-  const int K = P.k, kb32 = K / 32, lda = mx_code_stride(K);
-  const uint32_t xrows = (uint32_t)(P.x_rows > 0 ? P.x_rows : P.n_rows);
+  const int K = P.k, kb32 = K / 32, lda = mx_code_stride(K), nk = K / XK;
+  const int xrows = P.x_rows > 0 ? P.x_rows : P.n_rows;
 
-  // staging: A chunk c = tid + 512 j (j < 4) is row c / 8, 16-byte piece c % 8;
-  // B chunk c = tid + 512 j (j < 2) is row c / 4, piece c % 4; threads 0-255
-  // stage the scale dword of token row tid. Rows past the tile's end repeat
-  // its last row (results dropped). Token rows, one expert's weights and the
-  // scale rows are addressed by 32-bit offsets from uniform bases (the host
-  // checks that they fit).
-  const uint8_t* xq = reinterpret_cast<const uint8_t*>(P.x);
-  const uint8_t* wq = reinterpret_cast<const uint8_t*>(P.w) + grp * P.w_group_stride;
-  const uint8_t* ws = P.w_scales + grp * (P.w_group_stride / 16) + (uint32_t)n0 * (uint32_t)kb32;
-  const uint32_t a_piece = 16u * (tid & 7), b_piece = 16u * (tid & 3);
-  uint32_t a_off[4], b_off[2], s_row;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int r = (tid + XTH * j) >> 3;
+  // Loads of a slice: wavefront w fills token rows 32 w + 16 j + [0, 16)
+  // (j = 0, 1; lane l lands in row + l / 4, slot l % 4), weight rows
+  // 32 w + [0, 32) (lane l in row l / 2, slot l % 2) and the scale dwords of
+  // token rows 32 w + [0, 32) (lanes l and l + 32 load the same one, so every
+  // wavefront issues the same loads); each lane loads the global
+  // chunk its slot holds. Rows past the tile's end repeat its last row (their
+  // results are dropped). Buffer loads: uniform bases (x itself, the group's
+  // weights, the scale array), 32-bit per-lane offsets (the host checks that
+  // they fit) and the slice offset in a scalar register.
+  const uint8_t* wb = reinterpret_cast<const uint8_t*>(P.w) + grp * P.w_group_stride;
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(P.x), 0, 0x7FFFFFFF, XBUF_DWORD3);
+  const __amdgpu_buffer_rsrc_t wr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wb), 0, 0x7FFFFFFF, XBUF_DWORD3);
+  const __amdgpu_buffer_rsrc_t sr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(P.x_scales), 0, 0x7FFFFFFF, XBUF_DWORD3);
+  auto src_of = [&](int r) __attribute__((always_inline)) {
     const int row = m0 + min(r, mrows - 1);
-    const int src = P.row_src ? P.row_src[row] : row;
-    a_off[j] = (uint32_t)src * (uint32_t)lda;
-  }
+    return P.row_src ? P.row_src[row] : row;
+  };
+  uint32_t avo[2], bvo, svo;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    const int r = (tid + XTH * j) >> 2;
-    b_off[j] = (uint32_t)(n0 + min(r, nrows - 1)) * (uint32_t)(K / 2);
+    const int r = 32 * wave + 16 * j + (lane >> 2);
+    avo[j] = (uint32_t)src_of(r) * (uint32_t)lda + 16u * ((lane & 3) ^ swz_a(r));
   }
   {
-    const int row = m0 + min(tid & 255, mrows - 1);
-    s_row = (uint32_t)(P.row_src ? P.row_src[row] : row);
+    const int r = 32 * wave + (lane >> 1);
+    bvo = (uint32_t)(n0 + min(r, nrows - 1)) * (uint32_t)(K / 2) + 16u * ((lane & 1) ^ swz_b(r));
   }
+  svo = (uint32_t)src_of(32 * wave + (lane & 31)) * 4u;
 
   // the tile's weight scales [256 rows][kb32] into LDS (rows past the end
   // get scale 1; the run is a multiple of 16 bytes since n is of 16)
-  uint8_t* bsc = lds + 2 * XSTAGE;
   {
+    const uint8_t* ws = P.w_scales + grp * (P.w_group_stride / 16) + (uint32_t)n0 * (uint32_t)kb32;
     const int span = nrows * kb32;
     const u32x4 one = {0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu};
     for (int c = 16 * tid; c < XN * kb32; c += 16 * XTH) st16(bsc + c, c < span ? ld16(ws + c) : one);
   }
 
-  struct Regs {
-    u32x4 a[4], b[2];
-    uint32_t s;
+  auto stage_of = [&](int s) __attribute__((always_inline)) {
+    return s == 0 ? d0 : s == 1 ? d1 : s == 2 ? d2 : s == 3 ? d3 : d4;
   };
-  // Past the end of the reduction (a last stage of 64) the pieces are zero:
-  // the load address is clamped into the row and the value replaced, so no
-  // load is conditional and none leaves the row; scale bytes past the end
-  // become 1.
-  auto fetch = [&](Regs& g, int st) __attribute__((always_inline)) {
-    const int k0 = st * XK;
-    const u32x4 z = {0u, 0u, 0u, 0u};
-    const int ka = k0 + (int)a_piece, kb = k0 / 2 + (int)b_piece;  // byte offsets in a row
-    const uint32_t ka_c = (uint32_t)min(ka, K - 16), kb_c = (uint32_t)min(kb, K / 2 - 16);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const u32x4 v = ld16(xq + (a_off[j] + ka_c));
-      g.a[j] = ka < K ? v : z;
-    }
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const u32x4 v = ld16(wq + (b_off[j] + kb_c));
-      g.b[j] = kb < K / 2 ? v : z;
-    }
-    if (tid < 256) {
-      uint32_t s = *reinterpret_cast<const uint32_t*>(P.x_scales + ((uint32_t)st * xrows + s_row) * 4u);
-      const int valid = kb32 - 4 * st;  // uniform
-      if (valid < 4) {
-        const uint32_t keep = (1u << (8 * valid)) - 1u;
-        s = (s & keep) | (0x7F7F7F7Fu & ~keep);
-      }
-      g.s = s;
-    }
+  // the loads of slice ks into a stage (4 per wavefront);
+  // slices past the end re-read the last one (never multiplied), so every
+  // slice issues the same loads and the waits below count whole slices
+  auto dma = [&](uint8_t* stg, int ks) __attribute__((always_inline)) {
+    ks = min(ks, nk - 1);
+    const int ka = uniform(ks * XK), kb = uniform(ks * (XK / 2));
+    const int kq = uniform((ks >> 1) * xrows * 4);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr_t)(stg + 32 * wave * 64), 16, avo[0], ka, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr_t)(stg + (32 * wave + 16) * 64), 16, avo[1], ka, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_ptr_t)(stg + XS_A + 32 * wave * 32), 16, bvo, kb, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(sr, (lds_ptr_t)(stg + XS_A + XS_B + 256 * wave), 4, svo, kq, 0, 0);
   };
-  auto store = [&](const Regs& g, uint8_t* stage) __attribute__((always_inline)) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) st16(stage + ((tid + XTH * j) >> 3) * XA_LD + a_piece, g.a[j]);
-#pragma unroll
-    for (int j = 0; j < 2; ++j) st16(stage + XA_BYTES + ((tid + XTH * j) >> 2) * XB_LD + b_piece, g.b[j]);
-    if (tid < 256) *reinterpret_cast<uint32_t*>(stage + XA_BYTES + XB_BYTES + 4 * tid) = g.s;
+  // wait until at most this wavefront's two newest slices are in flight (and
+  // its LDS reads are done), then the barrier that publishes everyone's older
+  // slices
+  auto publish = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(8 | (7 << 4));  // vmcnt(8) expcnt(7) lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
   };
 
-  // wavefront (wm, wn): token rows wm * 128 + [0, 128), weight rows wn * 64 + [0, 64)
-  const int wm = wave >> 2, wn = wave & 3;
+  // wavefront (wm, wn): token rows wm * 64 + [0, 64), weight rows wn * 128 + [0, 128)
+  const int wm = wave >> 1, wn = wave & 1;
   const int fr = lane & 31, fg = lane >> 5;
-  v16f acc[4][2];
+  // per-lane fragment offsets within a stage: token-row halves h = 0, 1 of
+  // product 0 (product 1 is 32 rows = 2 KB further), weight rows of product 0
+  // (product ct is 1 KB further), the scale bytes; weight-scale rows in LDS
+  uint32_t a0, a1, b0, q0, brow[4];
+  {
+    const int r = wm * 64 + fr;
+    a0 = r * 64 + 16 * (fg ^ swz_a(r));
+    a1 = r * 64 + 16 * ((2 + fg) ^ swz_a(r));
+    q0 = XS_A + XS_B + 512 * wm + 4 * fr + fg;  // row r: dword r % 32 of block r / 32
+    const int rb = wn * 128 + fr;
+    b0 = XS_A + rb * 32 + 16 * (fg ^ swz_b(rb));
 #pragma unroll
-  for (int rt = 0; rt < 4; ++rt)
+    for (int ct = 0; ct < 4; ++ct) brow[ct] = (rb + 32 * ct) * kb32 + fg;
+  }
+  struct Frag {
+    u32x4 a[2][2], b[4];
+    int sa[2], sb[4];
+  };
+  // fragments of slice ks (of parity PAR) from a stage; the offsets pass
+  // through an empty asm statement so that the stage addresses are formed
+  // per slice rather than kept in registers for all five stages
+  auto read = [&](Frag& f, const uint8_t* stg, int ks, auto PAR_) __attribute__((always_inline)) {
+    constexpr int PAR = decltype(PAR_)::value;
+    asm volatile("" : "+v"(a0), "+v"(a1), "+v"(b0), "+v"(q0));
 #pragma unroll
-    for (int ct = 0; ct < 2; ++ct)
+    for (int rt = 0; rt < 2; ++rt) {
+      f.a[rt][0] = ld16(stg + a0 + 2048 * rt);
+      f.a[rt][1] = ld16(stg + a1 + 2048 * rt);
+      f.sa[rt] = stg[q0 + 256 * rt + 2 * PAR];
+    }
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      f.b[ct] = ld16(stg + b0 + 1024 * ct);
+      f.sb[ct] = bsc[brow[ct] + 2 * ks];
+    }
+  };
+  v16f acc[2][4];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
       for (int j = 0; j < 16; ++j) acc[rt][ct][j] = 0.f;
-
-  // the two product depths of stage st, one at a time (the next depth's
-  // fragments are not read ahead: their registers would spill the accumulators)
-  auto compute = [&](const uint8_t* stage, int st) __attribute__((always_inline)) {
-    const uint8_t* sa = stage + XA_BYTES + XB_BYTES;
-#pragma unroll 1
-    for (int ks = 0; ks < 2; ++ks) {
-      union Op {
+  auto mfma = [&](const Frag& f) __attribute__((always_inline)) {
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      union {
         v8i v;
         u32x4 h[2];
-      };
-      Op a[4], b[2];
-      int sca[4], scb[2];
-      const int blk = min(4 * st + 2 * ks + fg, kb32 - 1);
+      } a;
+      a.h[0] = f.a[rt][0];
+      a.h[1] = f.a[rt][1];
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        const int row = wm * 128 + rt * 32 + fr;
-        const uint8_t* p = stage + row * XA_LD + 64 * ks + 16 * fg;
-        a[rt].h[0] = ld16(p);
-        a[rt].h[1] = ld16(p + 32);
-        sca[rt] = sa[row * 4 + 2 * ks + fg];
+      for (int ct = 0; ct < 4; ++ct) {
+        union {
+          v8i v;
+          u32x4 h[2];
+        } b;
+        b.h[0] = f.b[ct];
+        b.h[1] = u32x4{0u, 0u, 0u, 0u};
+        acc[rt][ct] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a.v, b.v, acc[rt][ct], 0, 4, 0, f.sa[rt], 0,
+                                                                      f.sb[ct]);
       }
-#pragma unroll
-      for (int ct = 0; ct < 2; ++ct) {
-        const int row = wn * 64 + ct * 32 + fr;
-        b[ct].h[0] = ld16(stage + XA_BYTES + row * XB_LD + 32 * ks + 16 * fg);
-        b[ct].h[1] = u32x4{0u, 0u, 0u, 0u};
-        scb[ct] = bsc[row * kb32 + blk];
-      }
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt)
-#pragma unroll
-        for (int ct = 0; ct < 2; ++ct)
-          acc[rt][ct] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[rt].v, b[ct].v, acc[rt][ct], 0, 4, 0,
-                                                                        sca[rt], 0, scb[ct]);
     }
   };
 
-  // Stage s is multiplied out of LDS buffer s % 2 while stage s + 1 is
-  // loaded into registers and then written to the other buffer; one barrier
-  // per stage.
-  const int ns = (K + XK - 1) / XK;
-  {
-    Regs r;
-    fetch(r, 0);
-    store(r, lds);
-  }
-  __syncthreads();
-  for (int s = 0; s < ns; ++s) {
-    uint8_t* cur = lds + (s & 1) * XSTAGE;
-    uint8_t* nxt = lds + ((s + 1) & 1) * XSTAGE;
-    Regs r;
-    const bool more = s + 1 < ns;  // uniform
-    if (more) fetch(r, s + 1);
-    // a last stage of 64 (k % 128 == 64) has its second half zero-filled: its
-    // products add zero, and one code path keeps the accumulators in place
-    compute(cur, s);
-    if (more) store(r, nxt);
-    __syncthreads();
-  }
+  // prologue: slices 0 .. 3 requested, 0 and 1 published, slice 0 read
+#pragma unroll
+  for (int s = 0; s < 4; ++s) dma(stage_of(s), s);
+  publish();
+  Frag fa[2];
+  read(fa[0], d0, 0, std::integral_constant<int, 0>{});
 
-  // acc[rt][ct][j] = C[m = wm*128 + 32 rt + 8 (j/4) + 4 fg + j%4][n = wn*64 + 32 ct + fr];
-  // the fp32 tile goes through LDS (buffer 0, free after the last barrier)
-  float* cr = reinterpret_cast<float*>(lds);
+  // slice i uses stage i % 5 and fragment set i % 2 (the loop is unrolled
+  // ten times); the fragments read past the last slice are never used
+  auto slice = [&](auto S_, auto H_, int i) __attribute__((always_inline)) {
+    constexpr int S = decltype(S_)::value, H = decltype(H_)::value;
+    __builtin_amdgcn_sched_barrier(0);  // nothing moves between slices
+    dma(stage_of((S + 4) % 5), i + 4);
+    read(fa[H ^ 1], stage_of((S + 1) % 5), i + 1, std::integral_constant<int, H ^ 1>{});
+    mfma(fa[H]);
+    publish();
+  };
+  using C0 = std::integral_constant<int, 0>;
+  using C1 = std::integral_constant<int, 1>;
+  using C2 = std::integral_constant<int, 2>;
+  using C3 = std::integral_constant<int, 3>;
+  using C4 = std::integral_constant<int, 4>;
+  int i = 0;
+  for (; i + 10 <= nk; i += 10) {
+    slice(C0{}, C0{}, i);
+    slice(C1{}, C1{}, i + 1);
+    slice(C2{}, C0{}, i + 2);
+    slice(C3{}, C1{}, i + 3);
+    slice(C4{}, C0{}, i + 4);
+    slice(C0{}, C1{}, i + 5);
+    slice(C1{}, C0{}, i + 6);
+    slice(C2{}, C1{}, i + 7);
+    slice(C3{}, C0{}, i + 8);
+    slice(C4{}, C1{}, i + 9);
+  }
+  if (i < nk) slice(C0{}, C0{}, i);
+  if (i + 1 < nk) slice(C1{}, C1{}, i + 1);
+  if (i + 2 < nk) slice(C2{}, C0{}, i + 2);
+  if (i + 3 < nk) slice(C3{}, C1{}, i + 3);
+  if (i + 4 < nk) slice(C4{}, C0{}, i + 4);
+  if (i + 5 < nk) slice(C0{}, C1{}, i + 5);
+  if (i + 6 < nk) slice(C1{}, C0{}, i + 6);
+  if (i + 7 < nk) slice(C2{}, C1{}, i + 7);
+  if (i + 8 < nk) slice(C3{}, C0{}, i + 8);
+  __builtin_amdgcn_s_waitcnt(0);  // every load landed and every read done before stage 0 holds the fp32 tile
+  __syncthreads();
+
+  // acc[rt][ct][j] = C[m = wm*64 + 32 rt + 8 (j/4) + 4 fg + j%4][n = wn*128 + 32 ct + fr]
+  float* cr = reinterpret_cast<float*>(d0);
   const EpiBias eb = epilogue_bias<EPI>(P, n0 >> 4, nrows >> 4, grp);
   for (int e0 = 0; e0 < XM; e0 += XEP) {
     if (e0 >= mrows) break;  // uniform
-    if (wm == e0 / 128) {
-      const int rt = (e0 % 128) / 32;
+    if (wm == e0 / 64) {
+      const int q = (e0 % 64) / 16;  // product rt = q / 2, its rows 16 (q % 2) + [0, 16)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (q == rt) {
+      for (int qq = 0; qq < 4; ++qq)
+        if (qq == q) {
 #pragma unroll
-          for (int ct = 0; ct < 2; ++ct)
+          for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
-            for (int j = 0; j < 16; ++j)
-              cr[(8 * (j >> 2) + 4 * fg + (j & 3)) * XCLD + wn * 64 + ct * 32 + fr] = acc[q][ct][j];
+            for (int j = 8 * (qq & 1); j < 8 * (qq & 1) + 8; ++j)
+              cr[(8 * (j >> 2) + 4 * fg + (j & 3) - 16 * (qq & 1)) * XCLD + wn * 128 + ct * 32 + fr] = acc[qq >> 1][ct][j];
         }
     }
     __syncthreads();
@@ -315,13 +359,13 @@ __global__ __launch_bounds__(256) void mx_quant_kernel(MxQuant P) {
 }  // namespace
 
 bool mx_gemm_applies(const Gemm& g) {
-  // 32-bit offsets: token rows and their scales from x itself, one group's
-  // codes and scales
+  // buffer loads with 32-bit offsets below 2^31: token rows and their scales
+  // from x itself, one group's codes
   const int64_t xr = g.x_rows > 0 ? g.x_rows : g.n_rows;
   return g.k > 0 && g.k % 64 == 0 && g.k <= MX_MAX_K && g.n % 16 == 0 && g.n_groups <= TILE_MAXG && g.x_scales &&
          g.w_scales && (uintptr_t)g.w_scales % 16 == 0 && (uintptr_t)g.x % 16 == 0 &&
-         (uintptr_t)g.x_scales % 4 == 0 && xr * mx_code_stride(g.k) < (1LL << 32) &&
-         mx_scale_bytes(xr, g.k) < (1LL << 32) && (int64_t)g.n * g.k / 2 < (1LL << 32);
+         (uintptr_t)g.x_scales % 4 == 0 && xr * mx_code_stride(g.k) < (1LL << 31) &&
+         mx_scale_bytes(xr, g.k) < (1LL << 31) && (int64_t)g.n * g.k / 2 < (1LL << 31);
 }
 
 hipError_t launch_gemm_mx(const Gemm& g, hipStream_t s) {
