@@ -81,14 +81,17 @@ enum {
   MCPU_DEVERR_TOKEN = 32  /* a token id outside [0, vocab) (embed_tokens); its row was zeroed */
 };
 
-/* Layer configuration (host struct, by value semantics).
+/* Layer configuration (host struct, by value semantics). Paper: the policy
+ * is gpt-oss-20b (Sec. 4 and the training-details appendix); its layer
+ * shape is one instance of this struct.
  *  hidden H, n_q_heads Hq, n_kv_heads Hkv (Hq % Hkv == 0, Hq / Hkv <= 16),
  *  head_dim d in {32, 64}, n_experts E <= 64, top_k k <= min(E, 8),
  *  ffn_dim I (expert SwiGLU width); H, I and Hq * d multiples of 32.
  *  page_size must be 16. window 0 = full attention, else keys
  *  [pos - window + 1, pos]. dtype: MCPU_F32 or MCPU_BF16 for the matrices,
  *  the KV cache and matrix-core operands. expert_fmt: MCPU_EXPERT_DENSE
- *  (experts in dtype) or MCPU_EXPERT_MXFP4.
+ *  (experts in dtype), MCPU_EXPERT_MXFP4 or MCPU_EXPERT_MXFP4_NATIVE (bf16
+ *  layers only).
  *  SwiGLU: a = min(gate, L) * sigmoid(alpha * min(gate, L)) * (clamp(up, -L, L) + beta)
  *  with alpha = swiglu_alpha, L = swiglu_limit (may be +inf), beta = swiglu_beta. */
 typedef struct mcpu_layer_cfg {
@@ -97,7 +100,8 @@ typedef struct mcpu_layer_cfg {
   float rms_eps, swiglu_alpha, swiglu_limit, swiglu_beta;
 } mcpu_layer_cfg;
 
-/* Layer parameters: device pointers owned by the caller. Matrices are
+/* Layer parameters (the policy's weights, Sec. 4): device pointers owned by
+ * the caller. Matrices are
  * row-major with the reduction dimension contiguous, in the layer dtype
  * ("T") unless stated. Vectors are fp32.
  *  g1, g2 [H]            RMSNorm gains before attention and before the MoE
@@ -140,7 +144,8 @@ typedef struct mcpu_layer_weights {
   const void* w_d_packed;
 } mcpu_layer_weights;
 
-/* Weights in streaming order (bf16 only). src is [n_groups, rows, cols]
+/* Weights in streaming order (bf16 only), a layout aid for the decode-sized
+ * expert GEMMs of the Run stage's generation (Sec. 3.2). src is [n_groups, rows, cols]
  * row-major with cols contiguous; rows a multiple of 16, cols of 64. dst
  * (mcpu_packed_weights_bytes bytes, caller-owned, not aliasing src) receives,
  * per group, row block rb (16 rows) and column chunk c (128 columns), a
@@ -157,7 +162,10 @@ int mcpu_pack_weights(int32_t dtype, const void* src, void* dst, int32_t n_group
                       hipStream_t stream);
 
 /* Opaque page pool: host-side free list over a caller-owned pair of device
- * pools (K and V, each n_pages * Hkv * 16 * d elements of the layer dtype). */
+ * pools (K and V, each n_pages * Hkv * 16 * d elements of the layer dtype).
+ * Paper: trajectories are multi-turn and their contexts grow by every turn's
+ * tool observation (Sec. 1, Sec. 3.2), so cache pages are taken as a
+ * sequence grows and returned when it ends. */
 typedef struct mcpu_kv_pool mcpu_kv_pool;
 
 /* Thread-local description of the last non-OK return of this thread. */
@@ -171,15 +179,18 @@ int kv_pool_destroy(mcpu_kv_pool* pool);
 /* Number of free pages. */
 int32_t kv_pool_free_pages(const mcpu_kv_pool* pool);
 
-/* Allocate n pages, all or nothing, writing their ids to host array out_ids.
+/* Allocate n pages, all or nothing, writing their ids to host array out_ids
+ * (per-turn growth of a trajectory's context, Sec. 3.2).
  * MCPU_ENOMEM (nothing allocated) when fewer than n are free. Ids come out in
  * ascending order of the free list, lowest first. */
 int kv_pages_alloc(mcpu_kv_pool* pool, int32_t n, int32_t* out_ids);
-/* Return n pages (host array). MCPU_EINVAL, freeing nothing, if any id is out
+/* Return n pages (a finished trajectory, or sliding-window pages left behind
+ * the window). MCPU_EINVAL, freeing nothing, if any id is out
  * of range, not allocated, or repeated. */
 int kv_pages_free(mcpu_kv_pool* pool, int32_t n, const int32_t* ids);
 
-/* Write new keys and values into the cache (the append of a step).
+/* Write new keys and values into the cache (the append of a step; Sec. 1 and
+ * Sec. 3.2: generated tokens and tool observations join the context).
  *  batch sequences; page_table [batch, max_pages], seq_lens [batch] and cu_q
  *  [batch+1] are device int32; new token row r in [cu_q[b], cu_q[b+1]) of
  *  sequence b goes to position seq_lens[b] + r - cu_q[b]. cu_q == NULL means
@@ -192,7 +203,9 @@ int kv_pages_append(mcpu_kv_pool* pool, int32_t batch, const int32_t* page_table
                     int32_t n_tokens, const void* k_new, const void* v_new, void* workspace,
                     size_t ws_bytes, hipStream_t stream);
 
-/* Attention of already-appended queries over the paged cache, with sinks.
+/* Attention of already-appended queries over the paged cache, with sinks
+ * (the attention of the policy's layers, Sec. 4, over contexts that grow by
+ * appended observations, Sec. 1).
  *  q [n_tokens, Hq, d] (layer dtype, rotated), o [n_tokens, Hq * d] (layer dtype).
  *  Token row r of sequence b sits at position p = seq_lens[b] + (r - cu_q[b])
  *  and attends keys [lo, p] (lo = 0, or max(0, p - window + 1)):
@@ -212,7 +225,8 @@ int paged_attention(const mcpu_layer_cfg* cfg, const float* sinks, mcpu_kv_pool*
                     const int32_t* host_cu_q, const void* q, void* o, void* workspace,
                     size_t ws_bytes, hipStream_t stream);
 
-/* MoE sub-block on the residual stream: h, out [n_tokens, H] fp32 (may alias).
+/* MoE sub-block on the residual stream (the policy's mixture-of-experts
+ * feed-forward, Sec. 4): h, out [n_tokens, H] fp32 (may alias).
  *  hn = RMSNorm(h; g2); logits = hn . w_r^T + b_r (fp32); S = the top_k
  *  experts by logit (ties to the lower index); w_e = softmax over S;
  *  out = h + sum_{e in S} w_e * (SwiGLU(hn . w_gu[e]^T + b_gu[e]) . w_d[e]^T + b_d[e]).
@@ -243,7 +257,9 @@ typedef struct mcpu_taps {
   float* logits;
 } mcpu_taps;
 
-/* One decoder-layer step for a batch of sequences:
+/* One decoder-layer step for a batch of sequences: the unit of the Run
+ * stage's generation, which dominates rollout time (Sec. 3.2) and whose
+ * throughput Sec. 4.2 measures in tokens/s:
  *  xn = RMSNorm(x_in; g1); [q|k|v] = xn . w_qkv^T + b_qkv; q, k rotated at
  *  their positions; k, v appended to the cache; o = paged_attention(q);
  *  h1 = x_in + o . w_o^T + b_o; x_out = moe_forward(h1).
@@ -326,7 +342,8 @@ int lm_head_sample(const mcpu_lm_head* lm, int32_t n_tokens, const float* x, con
                    float* logprob_out, float* target_logprob_out, float* lse_out, void* workspace,
                    size_t ws_bytes, hipStream_t stream);
 
-/* MXFP8 quantization of bf16 rows, the activation format of the native
+/* MXFP8 quantization of bf16 rows (OCP Microscaling Formats v1.0; the
+ * policy's experts are MXFP4, Sec. 4), the activation format of the native
  * MXFP4 experts (see moe_forward): in [rows, cols] bf16 (16-byte aligned,
  * cols a multiple of 32) -> codes [rows, cols] FP8 E4M3 (16-byte aligned) and
  * scales [rows, cols / 32] E8M0; an all-zero block gets scale byte 0.
@@ -342,7 +359,8 @@ int mcpu_mxfp8_quantize(const void* in, int64_t rows, int32_t cols, uint8_t* cod
 int embed_tokens(const void* table, int32_t vocab, int32_t hidden, int32_t n_tokens, const int32_t* tokens,
                  float* x_out, void* workspace, size_t ws_bytes, hipStream_t stream);
 
-/* Kernel timing, a profiling aid. mcpu_timing_start(kernel, n) arms the
+/* Kernel timing, a profiling aid for the throughput measurements of the
+ * generation step (Sec. 4.2). mcpu_timing_start(kernel, n) arms the
  * library to record a HIP event pair on the launching stream around each of
  * the next n launches of that kernel (n = 0 disarms it); mcpu_timing_read
  * waits for the recorded events and writes up to n durations in milliseconds
@@ -368,7 +386,8 @@ enum {
 int mcpu_timing_start(int kernel, int n);
 int mcpu_timing_read(int kernel, float* ms, int n, int* n_recorded);
 
-/* Synchronise the stream, read the workspace's device error word, clear it.
+/* Error reporting of every entry point above (not from the paper).
+ * Synchronise the stream, read the workspace's device error word, clear it.
  * Returns MCPU_OK, MCPU_EDEVICE (bits in *bits if non-NULL) or MCPU_EHIP. */
 int mcpu_check_device_errors(void* workspace, hipStream_t stream, int32_t* bits);
 
