@@ -120,7 +120,10 @@ typedef struct mcpu_layer_cfg {
  *    in the streaming order written by mcpu_pack_weights. The grouped GEMMs
  *    of short expert groups (decode batches of a few hundred tokens) then
  *    read each 16-row by 128-column block as 4 KiB in a row; w_gu and w_d
- *    stay required for the other tilings. */
+ *    stay required for the other tilings.
+ *    MCPU_EXPERT_MXFP4_NATIVE: required, the slice-order copies of the MXFP4
+ *    experts (codes and scales) written by mcpu_pack_mxfp4, 256-byte
+ *    aligned; the products read only these. */
 typedef struct mcpu_layer_weights {
   const float* g1;
   const void* w_qkv;
@@ -160,6 +163,25 @@ typedef struct mcpu_layer_weights {
 size_t mcpu_packed_weights_bytes(int32_t n_groups, int32_t rows, int32_t cols);
 int mcpu_pack_weights(int32_t dtype, const void* src, void* dst, int32_t n_groups, int32_t rows, int32_t cols,
                       hipStream_t stream);
+
+/* MXFP4 expert weights in slice order, for MCPU_EXPERT_MXFP4_NATIVE (written
+ * once, like the streaming-order copies above). codes [n_groups, rows,
+ * cols/2] (E2M1, low nibble = even column, 16-byte aligned) and scales
+ * [n_groups, rows, cols/32] (E8M0) as for MCPU_EXPERT_MXFP4; rows a multiple
+ * of 16, cols of 64. dst (mcpu_packed_mxfp4_bytes bytes, 256-byte aligned,
+ * caller-owned, overlapping neither source) receives
+ *   codes: group g, 64-column slice s, row r: the row's 32 code bytes of the
+ *     slice at ((g * cols/64 + s) * rows + r) * 32;
+ *   scales, from byte C = ceil(n_groups * rows * cols/2 / 256) * 256: group g,
+ *     128-column group q, row r: the four scale bytes of blocks 4q .. 4q+3 at
+ *     C + ((g * ceil(cols/128) + q) * rows + r) * 4 (127 past the last block),
+ * so that one 64-wide reduction slice of 256 consecutive rows is one
+ * contiguous run of codes and one of scales. Asynchronous on stream; returns
+ * 0 or MCPU_EINVAL (bad sizes, NULL, misaligned or overlapping buffers, then
+ * nothing is launched). */
+size_t mcpu_packed_mxfp4_bytes(int32_t n_groups, int32_t rows, int32_t cols);
+int mcpu_pack_mxfp4(const uint8_t* codes, const uint8_t* scales, void* dst, int32_t n_groups, int32_t rows,
+                    int32_t cols, hipStream_t stream);
 
 /* Opaque page pool: host-side free list over a caller-owned pair of device
  * pools (K and V, each n_pages * Hkv * 16 * d elements of the layer dtype).
@@ -239,8 +261,8 @@ int paged_attention(const mcpu_layer_cfg* cfg, const float* sinks, mcpu_kv_pool*
  *  along the reduction share the E8M0 scale 2^(floor(log2 max|v|) - 8), and
  *  each element is v / scale rounded to nearest-even FP8 E4M3, saturating at
  *  448; products on the scaled matrix cores, fp32 accumulation (hidden and
- *  ffn_dim multiples of 64 and at most 3072, else MCPU_EUNSUPPORTED; s_gu and
- *  s_d 16-byte aligned). */
+ *  ffn_dim multiples of 64, else MCPU_EUNSUPPORTED; the weights come from
+ *  w_gu_packed / w_d_packed). */
 size_t moe_forward_workspace_size(const mcpu_layer_cfg* cfg, int32_t max_tokens);
 int moe_forward(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, int32_t n_tokens,
                 const float* h, float* out, int32_t* topk_idx, float* topk_w,

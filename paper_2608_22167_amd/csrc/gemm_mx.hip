@@ -19,18 +19,20 @@
 // of 64 (one product deep) through a ring of five LDS stages that 16-byte
 // buffer loads fill straight from global memory (a wavefront's load fills
 // 1 KB of LDS, lane l at byte 16 l), so staging costs neither registers nor
-// LDS write instructions. While slice i is multiplied, the fragments of
-// slice i + 1 are read, and slice i + 4 is requested into the stage slice
-// i - 1 left; before each barrier a wavefront waits for its own loads of
-// slice i + 2, which the barrier then publishes.
+// LDS write instructions. Every operand is in slice order (kernels.h), so a
+// slice of the tile is four contiguous runs: 16 KB of activation codes, 8 KB
+// of weight codes and 1 KB of scale dwords each, read as whole cache lines.
+// While slice i is multiplied, the fragments of slice i + 1 are read, and
+// slice i + 4 is requested into the stage slice i - 1 left; before each
+// barrier a wavefront waits for its own loads of slice i + 2, which the
+// barrier then publishes.
 //   Stage layout: token rows 64 B (chunk q of row r in slot q ^ ((r >> 1) & 3)),
 // weight rows 32 B (chunk q in slot q ^ (((r >> 2) ^ (r >> 3)) & 1)), which
-// keeps the fragment reads free of bank conflicts, then the token rows' scale
-// dwords (32 rows per 256 B). Scales: the activation rows' four scale bytes of two slices are one
-// dword (the operand layout groups them so); the tile's weight scales, a
-// contiguous run of 256 rows, are copied to LDS once and read from there for
-// the whole reduction. The finished fp32 tile goes through LDS to the fused
-// epilogue (gemm_epilogue.h), 16 rows at a time.
+// keeps the fragment reads free of bank conflicts, then the token rows' and
+// the weight rows' scale dwords (32 rows per 256 B: lanes l and l + 32 of a
+// load fetch the same dword, so every wavefront issues the same five loads per
+// slice). The finished fp32 tile goes through LDS to the fused epilogue
+// (gemm_epilogue.h), 16 rows at a time.
 #include <type_traits>
 
 #include "device.h"
@@ -48,11 +50,10 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 constexpr int XM = 256, XN = 256, XK = 64;  // output tile, reduction per slice
 constexpr int XTH = 512;
 constexpr int XS_A = XM * XK, XS_B = XN * XK / 2, XS_S = 8 * 256;
-constexpr int XSTAGE = XS_A + XS_B + XS_S;  // 26 KB
-constexpr int XBS_BYTES = XN * (MX_MAX_K / 32);  // the tile's weight scales
+constexpr int XSTAGE = XS_A + XS_B + 2 * XS_S;  // 28 KB
 constexpr int XEP = 16, XCLD = XN + 4;      // epilogue pass rows, fp32 row stride
 static_assert(XEP * XCLD * 4 <= XSTAGE, "an epilogue pass fits one stage");
-static_assert(5 * XSTAGE + XBS_BYTES + 4 * (TILE_MAXG + 1) <= 160 * 1024, "LDS");
+static_assert(5 * XSTAGE + 4 * (TILE_MAXG + 1) <= 160 * 1024, "LDS");
 constexpr int XGM = 2;                      // m-tiles per band
 constexpr int XBUF_DWORD3 = 0x00020000;     // raw buffer descriptor word 3 (gfx9 family)
 
@@ -60,6 +61,9 @@ __device__ __forceinline__ u32x4 ld16(const void* p) { return *reinterpret_cast<
 __device__ __forceinline__ void st16(void* p, u32x4 v) { *reinterpret_cast<u32x4*>(p) = v; }
 __device__ __forceinline__ int swz_a(int r) { return (r >> 1) & 3; }
 __device__ __forceinline__ int swz_b(int r) { return ((r >> 2) ^ (r >> 3)) & 1; }
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const uint8_t* base) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), 0, 0x7FFFFFFF, XBUF_DWORD3);
+}
 
 template <int EPI>
 __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
@@ -68,7 +72,6 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   __shared__ __align__(1024) uint8_t d2[XSTAGE];
   __shared__ __align__(1024) uint8_t d3[XSTAGE];
   __shared__ __align__(1024) uint8_t d4[XSTAGE];
-  __shared__ __align__(16) uint8_t bsc[XBS_BYTES];
   __shared__ int mt_start[TILE_MAXG + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
 
@@ -79,70 +82,58 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   const int m0 = uniform(gr0 + mt * XM);
   const int mrows = min(XM, gr1 - m0);
   const int n0 = uniform(tn * XN), nrows = min(XN, P.n - n0);
-  const int K = P.k, kb32 = K / 32, lda = mx_code_stride(K), nk = K / XK;
+  const int K = P.k, N = P.n, nk = K / XK;
   const int xrows = P.x_rows > 0 ? P.x_rows : P.n_rows;
 
   // Loads of a slice: wavefront w fills token rows 32 w + 16 j + [0, 16)
   // (j = 0, 1; lane l lands in row + l / 4, slot l % 4), weight rows
   // 32 w + [0, 32) (lane l in row l / 2, slot l % 2) and the scale dwords of
-  // token rows 32 w + [0, 32) (lanes l and l + 32 load the same one, so every
-  // wavefront issues the same loads); each lane loads the global
-  // chunk its slot holds. Rows past the tile's end repeat its last row (their
-  // results are dropped). Buffer loads: uniform bases (x itself, the group's
-  // weights, the scale array), 32-bit per-lane offsets (the host checks that
-  // they fit) and the slice offset in a scalar register.
-  const uint8_t* wb = reinterpret_cast<const uint8_t*>(P.w) + grp * P.w_group_stride;
-  const __amdgpu_buffer_rsrc_t xr =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(P.x), 0, 0x7FFFFFFF, XBUF_DWORD3);
-  const __amdgpu_buffer_rsrc_t wr =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wb), 0, 0x7FFFFFFF, XBUF_DWORD3);
-  const __amdgpu_buffer_rsrc_t sr =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(P.x_scales), 0, 0x7FFFFFFF, XBUF_DWORD3);
-  auto src_of = [&](int r) __attribute__((always_inline)) {
-    const int row = m0 + min(r, mrows - 1);
-    return P.row_src ? P.row_src[row] : row;
-  };
-  uint32_t avo[2], bvo, svo;
+  // token rows and of weight rows 32 w + [0, 32); each lane loads the global
+  // chunk its slot holds. Token rows past the tile's end read the next x rows
+  // (the last one at the end of x), weight rows past n repeat the last one;
+  // their results are dropped. Buffer loads: per-slice bases, 32-bit per-lane
+  // row offsets.
+  const uint8_t* xq = reinterpret_cast<const uint8_t*>(P.x);
+  const uint8_t* wq = reinterpret_cast<const uint8_t*>(P.w) + grp * P.w_group_stride;
+  const uint8_t* ws = P.w_scales + grp * mx_scale_bytes(N, K);
+  uint32_t avo[2], bvo, svo, tvo;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int r = 32 * wave + 16 * j + (lane >> 2);
-    avo[j] = (uint32_t)src_of(r) * (uint32_t)lda + 16u * ((lane & 3) ^ swz_a(r));
+    avo[j] = (uint32_t)min(m0 + r, xrows - 1) * 64u + 16u * ((lane & 3) ^ swz_a(r));
   }
   {
     const int r = 32 * wave + (lane >> 1);
-    bvo = (uint32_t)(n0 + min(r, nrows - 1)) * (uint32_t)(K / 2) + 16u * ((lane & 1) ^ swz_b(r));
-  }
-  svo = (uint32_t)src_of(32 * wave + (lane & 31)) * 4u;
-
-  // the tile's weight scales [256 rows][kb32] into LDS (rows past the end
-  // get scale 1; the run is a multiple of 16 bytes since n is of 16)
-  {
-    const uint8_t* ws = P.w_scales + grp * (P.w_group_stride / 16) + (uint32_t)n0 * (uint32_t)kb32;
-    const int span = nrows * kb32;
-    const u32x4 one = {0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu, 0x7F7F7F7Fu};
-    for (int c = 16 * tid; c < XN * kb32; c += 16 * XTH) st16(bsc + c, c < span ? ld16(ws + c) : one);
+    bvo = (uint32_t)(n0 + min(r, nrows - 1)) * 32u + 16u * ((lane & 1) ^ swz_b(r));
+    const int q = 32 * wave + (lane & 31);
+    svo = (uint32_t)min(m0 + q, xrows - 1) * 4u;
+    tvo = (uint32_t)(n0 + min(q, nrows - 1)) * 4u;
   }
 
   auto stage_of = [&](int s) __attribute__((always_inline)) {
     return s == 0 ? d0 : s == 1 ? d1 : s == 2 ? d2 : s == 3 ? d3 : d4;
   };
-  // the loads of slice ks into a stage (4 per wavefront);
-  // slices past the end re-read the last one (never multiplied), so every
-  // slice issues the same loads and the waits below count whole slices
+  // the loads of slice ks into a stage (5 per wavefront); slices past the
+  // end re-read the last one (never multiplied), so every slice issues the
+  // same loads and the waits below count whole slices
   auto dma = [&](uint8_t* stg, int ks) __attribute__((always_inline)) {
-    ks = min(ks, nk - 1);
-    const int ka = uniform(ks * XK), kb = uniform(ks * (XK / 2));
-    const int kq = uniform((ks >> 1) * xrows * 4);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr_t)(stg + 32 * wave * 64), 16, avo[0], ka, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr_t)(stg + (32 * wave + 16) * 64), 16, avo[1], ka, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_ptr_t)(stg + XS_A + 32 * wave * 32), 16, bvo, kb, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(sr, (lds_ptr_t)(stg + XS_A + XS_B + 256 * wave), 4, svo, kq, 0, 0);
+    ks = uniform(min(ks, nk - 1));
+    const __amdgpu_buffer_rsrc_t xr = rsrc(xq + (size_t)ks * xrows * 64);
+    const __amdgpu_buffer_rsrc_t wr = rsrc(wq + (size_t)ks * N * 32);
+    const __amdgpu_buffer_rsrc_t sr = rsrc(P.x_scales + (size_t)(ks >> 1) * xrows * 4);
+    const __amdgpu_buffer_rsrc_t tr = rsrc(ws + (size_t)(ks >> 1) * N * 4);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr_t)(stg + 32 * wave * 64), 16, avo[0], 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr_t)(stg + (32 * wave + 16) * 64), 16, avo[1], 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_ptr_t)(stg + XS_A + 32 * wave * 32), 16, bvo, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(sr, (lds_ptr_t)(stg + XS_A + XS_B + 256 * wave), 4, svo, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(tr, (lds_ptr_t)(stg + XS_A + XS_B + XS_S + 256 * wave), 4, tvo, 0, 0,
+                                             0);
   };
   // wait until at most this wavefront's two newest slices are in flight (and
   // its LDS reads are done), then the barrier that publishes everyone's older
   // slices
   auto publish = [&]() __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(8 | (7 << 4));  // vmcnt(8) expcnt(7) lgkmcnt(0)
+    __builtin_amdgcn_s_waitcnt(10 | (7 << 4));  // vmcnt(10) expcnt(7) lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
   };
 
@@ -151,8 +142,9 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   const int fr = lane & 31, fg = lane >> 5;
   // per-lane fragment offsets within a stage: token-row halves h = 0, 1 of
   // product 0 (product 1 is 32 rows = 2 KB further), weight rows of product 0
-  // (product ct is 1 KB further), the scale bytes; weight-scale rows in LDS
-  uint32_t a0, a1, b0, q0, brow[4];
+  // (product ct is 1 KB further), the scale bytes (the next 32 rows' dwords
+  // are 256 B further)
+  uint32_t a0, a1, b0, q0, p0;
   {
     const int r = wm * 64 + fr;
     a0 = r * 64 + 16 * (fg ^ swz_a(r));
@@ -160,19 +152,18 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
     q0 = XS_A + XS_B + 512 * wm + 4 * fr + fg;  // row r: dword r % 32 of block r / 32
     const int rb = wn * 128 + fr;
     b0 = XS_A + rb * 32 + 16 * (fg ^ swz_b(rb));
-#pragma unroll
-    for (int ct = 0; ct < 4; ++ct) brow[ct] = (rb + 32 * ct) * kb32 + fg;
+    p0 = XS_A + XS_B + XS_S + 1024 * wn + 4 * fr + fg;
   }
   struct Frag {
     u32x4 a[2][2], b[4];
     int sa[2], sb[4];
   };
-  // fragments of slice ks (of parity PAR) from a stage; the offsets pass
-  // through an empty asm statement so that the stage addresses are formed
-  // per slice rather than kept in registers for all five stages
-  auto read = [&](Frag& f, const uint8_t* stg, int ks, auto PAR_) __attribute__((always_inline)) {
+  // fragments of a slice of parity PAR from a stage; the offsets pass through
+  // an empty asm statement so that the stage addresses are formed per slice
+  // rather than kept in registers for all five stages
+  auto read = [&](Frag& f, const uint8_t* stg, auto PAR_) __attribute__((always_inline)) {
     constexpr int PAR = decltype(PAR_)::value;
-    asm volatile("" : "+v"(a0), "+v"(a1), "+v"(b0), "+v"(q0));
+    asm volatile("" : "+v"(a0), "+v"(a1), "+v"(b0), "+v"(q0), "+v"(p0));
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
       f.a[rt][0] = ld16(stg + a0 + 2048 * rt);
@@ -182,7 +173,7 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) {
       f.b[ct] = ld16(stg + b0 + 1024 * ct);
-      f.sb[ct] = bsc[brow[ct] + 2 * ks];
+      f.sb[ct] = stg[p0 + 256 * ct + 2 * PAR];
     }
   };
   v16f acc[2][4];
@@ -220,7 +211,7 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   for (int s = 0; s < 4; ++s) dma(stage_of(s), s);
   publish();
   Frag fa[2];
-  read(fa[0], d0, 0, std::integral_constant<int, 0>{});
+  read(fa[0], d0, std::integral_constant<int, 0>{});
 
   // slice i uses stage i % 5 and fragment set i % 2 (the loop is unrolled
   // ten times); the fragments read past the last slice are never used
@@ -228,7 +219,7 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
     constexpr int S = decltype(S_)::value, H = decltype(H_)::value;
     __builtin_amdgcn_sched_barrier(0);  // nothing moves between slices
     dma(stage_of((S + 4) % 5), i + 4);
-    read(fa[H ^ 1], stage_of((S + 1) % 5), i + 1, std::integral_constant<int, H ^ 1>{});
+    read(fa[H ^ 1], stage_of((S + 1) % 5), std::integral_constant<int, H ^ 1>{});
     mfma(fa[H]);
     publish();
   };
@@ -317,7 +308,8 @@ __global__ __launch_bounds__(256) void mx_quant_kernel(MxQuant P) {
   if (blk >= (int64_t)P.rows * per_row) return;
   const int64_t row = blk / per_row;
   const int c0 = (int)(blk - row * per_row) * 32;
-  const bf16* src = reinterpret_cast<const bf16*>(P.in) + row * P.cols + c0;
+  const int64_t src_row = P.row_src ? P.row_src[row] : row;
+  const bf16* src = reinterpret_cast<const bf16*>(P.in) + src_row * P.cols + c0;
   float v[32];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -337,8 +329,8 @@ __global__ __launch_bounds__(256) void mx_quant_kernel(MxQuant P) {
     e = (int)((__float_as_uint(amax) >> 23) & 0xFF) - 127 - 8;
     e = max(-127, min(127, e));
   }
-  // the GEMM operand layout: code rows padded to whole 128-byte lines, the
-  // four scale bytes of a row's 128 columns in one dword
+  // the GEMM operand layout: 64-column slices of all rows in turn, the four
+  // scale bytes of a row's 128 columns in one dword
   const int64_t sidx = P.gemm_layout ? ((int64_t)(c0 / 128) * P.rows + row) * 4 + (c0 / 32) % 4
                                      : row * per_row + c0 / 32;
   P.scales[sidx] = (uint8_t)(e + 127);
@@ -351,21 +343,40 @@ __global__ __launch_bounds__(256) void mx_quant_kernel(MxQuant P) {
     for (int i = 0; i < 4; ++i) w |= e4m3_of(v[4 * q + i] * inv) << (8 * i);
     out[q] = w;
   }
-  uint8_t* dst = P.codes + row * (P.gemm_layout ? mx_code_stride(P.cols) : P.cols) + c0;
+  uint8_t* dst = P.codes + (P.gemm_layout ? ((int64_t)(c0 / 64) * P.rows + row) * 64 + c0 % 64 : row * P.cols + c0);
   st16(dst, u32x4{out[0], out[1], out[2], out[3]});
   st16(dst + 16, u32x4{out[4], out[5], out[6], out[7]});
+}
+
+// MXFP4 weights into slice order: a thread per (group, row, block of 32):
+// 16 code bytes to their 64-column slice, the scale byte to its dword; the
+// unused bytes of a last, partial dword get 127 (scale 1)
+__global__ __launch_bounds__(256) void mx_pack_kernel(MxPack P) {
+  const int kb = P.cols / 32, kq = (kb + 3) / 4;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)P.groups * P.rows * kq * 4) return;
+  const int b = (int)(t % (kq * 4));
+  const int64_t gr = t / (kq * 4);  // group * rows + row
+  const int g = (int)(gr / P.rows), r = (int)(gr - (int64_t)g * P.rows);
+  uint8_t* ds = P.dst + mx_packed_codes_bytes(P.groups, P.rows, P.cols) +
+                ((int64_t)g * kq + b / 4) * P.rows * 4 + (int64_t)r * 4 + b % 4;
+  if (b >= kb) {
+    *ds = 127;
+    return;
+  }
+  *ds = P.scales[gr * kb + b];
+  const u32x4 c = ld16(P.codes + gr * (P.cols / 2) + 16 * b);
+  st16(P.dst + (((int64_t)g * (P.cols / 64) + b / 2) * P.rows + r) * 32 + 16 * (b % 2), c);
 }
 
 }  // namespace
 
 bool mx_gemm_applies(const Gemm& g) {
-  // buffer loads with 32-bit offsets below 2^31: token rows and their scales
-  // from x itself, one group's codes
+  // buffer loads address a slice's rows with 32-bit offsets below 2^31
   const int64_t xr = g.x_rows > 0 ? g.x_rows : g.n_rows;
-  return g.k > 0 && g.k % 64 == 0 && g.k <= MX_MAX_K && g.n % 16 == 0 && g.n_groups <= TILE_MAXG && g.x_scales &&
-         g.w_scales && (uintptr_t)g.w_scales % 16 == 0 && (uintptr_t)g.x % 16 == 0 &&
-         (uintptr_t)g.x_scales % 4 == 0 && xr * mx_code_stride(g.k) < (1LL << 31) &&
-         mx_scale_bytes(xr, g.k) < (1LL << 31) && (int64_t)g.n * g.k / 2 < (1LL << 31);
+  return g.k > 0 && g.k % 64 == 0 && g.n % 16 == 0 && g.n_groups <= TILE_MAXG && g.x_scales && g.w_scales &&
+         !g.row_src && (uintptr_t)g.x % 16 == 0 && (uintptr_t)g.w % 16 == 0 && (uintptr_t)g.x_scales % 4 == 0 &&
+         (uintptr_t)g.w_scales % 4 == 0 && xr * 64 < (1LL << 31) && g.w_group_stride == (int64_t)g.n * g.k / 2;
 }
 
 hipError_t launch_gemm_mx(const Gemm& g, hipStream_t s) {
@@ -378,6 +389,13 @@ hipError_t launch_gemm_mx(const Gemm& g, hipStream_t s) {
     case EPI_BIAS: hipLaunchKernelGGL((gemm_mx_kernel<EPI_BIAS>), gd, bd, 0, s, g); break;
     default: return hipErrorNotSupported;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_mx_pack(const MxPack& p, hipStream_t s) {
+  if (p.groups <= 0 || p.rows <= 0 || p.cols <= 0 || p.cols % 64) return hipErrorInvalidValue;
+  const int64_t n = (int64_t)p.groups * p.rows * ((p.cols / 32 + 3) / 4) * 4;
+  hipLaunchKernelGGL(mx_pack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, p);
   return hipGetLastError();
 }
 

@@ -182,26 +182,45 @@ struct Gemm {
 constexpr uint32_t LOGIT_RNG_TAG = 0x4C4D5330u;  // counter word 3 of the sampling draws
 hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s);
 // Scaled matrix-core products (gemm_mx.hip): MXFP8 activations (x, x_scales)
-// times MXFP4 weights (w, w_scales); k a multiple of 64 and at most MX_MAX_K
-// (the tile's weight scales stay in LDS for the whole reduction), n a
-// multiple of 16, w_scales 16-byte aligned. The activations are in the GEMM
-// operand layout that mx_quant writes: codes [x_rows][mx_code_stride(k)]
-// (every row starts on a 128-byte line) and scales in dwords of four blocks,
-// [ceil(k / 128)][x_rows][4].
-constexpr int MX_MAX_K = 3072;
-__host__ __device__ constexpr int mx_code_stride(int k) { return (k + 127) / 128 * 128; }
+// times MXFP4 weights (w, w_scales), k a multiple of 64, n of 16, every
+// operand in slice order so that a 64-wide reduction slice of 256 rows is one
+// contiguous run:
+//   x: E4M3 code (row r, column k) at ((k / 64) * x_rows + r) * 64 + k % 64;
+//   x_scales: dword (k / 128) * x_rows + r, byte j = block 4 (k / 128) + j;
+//   w: per group, E2M1 bytes of (row r, slice s) at (s * n + r) * 32 (low
+//      nibble first), groups w_group_stride bytes apart (n * k / 2);
+//   w_scales: per group, dword (k / 128) * n + r, groups n * ceil(k / 128) * 4
+//      bytes apart.
+// The rows of a group are x rows group_off[g] .. (row_src must be null).
 __host__ __device__ constexpr int64_t mx_scale_bytes(int64_t rows, int k) { return (int64_t)((k + 127) / 128) * rows * 4; }
 bool mx_gemm_applies(const Gemm& g);
 hipError_t launch_gemm_mx(const Gemm& g, hipStream_t s);
-// bf16 rows -> MXFP8 (E4M3 codes, E8M0 scales per 32 columns)
+// bf16 rows -> MXFP8 (E4M3 codes, E8M0 scales per 32 columns); output row r
+// quantizes input row row_src[r] (row r when null)
 struct MxQuant {
-  const void* in;  // [rows][cols] bf16
-  int64_t rows;
+  const void* in;  // [*][cols] bf16
+  const int32_t* row_src;
+  int64_t rows;    // output rows
   int cols;
   uint8_t* codes;
   uint8_t* scales;
-  int gemm_layout;  // 0: codes [rows][cols], scales [rows][cols / 32]; 1: the GEMM operand layout
+  int gemm_layout;  // 0: codes [rows][cols], scales [rows][cols / 32]; 1: the slice order above
 };
+// MXFP4 weights [groups][rows][cols / 2] + scales [groups][rows][cols / 32]
+// -> the slice order above (codes, then scales at mx_packed_scales_offset)
+struct MxPack {
+  const uint8_t* codes;
+  const uint8_t* scales;
+  uint8_t* dst;
+  int groups, rows, cols;
+};
+__host__ __device__ inline size_t mx_packed_codes_bytes(int groups, int rows, int cols) {
+  return ((size_t)groups * rows * (cols / 2) + 255) & ~size_t(255);
+}
+__host__ __device__ inline size_t mx_packed_bytes(int groups, int rows, int cols) {
+  return mx_packed_codes_bytes(groups, rows, cols) + (size_t)groups * mx_scale_bytes(rows, cols);
+}
+hipError_t launch_mx_pack(const MxPack& p, hipStream_t s);
 hipError_t launch_mx_quant(const MxQuant& p, hipStream_t s);
 // LDS-tiled path (gemm_tiled.hip): bf16, k a multiple of 64, at least
 // TILED_MIN_TOTAL_ROWS rows in all and groups averaging TILED_MIN_ROWS rows;

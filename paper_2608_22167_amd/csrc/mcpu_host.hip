@@ -70,10 +70,8 @@ int check_cfg(const mcpu_layer_cfg* c) {
     return fail(MCPU_EINVAL, "expert_fmt %d", c->expert_fmt);
   if (c->expert_fmt != MCPU_EXPERT_DENSE && c->dtype != MCPU_BF16)
     return fail(MCPU_EUNSUPPORTED, "MXFP4 experts need a bf16 layer");
-  if (c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE &&
-      (c->hidden % 64 || c->ffn_dim % 64 || c->hidden > MX_MAX_K || c->ffn_dim > MX_MAX_K))
-    return fail(MCPU_EUNSUPPORTED, "native MXFP4 experts need hidden and ffn_dim multiples of 64, at most %d",
-                MX_MAX_K);
+  if (c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE && (c->hidden % 64 || c->ffn_dim % 64))
+    return fail(MCPU_EUNSUPPORTED, "native MXFP4 experts need hidden and ffn_dim multiples of 64");
   if (!(c->rms_eps >= 0.f)) return fail(MCPU_EINVAL, "rms_eps");
   return MCPU_OK;
 }
@@ -238,10 +236,11 @@ MoeBufs carve_moe(Carve& cv, const mcpu_layer_cfg* c, int max_tokens) {
   m.y = cv.take<float>(T * K * c->hidden);
   m.hq = m.hs = m.aq = m.as = nullptr;
   if (c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE) {
-    // in the GEMM operand layout (whole-line code rows, scale dwords)
-    m.hq = cv.take<uint8_t>(T * mx_code_stride(c->hidden));
-    m.hs = cv.take<uint8_t>(mx_scale_bytes(T, c->hidden));
-    m.aq = cv.take<uint8_t>(T * K * mx_code_stride(c->ffn_dim));
+    // in the GEMM operand layout, one row per (token, expert) assignment in
+    // expert order
+    m.hq = cv.take<uint8_t>(T * K * c->hidden);
+    m.hs = cv.take<uint8_t>(mx_scale_bytes(T * K, c->hidden));
+    m.aq = cv.take<uint8_t>(T * K * c->ffn_dim);
     m.as = cv.take<uint8_t>(mx_scale_bytes(T * K, c->ffn_dim));
   }
   return m;
@@ -255,8 +254,14 @@ int check_weights(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, bool att
     return fail(MCPU_EINVAL, "MXFP4 experts need the scale arrays s_gu and s_d");
   if (attn && (!w->g1 || !w->w_qkv || !w->b_qkv || !w->w_o || !w->b_o || !w->rope_cos || !w->rope_sin))
     return fail(MCPU_EINVAL, "an attention weight pointer is NULL");
-  if ((w->w_gu_packed || w->w_d_packed) && (c->expert_fmt != MCPU_EXPERT_DENSE || c->dtype != MCPU_BF16))
+  if (c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE) {
+    if (!w->w_gu_packed || !w->w_d_packed)
+      return fail(MCPU_EINVAL, "native MXFP4 experts need the slice-order copies w_gu_packed and w_d_packed");
+    if ((uintptr_t)w->w_gu_packed % 256 || (uintptr_t)w->w_d_packed % 256)
+      return fail(MCPU_EINVAL, "w_gu_packed and w_d_packed must be 256-byte aligned");
+  } else if ((w->w_gu_packed || w->w_d_packed) && (c->expert_fmt != MCPU_EXPERT_DENSE || c->dtype != MCPU_BF16)) {
     return fail(MCPU_EINVAL, "packed expert weights need bf16 dense experts");
+  }
   if (w->w_gu_packed && (2 * c->ffn_dim % 16 || c->hidden % 64))
     return fail(MCPU_EINVAL, "packed w_gu needs 2 * ffn_dim %% 16 == 0 and hidden %% 64 == 0");
   if (w->w_d_packed && (c->hidden % 16 || c->ffn_dim % 64))
@@ -294,17 +299,23 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   // per-expert stride: elements for dense experts, bytes of E2M1 codes for MXFP4
   const int64_t fdiv = c->expert_fmt != MCPU_EXPERT_DENSE ? 2 : 1;
   const bool native = c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE;
-  if (native) {  // the first product reads the normalised rows in MXFP8
+  if (native) {  // the first product reads the normalised rows in MXFP8, in expert order
     MxQuant q{};
-    q.in = m.hn; q.rows = T; q.cols = H; q.codes = m.hq; q.scales = m.hs; q.gemm_layout = 1;
+    q.in = m.hn; q.row_src = m.src_tok; q.rows = (int64_t)T * K; q.cols = H; q.codes = m.hq; q.scales = m.hs;
+    q.gemm_layout = 1;
     HIP_TRY(launch_mx_quant(q, st));
   }
   Gemm g1{};
   g1.w = w->w_gu; g1.w_scales = w->s_gu; g1.w_group_stride = (int64_t)2 * I * H / fdiv; g1.n = 2 * I; g1.k = H;
-  g1.x = native ? (const void*)m.hq : m.hn; g1.x_scales = native ? m.hs : nullptr; g1.row_src = m.src_tok; g1.group_off = m.group_off; g1.n_rows = T * K; g1.n_groups = E;
+  g1.x = m.hn; g1.row_src = m.src_tok; g1.group_off = m.group_off; g1.n_rows = T * K; g1.n_groups = E;
   g1.epi = EPI_SWIGLU; g1.bias = w->b_gu; g1.bias_group_stride = 2 * I; g1.out = m.act;
   g1.swiglu_alpha = c->swiglu_alpha; g1.swiglu_limit = c->swiglu_limit; g1.swiglu_beta = c->swiglu_beta;
   g1.err = err; g1.max_rows_per_group = max_rows; g1.x_rows = T; g1.w_packed = w->w_gu_packed;
+  if (native) {  // slice-order operands, rows already in expert order
+    g1.w = w->w_gu_packed; g1.w_packed = nullptr;
+    g1.w_scales = (const uint8_t*)w->w_gu_packed + mx_packed_codes_bytes(E, 2 * I, H);
+    g1.x = m.hq; g1.x_scales = m.hs; g1.row_src = nullptr; g1.x_rows = T * K;
+  }
   {
     Timed tm(MCPU_KERNEL_EXPERT_GU, st);
     HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g1, st));
@@ -317,9 +328,14 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   }
   Gemm g2{};
   g2.w = w->w_d; g2.w_scales = w->s_d; g2.w_group_stride = (int64_t)H * I / fdiv; g2.n = H; g2.k = I;
-  g2.x = native ? (const void*)m.aq : m.act; g2.x_scales = native ? m.as : nullptr; g2.group_off = m.group_off; g2.n_rows = T * K; g2.n_groups = E;
+  g2.x = m.act; g2.group_off = m.group_off; g2.n_rows = T * K; g2.n_groups = E;
   g2.epi = EPI_BIAS; g2.bias = w->b_d; g2.bias_group_stride = H; g2.out = m.y;
   g2.err = err; g2.max_rows_per_group = max_rows; g2.w_packed = w->w_d_packed;
+  if (native) {
+    g2.w = w->w_d_packed; g2.w_packed = nullptr;
+    g2.w_scales = (const uint8_t*)w->w_d_packed + mx_packed_codes_bytes(E, H, I);
+    g2.x = m.aq; g2.x_scales = m.as; g2.x_rows = T * K;
+  }
   {
     Timed tm(MCPU_KERNEL_EXPERT_DOWN, st);
     HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g2, st));
@@ -524,6 +540,27 @@ int mcpu_pack_weights(int32_t dtype, const void* src, void* dst, int32_t n_group
   const uintptr_t d0 = (uintptr_t)dst, d1 = d0 + bytes;
   if (s0 < d1 && d0 < s1) return fail(MCPU_EINVAL, "src and dst overlap");
   HIP_TRY(launch_pack_weights(src, dst, n_groups, rows, cols, stream));
+  return MCPU_OK;
+}
+
+size_t mcpu_packed_mxfp4_bytes(int32_t n_groups, int32_t rows, int32_t cols) {
+  if (n_groups <= 0 || rows <= 0 || rows % 16 || cols <= 0 || cols % 64) return 0;
+  return mx_packed_bytes(n_groups, rows, cols);
+}
+
+int mcpu_pack_mxfp4(const uint8_t* codes, const uint8_t* scales, void* dst, int32_t n_groups, int32_t rows,
+                    int32_t cols, hipStream_t stream) {
+  const size_t bytes = mcpu_packed_mxfp4_bytes(n_groups, rows, cols);
+  if (bytes == 0) return fail(MCPU_EINVAL, "groups %d, rows %d (multiple of 16), cols %d (multiple of 64)", n_groups, rows, cols);
+  if (!codes || !scales || !dst) return fail(MCPU_EINVAL, "NULL pointer");
+  if ((uintptr_t)codes % 16 || (uintptr_t)dst % 256) return fail(MCPU_EINVAL, "codes must be 16-byte and dst 256-byte aligned");
+  const uintptr_t d0 = (uintptr_t)dst, d1 = d0 + bytes;
+  const uintptr_t c0 = (uintptr_t)codes, c1 = c0 + (size_t)n_groups * rows * (cols / 2);
+  const uintptr_t s0 = (uintptr_t)scales, s1 = s0 + (size_t)n_groups * rows * (cols / 32);
+  if ((c0 < d1 && d0 < c1) || (s0 < d1 && d0 < s1)) return fail(MCPU_EINVAL, "source and dst overlap");
+  MxPack p{};
+  p.codes = codes; p.scales = scales; p.dst = (uint8_t*)dst; p.groups = n_groups; p.rows = rows; p.cols = cols;
+  HIP_TRY(launch_mx_pack(p, stream));
   return MCPU_OK;
 }
 

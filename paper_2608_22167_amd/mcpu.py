@@ -29,7 +29,7 @@ EXPORTED = ("mcpu_last_error", "kv_pool_create", "kv_pool_destroy", "kv_pool_fre
             "decode_layer_workspace_size", "decode_layer", "mcpu_check_device_errors",
             "mcpu_timing_start", "mcpu_timing_read", "mcpu_packed_weights_bytes", "mcpu_pack_weights",
             "lm_head_workspace_size", "lm_head_sample", "embed_tokens", "decode_layer_noalloc",
-            "mcpu_mxfp8_quantize")
+            "mcpu_mxfp8_quantize", "mcpu_packed_mxfp4_bytes", "mcpu_pack_mxfp4")
 NOALLOC_SCRATCH_BYTES = 128 << 20  # the static scratch of decode_layer_noalloc, per GPU
 
 KERNELS = ("attn_plan", "rmsnorm", "qkv", "attn_split", "attn_combine", "oproj", "router", "permute",
@@ -107,6 +107,9 @@ def lib():
                                      vp, vp, sz, vp]
         L.embed_tokens.argtypes = [vp, i32, i32, i32, vp, vp, vp, sz, vp]
         L.mcpu_mxfp8_quantize.argtypes = [vp, ctypes.c_int64, i32, vp, vp, vp]
+        L.mcpu_packed_mxfp4_bytes.argtypes = [i32, i32, i32]
+        L.mcpu_packed_mxfp4_bytes.restype = sz
+        L.mcpu_pack_mxfp4.argtypes = [vp, vp, vp, i32, i32, i32, vp]
         L.mcpu_timing_start.argtypes = [i32, i32]
         L.mcpu_timing_read.argtypes = [i32, vp, i32, i32p]
         _LIB = L
@@ -168,9 +171,24 @@ def packed_weights(w: torch.Tensor, stream=None) -> torch.Tensor:
     return out
 
 
+def packed_mxfp4(codes: torch.Tensor, scales: torch.Tensor, stream=None) -> torch.Tensor:
+    """Slice-order copy of MXFP4 weights (mcpu_pack_mxfp4): codes uint8
+    [groups, rows, cols/2], scales uint8 [groups, rows, cols/32]."""
+    assert codes.dtype == torch.uint8 and scales.dtype == torch.uint8 and codes.dim() == 3 and codes.is_cuda
+    assert codes.is_contiguous() and scales.is_contiguous()
+    g, rows, half = (int(d) for d in codes.shape)
+    n = lib().mcpu_packed_mxfp4_bytes(g, rows, 2 * half)
+    if n == 0:
+        raise McpuError(MCPU_EINVAL, f"MXFP4 weights {tuple(codes.shape)} cannot be packed (rows % 16, cols % 64)")
+    out = torch.empty(n, dtype=torch.uint8, device=codes.device)
+    _check(lib().mcpu_pack_mxfp4(_ptr(codes), _ptr(scales), _ptr(out), g, rows, 2 * half, _stream(stream)))
+    return out
+
+
 class DeviceWeights:
     """Layer parameters copied to the GPU, with the mcpu_layer_weights struct.
-    With pack=True, bf16 dense experts also get their streaming-order copies."""
+    With pack=True, bf16 dense experts also get their streaming-order copies;
+    native MXFP4 experts always get their slice-order copies."""
 
     def __init__(self, shape, W, device="cuda", pack=True):
         self.t = {k: v.to(device).contiguous() for k, v in W.items()}
@@ -179,6 +197,9 @@ class DeviceWeights:
         if pack and not mx and shape.dtype == "bf16" and shape.hidden % 64 == 0 and shape.ffn_dim % 64 == 0:
             t["w_gu_packed"] = packed_weights(t["w_gu"])
             t["w_d_packed"] = packed_weights(t["w_d"])
+        if shape.expert_fmt == "mxfp4_native" and "w_gu_packed" not in t:
+            t["w_gu_packed"] = packed_mxfp4(t["w_gu_codes"], t["w_gu_scales"])
+            t["w_d_packed"] = packed_mxfp4(t["w_d_codes"], t["w_d_scales"])
         p = lambda k: _ptr(t[k]) if k in t else None
         self.struct = LayerWeights(
             g1=p("g1"), w_qkv=p("w_qkv"), b_qkv=p("b_qkv"), w_o=p("w_o"), b_o=p("b_o"), g2=p("g2"),

@@ -99,6 +99,40 @@ def test_packed_weights_size_and_argument_checks():
     assert L.mcpu_pack_weights(mcpu.MCPU_BF16, a, a + 1024, 1, 16, 64, None) == mcpu.MCPU_EINVAL  # overlap
 
 
+def test_packed_mxfp4_size_and_argument_checks():
+    """mcpu_packed_mxfp4_bytes: the codes (rounded up to 256 bytes), then one
+    scale dword per row and 128 columns; mcpu_pack_mxfp4 rejects bad
+    arguments on the host (dummy addresses: every case returns before a
+    launch)."""
+    L = mcpu.lib()
+    assert L.mcpu_packed_mxfp4_bytes(32, 5760, 2880) == 32 * 5760 * 1440 + 32 * 23 * 5760 * 4
+    assert L.mcpu_packed_mxfp4_bytes(1, 16, 64) == 512 + 16 * 4     # 512 code bytes, already whole
+    assert L.mcpu_packed_mxfp4_bytes(1, 16, 192) == 1536 + 2 * 16 * 4
+    for bad in [(0, 16, 64), (1, 8, 64), (1, 16, 96), (1, 16, 0), (-1, 16, 64)]:
+        assert L.mcpu_packed_mxfp4_bytes(*bad) == 0, bad
+    a, s, b = 1 << 20, 1 << 24, 1 << 30
+    assert L.mcpu_pack_mxfp4(a, s, b, 1, 16, 96, None) == mcpu.MCPU_EINVAL
+    assert L.mcpu_pack_mxfp4(None, s, b, 1, 16, 64, None) == mcpu.MCPU_EINVAL
+    assert L.mcpu_pack_mxfp4(a, s, b + 16, 1, 16, 64, None) == mcpu.MCPU_EINVAL      # dst not 256-aligned
+    assert L.mcpu_pack_mxfp4(a + 8, s, b, 1, 16, 64, None) == mcpu.MCPU_EINVAL       # codes misaligned
+    assert L.mcpu_pack_mxfp4(a, s, a + 256, 1, 16, 64, None) == mcpu.MCPU_EINVAL     # overlaps the codes
+    assert L.mcpu_pack_mxfp4(a, b + 256, b, 1, 16, 64, None) == mcpu.MCPU_EINVAL     # overlaps the scales
+
+
+def test_native_experts_need_their_slice_order_copies():
+    """A native-MXFP4 layer without w_gu_packed / w_d_packed is rejected
+    before any launch."""
+    import dataclasses
+    shape = dataclasses.replace(W.GPT_OSS_20B, expert_fmt="mxfp4_native")
+    L = mcpu.lib()
+    cfg = mcpu.make_cfg(shape)
+    w = _dummy_weights(mxfp4=True)
+    rc = L.moe_forward(ctypes.byref(cfg), ctypes.byref(w), 4, _DUMMY, _DUMMY, None, None, None, _DUMMY + (1 << 24),
+                       1 << 30, None)
+    assert rc == mcpu.MCPU_EINVAL
+    assert b"w_gu_packed" in L.mcpu_last_error()
+
+
 # dummy device addresses: never dereferenced, every call below returns on the host
 _DUMMY = 1 << 32
 

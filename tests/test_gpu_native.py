@@ -1,6 +1,7 @@
 """Native MXFP4 experts on the GPU (MXFP4 weights x MXFP8 activations on the
 scaled matrix cores) against the reference with its MXFP8 activation rule,
-through the C ABI: the quantizer bit for bit, the MoE sub-block at a few to
+through the C ABI: the quantizer and the weights' slice-order copy bit for
+bit, the MoE sub-block at a few to
 thousands of rows per expert (ragged tiles and reduction tails), whole
 layers, and the mixed prefill step at full size on sampled sequences."""
 from dataclasses import replace
@@ -39,6 +40,28 @@ def test_mxfp8_quantize_bit_exact():
     rc, rs = O.mxfp8_quant(xb.double().numpy())
     np.testing.assert_array_equal(scales.cpu().numpy(), rs)
     np.testing.assert_array_equal(codes.cpu().numpy(), rc)
+
+
+@pytest.mark.parametrize("groups,rows,cols", [(2, 32, 192), (1, 16, 2880), (3, 48, 64)])
+def test_pack_mxfp4_layout_byte_exact(groups, rows, cols):
+    """mcpu_pack_mxfp4 against the slice order the header states, rebuilt
+    with numpy reshapes (192 columns: a last scale dword with two unused
+    bytes, which hold 127)."""
+    rng = np.random.default_rng(groups * 1000 + cols)
+    codes = rng.integers(0, 256, (groups, rows, cols // 2), dtype=np.uint8)
+    scales = rng.integers(2, 253, (groups, rows, cols // 32), dtype=np.uint8)
+    out = mcpu.packed_mxfp4(torch.from_numpy(codes).cuda(), torch.from_numpy(scales).cuda())
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    cb = (groups * rows * cols // 2 + 255) // 256 * 256
+    want_c = codes.reshape(groups, rows, cols // 64, 32).transpose(0, 2, 1, 3).reshape(-1)
+    np.testing.assert_array_equal(got[:want_c.size], want_c)
+    kq = (cols // 32 + 3) // 4
+    sp = np.full((groups, rows, kq * 4), 127, np.uint8)
+    sp[:, :, :cols // 32] = scales
+    want_s = sp.reshape(groups, rows, kq, 4).transpose(0, 2, 1, 3).reshape(-1)
+    np.testing.assert_array_equal(got[cb:cb + want_s.size], want_s)
+    assert got.size == cb + want_s.size
 
 
 def _moe_check(s, T, seed, h_seed=4, sample=None):
