@@ -16,22 +16,22 @@
 //
 // Tile 256 token rows x 256 weight rows, eight wavefronts (4 x 2), each
 // owning 64 x 128 = 2 x 4 products of 32 x 32. The reduction runs in slices
-// of 64 (one product deep) through a ring of five LDS stages that 16-byte
+// of 64 (one product deep) through a ring of six LDS stages that 16-byte
 // buffer loads fill straight from global memory (a wavefront's load fills
 // 1 KB of LDS, lane l at byte 16 l), so staging costs neither registers nor
 // LDS write instructions. Every operand is in slice order (kernels.h), so a
 // slice of the tile is four contiguous runs: 16 KB of activation codes, 8 KB
 // of weight codes and 1 KB of scale dwords each, read as whole cache lines.
 // While slice i is multiplied, the fragments of slice i + 1 are read, and
-// slice i + 4 is requested into the stage slice i - 1 left; before each
+// slice i + 5 is requested into the stage slice i - 1 left; before each
 // barrier a wavefront waits for its own loads of slice i + 2, which the
-// barrier then publishes.
+// barrier then publishes (three slices stay in flight across it).
 //   Stage layout: token rows 64 B (chunk q of row r in slot q ^ ((r >> 1) & 3)),
 // weight rows 32 B (chunk q in slot q ^ (((r >> 2) ^ (r >> 3)) & 1)), which
 // keeps the fragment reads free of bank conflicts, then the token rows' and
-// the weight rows' scale dwords (32 rows per 256 B: lanes l and l + 32 of a
-// load fetch the same dword, so every wavefront issues the same five loads per
-// slice). The finished fp32 tile goes through LDS to the fused epilogue
+// the weight rows' scale dwords (1 KB each: wavefronts 0-3 load the former,
+// 4-7 the latter, so every wavefront issues the same four loads per slice).
+// The finished fp32 tile goes through LDS to the fused epilogue
 // (gemm_epilogue.h), 16 rows at a time.
 #include <type_traits>
 
@@ -49,11 +49,11 @@ typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 constexpr int XM = 256, XN = 256, XK = 64;  // output tile, reduction per slice
 constexpr int XTH = 512;
-constexpr int XS_A = XM * XK, XS_B = XN * XK / 2, XS_S = 8 * 256;
-constexpr int XSTAGE = XS_A + XS_B + 2 * XS_S;  // 28 KB
+constexpr int XS_A = XM * XK, XS_B = XN * XK / 2, XS_S = 4 * (XM + XN);
+constexpr int XSTAGE = XS_A + XS_B + XS_S;  // 26 KB
 constexpr int XEP = 16, XCLD = XN + 4;      // epilogue pass rows, fp32 row stride
 static_assert(XEP * XCLD * 4 <= XSTAGE, "an epilogue pass fits one stage");
-static_assert(5 * XSTAGE + 4 * (TILE_MAXG + 1) <= 160 * 1024, "LDS");
+static_assert(6 * XSTAGE + 4 * (TILE_MAXG + 1) <= 160 * 1024, "LDS");
 constexpr int XGM = 2;                      // m-tiles per band
 constexpr int XBUF_DWORD3 = 0x00020000;     // raw buffer descriptor word 3 (gfx9 family)
 
@@ -72,6 +72,7 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   __shared__ __align__(1024) uint8_t d2[XSTAGE];
   __shared__ __align__(1024) uint8_t d3[XSTAGE];
   __shared__ __align__(1024) uint8_t d4[XSTAGE];
+  __shared__ __align__(1024) uint8_t d5[XSTAGE];
   __shared__ int mt_start[TILE_MAXG + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = uniform(tid >> 6);
 
@@ -87,16 +88,16 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
 
   // Loads of a slice: wavefront w fills token rows 32 w + 16 j + [0, 16)
   // (j = 0, 1; lane l lands in row + l / 4, slot l % 4), weight rows
-  // 32 w + [0, 32) (lane l in row l / 2, slot l % 2) and the scale dwords of
-  // token rows and of weight rows 32 w + [0, 32); each lane loads the global
-  // chunk its slot holds. Token rows past the tile's end read the next x rows
+  // 32 w + [0, 32) (lane l in row l / 2, slot l % 2), and the scale dwords of
+  // token rows 64 w + [0, 64) (w < 4) or of weight rows 64 (w - 4) + [0, 64);
+  // each lane loads the global chunk its slot holds. Token rows past the tile's end read the next x rows
   // (the last one at the end of x), weight rows past n repeat the last one;
   // their results are dropped. Buffer loads: per-slice bases, 32-bit per-lane
   // row offsets.
   const uint8_t* xq = reinterpret_cast<const uint8_t*>(P.x);
   const uint8_t* wq = reinterpret_cast<const uint8_t*>(P.w) + grp * P.w_group_stride;
   const uint8_t* ws = P.w_scales + grp * mx_scale_bytes(N, K);
-  uint32_t avo[2], bvo, svo, tvo;
+  uint32_t avo[2], bvo, svo;
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int r = 32 * wave + 16 * j + (lane >> 2);
@@ -105,35 +106,32 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   {
     const int r = 32 * wave + (lane >> 1);
     bvo = (uint32_t)(n0 + min(r, nrows - 1)) * 32u + 16u * ((lane & 1) ^ swz_b(r));
-    const int q = 32 * wave + (lane & 31);
-    svo = (uint32_t)min(m0 + q, xrows - 1) * 4u;
-    tvo = (uint32_t)(n0 + min(q, nrows - 1)) * 4u;
+    const int q = 64 * (wave & 3) + lane;
+    svo = wave < 4 ? (uint32_t)min(m0 + q, xrows - 1) * 4u : (uint32_t)(n0 + min(q, nrows - 1)) * 4u;
   }
 
   auto stage_of = [&](int s) __attribute__((always_inline)) {
-    return s == 0 ? d0 : s == 1 ? d1 : s == 2 ? d2 : s == 3 ? d3 : d4;
+    return s == 0 ? d0 : s == 1 ? d1 : s == 2 ? d2 : s == 3 ? d3 : s == 4 ? d4 : d5;
   };
-  // the loads of slice ks into a stage (5 per wavefront); slices past the
+  // the loads of slice ks into a stage (4 per wavefront); slices past the
   // end re-read the last one (never multiplied), so every slice issues the
   // same loads and the waits below count whole slices
   auto dma = [&](uint8_t* stg, int ks) __attribute__((always_inline)) {
     ks = uniform(min(ks, nk - 1));
     const __amdgpu_buffer_rsrc_t xr = rsrc(xq + (size_t)ks * xrows * 64);
     const __amdgpu_buffer_rsrc_t wr = rsrc(wq + (size_t)ks * N * 32);
-    const __amdgpu_buffer_rsrc_t sr = rsrc(P.x_scales + (size_t)(ks >> 1) * xrows * 4);
-    const __amdgpu_buffer_rsrc_t tr = rsrc(ws + (size_t)(ks >> 1) * N * 4);
+    const __amdgpu_buffer_rsrc_t sr = wave < 4 ? rsrc(P.x_scales + (size_t)(ks >> 1) * xrows * 4)
+                                               : rsrc(ws + (size_t)(ks >> 1) * N * 4);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr_t)(stg + 32 * wave * 64), 16, avo[0], 0, 0, 0);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_ptr_t)(stg + (32 * wave + 16) * 64), 16, avo[1], 0, 0, 0);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_ptr_t)(stg + XS_A + 32 * wave * 32), 16, bvo, 0, 0, 0);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(sr, (lds_ptr_t)(stg + XS_A + XS_B + 256 * wave), 4, svo, 0, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(tr, (lds_ptr_t)(stg + XS_A + XS_B + XS_S + 256 * wave), 4, tvo, 0, 0,
-                                             0);
   };
-  // wait until at most this wavefront's two newest slices are in flight (and
-  // its LDS reads are done), then the barrier that publishes everyone's older
-  // slices
+  // wait until at most this wavefront's three newest slices are in flight
+  // (and its LDS reads are done), then the barrier that publishes everyone's
+  // older slices
   auto publish = [&]() __attribute__((always_inline)) {
-    __builtin_amdgcn_s_waitcnt(10 | (7 << 4));  // vmcnt(10) expcnt(7) lgkmcnt(0)
+    __builtin_amdgcn_s_waitcnt(12 | (7 << 4));  // vmcnt(12) expcnt(7) lgkmcnt(0)
     __builtin_amdgcn_s_barrier();
   };
 
@@ -143,16 +141,16 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   // per-lane fragment offsets within a stage: token-row halves h = 0, 1 of
   // product 0 (product 1 is 32 rows = 2 KB further), weight rows of product 0
   // (product ct is 1 KB further), the scale bytes (the next 32 rows' dwords
-  // are 256 B further)
+  // are 128 B further)
   uint32_t a0, a1, b0, q0, p0;
   {
     const int r = wm * 64 + fr;
     a0 = r * 64 + 16 * (fg ^ swz_a(r));
     a1 = r * 64 + 16 * ((2 + fg) ^ swz_a(r));
-    q0 = XS_A + XS_B + 512 * wm + 4 * fr + fg;  // row r: dword r % 32 of block r / 32
+    q0 = XS_A + XS_B + 4 * r + fg;
     const int rb = wn * 128 + fr;
     b0 = XS_A + rb * 32 + 16 * (fg ^ swz_b(rb));
-    p0 = XS_A + XS_B + XS_S + 1024 * wn + 4 * fr + fg;
+    p0 = XS_A + XS_B + 4 * XM + 4 * rb + fg;
   }
   struct Frag {
     u32x4 a[2][2], b[4];
@@ -168,12 +166,12 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
     for (int rt = 0; rt < 2; ++rt) {
       f.a[rt][0] = ld16(stg + a0 + 2048 * rt);
       f.a[rt][1] = ld16(stg + a1 + 2048 * rt);
-      f.sa[rt] = stg[q0 + 256 * rt + 2 * PAR];
+      f.sa[rt] = stg[q0 + 128 * rt + 2 * PAR];
     }
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) {
       f.b[ct] = ld16(stg + b0 + 1024 * ct);
-      f.sb[ct] = stg[p0 + 256 * ct + 2 * PAR];
+      f.sb[ct] = stg[p0 + 128 * ct + 2 * PAR];
     }
   };
   v16f acc[2][4];
@@ -206,20 +204,20 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
     }
   };
 
-  // prologue: slices 0 .. 3 requested, 0 and 1 published, slice 0 read
+  // prologue: slices 0 .. 4 requested, 0 and 1 published, slice 0 read
 #pragma unroll
-  for (int s = 0; s < 4; ++s) dma(stage_of(s), s);
+  for (int s = 0; s < 5; ++s) dma(stage_of(s), s);
   publish();
   Frag fa[2];
   read(fa[0], d0, std::integral_constant<int, 0>{});
 
-  // slice i uses stage i % 5 and fragment set i % 2 (the loop is unrolled
-  // ten times); the fragments read past the last slice are never used
+  // slice i uses stage i % 6 and fragment set i % 2 (the loop is unrolled
+  // six times); the fragments read past the last slice are never used
   auto slice = [&](auto S_, auto H_, int i) __attribute__((always_inline)) {
     constexpr int S = decltype(S_)::value, H = decltype(H_)::value;
     __builtin_amdgcn_sched_barrier(0);  // nothing moves between slices
-    dma(stage_of((S + 4) % 5), i + 4);
-    read(fa[H ^ 1], stage_of((S + 1) % 5), std::integral_constant<int, H ^ 1>{});
+    dma(stage_of((S + 5) % 6), i + 5);
+    read(fa[H ^ 1], stage_of((S + 1) % 6), std::integral_constant<int, H ^ 1>{});
     mfma(fa[H]);
     publish();
   };
@@ -228,28 +226,21 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   using C2 = std::integral_constant<int, 2>;
   using C3 = std::integral_constant<int, 3>;
   using C4 = std::integral_constant<int, 4>;
+  using C5 = std::integral_constant<int, 5>;
   int i = 0;
-  for (; i + 10 <= nk; i += 10) {
+  for (; i + 6 <= nk; i += 6) {
     slice(C0{}, C0{}, i);
     slice(C1{}, C1{}, i + 1);
     slice(C2{}, C0{}, i + 2);
     slice(C3{}, C1{}, i + 3);
     slice(C4{}, C0{}, i + 4);
-    slice(C0{}, C1{}, i + 5);
-    slice(C1{}, C0{}, i + 6);
-    slice(C2{}, C1{}, i + 7);
-    slice(C3{}, C0{}, i + 8);
-    slice(C4{}, C1{}, i + 9);
+    slice(C5{}, C1{}, i + 5);
   }
   if (i < nk) slice(C0{}, C0{}, i);
   if (i + 1 < nk) slice(C1{}, C1{}, i + 1);
   if (i + 2 < nk) slice(C2{}, C0{}, i + 2);
   if (i + 3 < nk) slice(C3{}, C1{}, i + 3);
   if (i + 4 < nk) slice(C4{}, C0{}, i + 4);
-  if (i + 5 < nk) slice(C0{}, C1{}, i + 5);
-  if (i + 6 < nk) slice(C1{}, C0{}, i + 6);
-  if (i + 7 < nk) slice(C2{}, C1{}, i + 7);
-  if (i + 8 < nk) slice(C3{}, C0{}, i + 8);
   __builtin_amdgcn_s_waitcnt(0);  // every load landed and every read done before stage 0 holds the fp32 tile
   __syncthreads();
 
