@@ -324,7 +324,10 @@ __global__ __launch_bounds__(PTH) void gemm_pipe_kernel(Gemm P) {
 // publishes them to all wavefronts). Rows
 // are 64 bytes with no padding; chunk q of row r sits in 16-byte slot
 // q ^ ((r >> 1) & 3) of its row, which keeps the fragment reads free of bank
-// conflicts, and each lane loads the global chunk its slot holds.
+// conflicts, and each lane loads the global chunk its slot holds. With the
+// weights' streaming-order copy (WP), a 16-row block's slice is one
+// contiguous KiB already in fragment order (lane l's 16 bytes at 16 l), so
+// the weight loads are whole contiguous lines and land as they are.
 // ---------------------------------------------------------------------------
 constexpr int DROW = PK * 2;              // bytes per staged row
 constexpr int DSTAGE = (PM + PN) * DROW;  // bytes per stage (32 KB)
@@ -335,8 +338,9 @@ __device__ __forceinline__ int dswz(int r) { return (r >> 1) & 3; }
 constexpr int BUF_DWORD3 = 0x00020000;  // raw buffer descriptor word 3 (gfx9 family)
 typedef __attribute__((address_space(3))) void* lds_void_t;
 
-template <int EPI>
+template <int EPI, bool WP>
 __global__ __launch_bounds__(PTH) void gemm_dma_kernel(Gemm P) {
+  static_assert(!(WP && EPI == EPI_QKV), "the projection's row order is not the copy's");
   __shared__ __align__(1024) uint8_t d0[DSTAGE];
   __shared__ __align__(1024) uint8_t d1[DSTAGE];
   __shared__ __align__(1024) uint8_t d2[DSTAGE];
@@ -363,7 +367,11 @@ __global__ __launch_bounds__(PTH) void gemm_dma_kernel(Gemm P) {
   // slice offset in a scalar register.
   const int lr = lane >> 2, chunk = (lane & 3) ^ dswz(lr);
   const uint8_t* xb = reinterpret_cast<const uint8_t*>(P.x) + (P.row_src ? 0 : (int64_t)m0 * P.k * 2);
-  const uint8_t* wb = reinterpret_cast<const uint8_t*>(P.w) + (int64_t)grp * P.w_group_stride * 2;
+  // streaming-order copy: per group rows / 16 blocks of ceil(k / 128) 4 KiB
+  // chunks; slice ks of block b at (b * chunks) * 4 KiB + ks KiB
+  const int wchunks = (P.k + 127) / 128;
+  const uint8_t* wb = WP ? reinterpret_cast<const uint8_t*>(P.w_packed) + (int64_t)grp * (P.n / 16) * wchunks * 4096
+                         : reinterpret_cast<const uint8_t*>(P.w) + (int64_t)grp * P.w_group_stride * 2;
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(xb), 0, 0x7FFFFFFF, BUF_DWORD3);
   const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wb), 0, 0x7FFFFFFF, BUF_DWORD3);
   uint32_t xvo[2], wvo[2];
@@ -376,7 +384,12 @@ __global__ __launch_bounds__(PTH) void gemm_dma_kernel(Gemm P) {
     const int rc = min(rr, nrows - 1);
     const int blk = (n0 + rc) >> 4, nl = rc & 15;
     const int wrow = EPI == EPI_QKV ? block_row<EPI_QKV>(P, blk, nl) : blk * 16 + nl;
-    wvo[j] = (uint32_t)wrow * (uint32_t)(P.k * 2) + chunk * 16;
+    if (WP) {
+      const int b = min(n0 / 16 + 2 * wave + j, P.n / 16 - 1);  // the wavefront's 16-row block
+      wvo[j] = (uint32_t)b * (uint32_t)(wchunks * 4096) + 16u * lane;
+    } else {
+      wvo[j] = (uint32_t)wrow * (uint32_t)(P.k * 2) + chunk * 16;
+    }
   }
   const int ldst = 32 * wave * DROW;  // this wavefront's rows within an operand
   const int nk = P.k / PK;
@@ -384,7 +397,7 @@ __global__ __launch_bounds__(PTH) void gemm_dma_kernel(Gemm P) {
   const int wm = wave & 1, wn = wave >> 1;
   const int fr = lane & 15, slot = ((lane >> 4) ^ dswz(fr)) * 16;
   const int xoff = (wm * (PM / 2) + fr) * DROW + slot;
-  const int woff = (PM + wn * PWN + fr) * DROW + slot;
+  const int woff = WP ? PM * DROW + wn * PWN * DROW + 16 * lane : (PM + wn * PWN + fr) * DROW + slot;
   f32x4 acc[PNF][PMF];
 #pragma unroll
   for (int nb = 0; nb < PNF; ++nb)
@@ -400,7 +413,7 @@ __global__ __launch_bounds__(PTH) void gemm_dma_kernel(Gemm P) {
     const int soff = uniform(min(ks, nk - 1) * (PK * 2));
     uint8_t* dst = stg + (p < 2 ? 0 : PM * DROW) + ldst + 16 * (p & 1) * DROW;
     if (p < 2) __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void_t)(dst), 16, xvo[p], soff, 0, 0);
-    else __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void_t)(dst), 16, wvo[p - 2], soff, 0, 0);
+    else __builtin_amdgcn_raw_ptr_buffer_load_lds(wr, (lds_void_t)(dst), 16, wvo[p - 2], WP ? soff * 16 : soff, 0, 0);
   };
   // each wavefront's own loads of all but the two latest slices done (4
   // loads per slice), LDS reads done, then the barrier that publishes them
@@ -520,19 +533,27 @@ hipError_t launch_gemm_pipe(int expert_fmt, const Gemm& g, hipStream_t s) {
   // or from x itself when rows are gathered, and within one group's weights
   const int64_t xr = g.row_src ? (g.x_rows > 0 ? g.x_rows : g.n_rows) : PM;
   const bool dma = xr * g.k * 2 < (1LL << 31) && (int64_t)g.n * g.k * 2 < (1LL << 31);
+  // the streaming-order weight copy, when given, for every epilogue but the
+  // projection's (whose row order is its own)
+  const bool wp = g.w_packed && g.k % PK == 0 && (int64_t)(g.n / 16) * ((g.k + 127) / 128) * 4096 < (1LL << 31);
 #define PIPE_LAUNCH(E)                                                                          \
   do {                                                                                          \
     if (expert_fmt != 0) hipLaunchKernelGGL((gemm_pipe_kernel<E, 1>), gd, bd, 0, s, g);        \
-    else if (dma) hipLaunchKernelGGL((gemm_dma_kernel<E>), gd, bd, 0, s, g);                    \
+    else if (dma && wp) hipLaunchKernelGGL((gemm_dma_kernel<E, true>), gd, bd, 0, s, g);        \
+    else if (dma) hipLaunchKernelGGL((gemm_dma_kernel<E, false>), gd, bd, 0, s, g);             \
     else hipLaunchKernelGGL((gemm_pipe_kernel<E, 0>), gd, bd, 0, s, g);                         \
   } while (0)
   switch (g.epi) {
-    case EPI_QKV: PIPE_LAUNCH(EPI_QKV); break;
+    case EPI_QKV:
+      if (dma) hipLaunchKernelGGL((gemm_dma_kernel<EPI_QKV, false>), gd, bd, 0, s, g);
+      else hipLaunchKernelGGL((gemm_pipe_kernel<EPI_QKV, 0>), gd, bd, 0, s, g);
+      break;
     case EPI_RESIDUAL: PIPE_LAUNCH(EPI_RESIDUAL); break;
     case EPI_SWIGLU: PIPE_LAUNCH(EPI_SWIGLU); break;
     case EPI_LOGITS:  // vocabulary logits: bf16 weights only
       if (expert_fmt != 0) return hipErrorNotSupported;
-      if (dma) hipLaunchKernelGGL((gemm_dma_kernel<EPI_LOGITS>), gd, bd, 0, s, g);
+      if (dma && wp) hipLaunchKernelGGL((gemm_dma_kernel<EPI_LOGITS, true>), gd, bd, 0, s, g);
+      else if (dma) hipLaunchKernelGGL((gemm_dma_kernel<EPI_LOGITS, false>), gd, bd, 0, s, g);
       else hipLaunchKernelGGL((gemm_pipe_kernel<EPI_LOGITS, 0>), gd, bd, 0, s, g);
       break;
     default: PIPE_LAUNCH(EPI_BIAS); break;

@@ -535,12 +535,13 @@ def test_pack_weights_layout_bit_exact():
     np.testing.assert_array_equal(got, want)
 
 
-def test_moe_forward_packed_weights_bitwise_equal_row_major():
-    """Short expert groups read the streaming-order copy when it is given; the
-    products see the same operands in the same order, so the outputs are
-    bit-identical to those from the row-major weights."""
+@pytest.mark.parametrize("T", [40, 16384])
+def test_moe_forward_packed_weights_bitwise_equal_row_major(T):
+    """Short expert groups (40 tokens: weight slabs) and 256-row tiles (16384
+    tokens: the direct-to-LDS GEMM) read the streaming-order copy when it is
+    given; the products see the same operands in the same order, so the
+    outputs are bit-identical to those from the row-major weights."""
     s = _moe_shape(576, 576, "dense")
-    T = 40
     wl = W.custom(s, [4], [1], 1075)
     h = W.synth_normal(9, 6, (T, s.hidden)).cuda()
     outs = []
