@@ -653,18 +653,39 @@ __device__ __forceinline__ int checked_expert(const Permute& P, int a) {
 // Ranks the assignments a0 .. a0 + nloc - 1 (at most PERM_CHUNK) stably by
 // expert and scatters them. base (per expert, the chunk's first row) comes
 // from the multi-chunk scan; without it the workgroup holds the whole batch
-// and writes group_off itself.
+// and writes group_off itself. A wavefront owns sub-chunks w, w + 4, ...; all
+// of its expert ids are loaded up front, so the ids cost one memory round
+// trip rather than one per sub-chunk and pass.
 __device__ void permute_chunk(const Permute& P, int a0, int nloc, const int32_t* base) {
   __shared__ int cnt[PERM_SUB][64];
+  constexpr int PW = PERM_SUB / 4;  // sub-chunks per wavefront
   const int E = P.n_experts;
   const int nch = (nloc + 63) / 64;
   const int wave = threadIdx.x >> 6, lane = lane_id();
+  int ex[PW];
+#pragma unroll
+  for (int i = 0; i < PW; ++i) {
+    const int a = (wave + 4 * i) * 64 + lane;
+    ex[i] = a < nloc ? P.idx[a0 + a] : 0;
+  }
   for (int i = threadIdx.x; i < PERM_SUB * 64; i += blockDim.x) (&cnt[0][0])[i] = 0;
+  // an id outside [0, E) sets the error bit and counts as expert 0
+  bool bad = false;
+#pragma unroll
+  for (int i = 0; i < PW; ++i) {
+    const bool valid = (wave + 4 * i) * 64 + lane < nloc;
+    if (valid && (ex[i] < 0 || ex[i] >= E)) {
+      bad = true;
+      ex[i] = 0;
+    }
+  }
+  if (bad) set_error(P.err, 4);
   __syncthreads();
   // per-sub-chunk histograms (integer counts; order-independent)
-  for (int c = wave; c < nch; c += 4) {
-    const int a = c * 64 + lane;
-    if (a < nloc) atomicAdd(&cnt[c][checked_expert(P, a0 + a)], 1);
+#pragma unroll
+  for (int i = 0; i < PW; ++i) {
+    const int c = wave + 4 * i;
+    if (c * 64 + lane < nloc) atomicAdd(&cnt[c][ex[i]], 1);
   }
   __syncthreads();
   // lane e of wave 0: running first row of expert e in each sub-chunk
@@ -689,14 +710,15 @@ __device__ void permute_chunk(const Permute& P, int a0, int nloc, const int32_t*
       }
   }
   __syncthreads();
-  for (int c = wave; c < nch; c += 4) {
+#pragma unroll
+  for (int i = 0; i < PW; ++i) {
+    const int c = wave + 4 * i;
+    if (c >= nch) break;  // uniform
     const int a = c * 64 + lane;
     const bool valid = a < nloc;
-    int e = valid ? P.idx[a0 + a] : 0;
-    if (e < 0 || e >= E) e = 0;
-    const int r = rank_in_chunk(e, valid);
+    const int r = rank_in_chunk(ex[i], valid);
     if (valid) {
-      const int pos = cnt[c][e] + r;
+      const int pos = cnt[c][ex[i]] + r;
       P.pos_of[a0 + a] = pos;
       P.src_tok[pos] = (a0 + a) / P.top_k;
     }
