@@ -65,6 +65,79 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const uint8_t* base) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), 0, 0x7FFFFFFF, XBUF_DWORD3);
 }
 
+// MXFP8 quantization of bf16 rows (OCP MX v1.0): the block's scale is
+// 2^(floor(log2 amax) - 8) as E8M0, the elements v / scale rounded to
+// nearest-even E4M3 with saturation at +-448; an all-zero block gets scale
+// byte 0. v / scale is exact (a power-of-two scaling of a bf16 value), and
+// the hardware's packed conversion rounds it to nearest even; it gives NaN
+// above 448, so values are clamped to +-448 first, and it keeps the sign of a
+// negative value that rounds to zero (0x80), which becomes code 0. (Checked
+// against a bit-arithmetic encoder over every bf16 value times 2^-24 .. 2^12.)
+__device__ __forceinline__ float sat448(float x) { return fminf(fmaxf(x, -448.f), 448.f); }
+__device__ __forceinline__ uint32_t e4m3x4(float a0, float a1, float a2, float a3) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(sat448(a0), sat448(a1), 0, false);  // bytes 0, 1
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(sat448(a2), sat448(a3), w, true);       // bytes 2, 3
+  const uint32_t u = (uint32_t)w, t = u ^ 0x80808080u;
+  const uint32_t z = ~(((t & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | t) & 0x80808080u;  // bytes that are 0x80
+  return u & ~z;
+}
+
+// The gate/up product's epilogue with MXFP8 output: 16 rows x 128 SwiGLU
+// columns per pass, four consecutive columns per thread; eight threads hold a
+// 32-column block, whose maximum they reduce by shuffles. Each value is the
+// bf16-rounded SwiGLU output (the value the unfused path stores), quantized
+// exactly as mx_quant_kernel does, and written in slice order.
+// A thread's eight gate/up biases, the same in every pass: loaded once per tile.
+struct MxBias {
+  float4 b0, b1;
+};
+__device__ __forceinline__ MxBias swiglu_mx_bias(const Gemm& P, int n0, int nrows, int grp) {
+  MxBias b{make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+  const int q = threadIdx.x & 31;
+  if (8 * q < nrows) {
+    const float* bias = P.bias + (int64_t)grp * P.bias_group_stride + n0 + 8 * q;
+    b.b0 = *reinterpret_cast<const float4*>(bias);
+    b.b1 = *reinterpret_cast<const float4*>(bias + 4);
+  }
+  return b;
+}
+
+__device__ __forceinline__ void swiglu_mx_pass(const Gemm& P, const float* cr, int ld, int row0, int mrows, int n0,
+                                               int nrows, const MxBias& bb) {
+  const int tid = threadIdx.x;
+  const int m = tid >> 5, q = tid & 31;  // row of the pass, 4-column group
+  // all eight threads of a block agree (n is a multiple of 64)
+  const bool valid = m < mrows && 8 * q < nrows;
+  const float4 b0 = bb.b0, b1 = bb.b1;
+  const float* c = cr + m * ld + 8 * q;
+  float a[4];
+  a[0] = swiglu(c[0] + b0.x, c[1] + b0.y, P.swiglu_alpha, P.swiglu_limit, P.swiglu_beta);
+  a[1] = swiglu(c[2] + b0.z, c[3] + b0.w, P.swiglu_alpha, P.swiglu_limit, P.swiglu_beta);
+  a[2] = swiglu(c[4] + b1.x, c[5] + b1.y, P.swiglu_alpha, P.swiglu_limit, P.swiglu_beta);
+  a[3] = swiglu(c[6] + b1.z, c[7] + b1.w, P.swiglu_alpha, P.swiglu_limit, P.swiglu_beta);
+  float amax = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    a[i] = bf16_to_f32(f32_to_bf16(a[i]));
+    amax = fmaxf(amax, fabsf(a[i]));
+  }
+  // the block's maximum over its eight threads (lanes 8 r .. 8 r + 7)
+#pragma unroll
+  for (int d = 1; d < 8; d <<= 1) amax = fmaxf(amax, __shfl_xor(amax, d, 64));
+  int e = -127;
+  if (amax > 0.f) {
+    e = (int)((__float_as_uint(amax) >> 23) & 0xFF) - 127 - 8;
+    e = max(-127, min(127, e));
+  }
+  const float inv = __uint_as_float((uint32_t)(127 - e) << 23);
+  const uint32_t w = e4m3x4(a[0] * inv, a[1] * inv, a[2] * inv, a[3] * inv);
+  if (!valid) return;
+  const int64_t R = P.n_rows, row = row0 + m;
+  const int k = n0 / 2 + 4 * q;  // SwiGLU column
+  *reinterpret_cast<uint32_t*>(reinterpret_cast<uint8_t*>(P.out) + ((int64_t)(k / 64) * R + row) * 64 + k % 64) = w;
+  if ((q & 7) == 0) P.out_scales[((int64_t)(k / 128) * R + row) * 4 + (k / 32) % 4] = (uint8_t)(e + 127);
+}
+
 template <int EPI>
 __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
   __shared__ __align__(1024) uint8_t d0[XSTAGE];
@@ -246,7 +319,10 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
 
   // acc[rt][ct][j] = C[m = wm*64 + 32 rt + 8 (j/4) + 4 fg + j%4][n = wn*128 + 32 ct + fr]
   float* cr = reinterpret_cast<float*>(d0);
-  const EpiBias eb = epilogue_bias<EPI>(P, n0 >> 4, nrows >> 4, grp);
+  EpiBias eb{};
+  MxBias mb{};
+  if constexpr (EPI == EPI_SWIGLU_MX) mb = swiglu_mx_bias(P, n0, nrows, grp);
+  else eb = epilogue_bias<EPI>(P, n0 >> 4, nrows >> 4, grp);
   for (int e0 = 0; e0 < XM; e0 += XEP) {
     if (e0 >= mrows) break;  // uniform
     if (wm == e0 / 64) {
@@ -262,45 +338,23 @@ __global__ __launch_bounds__(XTH) void gemm_mx_kernel(Gemm P) {
         }
     }
     __syncthreads();
-    epilogue<bf16, EPI>(P, cr, XCLD, m0 + e0, min(XEP, mrows - e0), n0 >> 4, nrows >> 4, grp, &eb);
+    if constexpr (EPI == EPI_SWIGLU_MX) swiglu_mx_pass(P, cr, XCLD, m0 + e0, min(XEP, mrows - e0), n0, nrows, mb);
+    else epilogue<bf16, EPI>(P, cr, XCLD, m0 + e0, min(XEP, mrows - e0), n0 >> 4, nrows >> 4, grp, &eb);
     __syncthreads();
   }
 }
 
-// MXFP8 quantization of bf16 rows (OCP MX v1.0): thread = one block of 32
-// consecutive elements; scale 2^(floor(log2 amax) - 8) as E8M0, elements
-// v / scale rounded to nearest-even E4M3 with saturation at +-448 (by bit
-// arithmetic on the binary32 value, exact: v / scale has at most 8
-// significant bits); an all-zero block gets scale byte 0.
-__device__ __forceinline__ uint32_t e4m3_of(float y) {
-  const uint32_t u = __float_as_uint(y), sign = (u >> 24) & 0x80u;
-  const float a = fabsf(y);
-  if (a >= 448.f) return sign | 0x7Eu;
-  uint32_t code;
-  if (a < 0x1p-6f) {
-    // subnormal: multiples of 2^-9, nearest-even (a * 2^9 is exact)
-    const float m = rintf(a * 512.f);
-    code = (uint32_t)m;  // 8 is the smallest normal, 2^-6
-  } else {
-    const uint32_t b = __float_as_uint(a);
-    int e = (int)(b >> 23) - 127;
-    uint32_t man = b & 0x7FFFFFu, r = man >> 20, rem = man & 0xFFFFFu;
-    if (rem > 0x80000u || (rem == 0x80000u && (r & 1u))) ++r;
-    if (r == 8u) { r = 0; ++e; }
-    code = ((uint32_t)(e + 7) << 3) | r;
-    if (code > 0x7Eu) code = 0x7Eu;
-  }
-  return code == 0 ? 0u : (sign | code);
-}
-
+// bf16 rows to MXFP8: a thread per block of 32 consecutive elements (16-byte
+// loads), the block maximum, the E8M0 exponent from the binary32 exponent
+// field, four codes per conversion; the codes and the scale go to each of the
+// row's output copies.
 __global__ __launch_bounds__(256) void mx_quant_kernel(MxQuant P) {
   const int64_t blk = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int per_row = P.cols / 32;
   if (blk >= (int64_t)P.rows * per_row) return;
   const int64_t row = blk / per_row;
   const int c0 = (int)(blk - row * per_row) * 32;
-  const int64_t src_row = P.row_src ? P.row_src[row] : row;
-  const bf16* src = reinterpret_cast<const bf16*>(P.in) + src_row * P.cols + c0;
+  const bf16* src = reinterpret_cast<const bf16*>(P.in) + row * P.cols + c0;
   float v[32];
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
@@ -320,23 +374,22 @@ __global__ __launch_bounds__(256) void mx_quant_kernel(MxQuant P) {
     e = (int)((__float_as_uint(amax) >> 23) & 0xFF) - 127 - 8;
     e = max(-127, min(127, e));
   }
-  // the GEMM operand layout: 64-column slices of all rows in turn, the four
-  // scale bytes of a row's 128 columns in one dword
-  const int64_t sidx = P.gemm_layout ? ((int64_t)(c0 / 128) * P.rows + row) * 4 + (c0 / 32) % 4
-                                     : row * per_row + c0 / 32;
-  P.scales[sidx] = (uint8_t)(e + 127);
   const float inv = __uint_as_float((uint32_t)(127 - e) << 23);  // 2^-e, a normal power of two for e in [-127, 119]
   uint32_t out[8];
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    uint32_t w = 0;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) w |= e4m3_of(v[4 * q + i] * inv) << (8 * i);
-    out[q] = w;
+  for (int q = 0; q < 8; ++q) out[q] = e4m3x4(v[4 * q] * inv, v[4 * q + 1] * inv, v[4 * q + 2] * inv, v[4 * q + 3] * inv);
+  // the GEMM operand layout: 64-column slices of all rows in turn, the four
+  // scale bytes of a row's 128 columns in one dword
+  for (int c = 0; c < P.copies; ++c) {
+    const int64_t dst_row = P.row_dst ? P.row_dst[row * P.copies + c] : row;
+    const int64_t sidx = P.gemm_layout ? ((int64_t)(c0 / 128) * P.out_rows + dst_row) * 4 + (c0 / 32) % 4
+                                       : dst_row * per_row + c0 / 32;
+    P.scales[sidx] = (uint8_t)(e + 127);
+    uint8_t* dst = P.codes + (P.gemm_layout ? ((int64_t)(c0 / 64) * P.out_rows + dst_row) * 64 + c0 % 64
+                                            : dst_row * P.cols + c0);
+    st16(dst, u32x4{out[0], out[1], out[2], out[3]});
+    st16(dst + 16, u32x4{out[4], out[5], out[6], out[7]});
   }
-  uint8_t* dst = P.codes + (P.gemm_layout ? ((int64_t)(c0 / 64) * P.rows + row) * 64 + c0 % 64 : row * P.cols + c0);
-  st16(dst, u32x4{out[0], out[1], out[2], out[3]});
-  st16(dst + 16, u32x4{out[4], out[5], out[6], out[7]});
 }
 
 // MXFP4 weights into slice order: a thread per (group, row, block of 32):
@@ -378,6 +431,11 @@ hipError_t launch_gemm_mx(const Gemm& g, hipStream_t s) {
   switch (g.epi) {
     case EPI_SWIGLU: hipLaunchKernelGGL((gemm_mx_kernel<EPI_SWIGLU>), gd, bd, 0, s, g); break;
     case EPI_BIAS: hipLaunchKernelGGL((gemm_mx_kernel<EPI_BIAS>), gd, bd, 0, s, g); break;
+    case EPI_SWIGLU_MX:
+      // whole 32-column blocks of SwiGLU output in every tile
+      if (g.n % 64 || !g.out_scales || g.n_rows <= 0) return hipErrorInvalidValue;
+      hipLaunchKernelGGL((gemm_mx_kernel<EPI_SWIGLU_MX>), gd, bd, 0, s, g);
+      break;
     default: return hipErrorNotSupported;
   }
   return hipGetLastError();

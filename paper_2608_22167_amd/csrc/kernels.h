@@ -109,7 +109,7 @@ hipError_t launch_kv_append(int dtype, int head_dim, const KvAppend& p, hipStrea
 
 // ---- weight-streaming GEMMs with fused epilogues -------------------------
 
-enum EpiKind { EPI_QKV = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_BIAS = 3, EPI_LOGITS = 4 };
+enum EpiKind { EPI_QKV = 0, EPI_RESIDUAL = 1, EPI_SWIGLU = 2, EPI_BIAS = 3, EPI_LOGITS = 4, EPI_SWIGLU_MX = 5 };
 
 // EPI_LOGITS: the output columns are vocabulary logits l (no bias). Nothing
 // [rows, n] is written; per row and 64-column slot the epilogue leaves one
@@ -144,7 +144,11 @@ struct Gemm {
   const float* bias;        // [groups][n]
   int64_t bias_group_stride;
   const float* residual;    // EPI_RESIDUAL: [rows][n] fp32
-  void* out;                // EPI_RESIDUAL/EPI_BIAS: fp32 [rows][n]; EPI_SWIGLU: dtype [rows][n/2]
+  void* out;                // EPI_RESIDUAL/EPI_BIAS: fp32 [rows][n]; EPI_SWIGLU: dtype [rows][n/2];
+                            // EPI_SWIGLU_MX (scaled matrix cores only): the SwiGLU rows stored as
+                            // bf16 and quantized to MXFP8, codes here and scales in out_scales,
+                            // both in slice order over n_rows rows
+  uint8_t* out_scales;
   float swiglu_alpha, swiglu_limit, swiglu_beta;
   // EPI_QKV
   int hq, hkv, head_dim;
@@ -195,16 +199,19 @@ hipError_t launch_gemm(int dtype, int expert_fmt, const Gemm& g, hipStream_t s);
 __host__ __device__ constexpr int64_t mx_scale_bytes(int64_t rows, int k) { return (int64_t)((k + 127) / 128) * rows * 4; }
 bool mx_gemm_applies(const Gemm& g);
 hipError_t launch_gemm_mx(const Gemm& g, hipStream_t s);
-// bf16 rows -> MXFP8 (E4M3 codes, E8M0 scales per 32 columns); output row r
-// quantizes input row row_src[r] (row r when null)
+// bf16 rows -> MXFP8 (E4M3 codes, E8M0 scales per 32 columns); input row r
+// is quantized once and written to output rows row_dst[r * copies + c],
+// c < copies (row r, one copy, when row_dst is null)
 struct MxQuant {
-  const void* in;  // [*][cols] bf16
-  const int32_t* row_src;
-  int64_t rows;    // output rows
+  const void* in;  // [rows][cols] bf16
+  const int32_t* row_dst;
+  int copies;
+  int64_t rows;      // input rows
+  int64_t out_rows;  // rows of the output (the slice order's row count)
   int cols;
   uint8_t* codes;
   uint8_t* scales;
-  int gemm_layout;  // 0: codes [rows][cols], scales [rows][cols / 32]; 1: the slice order above
+  int gemm_layout;  // 0: codes [out_rows][cols], scales [out_rows][cols / 32]; 1: the slice order above
 };
 // MXFP4 weights [groups][rows][cols / 2] + scales [groups][rows][cols / 32]
 // -> the slice order above (codes, then scales at mx_packed_scales_offset)

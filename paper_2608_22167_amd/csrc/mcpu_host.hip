@@ -232,10 +232,11 @@ MoeBufs carve_moe(Carve& cv, const mcpu_layer_cfg* c, int max_tokens) {
   m.pos_of = cv.take<int32_t>(T * K);
   m.src_tok = cv.take<int32_t>(T * K);
   m.chunk_cnt = cv.take<int32_t>((T * K + PERM_CHUNK - 1) / PERM_CHUNK * c->n_experts);
-  m.act = cv.take_bytes(T * K * c->ffn_dim * db);
+  const bool native = c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE;  // the SwiGLU output leaves in MXFP8
+  m.act = native ? nullptr : cv.take_bytes(T * K * c->ffn_dim * db);
   m.y = cv.take<float>(T * K * c->hidden);
   m.hq = m.hs = m.aq = m.as = nullptr;
-  if (c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE) {
+  if (native) {
     // in the GEMM operand layout, one row per (token, expert) assignment in
     // expert order
     m.hq = cv.take<uint8_t>(T * K * c->hidden);
@@ -301,8 +302,8 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   const bool native = c->expert_fmt == MCPU_EXPERT_MXFP4_NATIVE;
   if (native) {  // the first product reads the normalised rows in MXFP8, in expert order
     MxQuant q{};
-    q.in = m.hn; q.row_src = m.src_tok; q.rows = (int64_t)T * K; q.cols = H; q.codes = m.hq; q.scales = m.hs;
-    q.gemm_layout = 1;
+    q.in = m.hn; q.row_dst = m.pos_of; q.copies = K; q.rows = T; q.out_rows = (int64_t)T * K; q.cols = H;
+    q.codes = m.hq; q.scales = m.hs; q.gemm_layout = 1;
     HIP_TRY(launch_mx_quant(q, st));
   }
   Gemm g1{};
@@ -311,21 +312,18 @@ int run_moe(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, int T, const f
   g1.epi = EPI_SWIGLU; g1.bias = w->b_gu; g1.bias_group_stride = 2 * I; g1.out = m.act;
   g1.swiglu_alpha = c->swiglu_alpha; g1.swiglu_limit = c->swiglu_limit; g1.swiglu_beta = c->swiglu_beta;
   g1.err = err; g1.max_rows_per_group = max_rows; g1.x_rows = T; g1.w_packed = w->w_gu_packed;
-  if (native) {  // slice-order operands, rows already in expert order
+  if (native) {  // slice-order operands, rows already in expert order; the SwiGLU
+                 // output leaves in MXFP8 for the second product
     g1.w = w->w_gu_packed; g1.w_packed = nullptr;
     g1.w_scales = (const uint8_t*)w->w_gu_packed + mx_packed_codes_bytes(E, 2 * I, H);
     g1.x = m.hq; g1.x_scales = m.hs; g1.row_src = nullptr; g1.x_rows = T * K;
+    g1.epi = EPI_SWIGLU_MX; g1.out = m.aq; g1.out_scales = m.as;
   }
   {
     Timed tm(MCPU_KERNEL_EXPERT_GU, st);
     HIP_TRY(launch_gemm(c->dtype, c->expert_fmt, g1, st));
   }
 
-  if (native) {  // ... and the second its SwiGLU activations in MXFP8
-    MxQuant q{};
-    q.in = m.act; q.rows = (int64_t)T * K; q.cols = I; q.codes = m.aq; q.scales = m.as; q.gemm_layout = 1;
-    HIP_TRY(launch_mx_quant(q, st));
-  }
   Gemm g2{};
   g2.w = w->w_d; g2.w_scales = w->s_d; g2.w_group_stride = (int64_t)H * I / fdiv; g2.n = H; g2.k = I;
   g2.x = m.act; g2.group_off = m.group_off; g2.n_rows = T * K; g2.n_groups = E;
@@ -773,7 +771,7 @@ int mcpu_mxfp8_quantize(const void* in, int64_t rows, int32_t cols, uint8_t* cod
   if (!in || !codes || !scales) return fail(MCPU_EINVAL, "NULL pointer");
   if ((uintptr_t)in % 16 || (uintptr_t)codes % 16) return fail(MCPU_EINVAL, "in and codes must be 16-byte aligned");
   MxQuant q{};
-  q.in = in; q.rows = rows; q.cols = cols; q.codes = codes; q.scales = scales;
+  q.in = in; q.copies = 1; q.rows = q.out_rows = rows; q.cols = cols; q.codes = codes; q.scales = scales;
   HIP_TRY(launch_mx_quant(q, stream));
   return MCPU_OK;
 }
