@@ -135,9 +135,11 @@ def traffic_from_profile(kernel, workload_name):
 
 
 ATTN_SOURCES = ("attention.hip", "device.h", "kernels.h")
-GEMM_SOURCES = ("gemm.hip", "gemm_tiled.hip", "gemm_pipe.hip", "gemm_slab.hip", "gemm_epilogue.h", "device.h", "kernels.h")
+GEMM_SOURCES = ("gemm.hip", "gemm_tiled.hip", "gemm_pipe.hip", "gemm_slab.hip", "gemm_mx.hip", "gemm_epilogue.h", "device.h",
+                "kernels.h")
 KERNEL_SOURCES = {"attn_split": ATTN_SOURCES, "attn_prefill": ATTN_SOURCES, "qkv": GEMM_SOURCES,
-                  "oproj": GEMM_SOURCES, "expert_gu": GEMM_SOURCES, "expert_down": GEMM_SOURCES}
+                  "oproj": GEMM_SOURCES, "expert_gu": GEMM_SOURCES, "expert_down": GEMM_SOURCES,
+                  "lm_head": GEMM_SOURCES + ("lm_head.hip", "kernels_lm.h")}
 
 
 def timed_passes(fn, min_seconds=10.0, max_passes=50):
@@ -290,6 +292,71 @@ class StackBench:
                           f"layers, pages and used experts regenerated on the host, {dt:.2f} s wall"}
 
 
+class HeadBench:
+    """The vocabulary head of a generation step at batch 256: final RMSNorm,
+    the projection onto the 201,088-entry vocabulary with the sampling
+    epilogue (temperature 0.7, Gumbel-max draws), and the per-row reduction:
+    one lm_head_sample call per step."""
+
+    def __init__(self, T=256, seed=3001):
+        import torch
+        from paper_2608_22167_amd import mcpu, workload as W
+        self.shape = W.GPT_OSS_20B
+        H, V = self.shape.hidden, W.GPT_OSS_VOCAB
+        lm = W.lm_weights_device(seed, H, V)
+        del lm["embed"]
+        self.head = mcpu.DeviceLmHead(lm["g_final"], lm["w_lm"], self.shape.rms_eps)
+        self.lm_host = None
+        self.seed, self.T, self.H, self.V = seed, T, H, V
+        self.x = W.synth_normal(seed, 77, (T, H)).cuda()
+        self.seq = torch.arange(T, dtype=torch.int32, device="cuda")
+        self.pos = torch.full((T,), 4096, dtype=torch.int32, device="cuda")
+        self.tok = torch.empty(T, dtype=torch.int32, device="cuda")
+        self.lp = torch.empty(T, device="cuda")
+        self.ws = mcpu.workspace(mcpu.lm_head_workspace_size(H, V, T))
+        self.temperature = float(np.float32(0.7))
+        self.tokens, self.launches = T, 1
+
+    def run(self):
+        from paper_2608_22167_amd import mcpu
+        mcpu.lm_head_sample(self.head, self.x, self.temperature, seed=self.seed, seq_ids=self.seq,
+                            positions=self.pos, tokens=self.tok, logprob=self.lp, workspace=self.ws)
+
+    def errors(self):
+        from paper_2608_22167_amd import mcpu
+        return mcpu.mcpu_check_device_errors(self.ws)
+
+    def work(self):
+        # the head's weights once, the normalised rows, the per-slice records written
+        T, H, V = self.T, self.H, self.V
+        slots = (V + 63) // 64
+        return [{"lm_head": (V * H * 2 + T * H * 2 + T * slots * 32, 2 * T * V * H)}], T, 0
+
+    def dominant_launches(self, kernel):
+        return [0]
+
+    def config(self):
+        return {"workload": "lm_head_b256", "batch": self.T, "tokens": self.T, "vocab": self.V, "hidden": self.H,
+                "temperature": self.temperature, "sampling": "Gumbel-max over Philox4x32-10 draws",
+                "parallelism": "single GPU"}
+
+    def cpu_baseline(self, n_rows=4):
+        """The reference head (float64 logits, the same draws) on n_rows rows."""
+        from oracle import oracle as O
+        from paper_2608_22167_amd import workload as W
+        lm = W.lm_weights_host(self.seed, self.H, self.V, embed=False)
+        x = W.synth_normal(self.seed, 77, (self.T, self.H))[:n_rows]
+        seq = np.arange(n_rows, dtype=np.int32)
+        pos = np.full(n_rows, 4096, np.int32)
+        passes, dt = timed_passes(lambda: O.lm_head(x, lm["g_final"], lm["w_lm"], self.shape.rms_eps, self.temperature,
+                                                    seed=self.seed, seq_ids=seq, positions=pos))
+        return {"value": round(passes * n_rows / dt, 3), "unit": "tokens/s", "cores": cpu_cores(), "cpu": cpu_model(),
+                "kind": "oracle", "sample": f"{n_rows} of {self.T} rows, {passes} passes in {dt:.2f} s wall"}
+
+
+HEAD_WORKLOADS = ("lm_head_b256",)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -315,8 +382,11 @@ def main():
 
     torch.cuda.set_device(0)
     log(f"generating workload {args.workload}")
-    wl = make_workload(args.workload)
-    bench = StackBench(wl) if args.workload in STACK_WORKLOADS else LayerBench(wl)
+    if args.workload in HEAD_WORKLOADS:
+        bench = HeadBench()
+    else:
+        wl = make_workload(args.workload)
+        bench = StackBench(wl) if args.workload in STACK_WORKLOADS else LayerBench(wl)
     torch.cuda.synchronize()
     log(f"resident: {torch.cuda.memory_allocated() / 1e9:.1f} GB; {bench.tokens} tokens per step")
 
