@@ -281,7 +281,11 @@ __device__ __forceinline__ U32x4 philox4x32_10(U32x4 c, uint32_t k0, uint32_t k1
 // as -log1p(u - 1) (u - 1 is exact), so it keeps full precision as u -> 1.
 __device__ __forceinline__ float gumbel_of(uint32_t w) {
   const float u = ((float)(w >> 9) + 0.5f) * 0x1p-23f;
-  return -logf(-log1pf(u - 1.0f));
+  // t = -ln u needs relative accuracy down to 2^-24 (u next to 1: the largest
+  // noise), hence log1p of the exact u - 1; the outer logarithm only needs
+  // absolute accuracy (its value is the noise), which the hardware log2 gives
+  const float t = -log1pf(u - 1.0f);
+  return -__builtin_amdgcn_logf(t) * 0.693147180559945309f;
 }
 
 // page format (see include/mcpu.h)

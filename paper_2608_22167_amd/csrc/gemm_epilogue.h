@@ -266,18 +266,17 @@ __device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mro
     const int nslot = (nblk * 16 + LOGIT_SLOT - 1) / LOGIT_SLOT, c_end = (blk0 + nblk) * 16;
     const int sub = tid & 15;
     const float NEG = -__builtin_inff();
-    for (int it = tid >> 4; it < mrows * nslot; it += nt >> 4) {
+    const int items = mrows * nslot, stride = nt >> 4;
+    auto slot = [&](int it, int pos, int seq, int tgt) __attribute__((always_inline)) {
       const int m = it / nslot, j = it - m * nslot, row = m0 + m;
       const int c0 = blk0 * 16 + j * LOGIT_SLOT + 4 * sub;
       const float* cp = cr + m * ld + j * LOGIT_SLOT + 4 * sub;
       float sv[4], g[4] = {0.f, 0.f, 0.f, 0.f};
       if (!P.greedy && c0 < c_end) {
-        const U32x4 r = philox4x32_10(U32x4{(uint32_t)(c0 >> 2), (uint32_t)P.row_pos[row], (uint32_t)P.row_seq[row],
-                                            LOGIT_RNG_TAG},
+        const U32x4 r = philox4x32_10(U32x4{(uint32_t)(c0 >> 2), (uint32_t)pos, (uint32_t)seq, LOGIT_RNG_TAG},
                                       (uint32_t)P.seed, (uint32_t)(P.seed >> 32));
         g[0] = gumbel_of(r.x); g[1] = gumbel_of(r.y); g[2] = gumbel_of(r.z); g[3] = gumbel_of(r.w);
       }
-      const int tgt = P.target ? P.target[row] : -1;
       float mx = NEG, pert = NEG, sb = NEG, st = NEG;
       int bi = 0x7FFFFFFF;
 #pragma unroll
@@ -293,7 +292,7 @@ __device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mro
       for (int o = 8; o; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 16));
       float sum = 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sum += c0 + i < c_end ? expf(sv[i] - mx) : 0.f;
+      for (int i = 0; i < 4; ++i) sum += c0 + i < c_end ? __builtin_amdgcn_exp2f((sv[i] - mx) * 1.44269504088896341f) : 0.f;
 #pragma unroll
       for (int o = 8; o; o >>= 1) {
         sum += __shfl_xor(sum, o, 16);
@@ -307,6 +306,20 @@ __device__ void epilogue(const Gemm& P, const float* cr, int ld, int m0, int mro
         r.m = mx; r.l = sum; r.pert = pert; r.s_best = sb; r.idx = bi; r.s_tgt = st; r.pad[0] = r.pad[1] = 0.f;
         out[(int64_t)row * n_slots + (c0 / LOGIT_SLOT)] = r;
       }
+    };
+    // two items per round: the rows' positions, sequence ids and targets are
+    // loaded for both before either stores (a load may not pass a store to a
+    // possibly aliasing address)
+    for (int it = tid >> 4; it < items; it += 2 * stride) {
+      const int it2 = it + stride;
+      const bool two = it2 < items;  // uniform per 16 lanes
+      const int r1 = m0 + it / nslot, r2 = m0 + (two ? it2 : it) / nslot;
+      const bool draw = !P.greedy;
+      const int pos1 = draw ? P.row_pos[r1] : 0, seq1 = draw ? P.row_seq[r1] : 0;
+      const int pos2 = draw ? P.row_pos[r2] : 0, seq2 = draw ? P.row_seq[r2] : 0;
+      const int tg1 = P.target ? P.target[r1] : -1, tg2 = P.target ? P.target[r2] : -1;
+      slot(it, pos1, seq1, tg1);
+      if (two) slot(it2, pos2, seq2, tg2);
     }
   } else {  // EPI_RESIDUAL, EPI_BIAS: fp32 rows, 4 consecutive features per thread
     // As above: fixed features per thread (bias read once); residual rows of
