@@ -354,7 +354,116 @@ class HeadBench:
                 "kind": "oracle", "sample": f"{n_rows} of {self.T} rows, {passes} passes in {dt:.2f} s wall"}
 
 
+class ScoreBench:
+    """The log-probability pass of the policy update over whole trajectories
+    (8 seeded trajectories of 4096 tokens): embedding, one causal prefill of
+    every trajectory through the 24-layer stack (MXFP4 experts), and the
+    vocabulary head scoring each next token; one Generator.score call per
+    step, host marshalling of the targets and the copy of the log-probs back
+    included."""
+
+    metric = "scored tokens/s on 1 MI355X (trajectory log-prob recompute, gpt-oss-20b-shape stack)"
+
+    def __init__(self, n_traj=8, length=4096, seed=3001):
+        from paper_2608_22167_amd import workload as W
+        from paper_2608_22167_amd.generate import GenSpec, Generator
+        pages = n_traj * length // 16 + 64
+        self.spec = GenSpec(n_layers=24, base=W.GPT_OSS_20B, vocab=W.GPT_OSS_VOCAB, seed=seed,
+                            pages_full=pages, pages_sw=pages, max_ctx=length + 64)
+        self.gen = Generator(self.spec, max_tokens_per_step=n_traj * length)
+        self.ss = self.gen.ss
+        self.shape = self.ss.shape_full
+        rng = np.random.default_rng(seed)
+        self.traj = [rng.integers(0, self.spec.vocab, length) for _ in range(n_traj)]
+        self.n_traj, self.length = n_traj, length
+        self.tokens = n_traj * (length - 1)  # scored tokens per step
+        self.launches = self.spec.n_layers
+
+    def run(self):
+        self.gen.score(self.traj)
+
+    def errors(self):
+        return self.gen.check_errors()
+
+    def work(self):
+        z = np.zeros(self.n_traj, np.int64)
+        q = np.full(self.n_traj, self.length, np.int64)
+        # 131,072 routed rows reach every expert of every layer
+        idx = np.arange(self.shape.n_experts)
+        per = [layer_work(self.ss.shape(i), z, q, idx)[0] for i in range(self.spec.n_layers)]
+        V, H, T = self.spec.vocab, self.shape.hidden, self.tokens
+        per[0]["lm_head"] = (V * H * 2 + T * H * 2 + T * ((V + 63) // 64) * 32, 2 * T * V * H)
+        return per, self.tokens, 0
+
+    def dominant_launches(self, kernel):
+        return [0] if kernel == "lm_head" else list(range(self.spec.n_layers))
+
+    def config(self):
+        s = self.shape
+        return {"workload": "score_8x4096", "trajectories": self.n_traj, "tokens_per_trajectory": self.length,
+                "scored_tokens": self.tokens, "layers": self.spec.n_layers, "vocab": self.spec.vocab,
+                "temperature": self.spec.temperature,
+                "layer": f"hidden {s.hidden}, {s.n_q_heads}/{s.n_kv_heads} heads, d {s.head_dim}, "
+                         f"{s.n_experts} MXFP4 experts top-{s.top_k}, ffn {s.ffn_dim}",
+                "attention": f"alternating sliding window {self.ss.shape_sw.window} / full, + sinks",
+                "parallelism": "single GPU"}
+
+    def cpu_baseline(self, n=16, n_layers=2):
+        """The reference on the first n tokens of one trajectory: the first
+        n_layers layers (one sliding-window, one full) as one causal prefill,
+        then the head with targets on the n - 1 scored rows. The experts the
+        sample routes to are drawn once, before timing. Per scored token:
+        (n_layers-layer time x 24 / n_layers + head time) / (n - 1)."""
+        import torch
+        from oracle import oracle as O
+        from oracle import stack as OS
+        from paper_2608_22167_amd import workload as W
+        ss, s0 = self.ss, self.shape
+        tr = np.asarray(self.traj[0][:n], np.int64)
+        lm = W.lm_weights_host(self.spec.seed, s0.hidden, self.spec.vocab)
+        x0 = lm["embed"][torch.from_numpy(tr[:-1])].double()
+        n_pages = (n - 2) // 16 + 1
+        layers = []
+        for i in range(n_layers):
+            s = ss.shape(i)
+            ex = OS._Experts(ss)
+            Wd = W.stack_weights_host(ss, i, experts=[])
+            Wd["w_gu"], Wd["w_d"] = ex.w_gu, ex.w_d
+            wl = W.Workload(name="score_sample", shape=s, seed=ss.seed, seq_lens=np.zeros(1, np.int32),
+                            q_lens=np.array([n - 1], np.int32), page_table=np.arange(n_pages, dtype=np.int32)[None],
+                            n_pages=n_pages, weights=Wd)
+            wl.k_pool = torch.zeros((n_pages, s.n_kv_heads, 16, s.head_dim), dtype=torch.bfloat16)
+            wl.v_pool = torch.zeros_like(wl.k_pool)
+            layers.append((wl, O.Weights(s, Wd), ex))
+        x = x0
+        for i, (wl, wt, ex) in enumerate(layers):  # routing pass, then draw the experts it picked
+            wl.x_in = x
+            ex.draw(ss, i, O.decode_layer(wl, wt)["idx"])
+            x = torch.from_numpy(O.decode_layer(wl, wt)["out"])
+
+        def stack():
+            x = x0
+            for wl, wt, _ in layers:
+                wl.x_in = x
+                x = torch.from_numpy(O.decode_layer(wl, wt)["out"])
+            return x.numpy()
+        rows = stack()
+        p_l, t_l = timed_passes(stack, min_seconds=6.0, max_passes=20)
+        tg = tr[1:].astype(np.int32)
+        zero = np.zeros(n - 1, np.int32)
+        p_h, t_h = timed_passes(lambda: O.lm_head(rows, lm["g_final"], lm["w_lm"], s0.rms_eps, self.spec.temperature,
+                                                  seq_ids=zero, positions=zero, targets=tg),
+                                min_seconds=6.0, max_passes=20)
+        per_tok = (t_l / p_l * self.spec.n_layers / n_layers + t_h / p_h) / (n - 1)
+        return {"value": round(1.0 / per_tok, 3), "unit": "scored tokens/s", "cores": cpu_cores(), "cpu": cpu_model(),
+                "kind": "oracle",
+                "sample": f"the first {n} tokens of one trajectory: layers 0-{n_layers - 1} as one prefill "
+                          f"({p_l} passes in {t_l:.2f} s, scaled to {self.spec.n_layers} layers) and the head on "
+                          f"{n - 1} rows with targets ({p_h} passes in {t_h:.2f} s)"}
+
+
 HEAD_WORKLOADS = ("lm_head_b256",)
+SCORE_WORKLOADS = ("score_8x4096",)
 
 
 def main():
@@ -373,7 +482,7 @@ def main():
         print(json.dumps({"error": "this benchmark runs on one GPU; the decode step is not sharded "
                                    "across GPUs in this build", "n_gpus": args.gpus}))
         raise SystemExit(2)
-    heavy = args.workload in STACK_WORKLOADS or args.workload.startswith("mixed_prefill")
+    heavy = args.workload in STACK_WORKLOADS + SCORE_WORKLOADS or args.workload.startswith("mixed_prefill")
     K = args.steps if args.steps is not None else (5 if heavy else 50)
     warmup = args.warmup if args.warmup is not None else (2 if heavy else 10)
 
@@ -384,6 +493,8 @@ def main():
     log(f"generating workload {args.workload}")
     if args.workload in HEAD_WORKLOADS:
         bench = HeadBench()
+    elif args.workload in SCORE_WORKLOADS:
+        bench = ScoreBench()
     else:
         wl = make_workload(args.workload)
         bench = StackBench(wl) if args.workload in STACK_WORKLOADS else LayerBench(wl)
@@ -480,7 +591,8 @@ def main():
 
     decode_tokens = t_dec if t_pre else bench.tokens
     out = {
-        "metric": METRIC, "value": round(decode_tokens / (ms_step * 1e-3), 1), "unit": "tokens/s",
+        "metric": getattr(bench, "metric", METRIC), "value": round(decode_tokens / (ms_step * 1e-3), 1),
+        "unit": "tokens/s",
         "n_gpus": 1, "steps": K, "warmup": warmup, "ms_per_step": round(ms_step, 4),
         "ms_per_step_p10_p50_p90": [round(float(np.percentile(step_ms, p)), 4) for p in (10, 50, 90)],
         "caches_evicted_between_steps": flush is not None, "higher_is_better": True,

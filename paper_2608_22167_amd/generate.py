@@ -246,6 +246,7 @@ class Generator:
         tokens in all, with the next tokens as targets. Pages are taken from
         and returned to the pools."""
         tau = self.spec.temperature if temperature is None else temperature
+        trajectories = [np.asarray(t, np.int64) for t in trajectories]
         res = [np.zeros(max(len(t) - 1, 0), np.float64) for t in trajectories]
         states = [_Seq(sid_base + i) for i in range(len(trajectories))]
         try:
@@ -263,29 +264,28 @@ class Generator:
                     break
                 for s, q in zip(batch, q_lens):
                     self._grow(s, q)
-                tokens = np.concatenate([np.asarray(trajectories[i][s.length:s.length + q], np.int64)
+                tokens = np.concatenate([trajectories[i][s.length:s.length + q]
                                          for i, s, q in zip(idx, batch, q_lens)])
                 x, cu = self._forward(batch, q_lens, tokens)
                 # targets: the token after each row (the last row of a trajectory has none)
-                rows, tgts, where = [], [], []
+                rows, tgts, spans = [], [], []
                 for b, (i, s, q) in enumerate(zip(idx, batch, q_lens)):
-                    tr = trajectories[i]
-                    for j in range(q):
-                        p = s.length + j
-                        if p + 1 < len(tr):
-                            rows.append(cu[b] + j)
-                            tgts.append(tr[p + 1])
-                            where.append((i, p))
+                    n_t = min(q, len(trajectories[i]) - 1 - s.length)
+                    if n_t > 0:
+                        rows.append(cu[b] + np.arange(n_t, dtype=np.int32))
+                        tgts.append(trajectories[i][s.length + 1:s.length + 1 + n_t])
+                        spans.append((i, s.length, n_t))
                 if rows:
                     dev = self.device
-                    n = len(rows)
-                    tlp = torch.empty(n, device=dev)
-                    mcpu.lm_head_sample(self.head, x, tau, 0, None, None,
-                                        torch.from_numpy(np.array(tgts, np.int32)).to(dev), None, None, tlp,
-                                        workspace=self.lm_ws, x_rows=torch.from_numpy(np.array(rows, np.int32)).to(dev))
+                    rows, tgts = np.concatenate(rows), np.concatenate(tgts).astype(np.int32)
+                    tlp = torch.empty(len(rows), device=dev)
+                    mcpu.lm_head_sample(self.head, x, tau, 0, None, None, torch.from_numpy(tgts).to(dev), None, None,
+                                        tlp, workspace=self.lm_ws, x_rows=torch.from_numpy(rows).to(dev))
                     vals = tlp.cpu().numpy()
-                    for (i, p), v in zip(where, vals):
-                        res[i][p] = v
+                    at = 0
+                    for i, p, n_t in spans:
+                        res[i][p:p + n_t] = vals[at:at + n_t]
+                        at += n_t
                 for s, q in zip(batch, q_lens):
                     s.length += q
                     self._shrink(s)
