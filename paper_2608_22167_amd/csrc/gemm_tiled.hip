@@ -317,7 +317,7 @@ hipError_t launch_gemm_tiled(int expert_fmt, const Gemm& g, hipStream_t s) {
     return big ? tiled_launch<128, 128, 64, 2, 4, 1>(g, s) : tiled_launch<64, 128, 64, 4, 4, 1>(g, s);
   if (big) return tiled_launch<128, 128, 64, 2, 4, 0>(g, s);
   if (tiles(64, 128) < 512) return tiled_launch<64, 64, 64, 4, 4, 0>(g, s);
-  return tiled_launch<64, 128, 64, 4, 4, 0>(g, s);
+  return tiled_launch<64, 128, 64, 2, 4, 0>(g, s);
 }
 
 }  // namespace mcpu

@@ -620,25 +620,19 @@ hipError_t launch_router(int dtype, const Router& p, hipStream_t s) {
 
 constexpr int PERM_SUB = PERM_CHUNK / 64;  // 64-assignment sub-chunks per workgroup
 
-// rank of this lane among the lanes of its wavefront holding the same expert
-// and a lower lane id, by peeling one expert value per round with ballots
-__device__ __forceinline__ int rank_in_chunk(int e, bool valid) {
+// rank of this lane among the valid lanes of its wavefront holding the same
+// expert and a lower lane id: the lanes that agree with this one on every bit
+// of the expert id (one ballot per bit, nbits = ceil(log2 E)), counted below it
+__device__ __forceinline__ int rank_in_chunk(int e, bool valid, int nbits) {
   const int lane = lane_id();
   const uint64_t lt = lane == 0 ? 0ull : (~0ull >> (64 - lane));
-  bool todo = valid;
-  int rank = 0;
-  uint64_t pending = __ballot(todo);
-  while (pending) {
-    const int first = __ffsll((unsigned long long)pending) - 1;
-    const int e0 = __shfl(e, first, 64);
-    const uint64_t m = __ballot(todo && e == e0);
-    if (todo && e == e0) {
-      rank = __popcll(m & lt);
-      todo = false;
-    }
-    pending = __ballot(todo);
+  uint64_t same = __ballot(valid);
+  for (int b = 0; b < nbits; ++b) {  // uniform trip count
+    const bool bit = (e >> b) & 1;
+    const uint64_t ones = __ballot(bit);
+    same &= bit ? ones : ~ones;
   }
-  return rank;
+  return __popcll(same & lt);
 }
 
 __device__ __forceinline__ int checked_expert(const Permute& P, int a) {
@@ -661,6 +655,7 @@ __device__ void permute_chunk(const Permute& P, int a0, int nloc, const int32_t*
   constexpr int PW = PERM_SUB / 4;  // sub-chunks per wavefront
   const int E = P.n_experts;
   const int nch = (nloc + 63) / 64;
+  const int nbits = 32 - __clz(max(E - 1, 1));  // bits of the largest expert id
   const int wave = threadIdx.x >> 6, lane = lane_id();
   int ex[PW];
 #pragma unroll
@@ -716,7 +711,7 @@ __device__ void permute_chunk(const Permute& P, int a0, int nloc, const int32_t*
     if (c >= nch) break;  // uniform
     const int a = c * 64 + lane;
     const bool valid = a < nloc;
-    const int r = rank_in_chunk(ex[i], valid);
+    const int r = rank_in_chunk(ex[i], valid, nbits);
     if (valid) {
       const int pos = cnt[c][ex[i]] + r;
       P.pos_of[a0 + a] = pos;
