@@ -389,8 +389,8 @@ int embed_tokens(const void* table, int32_t vocab, int32_t hidden, int32_t n_tok
  * to host array ms, setting *n_recorded. Process-wide state: not thread-safe,
  * and recording adds two event records per timed launch. */
 enum {
-  MCPU_KERNEL_ATTN_PLAN = 0,
-  MCPU_KERNEL_RMSNORM = 1,
+  MCPU_KERNEL_ATTN_PLAN = 0,   /* attention plan; in decode_layer also RMSNorm_1 (one launch) */
+  MCPU_KERNEL_RMSNORM = 1,     /* not recorded: decode_layer runs RMSNorm_1 in the plan's launch */
   MCPU_KERNEL_QKV = 2,         /* QKV projection + RoPE + KV append */
   MCPU_KERNEL_ATTN_SPLIT = 3,  /* paged attention partials */
   MCPU_KERNEL_ATTN_COMBINE = 4,

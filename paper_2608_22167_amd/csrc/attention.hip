@@ -66,7 +66,51 @@ __device__ int block_exclusive_scan(int local, int* sums, int& total) {
   return excl;
 }
 
+// Workgroups 1.. of the plan launch: the layer's first RMSNorm, y = x /
+// sqrt(mean(x^2) + eps) * g, on four rows per workgroup (256 threads a row,
+// float4 j of a thread at features 4 (t + 256 j)), so that the norm and the
+// plan, both short and independent, share one launch.
+template <typename T>
+__device__ void plan_norm_rows(const RmsNorm& N) {
+  __shared__ float part[16];
+  constexpr int NVMAX = 8;  // hidden <= 8192
+  const int tid = threadIdx.x, sub = tid & 255, grp = tid >> 8, H = N.hidden;
+  const int row = (blockIdx.x - 1) * 4 + grp;
+  const bool live = row < N.n_tokens;
+  const float* x = N.x + (int64_t)(live ? row : 0) * H;
+  float4 xv[NVMAX], gv[NVMAX];
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < NVMAX; ++j) {
+    const int i = (sub + 256 * j) * 4;
+    if (i < H) {
+      xv[j] = *reinterpret_cast<const float4*>(x + i);
+      gv[j] = *reinterpret_cast<const float4*>(N.g + i);
+      ss += xv[j].x * xv[j].x + xv[j].y * xv[j].y + xv[j].z * xv[j].z + xv[j].w * xv[j].w;
+    }
+  }
+  ss = wave_sum(ss);
+  if (lane_id() == 0) part[tid >> 6] = ss;
+  __syncthreads();
+  const float tot = part[4 * grp] + part[4 * grp + 1] + part[4 * grp + 2] + part[4 * grp + 3];
+  const float inv = 1.0f / sqrtf(tot / (float)H + N.eps);
+  if (!live) return;
+  T* out = reinterpret_cast<T*>(N.out) + (int64_t)row * H;
+#pragma unroll
+  for (int j = 0; j < NVMAX; ++j) {
+    const int i = (sub + 256 * j) * 4;
+    if (i < H)
+      store4(out + i, make_float4(xv[j].x * inv * gv[j].x, xv[j].y * inv * gv[j].y,
+                                xv[j].z * inv * gv[j].z, xv[j].w * inv * gv[j].w));
+  }
+}
+
 __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnPlan P) {
+  if (blockIdx.x > 0) {
+    if (P.norm_dtype == 0) plan_norm_rows<float>(P.norm);
+    else plan_norm_rows<bf16>(P.norm);
+    return;
+  }
   __shared__ int sums[160];
   const int tid = threadIdx.x, nt = blockDim.x;
   for (int i = tid; i < P.n_zero; i += nt) P.zero[i] = 0;
@@ -124,7 +168,12 @@ __global__ __launch_bounds__(1024) void attn_plan_kernel(AttnPlan P) {
 }
 
 hipError_t launch_attn_plan(const AttnPlan& p, hipStream_t s) {
-  hipLaunchKernelGGL(attn_plan_kernel, dim3(1), dim3(1024), 0, s, p);
+  int blocks = 1;
+  if (p.norm_dtype >= 0) {
+    if (p.norm.hidden % 4 || p.norm.hidden > 8192) return hipErrorInvalidValue;
+    blocks += (p.norm.n_tokens + 3) / 4;
+  }
+  hipLaunchKernelGGL(attn_plan_kernel, dim3(blocks), dim3(1024), 0, s, p);
   return hipGetLastError();
 }
 

@@ -41,6 +41,13 @@ template <> struct Elem<bf16> {
   static __device__ __forceinline__ void store(bf16* p, int64_t i, float v) { p[i].bits = f32_to_bf16(v); }
 };
 
+// four consecutive elements from fp32 (p 16- or 8-byte aligned)
+__device__ __forceinline__ void store4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+__device__ __forceinline__ void store4(bf16* p, float4 v) {
+  *reinterpret_cast<uint2*>(p) = make_uint2((uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16),
+                                            (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16));
+}
+
 // ---------------------------------------------------------------------------
 // wavefront helpers (64 lanes)
 // ---------------------------------------------------------------------------

@@ -14,6 +14,14 @@ struct SplitDesc {
   int32_t t, b, p, lo, pg0, pg1, pad0, pad1;
 };
 
+struct RmsNorm {
+  const float* x;  // [T][H]
+  const float* g;
+  int n_tokens, hidden;
+  float eps;
+  void* out;       // [T][H] layer dtype
+};
+
 struct AttnPlan {
   const int32_t* seq_lens;  // [batch]
   const int32_t* cu_q;      // [batch+1] or nullptr (one token per sequence)
@@ -30,6 +38,10 @@ struct AttnPlan {
   int32_t* err;
   int32_t* zero;            // [n_zero] words cleared for the layer's later kernels
   int n_zero;
+  // optional RMSNorm riding on the same launch (the layer's first norm, which
+  // does not depend on the plan): workgroups 1.. normalise four rows each
+  RmsNorm norm;             // rows and output of the norm
+  int norm_dtype;           // -1: no norm; else the layer dtype of its output
 };
 
 // Chunked prefill: the new tokens of a sequence attend causally to its pages
@@ -258,14 +270,7 @@ hipError_t launch_gemm_slab(int expert_fmt, const Gemm& g, hipStream_t s);
 
 // ---- norms, router, permutation, combine --------------------------------
 
-struct RmsNorm {
-  const float* x;  // [T][H]
-  const float* g;
-  int n_tokens, hidden;
-  float eps;
-  void* out;       // [T][H] layer dtype
-};
-hipError_t launch_rmsnorm(int dtype, const RmsNorm& p, hipStream_t s);
+
 
 struct Router {
   const float* h;      // [T][H] residual stream

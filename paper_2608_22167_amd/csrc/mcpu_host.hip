@@ -208,6 +208,7 @@ AttnPlan make_plan(const mcpu_layer_cfg* c, int batch, const int32_t* seq_lens, 
   pl.prefill_min_q = ph.prefill_min_q; pl.prefill_qb = ph.prefill_qb; pl.host_total_blocks = ph.n_blocks;
   pl.tok_seq = ab.tok_seq; pl.tok_pos = ab.tok_pos; pl.split_start = ab.split_start;
   pl.split_desc = ab.split_desc; pl.blk_start = ab.blk_start; pl.err = err;
+  pl.norm_dtype = -1;  // no norm unless the caller adds one
   return pl;
 }
 
@@ -651,6 +652,9 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
   int32_t* part_cnt = cv.take<int32_t>(SPLIT_MAX_TILES);
   int32_t* err = err_word(workspace);
 
+  // the plan and RMSNorm_1 share one launch (the norm does not depend on it)
+  RmsNorm rn{};
+  rn.x = x_in; rn.g = w->g1; rn.n_tokens = T; rn.hidden = H; rn.eps = cfg->rms_eps; rn.out = xn;
   {
     Timed tm(MCPU_KERNEL_ATTN_PLAN, stream);
     AttnPlan pl = make_plan(cfg, batch, seq_lens, cu_q, ph, ab, err);
@@ -658,14 +662,9 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
       pl.zero = part_cnt;
       pl.n_zero = SPLIT_MAX_TILES;
     }
+    pl.norm = rn;
+    pl.norm_dtype = cfg->dtype;
     HIP_TRY(launch_attn_plan(pl, stream));
-  }
-
-  RmsNorm rn{};
-  rn.x = x_in; rn.g = w->g1; rn.n_tokens = T; rn.hidden = H; rn.eps = cfg->rms_eps; rn.out = xn;
-  {
-    Timed tm(MCPU_KERNEL_RMSNORM, stream);
-    HIP_TRY(launch_rmsnorm(cfg->dtype, rn, stream));
   }
 
   Gemm gq{};

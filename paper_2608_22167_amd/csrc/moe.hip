@@ -1,6 +1,5 @@
-// Normalisation, router, token permutation and expert combine for gfx950.
+// Router, token permutation and expert combine for gfx950.
 //
-//  rmsnorm      one workgroup per token: y = x / sqrt(mean(x^2) + eps) * g
 //  router       RMSNorm of the residual stream in fp32, fp32 router logits
 //               (bf16 router weights widened exactly), top-k (ties to the
 //               lower expert id), softmax over the selected logits: one
@@ -48,48 +47,6 @@ __device__ __forceinline__ float load_row(const float* x, const float* g, int H,
     ss += v ? xv[j].x * xv[j].x + xv[j].y * xv[j].y + xv[j].z * xv[j].z + xv[j].w * xv[j].w : 0.f;
   }
   return ss;
-}
-
-__device__ __forceinline__ void store4(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
-__device__ __forceinline__ void store4(bf16* p, float4 v) {
-  *reinterpret_cast<uint2*>(p) = make_uint2((uint32_t)f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16),
-                                            (uint32_t)f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16));
-}
-
-template <typename T, int NV>
-__global__ __launch_bounds__(256) void rmsnorm_kernel(RmsNorm P) {
-  __shared__ float scratch[8];
-  const int t = blockIdx.x, H = P.hidden;
-  float4 xv[NV], gv[NV];
-  const float ss = load_row<NV>(P.x + (int64_t)t * H, P.g, H, xv, gv);
-  const float inv = 1.0f / sqrtf(block_sum_256(ss, scratch) / (float)H + P.eps);
-  T* out = reinterpret_cast<T*>(P.out) + (int64_t)t * H;
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int i = (threadIdx.x + 256 * j) * 4;
-    if (i < H)
-      store4(out + i, make_float4(xv[j].x * inv * gv[j].x, xv[j].y * inv * gv[j].y, xv[j].z * inv * gv[j].z,
-                                  xv[j].w * inv * gv[j].w));
-  }
-}
-
-template <typename T>
-static void rmsnorm_nv(const RmsNorm& p, hipStream_t s) {
-  const int nv = (p.hidden + 1023) / 1024;
-  dim3 g(p.n_tokens), b(256);
-  if (nv <= 1) hipLaunchKernelGGL((rmsnorm_kernel<T, 1>), g, b, 0, s, p);
-  else if (nv <= 2) hipLaunchKernelGGL((rmsnorm_kernel<T, 2>), g, b, 0, s, p);
-  else if (nv <= 3) hipLaunchKernelGGL((rmsnorm_kernel<T, 3>), g, b, 0, s, p);
-  else if (nv <= 4) hipLaunchKernelGGL((rmsnorm_kernel<T, 4>), g, b, 0, s, p);
-  else hipLaunchKernelGGL((rmsnorm_kernel<T, 8>), g, b, 0, s, p);
-}
-
-hipError_t launch_rmsnorm(int dtype, const RmsNorm& p, hipStream_t s) {
-  if (p.n_tokens == 0) return hipSuccess;
-  if (p.hidden % 4 || p.hidden > 8192) return hipErrorInvalidValue;
-  if (dtype == 0) rmsnorm_nv<float>(p, s);
-  else rmsnorm_nv<bf16>(p, s);
-  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
