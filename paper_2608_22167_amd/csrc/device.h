@@ -284,14 +284,19 @@ __device__ __forceinline__ U32x4 philox4x32_10(U32x4 c, uint32_t k0, uint32_t k1
 }
 
 // Gumbel noise from a 32-bit draw: u = (top 23 bits + 1/2) / 2^23, strictly
-// inside (0, 1) and exact in binary32, then g = -log(-log u); -log u is taken
-// as -log1p(u - 1) (u - 1 is exact), so it keeps full precision as u -> 1.
+// inside (0, 1) and exact in binary32, then g = -log(-log u). t = -ln u needs
+// relative accuracy down to 2^-24 (u next to 1: the largest noise). For
+// e = 1 - u < 1/16 (exact: u >= 1/2) it comes from the series
+// e + e^2/2 + ... + e^6/6 (truncation below e^7/7, relative 2^-24 / 7); further
+// from 1 the hardware log2 is accurate relative to the result. The outer
+// logarithm only needs absolute accuracy (its value is the noise), which the
+// hardware log2 gives.
 __device__ __forceinline__ float gumbel_of(uint32_t w) {
   const float u = ((float)(w >> 9) + 0.5f) * 0x1p-23f;
-  // t = -ln u needs relative accuracy down to 2^-24 (u next to 1: the largest
-  // noise), hence log1p of the exact u - 1; the outer logarithm only needs
-  // absolute accuracy (its value is the noise), which the hardware log2 gives
-  const float t = -log1pf(u - 1.0f);
+  const float e = 1.0f - u;
+  const float ts = e * (1.0f + e * (0.5f + e * (0.333333343f + e * (0.25f + e * (0.200000003f + e * 0.166666672f)))));
+  const float tl = -__builtin_amdgcn_logf(u) * 0.693147180559945309f;
+  const float t = e < 0.0625f ? ts : tl;
   return -__builtin_amdgcn_logf(t) * 0.693147180559945309f;
 }
 
