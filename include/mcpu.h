@@ -123,7 +123,11 @@ typedef struct mcpu_layer_cfg {
  *    stay required for the other tilings.
  *    MCPU_EXPERT_MXFP4_NATIVE: required, the slice-order copies of the MXFP4
  *    experts (codes and scales) written by mcpu_pack_mxfp4, 256-byte
- *    aligned; the products read only these. */
+ *    aligned; the products read only these.
+ *  w_qkv_packed, w_o_packed  optional (NULL): bf16 w_qkv and w_o in the same
+ *    streaming order (mcpu_pack_weights with one group, rows in their own
+ *    order), read by the projections of steps of up to 64 tokens and by the
+ *    O projection of prefill-sized steps; w_qkv and w_o stay required. */
 typedef struct mcpu_layer_weights {
   const float* g1;
   const void* w_qkv;
@@ -145,6 +149,8 @@ typedef struct mcpu_layer_weights {
   int32_t rope_max_pos;
   const void* w_gu_packed;
   const void* w_d_packed;
+  const void* w_qkv_packed;
+  const void* w_o_packed;
 } mcpu_layer_weights;
 
 /* Weights in streaming order (bf16 only), a layout aid for the decode-sized

@@ -268,6 +268,14 @@ int check_weights(const mcpu_layer_cfg* c, const mcpu_layer_weights* w, bool att
     return fail(MCPU_EINVAL, "packed w_gu needs 2 * ffn_dim %% 16 == 0 and hidden %% 64 == 0");
   if (w->w_d_packed && (c->hidden % 16 || c->ffn_dim % 64))
     return fail(MCPU_EINVAL, "packed w_d needs hidden %% 16 == 0 and ffn_dim %% 64 == 0");
+  if ((w->w_qkv_packed || w->w_o_packed) && c->dtype != MCPU_BF16)
+    return fail(MCPU_EINVAL, "packed projection weights need a bf16 layer");
+  if (w->w_qkv_packed && ((c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim % 16 || c->hidden % 64))
+    return fail(MCPU_EINVAL, "packed w_qkv needs (Hq + 2 Hkv) d %% 16 == 0 and hidden %% 64 == 0");
+  if (w->w_o_packed && (c->hidden % 16 || c->n_q_heads * c->head_dim % 64))
+    return fail(MCPU_EINVAL, "packed w_o needs hidden %% 16 == 0 and Hq d %% 64 == 0");
+  if ((uintptr_t)w->w_qkv_packed % 16 || (uintptr_t)w->w_o_packed % 16)
+    return fail(MCPU_EINVAL, "w_qkv_packed and w_o_packed must be 16-byte aligned");
   return MCPU_OK;
 }
 
@@ -673,6 +681,7 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
   gq.k_pool = pool->k; gq.v_pool = pool->v; gq.page_table = page_table; gq.max_pages = max_pages;
   gq.n_pages = pool->n_pages; gq.tok_seq = ab.tok_seq; gq.tok_pos = ab.tok_pos; gq.rope_cos = w->rope_cos;
   gq.rope_sin = w->rope_sin; gq.rope_max_pos = w->rope_max_pos; gq.err = err; gq.max_rows_per_group = T;
+  gq.w_packed = cfg->dtype == MCPU_BF16 ? w->w_qkv_packed : nullptr;
   if (split_floats) { gq.part = part; gq.part_cnt = part_cnt; }
   {
     Timed tm(MCPU_KERNEL_QKV, stream);
@@ -686,6 +695,7 @@ int decode_layer(const mcpu_layer_cfg* cfg, const mcpu_layer_weights* w, mcpu_kv
   Gemm go{};
   go.w = w->w_o; go.n = H; go.k = Hq * D; go.x = o; go.n_rows = T; go.n_groups = 1; go.epi = EPI_RESIDUAL;
   go.bias = w->b_o; go.residual = x_in; go.out = h1; go.err = err; go.max_rows_per_group = T;
+  go.w_packed = cfg->dtype == MCPU_BF16 ? w->w_o_packed : nullptr;
   if (split_floats) { go.part = part; go.part_cnt = part_cnt; }
   {
     Timed tm(MCPU_KERNEL_OPROJ, stream);

@@ -54,7 +54,7 @@ class LayerWeights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "g1", "w_qkv", "b_qkv", "w_o", "b_o", "g2", "w_r", "b_r", "w_gu", "b_gu", "w_d", "b_d",
         "s_gu", "s_d", "sinks", "rope_cos", "rope_sin")] + [("rope_max_pos", ctypes.c_int32)] + [
-        (n, ctypes.c_void_p) for n in ("w_gu_packed", "w_d_packed")]
+        (n, ctypes.c_void_p) for n in ("w_gu_packed", "w_d_packed", "w_qkv_packed", "w_o_packed")]
 
 
 class LmHead(ctypes.Structure):
@@ -187,8 +187,9 @@ def packed_mxfp4(codes: torch.Tensor, scales: torch.Tensor, stream=None) -> torc
 
 class DeviceWeights:
     """Layer parameters copied to the GPU, with the mcpu_layer_weights struct.
-    With pack=True, bf16 dense experts also get their streaming-order copies;
-    native MXFP4 experts always get their slice-order copies."""
+    With pack=True, bf16 dense experts and the bf16 projections also get their
+    streaming-order copies; native MXFP4 experts always get their slice-order
+    copies."""
 
     def __init__(self, shape, W, device="cuda", pack=True):
         self.t = {k: v.to(device).contiguous() for k, v in W.items()}
@@ -197,6 +198,9 @@ class DeviceWeights:
         if pack and not mx and shape.dtype == "bf16" and shape.hidden % 64 == 0 and shape.ffn_dim % 64 == 0:
             t["w_gu_packed"] = packed_weights(t["w_gu"])
             t["w_d_packed"] = packed_weights(t["w_d"])
+        if pack and shape.dtype == "bf16" and shape.hidden % 64 == 0 and shape.attn_dim % 64 == 0 and "w_qkv" in t:
+            t["w_qkv_packed"] = packed_weights(t["w_qkv"].view(1, *t["w_qkv"].shape))
+            t["w_o_packed"] = packed_weights(t["w_o"].view(1, *t["w_o"].shape))
         if shape.expert_fmt == "mxfp4_native" and "w_gu_packed" not in t:
             t["w_gu_packed"] = packed_mxfp4(t["w_gu_codes"], t["w_gu_scales"])
             t["w_d_packed"] = packed_mxfp4(t["w_d_codes"], t["w_d_scales"])
@@ -209,7 +213,8 @@ class DeviceWeights:
             s_gu=p("w_gu_scales") if mx else None, s_d=p("w_d_scales") if mx else None,
             sinks=p("sinks"), rope_cos=p("rope_cos"), rope_sin=p("rope_sin"),
             rope_max_pos=int(t["rope_cos"].shape[0]) if "rope_cos" in t else 0,
-            w_gu_packed=p("w_gu_packed"), w_d_packed=p("w_d_packed"))
+            w_gu_packed=p("w_gu_packed"), w_d_packed=p("w_d_packed"), w_qkv_packed=p("w_qkv_packed"),
+            w_o_packed=p("w_o_packed"))
 
 
 # ---------------------------------------------------------------------------

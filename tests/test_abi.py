@@ -140,7 +140,7 @@ _DUMMY = 1 << 32
 def _dummy_weights(mxfp4=False, drop=None):
     names = [n for n, _ in mcpu.LayerWeights._fields_ if n != "rope_max_pos"]
     kw = {n: _DUMMY + 4096 * i for i, n in enumerate(names)}
-    kw["w_gu_packed"] = kw["w_d_packed"] = None
+    kw["w_gu_packed"] = kw["w_d_packed"] = kw["w_qkv_packed"] = kw["w_o_packed"] = None
     if not mxfp4:
         kw["s_gu"] = kw["s_d"] = None
     if drop:
@@ -178,6 +178,11 @@ def test_decode_layer_rejects_null_pointers_and_small_workspace():
     w = _dummy_weights(mxfp4=True, drop="s_gu")
     assert _decode_call(mx, w, mcpu.decode_layer_workspace_size(mx, 3, 3)) == mcpu.MCPU_EINVAL
     assert "scale" in L.mcpu_last_error().decode()
+    # streaming-order projection copies on a layer that is not bf16
+    w = _dummy_weights()
+    w.w_qkv_packed = _DUMMY + (6 << 24)
+    assert s.dtype != "bf16" and _decode_call(s, w, need) == mcpu.MCPU_EINVAL
+    assert "packed projection" in L.mcpu_last_error().decode()
     # workspace one byte short
     assert _decode_call(s, _dummy_weights(), need - 1) == mcpu.MCPU_ENOMEM
     assert "workspace" in L.mcpu_last_error().decode()

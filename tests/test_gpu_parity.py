@@ -458,6 +458,26 @@ def _moe_forward_check(s, T, seed, h_seed):
     PT.check("moe out", _np(out), ref["out"], "bf16")
 
 
+@pytest.mark.parametrize("T", [16, 50])
+def test_projections_packed_weights_bitwise_equal_row_major(T):
+    """Decode steps of up to 64 tokens: the split projections read the
+    streaming-order copies of w_qkv and w_o when they are given (QKV in its
+    rotary block order, row by row from the copy), multiplying the same
+    operands in the same order, so the layer's outputs equal those from the
+    row-major weights bit for bit."""
+    rng = np.random.default_rng(1091 + T)
+    wl = W.custom(W.GPT_OSS_20B, rng.integers(1, 400, size=T), np.ones(T), 1091 + T)
+    packed, step = run_layer(wl)
+    assert "w_qkv_packed" in step.weights.t and "w_o_packed" in step.weights.t
+    step.weights = mcpu.DeviceWeights(wl.shape, wl.weights, pack=False)
+    assert "w_qkv_packed" not in step.weights.t
+    step.run()
+    torch.cuda.synchronize()
+    assert step.device_errors() == 0
+    np.testing.assert_array_equal(_np(step.x_out), packed["out"])
+    np.testing.assert_array_equal(step.topk_idx.cpu().numpy(), packed["idx"])
+
+
 @pytest.mark.parametrize("fmt", ["dense", "mxfp4"])
 @pytest.mark.parametrize("hidden,ffn,T", [(512, 512, 1000), (1024, 1024, 3600)])
 def test_moe_forward_many_rows(fmt, hidden, ffn, T):
