@@ -436,7 +436,7 @@ hipError_t slab_launch(const Gemm& g, hipStream_t s, int64_t grid) {
 
 // Split plan of one matrix: 64-wide slabs, the reduction in up to four parts
 // (at least two chunks each), as many as bring the launch near SPLIT_WG
-// workgroups. Measured on MI355X for 16-64 rows against the gpt-oss-20b
+// workgroups (none past 64 rows, where the tiles alone make hundreds). Measured on MI355X for 16-64 rows against the gpt-oss-20b
 // projections (weights from HBM): 2880 x 4096 (45 slabs) in 14 us with four
 // parts against 17 with two and 22 unsplit; 5120 x 2880 (80 slabs) in 18.5 us
 // with two against 20.7 with four and 23 unsplit. Finer splits, 128-wide
@@ -450,7 +450,7 @@ struct SplitPlan {
 };
 SplitPlan split_plan(int n, int k, int n_rows) {
   SplitPlan p;
-  if (n <= 0 || k <= 0 || n % 16 || k % 64 || n_rows <= 0 || n_rows > SPLIT_MAX_ROWS) return p;
+  if (n <= 0 || k <= 0 || n % 16 || k % 64 || n_rows <= 0 || n_rows > SLAB_WIDE_MAX_ROWS) return p;
   if ((int64_t)n * k * 2 >= (1LL << 31) || (int64_t)n_rows * k * 2 >= (1LL << 31)) return p;
   const int tiles = ((n_rows + SM - 1) / SM) * ((n + NSPLIT - 1) / NSPLIT);
   if (tiles > SPLIT_MAX_TILES) return p;
@@ -458,6 +458,7 @@ SplitPlan split_plan(int n, int k, int n_rows) {
   p.tiles = tiles;
   const int want = (SPLIT_WG + tiles / 2) / tiles;  // SPLIT_WG / tiles, rounded
   p.k_splits = std::max(1, std::min({want, SPLIT_K, nk / 2, SPLIT_MAX_K}));
+  if (n_rows > SPLIT_MAX_ROWS) p.k_splits = 1;  // no partial tiles are provided past 64 rows
   return p;
 }
 
@@ -470,8 +471,11 @@ size_t slab_split_part_floats(int n, int k, int n_rows) {
 
 bool slab_gemm_applies(int dtype, int expert_fmt, const Gemm& g) {
   if (dtype != 1 || g.k <= 0 || g.k % 64 || g.n % 16 || g.n_groups > TILE_MAXG) return false;
-  if (!g.group_off)  // one matrix: only as a split reduction
-    return expert_fmt == 0 && g.n_groups == 1 && g.part && g.part_cnt && split_plan(g.n, g.k, g.n_rows).tiles > 0;
+  if (!g.group_off) {  // one matrix: a split reduction, or wide with its streaming-order copy
+    if (expert_fmt != 0 || g.n_groups != 1 || !g.part || !g.part_cnt) return false;
+    if (g.n_rows > SPLIT_MAX_ROWS && !(g.w_packed && g.n >= SLAB_WIDE_MIN_N)) return false;
+    return split_plan(g.n, g.k, g.n_rows).tiles > 0;
+  }
   // 32-bit buffer offsets: token rows from x itself, weights within one group
   const int64_t xr = g.x_rows > 0 ? g.x_rows : g.n_rows;
   if (xr * g.k * 2 >= (1LL << 31) || (int64_t)g.n * g.k * 2 >= (1LL << 31)) return false;

@@ -262,6 +262,11 @@ bool slab_gemm_applies(int dtype, int expert_fmt, const Gemm& g);
 // split the reduction so that every compute unit streams weights; the last
 // workgroup of a tile to finish sums the partial tiles in split order.
 constexpr int SPLIT_MAX_ROWS = 64;
+// Up to SLAB_WIDE_MAX_ROWS rows, a matrix of at least SLAB_WIDE_MIN_N output
+// rows whose streaming-order copy is given also takes the slabs (unsplit: the
+// launch already has a few hundred workgroups); narrower ones stay on tiles.
+constexpr int SLAB_WIDE_MAX_ROWS = 512;
+constexpr int SLAB_WIDE_MIN_N = 4096;
 constexpr int SPLIT_MAX_TILES = 1024;
 size_t slab_split_part_floats(int n, int k, int n_rows);  // 0: no split for this shape
 // bf16 [groups][rows][cols] -> streaming order (the layout mcpu_pack_weights documents)
