@@ -356,11 +356,21 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_kernel(AttnSplit P) {
 // is written in the layer dtype, so no partials and no combine pass are
 // needed. (The split-K kernel, whose pages follow a page-table load each and
 // keep two in flight, left short windows waiting on memory latency.)
-template <typename T, int D, int MAXP>
-__global__ __launch_bounds__(64) void attn_window_kernel(AttnSplit P) {
+//
+// The KV heads of a token go to one workgroup of WW wavefronts (wavefront w:
+// head w), the workgroups in eight contiguous ranges, one per XCD (workgroups
+// are dealt to the XCDs round robin): a token's pages, which hold all its KV
+// heads side by side, are then read by one compute unit.
+template <typename T, int D, int MAXP, int WW>
+__global__ __launch_bounds__(64 * WW) void attn_window_kernel(AttnSplit P) {
   const int lane = lane_id();
-  const int s = blockIdx.x / P.hkv, g = blockIdx.x - (blockIdx.x / P.hkv) * P.hkv;
-  if (s >= P.n_splits) return;
+  const int items = P.n_splits * P.hkv;
+  const int nblk = (items + WW - 1) / WW, chunk = (nblk + 7) >> 3;
+  const int blk = (blockIdx.x & 7) * chunk + (blockIdx.x >> 3);
+  if ((int)(blockIdx.x >> 3) >= chunk || blk >= nblk) return;
+  const int item = blk * WW + uniform(threadIdx.x >> 6);
+  if (item >= items) return;  // no barriers below: a wavefront may leave alone
+  const int s = item / P.hkv, g = item - (item / P.hkv) * P.hkv;
   const SplitRange R = split_range(P, s);
   if (R.pg0 == R.pg1) return;  // an invalid record (error bit set): no token to finish
   const int npg = min(R.pg1 - R.pg0, MAXP);
@@ -414,13 +424,20 @@ __global__ __launch_bounds__(64) void attn_window_kernel(AttnSplit P) {
   }
 }
 
+#ifndef MCPU_WINDOW_WAVES
+#define MCPU_WINDOW_WAVES 8
+#endif
+constexpr int WINDOW_WAVES = MCPU_WINDOW_WAVES;  // wavefronts per window workgroup
+
 template <typename T, int D, int WAVES = 1, int PF = 2>
 hipError_t split_impl(const AttnSplit& p, hipStream_t s) {
   int64_t items = (int64_t)p.n_splits * p.hkv;
   int blocks = (int)((items + WAVES - 1) / WAVES);
   if (blocks == 0) return hipSuccess;
   if (p.o) {
-    hipLaunchKernelGGL((attn_window_kernel<T, D, WINDOW_MAX_PAGES>), dim3((unsigned)items), dim3(64), 0, s, p);
+    constexpr int WW = WINDOW_WAVES;
+    const int64_t nblk = (items + WW - 1) / WW, grid = (nblk + 7) / 8 * 8;
+    hipLaunchKernelGGL((attn_window_kernel<T, D, WINDOW_MAX_PAGES, WW>), dim3((unsigned)grid), dim3(64 * WW), 0, s, p);
   } else {
     hipLaunchKernelGGL((attn_split_kernel<T, D, WAVES, PF>), dim3(blocks), dim3(64 * WAVES), 0, s, p);
   }
