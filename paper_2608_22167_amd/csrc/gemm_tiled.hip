@@ -320,9 +320,12 @@ hipError_t launch_gemm_tiled(int expert_fmt, const Gemm& g, hipStream_t s) {
   if (tiles(64, 128) < 512) return tiled_launch<64, 64, 64, 4, 4, 0>(g, s);
   // 128-wide n-tiles, or 160-wide where those divide n and 128-wide ones
   // do not (2880 = 18 x 160: the expert down projection, whose last 128-wide
-  // tile would be half empty; 114 -> 109 us at batch 256)
+  // tile would be half empty; 114 -> 109 us at batch 256). The 128-wide
+  // tiles run eight wavefronts (2 x 4, 32 weight rows each): more loads in
+  // flight per CU than four (gate/up 201 -> 199 us at batch 256); 160 rows do
+  // not split four ways into 16-row MFMA tiles.
   if (g.n % 128 && g.n % 160 == 0) return tiled_launch<64, 160, 64, 2, 4, 0>(g, s);
-  return tiled_launch<64, 128, 64, 2, 4, 0>(g, s);
+  return tiled_launch<64, 128, 64, 2, 8, 0>(g, s);
 }
 
 }  // namespace mcpu
