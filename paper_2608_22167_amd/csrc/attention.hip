@@ -303,7 +303,11 @@ __global__ __launch_bounds__(64 * WAVES) void attn_split_kernel(AttnSplit P) {
   // PF-deep ring of pages: while page i is consumed, pages i+1 .. i+PF-1 are
   // in flight and page i+PF is issued into its slot. Loads are branch-free: a
   // slot past the split re-reads the last page, a missing page reads page 0,
-  // and both are masked out of the softmax instead of skipped.
+  // and both are masked out of the softmax instead of skipped. (The wait for
+  // each page-table entry also waits for the pages in flight; reading 64
+  // entries with one vector load up front avoids that but costs 17 VGPRs,
+  // five wavefronts per SIMD down to four, and was 4% slower at 64
+  // sequences: this kernel hides its latency with occupancy.)
   const int npg = pg1 - pg0;
   PageFrags<T, D> ring[PF];
   bool ok[PF];
@@ -383,20 +387,24 @@ __global__ __launch_bounds__(64 * WW) void attn_window_kernel(AttnSplit P) {
   const T* kpool = reinterpret_cast<const T*>(P.k_pool);
   const T* vpool = reinterpret_cast<const T*>(P.v_pool);
   const int64_t head_off = (int64_t)g * PAGE * D, page_elems = (int64_t)P.hkv * PAGE * D;
+  // Every page is requested before the first is used, unconditionally (slots
+  // past the window re-read its last page, a missing page reads page 0; both
+  // masked), and the error bit is set after the loads: a conditional load or
+  // atomic among them leaves the compiler unable to count the loads in
+  // flight, and it then waits for each page before requesting the next.
   PageFrags<T, D> pages[MAXP];
   bool ok[MAXP];
+  bool bad = false;
 #pragma unroll
   for (int u = 0; u < MAXP; ++u) {
-    ok[u] = false;
-    if (u < npg) {  // wave-uniform
-      int id = __shfl(my_id, u, 64);
-      const bool good = id >= 0 && id < P.n_pages;
-      if (!good && lane == 0) set_error(P.err, 1);
-      ok[u] = good;
-      id = good ? id : 0;
-      pages[u].load(kpool + id * page_elems + head_off, vpool + id * page_elems + head_off, lane);
-    }
+    int id = __shfl(my_id, min(u, npg - 1), 64);
+    const bool good = id >= 0 && id < P.n_pages;
+    bad = bad || (!good && u < npg);
+    ok[u] = good && u < npg;
+    id = good ? id : 0;
+    pages[u].load(kpool + id * page_elems + head_off, vpool + id * page_elems + head_off, lane);
   }
+  if (bad && lane == 0) set_error(P.err, 1);
   SoftmaxAcc<D> st;
 #pragma unroll
   for (int u = 0; u < MAXP; ++u)
