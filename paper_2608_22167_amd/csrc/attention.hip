@@ -181,15 +181,17 @@ hipError_t launch_attn_plan(const AttnPlan& p, hipStream_t s) {
 // split: one wavefront per (split, KV head)
 // ---------------------------------------------------------------------------
 
+// One KV head's K and V of one page, loaded with the streaming policy: a page
+// is read by one wavefront (C2 attention 218 -> 194 us).
 template <typename T, int D>
 struct PageFrags {
   Frag<T> k[D / 32];   // chunk c holds dims 32c + 8 * (lane / 16) .. +7 of key lane % 16
   Frag4<T> v[D / 16];  // block n holds V[4 * (lane / 16) + r][16n + lane % 16]
   __device__ __forceinline__ void load(const T* kp, const T* vp, int lane) {
 #pragma unroll
-    for (int c = 0; c < D / 32; ++c) k[c].load(kp + (64 * c + lane) * 8);
+    for (int c = 0; c < D / 32; ++c) k[c].load_stream(kp + (64 * c + lane) * 8);
 #pragma unroll
-    for (int n = 0; n < D / 16; ++n) v[n].load(vp + (64 * n + lane) * 4);
+    for (int n = 0; n < D / 16; ++n) v[n].load_stream(vp + (64 * n + lane) * 4);
   }
 };
 

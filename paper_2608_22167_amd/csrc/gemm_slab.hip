@@ -39,6 +39,7 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int BUF_D3 = 0x00020000;  // raw buffer descriptor word 3 (gfx9 family)
+constexpr int AUX_NT = 2;           // buffer-load cache policy: the non-temporal bit
 
 constexpr int SM = 64;              // token rows per item (split projections; experts: 64 or 128)
 constexpr int SKC = 128;            // reduction indices per chunk
@@ -83,12 +84,13 @@ struct SlabW<NF, 0> {
     }
     rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), 0, 0x7FFFFFFF, BUF_D3);
   }
+  template <int AUX>
   __device__ __forceinline__ void fetch(Regs& r, int kc, int nsteps) const {
 #pragma unroll
     for (int nb = 0; nb < NF; ++nb)
 #pragma unroll
       for (int t = 0; t < 4; ++t)
-        r.f[nb][t] = __builtin_amdgcn_raw_buffer_load_b128(rs, vo[nb], uniform(kc * kstep + tstep * min(t, nsteps - 1)), 0);
+        r.f[nb][t] = __builtin_amdgcn_raw_buffer_load_b128(rs, vo[nb], uniform(kc * kstep + tstep * min(t, nsteps - 1)), AUX);
   }
   struct Dec {};
   __device__ __forceinline__ void prepare(const Regs&, Dec&, uint32_t&, uint32_t) const {}
@@ -118,13 +120,14 @@ struct SlabW<NF, 1> {
       so[nb] = (uint32_t)wrow[nb] * (uint32_t)(P.k / 32) + g;
     }
   }
+  template <int AUX>
   __device__ __forceinline__ void fetch(Regs& r, int kc, int nsteps) const {
     // in a half chunk, lane groups 2 and 3 read the first half again (their
     // weights are zeroed when decoded)
     const int off = nsteps == 4 ? 0 : -2 * (g >> 1);
 #pragma unroll
     for (int nb = 0; nb < NF; ++nb) {
-      r.c[nb] = __builtin_amdgcn_raw_buffer_load_b128(rc, vo[nb] + 16 * off, uniform(kc * (SKC / 2)), 0);
+      r.c[nb] = __builtin_amdgcn_raw_buffer_load_b128(rc, vo[nb] + 16 * off, uniform(kc * (SKC / 2)), AUX);
       r.s[nb] = __builtin_amdgcn_raw_buffer_load_b8(rsc, so[nb] + off, uniform(kc * (SKC / 32)), 0);
     }
   }
@@ -154,7 +157,7 @@ struct SlabW<NF, 1> {
   }
 };
 
-template <int NS, int WF, int RC, int EPI, bool SPLIT, int SMT, int NX>
+template <int NS, int WF, int RC, int EPI, bool SPLIT, int SMT, int NX, bool NTW>
 __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
   static_assert(SMT == 64 || SMT == 128, "items of 64 or 128 token rows");
   static_assert(!SPLIT || SMT == SM, "split tiles have 64 token rows");
@@ -222,7 +225,7 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
   // weights of this workgroup's chunk i (clamped to its last)
   auto wfetch = [&](typename SlabW<NF, WF>::Regs& r, int i) __attribute__((always_inline)) {
     const int kc = kb + min(i, nkl - 1);
-    wl.fetch(r, kc, kc == nk - 1 ? tail_steps : 4);
+    wl.template fetch<NTW ? AUX_NT : 0>(r, kc, kc == nk - 1 ? tail_steps : 4);
   };
   if constexpr (NX == 1) {
 #pragma unroll
@@ -427,22 +430,22 @@ __global__ __launch_bounds__(256, 2) void gemm_slab_kernel(Gemm P) {
   epilogue<bf16, EPI>(P, cr, CLD, m0, mrows, n0 >> 4, nrows >> 4, grp);
 }
 
-template <int NS, int WF, int RC, bool SPLIT, int SMT = SM, int NX = 1>
+template <int NS, int WF, int RC, bool SPLIT, int SMT = SM, int NX = 1, bool NTW = false>
 hipError_t slab_launch(const Gemm& g, hipStream_t s, int64_t grid) {
   if (grid > 0x7FFFFFFF) return hipErrorInvalidValue;
   dim3 gd((unsigned)grid), bd(256);
   switch (g.epi) {
-    case EPI_QKV: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_QKV, SPLIT, SMT, NX>), gd, bd, 0, s, g); break;
-    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_RESIDUAL, SPLIT, SMT, NX>), gd, bd, 0, s, g); break;
-    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_SWIGLU, SPLIT, SMT, NX>), gd, bd, 0, s, g); break;
+    case EPI_QKV: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_QKV, SPLIT, SMT, NX, NTW>), gd, bd, 0, s, g); break;
+    case EPI_RESIDUAL: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_RESIDUAL, SPLIT, SMT, NX, NTW>), gd, bd, 0, s, g); break;
+    case EPI_SWIGLU: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_SWIGLU, SPLIT, SMT, NX, NTW>), gd, bd, 0, s, g); break;
     case EPI_LOGITS:  // vocabulary logits: bf16 weights, one reduction pass
       if constexpr (WF == 0 && !SPLIT) {
-        hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_LOGITS, SPLIT, SMT, NX>), gd, bd, 0, s, g);
+        hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_LOGITS, SPLIT, SMT, NX, NTW>), gd, bd, 0, s, g);
         break;
       } else {
         return hipErrorNotSupported;
       }
-    default: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_BIAS, SPLIT, SMT, NX>), gd, bd, 0, s, g); break;
+    default: hipLaunchKernelGGL((gemm_slab_kernel<NS, WF, RC, EPI_BIAS, SPLIT, SMT, NX, NTW>), gd, bd, 0, s, g); break;
   }
   return hipGetLastError();
 }
@@ -523,7 +526,12 @@ hipError_t launch_gemm_slab(int expert_fmt, const Gemm& g, hipStream_t s) {
     if (expert_fmt != 0 || p.tiles == 0 || !g.part || !g.part_cnt) return hipErrorInvalidValue;
     Gemm gs = g;
     gs.k_splits = p.k_splits;
-    return slab_launch<NSPLIT, 0, 2, true, SM, 2>(gs, s, (int64_t)p.tiles * p.k_splits);
+    // up to 64 rows every weight slab is read by one workgroup: the streaming
+    // policy (the wide form's four or more m-tiles re-read each slab from L2,
+    // which streaming loads do not keep: QKV at 256 rows 28 -> 38 us)
+    if (g.n_rows <= SPLIT_MAX_ROWS)
+      return slab_launch<NSPLIT, 0, 2, true, SM, 2, true>(gs, s, (int64_t)p.tiles * p.k_splits);
+    return slab_launch<NSPLIT, 0, 2, true, SM, 2, false>(gs, s, (int64_t)p.tiles * p.k_splits);
   }
   if (expert_fmt != 0) {
     if (!g.w_scales) return hipErrorInvalidValue;
@@ -533,6 +541,9 @@ hipError_t launch_gemm_slab(int expert_fmt, const Gemm& g, hipStream_t s) {
       return slab_launch<128, 1, 2, false, 128>(g, s, tile_grid(g, 128, 128));
     return slab_launch<128, 1, 2, false>(g, s, tile_grid(g, SM, 128));
   }
+  // groups of up to 32 rows on average mostly fit one 64-row item, whose
+  // weights no other workgroup reads: the streaming policy (C2 experts 8% faster)
+  if ((int64_t)g.n_rows <= 32LL * g.n_groups) return slab_launch<128, 0, 2, false, SM, 1, true>(g, s, tile_grid(g, SM, 128));
   return slab_launch<128, 0, 2, false>(g, s, tile_grid(g, SM, 128));
 }
 
