@@ -23,6 +23,8 @@
 // The item sequence is cut into eight contiguous ranges, one per XCD
 // (workgroups are dealt to the XCDs round robin), so that reuse happens within
 // one XCD's L2. The finished fp32 tile goes through LDS to the fused epilogue.
+#include <type_traits>
+
 #include "device.h"
 #include "gemm_epilogue.h"
 #include "kernels.h"
@@ -68,9 +70,10 @@ struct TiledW {
       src[j] = reinterpret_cast<const bf16*>(P.w) + grp * P.w_group_stride + (int64_t)wrow[j] * P.k +
                (tid % cpr) * 8;
   }
+  template <bool NTL>
   __device__ __forceinline__ void fetch(Regs& g, int ks) const {
 #pragma unroll
-    for (int j = 0; j < J; ++j) g.r[j] = ld16(src[j] + ks * BK);
+    for (int j = 0; j < J; ++j) g.r[j] = NTL ? ld_stream16(src[j] + ks * BK) : ld16(src[j] + ks * BK);
   }
   static __device__ __forceinline__ void store(const Regs& g, bf16* ws, int tid, bool&) {
 #pragma unroll
@@ -101,10 +104,11 @@ struct TiledW<BN, BK, 1, NTH> {
       ssrc[j] = P.w_scales + grp * (P.w_group_stride / 16) + (int64_t)wrow[j] * (P.k / 32) + blk(tid, j);
     }
   }
+  template <bool NTL>
   __device__ __forceinline__ void fetch(Regs& g, int ks) const {
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-      g.r[j] = ld16(csrc[j] + ks * (BK / 2));
+      g.r[j] = NTL ? ld_stream16(csrc[j] + ks * (BK / 2)) : ld16(csrc[j] + ks * (BK / 2));
       g.s[j] = ssrc[j][ks * bpr];
     }
   }
@@ -178,11 +182,11 @@ __global__ __launch_bounds__(NW * 64) void gemm_tiled_kernel(Gemm P) {
   };
   const int nk = P.k / BK;
   // slices past the end re-read the last one (branch-free; never staged for use)
-  auto fetch = [&](Regs& g, int ks) __attribute__((always_inline)) {
+  auto fetch = [&](Regs& g, int ks, auto NTL_) __attribute__((always_inline)) {
     ks = min(ks, nk - 1);
 #pragma unroll
     for (int j = 0; j < XJ; ++j) g.x[j] = ld16(xsrc[j] + ks * BK);
-    wl.fetch(g.w, ks);
+    wl.template fetch<decltype(NTL_)::value>(g.w, ks);
   };
   bool bad_scale = false;
   auto stage = [&](const Regs& g, int buf) __attribute__((always_inline)) {
@@ -229,26 +233,44 @@ __global__ __launch_bounds__(NW * 64) void gemm_tiled_kernel(Gemm P) {
   // at the loop head see one load order on every path. The scheduling
   // barriers keep the loads ahead of the products and the LDS writes, which
   // wait for their loads, behind them.
-  Regs rs[R];
+  // Expert launches: weight tiles of a group with one m-tile are read by this
+  // workgroup alone, so they take streaming loads (see ld_stream16); a group
+  // with more m-tiles shares them through L2, which streaming loads do not
+  // fill, so those keep plain loads. The pipeline is instantiated for both,
+  // so every load count is static (C3 gate/up 199 -> 191 us). One-matrix
+  // launches keep one plain pipeline: the second costs registers (64 x 64
+  // tiles: 124 -> 154 VGPRs, a wavefront per SIMD).
+  auto pipeline = [&](auto NTL_) __attribute__((always_inline)) {
+    Regs rs[R];
 #pragma unroll
-  for (int u = 0; u < R; ++u) {
-    fetch(rs[u], u);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  stage(rs[0], 0);
-  fetch(rs[0], R);
-  __builtin_amdgcn_sched_barrier(0);
-  __syncthreads();
-  for (int ks = 0; ks < nk; ks += UN) {
-#pragma unroll
-    for (int u = 0; u < UN; ++u) {
-      if (ks + u < nk) compute(u & 1);
+    for (int u = 0; u < R; ++u) {
+      fetch(rs[u], u, NTL_);
       __builtin_amdgcn_sched_barrier(0);
-      stage(rs[(u + 1) % R], (u + 1) & 1);
-      fetch(rs[(u + 1) % R], ks + u + 1 + R);
-      __builtin_amdgcn_sched_barrier(0);
-      __syncthreads();
     }
+    stage(rs[0], 0);
+    fetch(rs[0], R, NTL_);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    for (int ks = 0; ks < nk; ks += UN) {
+#pragma unroll
+      for (int u = 0; u < UN; ++u) {
+        if (ks + u < nk) compute(u & 1);
+        __builtin_amdgcn_sched_barrier(0);
+        stage(rs[(u + 1) % R], (u + 1) & 1);
+        fetch(rs[(u + 1) % R], ks + u + 1 + R, NTL_);
+        __builtin_amdgcn_sched_barrier(0);
+        __syncthreads();
+      }
+    }
+  };
+  constexpr bool EXPERT = EPI == EPI_SWIGLU || EPI == EPI_BIAS;
+  if constexpr (EXPERT) {
+    if (uniform(mt_start[grp + 1] - mt_start[grp]) == 1)
+      pipeline(std::true_type{});
+    else
+      pipeline(std::false_type{});
+  } else {
+    pipeline(std::false_type{});
   }
   __syncthreads();  // the fp32 tile below reuses the operand buffers
   if (bad_scale) set_error(P.err, 16);
