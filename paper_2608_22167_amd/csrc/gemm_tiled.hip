@@ -272,6 +272,76 @@ __global__ __launch_bounds__(NW * 64) void gemm_tiled_kernel(Gemm P) {
   } else {
     pipeline(std::false_type{});
   }
+  if constexpr (EPI == EPI_LOGITS && WN == LOGIT_SLOT) {
+    // Vocabulary logits with one 64-column sampling slot per wavefront: each
+    // lane holds, per 16-row tile mb, columns 16 nb + 4 (lane / 16) + r (nb, r
+    // < 4) of row 16 mb + lane % 16, so a slot's record folds 16 values per
+    // lane and then the four lanes of a row (two cross-lane steps), straight
+    // from the product registers. Same record, draws and tie rule (lowest
+    // column on equal values) as the LDS epilogue.
+    LogitSlot* out = reinterpret_cast<LogitSlot*>(P.out);
+    const int n_slots = (P.n + LOGIT_SLOT - 1) / LOGIT_SLOT;
+    const int cb = n0 + wn * WN, c_end = n0 + nrows, gq = lane >> 4;
+    const bool draw = !P.greedy;
+    const float NEG = -__builtin_inff();
+    int pos[MT], seq[MT], tgt[MT];
+#pragma unroll
+    for (int mb = 0; mb < MT; ++mb) {
+      const int r = m0 + min(wm * (BM / 2) + 16 * mb + fr, mrows - 1);
+      pos[mb] = draw ? P.row_pos[r] : 0;
+      seq[mb] = draw ? P.row_seq[r] : 0;
+      tgt[mb] = P.target ? P.target[r] : -1;
+    }
+#pragma unroll
+    for (int mb = 0; mb < MT; ++mb) {
+      float sv[NT][4];
+      float mx = NEG, pert = NEG, sb = NEG, st = NEG;
+      int bi = 0x7FFFFFFF;
+#pragma unroll
+      for (int nb = 0; nb < NT; ++nb) {
+        const int c0 = cb + 16 * nb + 4 * gq;
+        float gn[4] = {0.f, 0.f, 0.f, 0.f};
+        if (draw && c0 < c_end) {
+          const U32x4 rr = philox4x32_10(U32x4{(uint32_t)(c0 >> 2), (uint32_t)pos[mb], (uint32_t)seq[mb], LOGIT_RNG_TAG},
+                                         (uint32_t)P.seed, (uint32_t)(P.seed >> 32));
+          gn[0] = gumbel_of(rr.x); gn[1] = gumbel_of(rr.y); gn[2] = gumbel_of(rr.z); gn[3] = gumbel_of(rr.w);
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {  // increasing columns: the first of equal values is the lowest
+          const bool ok = c0 + r < c_end;
+          sv[nb][r] = ok ? acc[nb][mb][r] * P.inv_temp : NEG;
+          mx = fmaxf(mx, sv[nb][r]);
+          const float pv = sv[nb][r] + gn[r];
+          if (ok && pv > pert) { pert = pv; sb = sv[nb][r]; bi = c0 + r; }
+          if (ok && c0 + r == tgt[mb]) st = sv[nb][r];
+        }
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      float sum = 0.f;
+#pragma unroll
+      for (int nb = 0; nb < NT; ++nb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          sum += cb + 16 * nb + 4 * gq + r < c_end ? __builtin_amdgcn_exp2f((sv[nb][r] - mx) * 1.44269504088896341f) : 0.f;
+#pragma unroll
+      for (int o = 16; o <= 32; o <<= 1) {
+        sum += __shfl_xor(sum, o, 64);
+        const float p2 = __shfl_xor(pert, o, 64), s2 = __shfl_xor(sb, o, 64);
+        const int i2 = __shfl_xor(bi, o, 64);
+        if (p2 > pert || (p2 == pert && i2 < bi)) { pert = p2; sb = s2; bi = i2; }
+        st = fmaxf(st, __shfl_xor(st, o, 64));
+      }
+      const int m = wm * (BM / 2) + 16 * mb + fr;
+      if (gq == 0 && m < mrows && cb < c_end) {
+        LogitSlot rec;
+        rec.m = mx; rec.l = sum; rec.pert = pert; rec.s_best = sb; rec.idx = bi; rec.s_tgt = st;
+        rec.pad[0] = rec.pad[1] = 0.f;
+        out[(int64_t)(m0 + m) * n_slots + cb / LOGIT_SLOT] = rec;
+      }
+    }
+    return;
+  }
   __syncthreads();  // the fp32 tile below reuses the operand buffers
   if (bad_scale) set_error(P.err, 16);
 

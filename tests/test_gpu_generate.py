@@ -79,8 +79,9 @@ def _small_head(hidden, vocab, seed):
 @pytest.mark.parametrize("T,vocab", [(1, 4096), (37, 4096), (300, 4096), (600, 65536)])
 @pytest.mark.parametrize("temperature", [TAU, 0.0])
 def test_lm_head_sample_small(T, vocab, temperature):
-    """Few rows (weight slabs), 300 rows (LDS tiles) and 600 rows over a
-    65536-id vocabulary (pipelined 256 x 256 tiles); sampling and greedy."""
+    """Few rows (weight slabs), 300 rows (64 x 64 tiles, records through LDS)
+    and 600 rows over a 65536-id vocabulary (128 x 128 tiles, records folded
+    from the product registers, a partial last row tile); sampling and greedy."""
     H = 256
     Wt, head = _small_head(H, vocab, 2001)
     rng = np.random.default_rng(T + vocab)
@@ -96,10 +97,11 @@ def test_lm_head_sample_small(T, vocab, temperature):
     print(f"  T={T} V={vocab} temperature={temperature}: {near} near-tie rows")
 
 
-@pytest.mark.parametrize("T", [64, 512])
+@pytest.mark.parametrize("T", [64, 256, 512])
 def test_lm_head_sample_full_vocabulary_sampled(T):
     """gpt-oss-20b shapes: hidden 2880, 201088 ids (1.16 GB of bf16 weights),
-    64 rows (streaming-order weight slabs) and 512 rows (pipelined tiles);
+    64 rows (streaming-order weight slabs), 256 rows (the benchmarked head) and
+    512 rows (128 x 128 tiles, records folded from the product registers);
     compared on seeded rows."""
     H, V = 2880, W.GPT_OSS_VOCAB
     Wd = W.lm_weights_device(2002, H, V)
